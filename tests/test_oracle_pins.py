@@ -1,0 +1,291 @@
+"""Pins of the fp64 oracle against what the paper and mathematics fix (CPU only).
+
+Each oracle function is checked against something other than itself: brute
+force, closed forms, finite differences of the forward definition, hand-worked
+integer examples, and the initial-codebook levels of eq. init_ab."""
+import os
+
+import numpy as np
+import pytest
+
+import oracle as orc
+
+GOLDEN = os.path.join(os.path.dirname(__file__), "golden")
+
+
+def _all_bf16_values():
+    bits = np.arange(1 << 16, dtype=np.uint32)
+    return (bits << 16).view(np.float32).astype(np.float64)
+
+
+def _nearest_code_bruteforce(z):
+    """Nearest of {0,1,2,3}; on an exact tie the even code.  Independent of rint/clip."""
+    out = np.empty(z.shape, dtype=np.int64)
+    for i, v in enumerate(z):
+        if np.isnan(v):
+            out[i] = 0
+            continue
+        best, bestd = None, None
+        for c in range(4):
+            dist = abs(v - c)
+            if bestd is None or dist < bestd or (dist == bestd and c % 2 == 0):
+                best, bestd = c, dist
+        out[i] = best
+    return out
+
+
+# ------------------------------------------------------------- widening -----
+
+def test_widen_bf16_known_bits():
+    bits = np.array([0x0000, 0x3F80, 0x4000, 0x4040, 0xBF00, 0x7F80, 0xFF80, 0x3F00], np.uint16)
+    v = orc.widen(bits, "bf16")
+    assert list(v) == [0.0, 1.0, 2.0, 3.0, -0.5, np.inf, -np.inf, 0.5]
+
+
+# ------------------------------------------------------------ quantiser -----
+
+def test_quantize_hand_cases():
+    z = np.array([-0.7, 0.5, 1.5, 3.6, 2.5, 3.5, -0.5, 3.2, 0.49, 0.51, 1e30, -1e30,
+                  np.inf, -np.inf, np.nan, -0.0, 2.4999, 1.0])
+    assert orc.quantize(z).tolist() == [0, 0, 2, 3, 2, 3, 0, 3, 0, 1, 3, 0, 3, 0, 0, 0, 2, 1]
+
+
+def test_quantize_exhaustive_bf16_is_nearest_code_ties_even():
+    z = _all_bf16_values()
+    got = orc.quantize(z).astype(np.int64)
+    assert got.min() >= 0 and got.max() <= 3
+    # brute force only where it matters (|z| <= 8); outside, the answer is 0 or 3
+    sel = np.abs(np.nan_to_num(z, nan=0.0)) <= 8.0
+    assert np.array_equal(got[sel], _nearest_code_bruteforce(z[sel]))
+    far = ~sel & ~np.isnan(z)
+    assert np.all(got[far & (z > 0)] == 3) and np.all(got[far & (z < 0)] == 0)
+    assert np.all(got[np.isnan(z)] == 0)
+
+
+def test_quantize_fp32_around_every_half_point():
+    pts = []
+    for h in [-1.5, -0.5, 0.5, 1.5, 2.5, 3.5, 4.5]:
+        x = np.float32(h)
+        lo, hi = x, x
+        for _ in range(64):
+            lo = np.nextafter(lo, np.float32(-np.inf))
+            hi = np.nextafter(hi, np.float32(np.inf))
+            pts += [lo, hi]
+        pts.append(x)
+    z = np.array(pts, dtype=np.float32).astype(np.float64)
+    z = np.concatenate([z, np.random.default_rng(7).uniform(-2, 5, 20000).astype(np.float32)])
+    assert np.array_equal(orc.quantize(z).astype(np.int64), _nearest_code_bruteforce(z))
+
+
+def test_mask_closed_forms_exhaustive_bf16():
+    z = _all_bf16_values()
+    fin = ~np.isnan(z)
+    rounded = orc.ste_mask(z, orc.MASK_ROUNDED)
+    latent = orc.ste_mask(z, orc.MASK_LATENT)
+    # round-half-even keeps -0.5 (-> -0) inside and pushes 3.5 (-> 4) outside
+    assert np.array_equal(rounded[fin], (z[fin] >= -0.5) & (z[fin] < 3.5))
+    assert np.array_equal(latent[fin], (z[fin] >= 0.0) & (z[fin] <= 3.0))
+    assert not rounded[~fin].any() and not latent[~fin].any()
+    hand = orc.ste_mask(np.array([-0.7, 0.5, 1.5, 3.6, 3.2, -0.5, 3.5]), orc.MASK_ROUNDED)
+    assert hand.tolist() == [False, True, True, False, True, True, False]
+    assert orc.ste_mask(np.array([3.2]), orc.MASK_LATENT).tolist() == [False]
+
+
+# --------------------------------------------------------------- decode -----
+
+UT4 = np.triu(np.ones((4, 4)))            # A[j, k] = 1 for k >= j (not symmetric)
+
+
+def test_decode_hand_example():
+    # row codes (0,1,2,3 | 3,2,1,0), A upper-triangular ones, b = (1,2,3,4):
+    # component j of group g = sum_{k >= j} z_k + b_j
+    codes = np.array([[0, 1, 2, 3, 3, 2, 1, 0]])
+    W = orc.decode(codes, UT4, np.array([1.0, 2, 3, 4]), 4)
+    assert W.tolist() == [[7, 8, 8, 7, 7, 5, 4, 4]]
+
+
+@pytest.mark.parametrize("d", [4, 8])
+def test_decode_identity_map_reproduces_codes(d):
+    codes = np.random.default_rng(d).integers(0, 4, size=(5, 4 * d))
+    W = orc.decode(codes, np.eye(d), np.zeros(d), d)
+    assert np.array_equal(W, codes.astype(np.float64))
+
+
+@pytest.mark.parametrize("d", [4, 8])
+def test_decode_zero_codes_give_offset(d):
+    b = np.arange(1.0, d + 1)
+    W = orc.decode(np.zeros((3, 2 * d), np.uint8), np.random.default_rng(1).standard_normal((d, d)), b, d)
+    assert np.array_equal(W, np.tile(b, (3, 2)))
+
+
+def test_init_levels_golden():
+    rows = [l.split() for l in open(os.path.join(GOLDEN, "init_ab_levels.txt")) if l.strip() and l[0] != "#"]
+    levels = np.array([float(r[1]) for r in rows])
+    A, b = orc.init_map(np.eye(4))
+    W = orc.decode(np.array([[0, 1, 2, 3], [3, 3, 3, 3]]), A, b, 4)
+    assert np.allclose(W[0], levels, rtol=0, atol=1e-15)
+    assert np.allclose(W[1], levels[3], rtol=0, atol=1e-15)
+
+
+@pytest.mark.parametrize("d", [4, 8])
+def test_init_codebook_zero_mean_identity_covariance(d):
+    # over all 4^d code vectors, z has mean mu*1 and covariance (5/4) I, so
+    # A z + B with eq. init_ab has mean 0 and covariance s^2 (5/4) G G^T = I exactly
+    G, _ = np.linalg.qr(np.random.default_rng(11 + d).standard_normal((d, d)))
+    A, b = orc.init_map(G)
+    grid = np.stack(np.meshgrid(*[np.arange(4)] * d, indexing="ij"), -1).reshape(-1, d)
+    W = orc.decode(grid.reshape(1, -1), A, b, d).reshape(-1, d)
+    assert np.allclose(W.mean(0), 0, atol=1e-12)
+    assert np.allclose(np.cov(W.T, bias=True), np.eye(d), atol=1e-12)
+
+
+# -------------------------------------------------------------- forward -----
+
+def test_forward_hand_example():
+    X = np.array([[1.0, 0, 2, -1, 0, 0, 0, 1]])
+    codes = np.array([[0, 1, 2, 3, 3, 2, 1, 0]])
+    W = orc.decode(codes, UT4, np.array([1.0, 2, 3, 4]), 4)
+    # 1*7 + 2*8 - 1*7 + 1*4
+    assert orc.forward(X, W).tolist() == [[20.0]]
+    assert orc.forward_reformulated(X, codes, UT4, np.array([1.0, 2, 3, 4]), 4).tolist() == [[20.0]]
+
+
+@pytest.mark.parametrize("d", [4, 8])
+def test_forward_equals_reformulated(d):
+    r = np.random.default_rng(3 + d)
+    N, m, n = 7, 9, 6 * d
+    X = r.standard_normal((N, n))
+    codes = r.integers(0, 4, size=(m, n))
+    A, b = r.standard_normal((d, d)), r.standard_normal(d)
+    Y1 = orc.forward(X, orc.decode(codes, A, b, d))
+    Y2 = orc.forward_reformulated(X, codes, A, b, d)
+    assert np.allclose(Y1, Y2, rtol=1e-12, atol=1e-12)
+
+
+def test_forward_zero_codes_closed_form():
+    r = np.random.default_rng(5)
+    d, N, m, n = 8, 4, 3, 32
+    X, A, b = r.standard_normal((N, n)), r.standard_normal((d, d)), r.standard_normal(d)
+    Y = orc.forward(X, orc.decode(np.zeros((m, n), np.uint8), A, b, d))
+    per_token = sum(X[:, c] * b[c % d] for c in range(n))
+    assert np.allclose(Y, per_token[:, None] * np.ones((1, m)), rtol=1e-12, atol=1e-12)
+
+
+# ------------------------------------------------------------- backward -----
+
+def test_backward_hand_example():
+    # N = m = 1, dY = 1: dW = X, dX = W_hat row, dA = sum_g outer(X_g, z_g), db = sum_g X_g,
+    # dcode[g*d+k] = sum_{j<=k} X[g*d+j] (A upper-triangular ones)
+    X = np.array([[1.0, 0, 2, -1, 0, 0, 0, 1]])
+    Z = np.array([[0.1, 1.2, 1.9, 3.3, 2.6, 2.2, 0.8, -0.3]])        # codes 0,1,2,3,3,2,1,0
+    out = orc.linear_backward(Z, UT4, np.array([1.0, 2, 3, 4]), X, np.array([[1.0]]), 4)
+    assert out["dX"].tolist() == [[7, 8, 8, 7, 7, 5, 4, 4]]
+    assert out["dA"].tolist() == [[0, 1, 2, 3], [0, 0, 0, 0], [0, 2, 4, 6], [3, 1, -1, -3]]
+    assert out["db"].tolist() == [1, 0, 2, 0]
+    assert out["dZ"].tolist() == [[1, 1, 3, 2, 0, 0, 0, 1]]
+
+
+def _fd(f, x, idx, h):
+    xp, xm = x.copy(), x.copy()
+    xp[idx] += h
+    xm[idx] -= h
+    return (f(xp) - f(xm)) / (2 * h)
+
+
+@pytest.mark.parametrize("d", [4, 8])
+def test_backward_matches_finite_differences(d):
+    # L = <dY, Y> is linear in X, A, b and W_hat (codes fixed), so central
+    # differences are exact up to fp64 rounding.
+    r = np.random.default_rng(20 + d)
+    N, m, n = 3, 4, 2 * d
+    X, dY = r.standard_normal((N, n)), r.standard_normal((N, m))
+    Z = r.uniform(-1.0, 4.0, size=(m, n))
+    A, b = r.standard_normal((d, d)), r.standard_normal(d)
+    codes = orc.quantize(Z)
+    out = orc.linear_backward(Z, A, b, X, dY, d)
+
+    def loss(X_=X, A_=A, b_=b):
+        return float(np.sum(dY * orc.forward(X_, orc.decode(codes, A_, b_, d))))
+
+    for idx in np.ndindex(X.shape):
+        assert np.isclose(_fd(lambda v: loss(X_=v), X, idx, 0.5), out["dX"][idx], rtol=1e-9, atol=1e-9)
+    for idx in np.ndindex(A.shape):
+        assert np.isclose(_fd(lambda v: loss(A_=v), A, idx, 0.5), out["dA"][idx], rtol=1e-9, atol=1e-9)
+    for j in range(d):
+        assert np.isclose(_fd(lambda v: loss(b_=v), b, (j,), 0.5), out["db"][j], rtol=1e-9, atol=1e-9)
+    W = orc.decode(codes, A, b, d)
+    for idx in np.ndindex(W.shape):
+        g = _fd(lambda v: float(np.sum(dY * orc.forward(X, v))), W, idx, 0.5)
+        assert np.isclose(g, out["dW"][idx], rtol=1e-9, atol=1e-9)
+    # straight-through: d/dcode with codes relaxed to reals, masked by the clip range
+    Cf = codes.astype(np.float64)
+    dcode = np.zeros_like(Cf)
+    for idx in np.ndindex(Cf.shape):
+        dcode[idx] = _fd(lambda v: float(np.sum(dY * orc.forward(X, orc.decode(v, A, b, d)))), Cf, idx, 0.5)
+    mask = orc.ste_mask(Z)
+    assert np.allclose(out["dZ"][mask], dcode[mask], rtol=1e-9, atol=1e-9)
+    assert np.all(out["dZ"][~mask] == 0.0)
+    assert (~mask).any() and mask.any()
+
+
+@pytest.mark.parametrize("d", [4, 8])
+def test_grad_latent_identity_map_is_weight_grad(d):
+    r = np.random.default_rng(40 + d)
+    N, m, n = 5, 6, 3 * d
+    X, dY = r.standard_normal((N, n)), r.standard_normal((N, m))
+    Z = r.uniform(0.0, 3.0, size=(m, n))        # every latent inside the clip range
+    out = orc.linear_backward(Z, np.eye(d), np.zeros(d), X, dY, d)
+    assert np.allclose(out["dZ"], dY.T @ X, rtol=1e-12, atol=1e-12)
+
+
+def test_mask_latent_mode_in_backward():
+    r = np.random.default_rng(9)
+    d, N, m, n = 4, 2, 3, 8
+    Z = np.array([[3.2, 0.2, 1.0, 2.0, -0.3, 1.1, 2.2, 3.0]] * m)
+    out_r = orc.linear_backward(Z, np.eye(d), np.zeros(d), r.standard_normal((N, n)),
+                                r.standard_normal((N, m)), d, orc.MASK_ROUNDED)
+    out_l = orc.linear_backward(Z, np.eye(d), np.zeros(d), r.standard_normal((N, n)),
+                                r.standard_normal((N, m)), d, orc.MASK_LATENT)
+    assert np.all(out_r["dZ"][:, [0, 4]] != 0)          # 3.2 and -0.3 round inside [0, 3]
+    assert np.all(out_l["dZ"][:, [0, 4]] == 0)          # but lie outside it
+
+
+# ------------------------------------------------------------- packing ------
+
+def test_pack_hand_values():
+    assert orc.pack2bit(np.array([[1, 2, 3, 0]])).tolist() == [[0x39]]
+    assert orc.pack2bit(np.array([[3, 3, 3, 3, 0, 0, 0, 0]])).tolist() == [[0xFF, 0x00]]
+    for c in range(8):
+        row = np.zeros((1, 8), np.uint8)
+        row[0, c] = 1
+        expect = [0, 0]
+        expect[c // 4] = 1 << (2 * (c % 4))
+        assert orc.pack2bit(row).tolist() == [expect]
+
+
+def test_pack_round_trip():
+    codes = np.random.default_rng(2).integers(0, 4, size=(7, 64)).astype(np.uint8)
+    p = orc.pack2bit(codes)
+    assert p.shape == (7, 16)
+    unpacked = np.stack([(p >> (2 * i)) & 3 for i in range(4)], axis=-1).reshape(7, 64)
+    assert np.array_equal(unpacked, codes)
+
+
+# ------------------------------------------------------------ optimiser -----
+
+def test_adamw_first_step_closed_form():
+    theta, g = np.array([1.0, -2.0, 0.5]), np.array([0.3, -4.0, 1e-3])
+    t1, m1, m2 = orc.adamw_step(theta, g, 0 * g, 0 * g, 1, lr=1e-2)
+    assert np.allclose(t1, theta - 1e-2 * g / (np.abs(g) + 1e-8), rtol=0, atol=1e-15)
+    t1w, _, _ = orc.adamw_step(theta, g, 0 * g, 0 * g, 1, lr=1e-2, weight_decay=0.1)
+    assert np.allclose(t1w, theta * (1 - 1e-3) - 1e-2 * g / (np.abs(g) + 1e-8), rtol=0, atol=1e-15)
+
+
+def test_adamw_constant_gradient_steps_are_equal():
+    # with a constant gradient the bias-corrected moments equal g and g^2 at every step
+    theta, g = np.array([0.0, 0.0]), np.array([2.0, -0.5])
+    m1, m2 = 0 * g, 0 * g
+    for step in range(1, 6):
+        new, m1, m2 = orc.adamw_step(theta, g, m1, m2, step, lr=0.1)
+        assert np.allclose(theta - new, 0.1 * g / (np.abs(g) + 1e-8), rtol=1e-12, atol=0)
+        theta = new
