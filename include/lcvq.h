@@ -1,0 +1,163 @@
+/*
+ * lcvq.h -- C ABI of the LC-VQ linear layer library (liblcvq.so, gfx950).
+ *
+ * The layer is the linear-constrained vector-quantised linear layer of
+ * LC-QAT (arXiv 2606.10531).  A weight matrix W (m out-features x n
+ * in-features) is held as latent proxy weights Z (the paper's W_p), one
+ * d x d map A and one offset b of length d shared by the whole matrix
+ * (eq. lc_codebook, Sec. 2.2).  The forward pass (Sec. 3.2) is
+ *
+ *   codes  = clip(round(Z), 0, 3)                     eq. quant_param, b = 2 bits
+ *   W_hat[r, g*d + j] = sum_k A[j,k] codes[r, g*d + k] + b[j]   def. forward
+ *   Y      = X W_hat^T                                X: N tokens x n
+ *
+ * and is evaluated in the reformulated order of def. forward_x
+ * (Y = (X blockdiag(A)) codes^T + (X b~) 1^T), so the dense W_hat is never
+ * written to device memory.  The backward pass uses the straight-through
+ * estimator of Sec. 3.3 (round() passes gradients; clip() zeroes them outside
+ * its range) and yields dX, dZ, dA and db.
+ *
+ * Conventions shared by every call
+ *  - All tensors are dense, row-major, caller-owned DEVICE pointers; the
+ *    library allocates nothing and keeps no mutable global state.
+ *  - `stream` is a hipStream_t passed as void* (NULL = the null stream).
+ *    Every call only enqueues work on it and returns; device-side results are
+ *    visible after the caller synchronises that stream.
+ *  - round() is IEEE round-half-to-even; clip bounds are inclusive; a NaN
+ *    latent gives code 0 and mask 0; +inf / -inf give codes 3 / 0, mask 0.
+ *  - Arguments are validated on the host before anything is enqueued; on any
+ *    error nothing is enqueued and outputs are untouched.  A zero-sized
+ *    problem returns LCVQ_OK without enqueuing work.  Launch failures return
+ *    LCVQ_EHIP.  lcvq_last_error() gives a human-readable detail for the
+ *    calling thread's last non-OK status.
+ *  - Outputs must not alias inputs.  Calls that share a workspace must not
+ *    overlap in time (use one stream, or one workspace per stream).
+ */
+#ifndef LCVQ_H
+#define LCVQ_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  LCVQ_OK = 0,
+  LCVQ_EINVAL = 1,        /* null required pointer, negative size, bad enum, n % d != 0 */
+  LCVQ_EUNSUPPORTED = 2,  /* d not in {4, 8}; bf16 path with m or n not a multiple of 8 */
+  LCVQ_EALIGN = 3,        /* a device pointer not 16-byte aligned */
+  LCVQ_EWORKSPACE = 4,    /* workspace smaller than lcvq_workspace_bytes() */
+  LCVQ_EHIP = 5           /* the HIP runtime refused a launch */
+} lcvq_status_t;
+
+/* Element type of Z, X, Y, dY, dX (and of dZ unless dz_dtype says otherwise).
+ * A, b, dA and db are always fp32. */
+typedef enum { LCVQ_F32 = 0, LCVQ_BF16 = 1 } lcvq_dtype_t;
+
+/* What a code source holds. */
+typedef enum {
+  LCVQ_SRC_LATENT = 0,    /* latent Z (m x n, fp32 or bf16): codes = clip(round(Z), 0, 3) */
+  LCVQ_SRC_CODES_U8 = 1,  /* one byte per code (m x n, values above 3 are taken as 3) */
+  LCVQ_SRC_PACKED2 = 2    /* packed 2-bit codes, layout of lcvq_pack2bit */
+} lcvq_src_t;
+
+/* Where the straight-through gradient is passed (Sec. 3.3 with the chain rule
+ * of clip()). */
+typedef enum {
+  LCVQ_MASK_ROUNDED = 0,  /* default: 0 <= round(Z) <= 3, i.e. Z in [-0.5, 3.5) */
+  LCVQ_MASK_LATENT = 1    /* 0 <= Z <= 3 */
+} lcvq_mask_t;
+
+typedef enum { LCVQ_OP_FWD = 0, LCVQ_OP_BWD = 1 } lcvq_op_t;
+
+/*
+ * lcvq_pack2bit -- packed 2-bit codes, four per byte.
+ * The paper fixes the width only (2-bit codes, Sec. 2.1 / 3.2); this layout is
+ * the library's: the code of column c of row r sits at bits 2*(c % 4) and
+ * 2*(c % 4) + 1 of byte r*(n/4) + c/4 (least significant first), so a
+ * little-endian 32-bit word holds 16 consecutive codes.
+ *   src      m x n latent Z (src_kind LATENT, element type src_dtype) or
+ *            m x n uint8 codes (src_kind CODES_U8, src_dtype ignored)
+ *   packed   m * n / 4 bytes, written
+ * Requires n % 4 == 0 (else LCVQ_EINVAL); src and packed 16-byte aligned.
+ */
+lcvq_status_t lcvq_pack2bit(const void *src, int32_t src_kind, int32_t src_dtype,
+                            int64_t m, int64_t n, uint8_t *packed, void *stream);
+
+/*
+ * lcvq_dequant -- the dense effective weight W_hat (def. forward, Sec. 3.2):
+ *   W_hat[r, g*d + j] = sum_k A[j*d + k] * code[r, g*d + k] + b[j]
+ * with codes taken from `src` (lcvq_src_t `src_kind`; element type `src_dtype`
+ * for LATENT).  A is d x d row-major fp32, b has d fp32 entries.  W_hat is
+ * m x n of element type `out_dtype` (bf16 results are rounded to nearest even
+ * from fp32 arithmetic).  d in {4, 8}; n % d == 0.  This is a utility for
+ * export and inspection: the training calls below never form W_hat.
+ */
+lcvq_status_t lcvq_dequant(int64_t m, int64_t n, int32_t d, int32_t src_kind, int32_t src_dtype,
+                           const void *src, const float *A, const float *b,
+                           void *W_hat, int32_t out_dtype, void *stream);
+
+/*
+ * lcvq_workspace_bytes -- device workspace needed by lcvq_linear_fwd
+ * (op = LCVQ_OP_FWD) or lcvq_linear_bwd (op = LCVQ_OP_BWD) for these sizes and
+ * element type.  Returns 0 for invalid arguments.  The workspace holds
+ * transient, library-private data (transformed activations, codes in the
+ * matrix-core operand layout, per-token sums); its contents are undefined
+ * between calls.
+ */
+size_t lcvq_workspace_bytes(int32_t op, int64_t N, int64_t m, int64_t n, int32_t d, int32_t dtype);
+
+/*
+ * lcvq_linear_fwd -- Y = X W_hat^T for one LC-VQ weight matrix, computed as in
+ * def. forward_x (Sec. 3.2): X' = X blockdiag(A) and s = X b~ once per call,
+ * then Y = X' codes^T + s 1^T with the codes fed to the matrix cores exactly.
+ *   N, m, n   tokens, out-features, in-features; d in {4, 8}; n % d == 0
+ *   dtype     element type of Z, X and Y (LCVQ_F32 or LCVQ_BF16)
+ *   Z         m x n latent proxy weights
+ *   A, b      map (d x d, row-major, A[j*d + k]) and offset (d), fp32
+ *   X         N x n activations;  Y  N x m output (written)
+ *   packed_codes_out  NULL, or m*n/4 bytes that receive the codes of this call
+ *             in the lcvq_pack2bit layout
+ *   workspace device buffer of at least lcvq_workspace_bytes(LCVQ_OP_FWD, ...)
+ * bf16 additionally requires m % 8 == 0 and n % 8 == 0.
+ */
+lcvq_status_t lcvq_linear_fwd(int64_t N, int64_t m, int64_t n, int32_t d, int32_t dtype,
+                              const void *Z, const float *A, const float *b,
+                              const void *X, void *Y, uint8_t *packed_codes_out,
+                              void *workspace, size_t workspace_bytes, void *stream);
+
+/*
+ * lcvq_linear_bwd -- straight-through backward of lcvq_linear_fwd (Sec. 3.3):
+ *   dX = dY W_hat                                   (N x n, written, type dtype)
+ *   dW = dY^T X  (never stored)
+ *   dZ[r, g*d + k] = mask[r, g*d + k] * sum_j dW[r, g*d + j] A[j, k]
+ *   dA[j, k] = sum_{r,g} dW[r, g*d + j] code[r, g*d + k]
+ *   db[j]    = sum_{r,g} dW[r, g*d + j]
+ *   mask_mode  lcvq_mask_t
+ *   accumulate 0: dZ, dA, db are overwritten; 1: results are added to them
+ *              (gradient accumulation).  dX is always overwritten.
+ *   dX, dZ, dA, db  each may be NULL to skip it (dA and db are produced
+ *              together: both NULL or both non-NULL)
+ *   dz_dtype   element type of dZ: LCVQ_F32, or LCVQ_BF16 when dtype is bf16
+ * dA/db are summed with floating-point atomics, so their last bits may vary
+ * from run to run.
+ */
+lcvq_status_t lcvq_linear_bwd(int64_t N, int64_t m, int64_t n, int32_t d, int32_t dtype,
+                              const void *Z, const float *A, const float *b,
+                              const void *X, const void *dY, int32_t mask_mode, int32_t accumulate,
+                              void *dX, void *dZ, int32_t dz_dtype, float *dA, float *db,
+                              void *workspace, size_t workspace_bytes, void *stream);
+
+/* Static description of a status code. */
+const char *lcvq_status_string(lcvq_status_t status);
+
+/* Detail message of the calling thread's most recent non-OK status ("" if none). */
+const char *lcvq_last_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* LCVQ_H */

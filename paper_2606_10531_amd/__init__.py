@@ -1,0 +1,136 @@
+"""LC-VQ linear layer (LC-QAT, arXiv 2606.10531) on MI355X (gfx950).
+
+Thin torch binding of liblcvq.so: every function checks devices, dtypes and
+contiguity, allocates outputs and workspace with torch, and passes raw device
+pointers plus the current HIP stream to the C ABI.  All arithmetic runs in the
+library's HIP kernels; there is no CPU or PyTorch fallback.
+"""
+from __future__ import annotations
+
+import ctypes
+
+import torch
+
+from . import _lib
+from ._lib import (BF16, F32, MASK_LATENT, MASK_ROUNDED, OP_BWD, OP_FWD,  # noqa: F401
+                   SRC_CODES_U8, SRC_LATENT, SRC_PACKED2, LcvqError)
+
+__all__ = ["linear_fwd", "linear_bwd", "pack2bit", "dequant", "workspace_bytes", "LcvqError",
+           "MASK_ROUNDED", "MASK_LATENT", "SRC_LATENT", "SRC_CODES_U8", "SRC_PACKED2"]
+
+_DT = {torch.float32: F32, torch.bfloat16: BF16}
+
+
+def _dtype_code(t: torch.Tensor) -> int:
+    if t.dtype not in _DT:
+        raise TypeError(f"unsupported dtype {t.dtype} (float32 or bfloat16)")
+    return _DT[t.dtype]
+
+
+def _dev(t: torch.Tensor, name: str) -> int:
+    if not isinstance(t, torch.Tensor):
+        raise TypeError(f"{name} must be a tensor")
+    if t.device.type != "cuda":
+        raise ValueError(f"{name} must be on the GPU (got {t.device})")
+    if not t.is_contiguous():
+        raise ValueError(f"{name} must be contiguous")
+    return t.data_ptr()
+
+
+def _opt(t, name):
+    return None if t is None else _dev(t, name)
+
+
+def _stream(device) -> ctypes.c_void_p:
+    return ctypes.c_void_p(torch.cuda.current_stream(device).cuda_stream)
+
+
+def workspace_bytes(op: int, N: int, m: int, n: int, d: int, dtype: torch.dtype) -> int:
+    return int(_lib.load().lcvq_workspace_bytes(op, N, m, n, d, _DT[dtype]))
+
+
+def _workspace(op, N, m, n, d, dtype, device, workspace):
+    need = workspace_bytes(op, N, m, n, d, dtype)
+    if workspace is None:
+        workspace = torch.empty(max(need, 256), dtype=torch.uint8, device=device)
+    elif workspace.numel() * workspace.element_size() < need:
+        raise ValueError(f"workspace has {workspace.numel() * workspace.element_size()} bytes, need {need}")
+    return workspace
+
+
+def pack2bit(src: torch.Tensor, out: torch.Tensor | None = None) -> torch.Tensor:
+    """Packed 2-bit codes (m x n/4 uint8) of a latent tensor (fp32/bf16) or of uint8 codes."""
+    m, n = src.shape
+    if src.dtype == torch.uint8:
+        kind, sdt = SRC_CODES_U8, F32
+    else:
+        kind, sdt = SRC_LATENT, _dtype_code(src)
+    if out is None:
+        out = torch.empty((m, n // 4), dtype=torch.uint8, device=src.device)
+    _lib.check(_lib.load().lcvq_pack2bit(_dev(src, "src"), kind, sdt, m, n, _dev(out, "out"),
+                                         _stream(src.device)), "lcvq_pack2bit")
+    return out
+
+
+def dequant(src: torch.Tensor, A: torch.Tensor, b: torch.Tensor, d: int, n: int | None = None,
+            src_kind: int | None = None, out_dtype: torch.dtype = torch.bfloat16,
+            out: torch.Tensor | None = None) -> torch.Tensor:
+    """Dense W_hat (m x n) from latents, uint8 codes or packed 2-bit codes (pass n for packed)."""
+    if src_kind is None:
+        src_kind = SRC_CODES_U8 if src.dtype == torch.uint8 else SRC_LATENT
+    m = src.shape[0]
+    if n is None:
+        n = src.shape[1] * (4 if src_kind == SRC_PACKED2 else 1)
+    sdt = _dtype_code(src) if src_kind == SRC_LATENT else F32
+    if out is None:
+        out = torch.empty((m, n), dtype=out_dtype, device=src.device)
+    _lib.check(_lib.load().lcvq_dequant(m, n, d, src_kind, sdt, _dev(src, "src"), _dev(A, "A"), _dev(b, "b"),
+                                        _dev(out, "out"), _DT[out.dtype], _stream(src.device)), "lcvq_dequant")
+    return out
+
+
+def linear_fwd(Z: torch.Tensor, A: torch.Tensor, b: torch.Tensor, X: torch.Tensor, d: int,
+               packed_out: torch.Tensor | None = None, workspace: torch.Tensor | None = None,
+               out: torch.Tensor | None = None) -> torch.Tensor:
+    """Y = X W_hat^T (N x m) for latents Z (m x n), map A (d x d fp32), offset b (d fp32)."""
+    m, n = Z.shape
+    N = X.shape[0]
+    dt = _dtype_code(X)
+    if Z.dtype != X.dtype:
+        raise TypeError("Z and X must share a dtype")
+    if out is None:
+        out = torch.empty((N, m), dtype=X.dtype, device=X.device)
+    ws = _workspace(OP_FWD, N, m, n, d, X.dtype, X.device, workspace)
+    _lib.check(_lib.load().lcvq_linear_fwd(N, m, n, d, dt, _dev(Z, "Z"), _dev(A, "A"), _dev(b, "b"), _dev(X, "X"),
+                                           _dev(out, "Y"), _opt(packed_out, "packed_out"), _dev(ws, "workspace"),
+                                           ws.numel(), _stream(X.device)), "lcvq_linear_fwd")
+    return out
+
+
+def linear_bwd(Z: torch.Tensor, A: torch.Tensor, b: torch.Tensor, X: torch.Tensor, dY: torch.Tensor, d: int,
+               mask_mode: int = MASK_ROUNDED, accumulate: bool = False, need_dX: bool = True,
+               need_dZ: bool = True, need_map: bool = True, dz_dtype: torch.dtype | None = None,
+               dX: torch.Tensor | None = None, dZ: torch.Tensor | None = None, dA: torch.Tensor | None = None,
+               db: torch.Tensor | None = None, workspace: torch.Tensor | None = None):
+    """Straight-through backward: returns (dX, dZ, dA, db); skipped outputs are None."""
+    m, n = Z.shape
+    N = X.shape[0]
+    dt = _dtype_code(X)
+    dev = X.device
+    if dz_dtype is None:
+        dz_dtype = dZ.dtype if dZ is not None else Z.dtype
+    if need_dX and dX is None:
+        dX = torch.empty((N, n), dtype=X.dtype, device=dev)
+    if need_dZ and dZ is None:
+        dZ = (torch.zeros if accumulate else torch.empty)((m, n), dtype=dz_dtype, device=dev)
+    if need_map and dA is None:
+        dA = torch.zeros((d, d), dtype=torch.float32, device=dev)
+        db = torch.zeros((d,), dtype=torch.float32, device=dev)
+    ws = _workspace(OP_BWD, N, m, n, d, X.dtype, dev, workspace)
+    _lib.check(_lib.load().lcvq_linear_bwd(
+        N, m, n, d, dt, _dev(Z, "Z"), _dev(A, "A"), _dev(b, "b"), _dev(X, "X"), _dev(dY, "dY"), mask_mode,
+        1 if accumulate else 0, _opt(dX if need_dX else None, "dX"), _opt(dZ if need_dZ else None, "dZ"),
+        _DT[dz_dtype], _opt(dA if need_map else None, "dA"), _opt(db if need_map else None, "db"),
+        _dev(ws, "workspace"), ws.numel(), _stream(dev)), "lcvq_linear_bwd")
+    return (dX if need_dX else None, dZ if need_dZ else None, dA if need_map else None,
+            db if need_map else None)

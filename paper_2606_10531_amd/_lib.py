@@ -1,0 +1,73 @@
+"""ctypes declarations of liblcvq.so (the C ABI in include/lcvq.h)."""
+from __future__ import annotations
+
+import ctypes
+import os
+
+LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "liblcvq.so")
+
+# lcvq_status_t
+OK, EINVAL, EUNSUPPORTED, EALIGN, EWORKSPACE, EHIP = range(6)
+# lcvq_dtype_t
+F32, BF16 = 0, 1
+# lcvq_src_t
+SRC_LATENT, SRC_CODES_U8, SRC_PACKED2 = 0, 1, 2
+# lcvq_mask_t
+MASK_ROUNDED, MASK_LATENT = 0, 1
+# lcvq_op_t
+OP_FWD, OP_BWD = 0, 1
+
+_P = ctypes.c_void_p
+_I64 = ctypes.c_int64
+_I32 = ctypes.c_int32
+_SZ = ctypes.c_size_t
+
+SIGNATURES = {
+    "lcvq_pack2bit": (_I32, [_P, _I32, _I32, _I64, _I64, _P, _P]),
+    "lcvq_dequant": (_I32, [_I64, _I64, _I32, _I32, _I32, _P, _P, _P, _P, _I32, _P]),
+    "lcvq_workspace_bytes": (_SZ, [_I32, _I64, _I64, _I64, _I32, _I32]),
+    "lcvq_linear_fwd": (_I32, [_I64, _I64, _I64, _I32, _I32, _P, _P, _P, _P, _P, _P, _P, _SZ, _P]),
+    "lcvq_linear_bwd": (_I32, [_I64, _I64, _I64, _I32, _I32, _P, _P, _P, _P, _P, _I32, _I32,
+                               _P, _P, _I32, _P, _P, _P, _SZ, _P]),
+    "lcvq_status_string": (ctypes.c_char_p, [_I32]),
+    "lcvq_last_error": (ctypes.c_char_p, []),
+}
+
+_lib = None
+
+
+class LcvqError(RuntimeError):
+    """A non-OK status returned by liblcvq."""
+
+    def __init__(self, status: int, func: str, detail: str):
+        self.status = status
+        super().__init__(f"{func}: {status_string(status)} ({detail})")
+
+
+def load() -> ctypes.CDLL:
+    """The loaded library; raises if it has not been built."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise RuntimeError(f"{LIB_PATH} is missing: build it with paper_2606_10531_amd.build.build() "
+                               "(the LC-VQ layer has no non-HIP fallback)")
+        lib = ctypes.CDLL(LIB_PATH)
+        for name, (res, args) in SIGNATURES.items():
+            fn = getattr(lib, name)
+            fn.restype = res
+            fn.argtypes = args
+        _lib = lib
+    return _lib
+
+
+def status_string(status: int) -> str:
+    return load().lcvq_status_string(status).decode()
+
+
+def last_error() -> str:
+    return load().lcvq_last_error().decode()
+
+
+def check(status: int, func: str) -> None:
+    if status != OK:
+        raise LcvqError(status, func, last_error())

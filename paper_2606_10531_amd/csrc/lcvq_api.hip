@@ -1,0 +1,297 @@
+// C ABI of the LC-VQ linear layer: argument validation, workspace layout and
+// the launch sequence of each call.  Every check runs on the host before the
+// first launch, so a rejected call enqueues nothing.
+#include <stdarg.h>
+#include <stdio.h>
+
+#include "../../include/lcvq.h"
+#include "lcvq_prep.hpp"
+
+namespace {
+
+thread_local char g_err[512];
+
+lcvq_status_t fail(lcvq_status_t s, const char *fmt, ...) {
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(g_err, sizeof(g_err), fmt, ap);
+  va_end(ap);
+  return s;
+}
+lcvq_status_t ok() {
+  g_err[0] = 0;
+  return LCVQ_OK;
+}
+lcvq_status_t hip_fail(hipError_t e, const char *what) {
+  return fail(LCVQ_EHIP, "%s: %s", what, hipGetErrorString(e));
+}
+
+bool aligned16(const void *p) { return ((uintptr_t)p & 15u) == 0; }
+size_t up256(size_t x) { return (x + 255) & ~(size_t)255; }
+
+// Largest row length of an operand streamed through the 256-row tiles with
+// 32-bit buffer offsets (256 rows * ld * 4 bytes must stay below 2^31).
+constexpr int64_t kMaxLd = (int64_t)1 << 21;
+
+struct FwdLayout {
+  size_t xp, s, frag, total;
+  int64_t Np, ldp;
+};
+struct BwdLayout {
+  size_t rs, frag, total;
+  int64_t Np;
+};
+
+FwdLayout fwd_layout(int64_t N, int64_t m, int64_t n, bool bf16) {
+  FwdLayout L{};
+  if (bf16) {
+    L.Np = lcvq::round_up(N, 256);
+    L.ldp = lcvq::round_up(n, 64);
+    const size_t xp = (size_t)L.Np * L.ldp * 2, s = (size_t)L.Np * 4;
+    const size_t frag = (size_t)(lcvq::round_up(m, 256) / 32) * (L.ldp / 64) * 1024;
+    L.xp = 0;
+    L.s = up256(xp);
+    L.frag = L.s + up256(s);
+    L.total = L.frag + up256(frag);
+  } else {
+    L.Np = N;
+    L.ldp = n;
+    L.xp = 0;
+    L.s = up256((size_t)N * n * 4);
+    L.frag = L.s + up256((size_t)N * 4);
+    L.total = L.frag;
+  }
+  return L;
+}
+
+BwdLayout bwd_layout(int64_t N, int64_t m, int64_t n, bool bf16) {
+  BwdLayout L{};
+  L.Np = N;
+  L.rs = 0;
+  const size_t rs = up256((size_t)N * 4);
+  if (bf16) {
+    const size_t frag = (size_t)(lcvq::round_up(n, 256) / 32) * (lcvq::round_up(m, 64) / 64) * 1024;
+    L.frag = rs;
+    L.total = rs + up256(frag);
+  } else {
+    L.frag = rs;
+    L.total = rs;
+  }
+  return L;
+}
+
+// Zero-fill without hipMemsetAsync (safe to capture in a graph).
+__global__ void k_fill_zero(uint32_t *p, int64_t words) {
+  for (int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x; i < words; i += (int64_t)gridDim.x * 256) p[i] = 0u;
+}
+hipError_t fill_zero(void *p, size_t bytes, hipStream_t st) {
+  if (p == nullptr || bytes == 0) return hipSuccess;
+  const int64_t words = (int64_t)(bytes / 4);
+  int64_t g = (words + 255) / 256;
+  if (g > 65536) g = 65536;
+  if (g < 1) g = 1;
+  k_fill_zero<<<(unsigned)g, 256, 0, st>>>((uint32_t *)p, words);
+  return hipGetLastError();
+}
+
+lcvq_status_t check_common(int64_t N, int64_t m, int64_t n, int32_t d, int32_t dtype) {
+  if (N < 0 || m < 0 || n < 0) return fail(LCVQ_EINVAL, "negative size (N=%lld m=%lld n=%lld)", (long long)N, (long long)m, (long long)n);
+  if (d != 4 && d != 8) return fail(LCVQ_EUNSUPPORTED, "group size d=%d (supported: 4, 8)", d);
+  if (n % d != 0) return fail(LCVQ_EINVAL, "n=%lld is not a multiple of d=%d", (long long)n, d);
+  if (dtype != LCVQ_F32 && dtype != LCVQ_BF16) return fail(LCVQ_EINVAL, "dtype=%d", dtype);
+  if (dtype == LCVQ_BF16) {
+    if (m % 8 != 0 || n % 8 != 0)
+      return fail(LCVQ_EUNSUPPORTED, "bf16 path needs m and n multiples of 8 (m=%lld n=%lld)", (long long)m, (long long)n);
+    if (m >= kMaxLd || n >= kMaxLd) return fail(LCVQ_EUNSUPPORTED, "m or n above %lld", (long long)kMaxLd);
+  }
+  return LCVQ_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+const char *lcvq_status_string(lcvq_status_t s) {
+  switch (s) {
+    case LCVQ_OK: return "ok";
+    case LCVQ_EINVAL: return "invalid argument";
+    case LCVQ_EUNSUPPORTED: return "unsupported configuration";
+    case LCVQ_EALIGN: return "pointer not 16-byte aligned";
+    case LCVQ_EWORKSPACE: return "workspace too small";
+    case LCVQ_EHIP: return "HIP runtime error";
+  }
+  return "unknown status";
+}
+
+const char *lcvq_last_error(void) { return g_err; }
+
+size_t lcvq_workspace_bytes(int32_t op, int64_t N, int64_t m, int64_t n, int32_t d, int32_t dtype) {
+  if (N < 0 || m < 0 || n < 0 || (d != 4 && d != 8) || (dtype != LCVQ_F32 && dtype != LCVQ_BF16)) return 0;
+  const bool bf16 = dtype == LCVQ_BF16;
+  if (op == LCVQ_OP_FWD) return fwd_layout(N, m, n, bf16).total;
+  if (op == LCVQ_OP_BWD) return bwd_layout(N, m, n, bf16).total;
+  return 0;
+}
+
+lcvq_status_t lcvq_pack2bit(const void *src, int32_t src_kind, int32_t src_dtype, int64_t m, int64_t n,
+                            uint8_t *packed, void *stream) {
+  if (m < 0 || n < 0) return fail(LCVQ_EINVAL, "negative size");
+  if (n % 4 != 0) return fail(LCVQ_EINVAL, "n=%lld is not a multiple of 4", (long long)n);
+  if (src_kind != LCVQ_SRC_LATENT && src_kind != LCVQ_SRC_CODES_U8)
+    return fail(LCVQ_EINVAL, "src_kind=%d (pack takes LATENT or CODES_U8)", src_kind);
+  if (src_kind == LCVQ_SRC_LATENT && src_dtype != LCVQ_F32 && src_dtype != LCVQ_BF16)
+    return fail(LCVQ_EINVAL, "src_dtype=%d", src_dtype);
+  if (m == 0 || n == 0) return ok();
+  if (src == nullptr || packed == nullptr) return fail(LCVQ_EINVAL, "null pointer");
+  if (!aligned16(src) || !aligned16(packed)) return fail(LCVQ_EALIGN, "src/packed must be 16-byte aligned");
+  hipError_t e = lcvq::launch_pack2bit(src, src_kind, src_dtype == LCVQ_BF16, m, n, packed, (hipStream_t)stream);
+  return e == hipSuccess ? ok() : hip_fail(e, "pack2bit launch");
+}
+
+lcvq_status_t lcvq_dequant(int64_t m, int64_t n, int32_t d, int32_t src_kind, int32_t src_dtype,
+                           const void *src, const float *A, const float *b, void *W_hat, int32_t out_dtype,
+                           void *stream) {
+  if (m < 0 || n < 0) return fail(LCVQ_EINVAL, "negative size");
+  if (d != 4 && d != 8) return fail(LCVQ_EUNSUPPORTED, "group size d=%d (supported: 4, 8)", d);
+  if (n % d != 0) return fail(LCVQ_EINVAL, "n=%lld is not a multiple of d=%d", (long long)n, d);
+  if (src_kind < LCVQ_SRC_LATENT || src_kind > LCVQ_SRC_PACKED2) return fail(LCVQ_EINVAL, "src_kind=%d", src_kind);
+  if (src_kind == LCVQ_SRC_LATENT && src_dtype != LCVQ_F32 && src_dtype != LCVQ_BF16)
+    return fail(LCVQ_EINVAL, "src_dtype=%d", src_dtype);
+  if (out_dtype != LCVQ_F32 && out_dtype != LCVQ_BF16) return fail(LCVQ_EINVAL, "out_dtype=%d", out_dtype);
+  if (m == 0 || n == 0) return ok();
+  if (src == nullptr || A == nullptr || b == nullptr || W_hat == nullptr) return fail(LCVQ_EINVAL, "null pointer");
+  if (!aligned16(src) || !aligned16(W_hat)) return fail(LCVQ_EALIGN, "src/W_hat must be 16-byte aligned");
+  hipError_t e = lcvq::launch_dequant(src, src_kind, src_dtype == LCVQ_BF16, m, n, d, A, b, W_hat,
+                                      out_dtype == LCVQ_BF16, (hipStream_t)stream);
+  return e == hipSuccess ? ok() : hip_fail(e, "dequant launch");
+}
+
+lcvq_status_t lcvq_linear_fwd(int64_t N, int64_t m, int64_t n, int32_t d, int32_t dtype, const void *Z,
+                              const float *A, const float *b, const void *X, void *Y, uint8_t *packed_codes_out,
+                              void *workspace, size_t workspace_bytes, void *stream) {
+  lcvq_status_t s = check_common(N, m, n, d, dtype);
+  if (s != LCVQ_OK) return s;
+  const bool bf16 = dtype == LCVQ_BF16;
+  const size_t es = bf16 ? 2 : 4;
+  hipStream_t st = (hipStream_t)stream;
+  if (N == 0 || m == 0 || n == 0) {
+    // Y = X W_hat^T is an N x m matrix of zeros when n == 0; codes exist only if m*n > 0.
+    if (N > 0 && m > 0) {
+      if (Y == nullptr) return fail(LCVQ_EINVAL, "null Y");
+      if (!aligned16(Y)) return fail(LCVQ_EALIGN, "Y must be 16-byte aligned");
+      hipError_t e = fill_zero(Y, (size_t)N * m * es, st);
+      if (e != hipSuccess) return hip_fail(e, "zero fill");
+    }
+    if (m > 0 && n > 0 && packed_codes_out != nullptr) return lcvq_pack2bit(Z, LCVQ_SRC_LATENT, dtype, m, n, packed_codes_out, stream);
+    return ok();
+  }
+  if (Z == nullptr || A == nullptr || b == nullptr || X == nullptr || Y == nullptr)
+    return fail(LCVQ_EINVAL, "null required pointer (Z, A, b, X, Y)");
+  if (!aligned16(Z) || !aligned16(X) || !aligned16(Y) || (packed_codes_out && !aligned16(packed_codes_out)) ||
+      !aligned16(workspace))
+    return fail(LCVQ_EALIGN, "Z, X, Y, packed_codes_out and workspace must be 16-byte aligned");
+  const FwdLayout L = fwd_layout(N, m, n, bf16);
+  if (workspace == nullptr || workspace_bytes < L.total)
+    return fail(LCVQ_EWORKSPACE, "workspace %zu bytes, need %zu", workspace_bytes, L.total);
+  char *ws = (char *)workspace;
+  float *svec = (float *)(ws + L.s);
+  hipError_t e;
+  if (bf16) {
+    uint32_t *frag = (uint32_t *)(ws + L.frag);
+    e = lcvq::launch_quant_frag(Z, true, m, n, false, frag, packed_codes_out, st);
+    if (e != hipSuccess) return hip_fail(e, "quantise launch");
+    e = lcvq::launch_act_transform(X, true, N, L.Np, n, d, A, b, ws + L.xp, L.ldp, svec, st);
+    if (e != hipSuccess) return hip_fail(e, "activation transform launch");
+    e = lcvq::launch_fwd_bf16(frag, (const uint16_t *)(ws + L.xp), L.ldp, svec, (uint16_t *)Y, N, m, n, st);
+    if (e != hipSuccess) return hip_fail(e, "forward product launch");
+  } else {
+    e = lcvq::launch_act_transform(X, false, N, N, n, d, A, b, ws + L.xp, n, svec, st);
+    if (e != hipSuccess) return hip_fail(e, "activation transform launch");
+    e = lcvq::launch_fwd_f32((const float *)Z, (const float *)(ws + L.xp), svec, (float *)Y, N, m, n, st);
+    if (e != hipSuccess) return hip_fail(e, "forward product launch");
+    if (packed_codes_out != nullptr) {
+      e = lcvq::launch_pack2bit(Z, LCVQ_SRC_LATENT, false, m, n, packed_codes_out, st);
+      if (e != hipSuccess) return hip_fail(e, "pack launch");
+    }
+  }
+  return ok();
+}
+
+lcvq_status_t lcvq_linear_bwd(int64_t N, int64_t m, int64_t n, int32_t d, int32_t dtype, const void *Z,
+                              const float *A, const float *b, const void *X, const void *dY, int32_t mask_mode,
+                              int32_t accumulate, void *dX, void *dZ, int32_t dz_dtype, float *dA, float *db,
+                              void *workspace, size_t workspace_bytes, void *stream) {
+  lcvq_status_t s = check_common(N, m, n, d, dtype);
+  if (s != LCVQ_OK) return s;
+  if (mask_mode != LCVQ_MASK_ROUNDED && mask_mode != LCVQ_MASK_LATENT) return fail(LCVQ_EINVAL, "mask_mode=%d", mask_mode);
+  if (accumulate != 0 && accumulate != 1) return fail(LCVQ_EINVAL, "accumulate=%d", accumulate);
+  if ((dA == nullptr) != (db == nullptr)) return fail(LCVQ_EINVAL, "dA and db must both be given or both be NULL");
+  const bool bf16 = dtype == LCVQ_BF16;
+  if (dz_dtype != LCVQ_F32 && !(dz_dtype == LCVQ_BF16 && bf16))
+    return fail(LCVQ_EINVAL, "dz_dtype=%d with dtype=%d", dz_dtype, dtype);
+  const size_t es = bf16 ? 2 : 4, dzs = dz_dtype == LCVQ_BF16 ? 2 : 4;
+  hipStream_t st = (hipStream_t)stream;
+  hipError_t e;
+  if (N == 0 || m == 0 || n == 0) {
+    // Every product has an empty sum: dX = 0, dZ = 0, dA = db = 0 (or left as they are when accumulating).
+    if (dX != nullptr && N > 0 && n > 0) {
+      if (!aligned16(dX)) return fail(LCVQ_EALIGN, "dX must be 16-byte aligned");
+      if ((e = fill_zero(dX, (size_t)N * n * es, st)) != hipSuccess) return hip_fail(e, "zero fill");
+    }
+    if (!accumulate) {
+      if (dZ != nullptr && m > 0 && n > 0) {
+        if (!aligned16(dZ)) return fail(LCVQ_EALIGN, "dZ must be 16-byte aligned");
+        if ((e = fill_zero(dZ, (size_t)m * n * dzs, st)) != hipSuccess) return hip_fail(e, "zero fill");
+      }
+      if (dA != nullptr) {
+        if ((e = fill_zero(dA, (size_t)d * d * 4, st)) != hipSuccess) return hip_fail(e, "zero fill");
+        if ((e = fill_zero(db, (size_t)d * 4, st)) != hipSuccess) return hip_fail(e, "zero fill");
+      }
+    }
+    return ok();
+  }
+  if (Z == nullptr || A == nullptr || b == nullptr || X == nullptr || dY == nullptr)
+    return fail(LCVQ_EINVAL, "null required pointer (Z, A, b, X, dY)");
+  if (!aligned16(Z) || !aligned16(X) || !aligned16(dY) || (dX && !aligned16(dX)) || (dZ && !aligned16(dZ)) ||
+      !aligned16(workspace))
+    return fail(LCVQ_EALIGN, "Z, X, dY, dX, dZ and workspace must be 16-byte aligned");
+  const BwdLayout L = bwd_layout(N, m, n, bf16);
+  if (workspace == nullptr || workspace_bytes < L.total)
+    return fail(LCVQ_EWORKSPACE, "workspace %zu bytes, need %zu", workspace_bytes, L.total);
+  char *ws = (char *)workspace;
+  float *rs = (float *)(ws + L.rs);
+  const bool want_map = dA != nullptr;
+  float *zA = (want_map && !accumulate) ? dA : nullptr;
+  float *zb = (want_map && !accumulate) ? db : nullptr;
+
+  if (dX != nullptr) {
+    e = lcvq::launch_rowsum(dY, bf16, N, N, m, rs, zA, zb, d, st);
+    if (e != hipSuccess) return hip_fail(e, "row-sum launch");
+    zA = zb = nullptr;  // cleared by the row-sum launch
+    if (bf16) {
+      uint32_t *frag = (uint32_t *)(ws + L.frag);
+      e = lcvq::launch_quant_frag(Z, true, m, n, true, frag, nullptr, st);
+      if (e != hipSuccess) return hip_fail(e, "quantise launch");
+      e = lcvq::launch_dx_bf16(frag, (const uint16_t *)dY, rs, A, b, d, (uint16_t *)dX, N, m, n, st);
+    } else {
+      e = lcvq::launch_dx_f32((const float *)Z, (const float *)dY, rs, A, b, d, (float *)dX, N, m, n, st);
+    }
+    if (e != hipSuccess) return hip_fail(e, "input-gradient launch");
+  }
+  if (zA != nullptr) {
+    if ((e = fill_zero(zA, (size_t)d * d * 4, st)) != hipSuccess) return hip_fail(e, "zero fill");
+    if ((e = fill_zero(zb, (size_t)d * 4, st)) != hipSuccess) return hip_fail(e, "zero fill");
+  }
+  if (dZ != nullptr || want_map) {
+    if (bf16)
+      e = lcvq::launch_dz_bf16((const uint16_t *)X, (const uint16_t *)dY, (const uint16_t *)Z, A, d, mask_mode,
+                               accumulate, dZ, dz_dtype == LCVQ_BF16, dA, db, N, m, n, st);
+    else
+      e = lcvq::launch_dz_f32((const float *)X, (const float *)dY, (const float *)Z, A, d, mask_mode, accumulate,
+                              (float *)dZ, dA, db, N, m, n, st);
+    if (e != hipSuccess) return hip_fail(e, "weight-gradient launch");
+  }
+  return ok();
+}
+
+}  // extern "C"

@@ -1,0 +1,99 @@
+// Shared device helpers of the LC-VQ kernels (gfx950 / CDNA4).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace lcvq {
+
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+typedef float floatx16 __attribute__((ext_vector_type(16)));
+typedef float floatx4 __attribute__((ext_vector_type(4)));
+typedef short shortx4 __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
+
+typedef __attribute__((address_space(3))) void lds_void;
+
+constexpr int kMaxCode = 3;  // 2^b - 1 with b = 2 bits
+
+// ---- bf16 <-> fp32 -------------------------------------------------------
+
+__device__ __forceinline__ float bf16_lo(uint32_t w) { return __uint_as_float(w << 16); }
+__device__ __forceinline__ float bf16_hi(uint32_t w) { return __uint_as_float(w & 0xffff0000u); }
+__device__ __forceinline__ float bf16_to_f32(uint16_t h) { return __uint_as_float((uint32_t)h << 16); }
+
+// fp32 -> bf16 bits, round to nearest even (NaN kept quiet).
+__device__ __forceinline__ uint32_t f32_to_bf16(float f) {
+  uint32_t u = __float_as_uint(f);
+  if ((u & 0x7fffffffu) > 0x7f800000u) return (u >> 16) | 0x40u;
+  return (u + 0x7fffu + ((u >> 16) & 1u)) >> 16;
+}
+__device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
+  return f32_to_bf16(lo) | (f32_to_bf16(hi) << 16);
+}
+
+// ---- the quantiser of eq. quant_param ------------------------------------
+// code = clip(rint(z), 0, 3); rint is round-half-to-even (v_rndne_f32).
+// fmaxf(NaN, 0) = 0, so a NaN latent gives code 0.
+__device__ __forceinline__ uint32_t quant_code(float z) {
+  float u = __builtin_rintf(z);
+  return (uint32_t)fminf(fmaxf(u, 0.0f), (float)kMaxCode);
+}
+// Straight-through mask: mode 0 "rounded" (0 <= rint(z) <= 3), mode 1 "latent".
+__device__ __forceinline__ bool ste_pass(float z, int mode) {
+  float v = mode == 0 ? __builtin_rintf(z) : z;
+  return v >= 0.0f && v <= (float)kMaxCode;
+}
+
+// ---- codes in the matrix-core operand layout -----------------------------
+// Row permutation of a 32-row MFMA block.  In a 32x32 accumulator, lane L
+// holds rows 8 (i / 4) + 4 (L / 32) + (i % 4), i = 0..15.  Feeding weight-side
+// index perm32(m) into MFMA row m makes register i of lane L hold weight-side
+// index 16 (L / 32) + i, so every group of d = 4 or 8 consecutive columns is
+// lane-local and the lane's 16 results are contiguous in memory.
+__host__ __device__ __forceinline__ int perm32(int m) { return (m & 3) + 4 * (m >> 3) + 16 * ((m >> 2) & 1); }
+
+// A 32 x 64 (M x K) slab of codes occupies 1 KiB: lane L owns 16 bytes holding
+// the codes of weight-side index perm32(L % 32) of the slab and K = 16 kk +
+// 8 (L / 32) + i (dword kk, nibble i at bits 4i..4i+3).  That is exactly the
+// A operand of v_mfma_f32_32x32x16_bf16 for four K-substeps of 16.
+// Slabs are stored M-slab-major: slab (mb, kb) at byte ((mb * KB) + kb) * 1024.
+__device__ __forceinline__ uint32_t frag_dword_index(int mb, int kb, int KB, int lane, int kk) {
+  return ((uint32_t)(mb * KB + kb) * 64u + (uint32_t)lane) * 4u + (uint32_t)kk;
+}
+
+// Eight 4-bit codes (0..3) -> eight exact bf16 values via the fp4 (e2m1)
+// converter: nibble c encodes c / 2 in e2m1 for c <= 3, and the scale 2 makes
+// it exactly c.
+__device__ __forceinline__ bf16x8 nibbles_to_bf16x8(uint32_t w) {
+  bf16x2 p0 = __builtin_amdgcn_cvt_scalef32_pk_bf16_fp4(w, 2.0f, 0);
+  bf16x2 p1 = __builtin_amdgcn_cvt_scalef32_pk_bf16_fp4(w, 2.0f, 1);
+  bf16x2 p2 = __builtin_amdgcn_cvt_scalef32_pk_bf16_fp4(w, 2.0f, 2);
+  bf16x2 p3 = __builtin_amdgcn_cvt_scalef32_pk_bf16_fp4(w, 2.0f, 3);
+  bf16x8 r;
+  r[0] = p0[0]; r[1] = p0[1]; r[2] = p1[0]; r[3] = p1[1];
+  r[4] = p2[0]; r[5] = p2[1]; r[6] = p3[0]; r[7] = p3[1];
+  return r;
+}
+
+// ---- misc ----------------------------------------------------------------
+__host__ __device__ __forceinline__ int64_t round_up(int64_t x, int64_t m) { return (x + m - 1) / m * m; }
+__host__ __device__ __forceinline__ int64_t ceil_div(int64_t x, int64_t m) { return (x + m - 1) / m; }
+
+// ---- buffer resources ----------------------------------------------------
+// Raw buffer over [base, base + bytes) (bytes clamped below 2^31).  Loads at an
+// offset >= bytes return zero, which zero-pads tiles at ragged edges; lanes
+// with nothing to load use kOffNone.
+constexpr uint32_t kOffNone = 0x80000000u;
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const void *base, int64_t bytes) {
+  int64_t b = bytes < 0 ? 0 : (bytes > 0x7fffffffLL ? 0x7fffffffLL : bytes);
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void *>(base), (short)0, (int)b, 0x00020000);
+}
+// 16 bytes per lane from the buffer straight into LDS at lds_base + 16 * lane.
+__device__ __forceinline__ void buffer_to_lds16(__amdgpu_buffer_rsrc_t r, lds_void *lds_base, uint32_t off) {
+  __builtin_amdgcn_raw_ptr_buffer_load_lds(r, lds_base, 16, (int)off, 0, 0, 0);
+}
+
+}  // namespace lcvq

@@ -1,0 +1,391 @@
+// Streaming (HBM-bound) kernels of the LC-VQ layer:
+//   * quantise latents into the matrix-core operand layout (+ 2-bit packing)
+//   * the activation transform X' = X blockdiag(A), s = X b~   (def. forward_x)
+//   * per-token sums of dY
+//   * stand-alone 2-bit packing and dense decode
+#include "lcvq_prep.hpp"
+
+namespace lcvq {
+
+// ---- element loads ---------------------------------------------------------
+
+__device__ __forceinline__ void load8(const uint16_t *p, float v[8]) {
+  u32x4 w = *reinterpret_cast<const u32x4 *>(p);
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    v[2 * i] = bf16_lo(w[i]);
+    v[2 * i + 1] = bf16_hi(w[i]);
+  }
+}
+__device__ __forceinline__ void load8(const float *p, float v[8]) {
+  floatx4 a = *reinterpret_cast<const floatx4 *>(p);
+  floatx4 b = *reinterpret_cast<const floatx4 *>(p + 4);
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    v[i] = a[i];
+    v[4 + i] = b[i];
+  }
+}
+__device__ __forceinline__ void load4(const uint16_t *p, float v[4]) {
+  u32x2 w = *reinterpret_cast<const u32x2 *>(p);
+  v[0] = bf16_lo(w[0]); v[1] = bf16_hi(w[0]); v[2] = bf16_lo(w[1]); v[3] = bf16_hi(w[1]);
+}
+__device__ __forceinline__ void load4(const float *p, float v[4]) {
+  floatx4 a = *reinterpret_cast<const floatx4 *>(p);
+  v[0] = a[0]; v[1] = a[1]; v[2] = a[2]; v[3] = a[3];
+}
+template <int D, typename T>
+__device__ __forceinline__ void loadD(const T *p, float v[D]) {
+  if constexpr (D == 8) load8(p, v); else load4(p, v);
+}
+
+__device__ __forceinline__ void store4(uint16_t *p, const float v[4]) {
+  u32x2 w;
+  w[0] = pack_bf16x2(v[0], v[1]);
+  w[1] = pack_bf16x2(v[2], v[3]);
+  *reinterpret_cast<u32x2 *>(p) = w;
+}
+__device__ __forceinline__ void store4(float *p, const float v[4]) {
+  floatx4 a = {v[0], v[1], v[2], v[3]};
+  *reinterpret_cast<floatx4 *>(p) = a;
+}
+template <int D, typename T>
+__device__ __forceinline__ void storeD(T *p, const float v[D]) {
+  store4(p, v);
+  if constexpr (D == 8) store4(p + 4, v + 4);
+}
+
+__device__ __forceinline__ float block_sum256(float v, float *red /* >= 4 floats of LDS */) {
+#pragma unroll
+  for (int o = 32; o >= 1; o >>= 1) v += __shfl_xor(v, o, 64);
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  if (lane == 0) red[wave] = v;
+  __syncthreads();
+  float t = red[0] + red[1] + red[2] + red[3];
+  __syncthreads();
+  return t;
+}
+
+// ---- quantise into the operand layout --------------------------------------
+// One block per 64 x 64 tile of Z (rows r, columns c).  kTrans = false: the
+// operand's M axis is r and its K axis c (forward product); kTrans = true: M is
+// c and K is r (input-gradient product).  Tiles beyond Z hold code 0.
+template <typename ZT, bool kTrans>
+__global__ __launch_bounds__(256) void k_quant_frag(const ZT *__restrict__ Z, int64_t m, int64_t n,
+                                                     uint32_t *__restrict__ frag, int KB,
+                                                     uint8_t *__restrict__ packed) {
+  __shared__ uint8_t codes[64][64 + 4];
+  const int tid = threadIdx.x;
+  const int64_t r0 = (int64_t)blockIdx.y * 64, c0 = (int64_t)blockIdx.x * 64;
+#pragma unroll
+  for (int i = 0; i < 2; ++i) {
+    const int id = tid + 256 * i, rr = id >> 3, cc = (id & 7) * 8;
+    const int64_t r = r0 + rr, c = c0 + cc;
+    float v[8];
+    if (r < m && c < n) {
+      load8(Z + r * n + c, v);
+    } else {
+#pragma unroll
+      for (int j = 0; j < 8; ++j) v[j] = 0.0f;
+    }
+#pragma unroll
+    for (int j = 0; j < 8; ++j) codes[rr][cc + j] = (uint8_t)quant_code(v[j]);
+  }
+  __syncthreads();
+#pragma unroll
+  for (int i = 0; i < 2; ++i) {
+    const int id = tid + 256 * i, slab = id >> 8, lane = (id >> 2) & 63, kk = id & 3;
+    const int mloc = slab * 32 + perm32(lane & 31), kloc = 16 * kk + 8 * (lane >> 5);
+    uint32_t w = 0;
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
+      const uint32_t c = kTrans ? codes[kloc + j][mloc] : codes[mloc][kloc + j];
+      w |= c << (4 * j);
+    }
+    const int mb = (kTrans ? (int)blockIdx.x : (int)blockIdx.y) * 2 + slab;
+    const int kb = kTrans ? (int)blockIdx.y : (int)blockIdx.x;
+    frag[frag_dword_index(mb, kb, KB, lane, kk)] = w;
+  }
+  if (!kTrans && packed != nullptr) {
+    // 2-bit packing of the same tile: thread -> (row, 16 codes), stored as two
+    // 16-bit words (n % 8 == 0 keeps them aligned).
+    const int rr = tid >> 2, w = tid & 3;
+    const int64_t r = r0 + rr;
+    if (r < m) {
+#pragma unroll
+      for (int h = 0; h < 2; ++h) {
+        const int64_t c = c0 + 16 * w + 8 * h;
+        if (c < n) {
+          uint32_t bits = 0;
+#pragma unroll
+          for (int j = 0; j < 8; ++j) bits |= (uint32_t)codes[rr][16 * w + 8 * h + j] << (2 * j);
+          *reinterpret_cast<uint16_t *>(packed + r * (n / 4) + c / 4) = (uint16_t)bits;
+        }
+      }
+    }
+  }
+}
+
+// ---- activation transform (def. forward_x) ---------------------------------
+// One block per (padded) token row: X'[t, g*D + k] = sum_j X[t, g*D + j] A[j, k]
+// and s[t] = sum_c X[t, c] b[c % D].  Rows t >= N and columns >= n of X' are
+// written as zero.
+template <typename XT, typename OT, int D>
+__global__ __launch_bounds__(256) void k_act_transform(const XT *__restrict__ X, int64_t N, int64_t n,
+                                                        const float *__restrict__ A,
+                                                        const float *__restrict__ b,
+                                                        OT *__restrict__ Xp, int64_t ldp,
+                                                        float *__restrict__ s) {
+  __shared__ float red[4];
+  const int64_t t = blockIdx.x;
+  const int64_t G = n / D, GP = ldp / D;
+  float a[D][D], bb[D];
+#pragma unroll
+  for (int j = 0; j < D; ++j) {
+    bb[j] = b[j];
+#pragma unroll
+    for (int k = 0; k < D; ++k) a[j][k] = A[j * D + k];
+  }
+  float acc_s = 0.0f;
+  for (int64_t g = threadIdx.x; g < GP; g += 256) {
+    float x[D], y[D];
+    if (t < N && g < G) {
+      loadD<D>(X + t * n + g * D, x);
+    } else {
+#pragma unroll
+      for (int j = 0; j < D; ++j) x[j] = 0.0f;
+    }
+#pragma unroll
+    for (int k = 0; k < D; ++k) {
+      float v = 0.0f;
+#pragma unroll
+      for (int j = 0; j < D; ++j) v = fmaf(x[j], a[j][k], v);
+      y[k] = v;
+    }
+#pragma unroll
+    for (int j = 0; j < D; ++j) acc_s = fmaf(x[j], bb[j], acc_s);
+    storeD<D>(Xp + t * ldp + g * D, y);
+  }
+  const float tot = block_sum256(acc_s, red);
+  if (threadIdx.x == 0) s[t] = tot;
+}
+
+// ---- per-token sums of dY (dX offset term) ---------------------------------
+// rs[t] = sum_r dY[t, r]; rows t in [N, Np) get 0.  Block 0 also clears dA/db
+// when the backward overwrites them.
+template <typename T, bool kVec>
+__global__ __launch_bounds__(256) void k_rowsum(const T *__restrict__ dY, int64_t N, int64_t m,
+                                                 float *__restrict__ rs, float *__restrict__ dA,
+                                                 float *__restrict__ db, int dd) {
+  __shared__ float red[4];
+  const int64_t t = blockIdx.x;
+  float acc = 0.0f;
+  if (t < N) {
+    const T *row = dY + t * m;
+    if constexpr (kVec) {
+      for (int64_t c = (int64_t)threadIdx.x * 8; c < m; c += 256 * 8) {
+        float v[8];
+        load8(row + c, v);
+#pragma unroll
+        for (int j = 0; j < 8; ++j) acc += v[j];
+      }
+    } else {
+      for (int64_t c = threadIdx.x; c < m; c += 256) {
+        if constexpr (sizeof(T) == 2) acc += bf16_to_f32(row[c]); else acc += (float)row[c];
+      }
+    }
+  }
+  const float tot = block_sum256(acc, red);
+  if (threadIdx.x == 0) rs[t] = tot;
+  if (blockIdx.x == 0 && dA != nullptr) {
+    for (int i = threadIdx.x; i < dd * dd; i += 256) dA[i] = 0.0f;
+    for (int i = threadIdx.x; i < dd; i += 256) db[i] = 0.0f;
+  }
+}
+
+// ---- stand-alone 2-bit packing ----------------------------------------------
+// Thread -> one 32-bit word of 16 consecutive codes of the flattened m x n
+// matrix (rows are n/4 bytes, so the flattened layout is the row layout).
+template <typename ST, bool kFromU8>
+__global__ __launch_bounds__(256) void k_pack2bit(const ST *__restrict__ src, int64_t total,
+                                                   uint8_t *__restrict__ packed) {
+  const int64_t words = total / 16;
+  for (int64_t w = (int64_t)blockIdx.x * 256 + threadIdx.x; w < words; w += (int64_t)gridDim.x * 256) {
+    uint32_t bits = 0;
+    if constexpr (kFromU8) {
+      u32x4 q = *reinterpret_cast<const u32x4 *>(reinterpret_cast<const uint8_t *>(src) + w * 16);
+#pragma unroll
+      for (int i = 0; i < 16; ++i) {
+        uint32_t c = (q[i >> 2] >> (8 * (i & 3))) & 0xffu;
+        bits |= (c > 3u ? 3u : c) << (2 * i);
+      }
+    } else {
+      float v[8];
+#pragma unroll
+      for (int h = 0; h < 2; ++h) {
+        load8(src + w * 16 + 8 * h, v);
+#pragma unroll
+        for (int i = 0; i < 8; ++i) bits |= quant_code(v[i]) << (2 * (8 * h + i));
+      }
+    }
+    *reinterpret_cast<uint32_t *>(packed + w * 4) = bits;
+  }
+  // tail: fewer than 16 codes left (total % 4 == 0, so whole bytes)
+  const int64_t done = words * 16;
+  if (blockIdx.x == 0 && (int64_t)threadIdx.x < (total - done) / 4) {
+    const int64_t e0 = done + 4 * threadIdx.x;
+    uint32_t byte = 0;
+    for (int i = 0; i < 4; ++i) {
+      uint32_t c;
+      if constexpr (kFromU8) {
+        c = reinterpret_cast<const uint8_t *>(src)[e0 + i];
+        c = c > 3u ? 3u : c;
+      } else if constexpr (sizeof(ST) == 2) {
+        c = quant_code(bf16_to_f32(reinterpret_cast<const uint16_t *>(src)[e0 + i]));
+      } else {
+        c = quant_code(reinterpret_cast<const float *>(src)[e0 + i]);
+      }
+      byte |= c << (2 * i);
+    }
+    packed[e0 / 4] = (uint8_t)byte;
+  }
+}
+
+// ---- stand-alone dense decode (def. forward) -------------------------------
+// Thread -> one group of D codes -> D outputs W_hat[r, g*D + j].  Groups never
+// straddle rows (n % D == 0), so the flattened group index is enough.
+template <int D, int kSrc, typename ZT, typename OT>
+__global__ __launch_bounds__(256) void k_dequant(const void *__restrict__ src, int64_t groups,
+                                                  const float *__restrict__ A,
+                                                  const float *__restrict__ b, OT *__restrict__ W) {
+  float a[D][D], bb[D];
+#pragma unroll
+  for (int j = 0; j < D; ++j) {
+    bb[j] = b[j];
+#pragma unroll
+    for (int k = 0; k < D; ++k) a[j][k] = A[j * D + k];
+  }
+  for (int64_t q = (int64_t)blockIdx.x * 256 + threadIdx.x; q < groups; q += (int64_t)gridDim.x * 256) {
+    float c[D];
+    if constexpr (kSrc == 0) {  // latent
+      float z[D];
+      loadD<D>(reinterpret_cast<const ZT *>(src) + q * D, z);
+#pragma unroll
+      for (int k = 0; k < D; ++k) c[k] = (float)quant_code(z[k]);
+    } else if constexpr (kSrc == 1) {  // one byte per code
+      const uint8_t *p = reinterpret_cast<const uint8_t *>(src) + q * D;
+      uint32_t w0 = *reinterpret_cast<const uint32_t *>(p);
+      uint32_t w1 = D == 8 ? *reinterpret_cast<const uint32_t *>(p + 4) : 0u;
+#pragma unroll
+      for (int k = 0; k < D; ++k) {
+        uint32_t v = ((k < 4 ? w0 : w1) >> (8 * (k & 3))) & 0xffu;
+        c[k] = (float)(v > 3u ? 3u : v);
+      }
+    } else {  // packed 2-bit
+      const uint8_t *p = reinterpret_cast<const uint8_t *>(src) + q * (D / 4);
+      uint32_t w = D == 8 ? (uint32_t)*reinterpret_cast<const uint16_t *>(p) : (uint32_t)*p;
+#pragma unroll
+      for (int k = 0; k < D; ++k) c[k] = (float)((w >> (2 * k)) & 3u);
+    }
+    float y[D];
+#pragma unroll
+    for (int j = 0; j < D; ++j) {
+      float v = bb[j];
+#pragma unroll
+      for (int k = 0; k < D; ++k) v = fmaf(a[j][k], c[k], v);
+      y[j] = v;
+    }
+    storeD<D>(W + q * D, y);
+  }
+}
+
+// ---- launchers -------------------------------------------------------------
+
+static inline int grid_for(int64_t items, int64_t per_block) {
+  int64_t g = ceil_div(items, per_block);
+  if (g > 65536) g = 65536;
+  return (int)(g < 1 ? 1 : g);
+}
+
+hipError_t launch_quant_frag(const void *Z, bool z_bf16, int64_t m, int64_t n, bool trans,
+                             uint32_t *frag, uint8_t *packed, hipStream_t st) {
+  // forward: M = r padded to 256, K = c padded to 64; transposed: M = c, K = r
+  const int64_t Mp = round_up(trans ? n : m, 256), Kp = round_up(trans ? m : n, 64);
+  const int KB = (int)(Kp / 64);
+  dim3 grid(trans ? (unsigned)(Mp / 64) : (unsigned)(Kp / 64), trans ? (unsigned)(Kp / 64) : (unsigned)(Mp / 64));
+  if (z_bf16) {
+    if (trans) k_quant_frag<uint16_t, true><<<grid, 256, 0, st>>>((const uint16_t *)Z, m, n, frag, KB, nullptr);
+    else k_quant_frag<uint16_t, false><<<grid, 256, 0, st>>>((const uint16_t *)Z, m, n, frag, KB, packed);
+  } else {
+    if (trans) k_quant_frag<float, true><<<grid, 256, 0, st>>>((const float *)Z, m, n, frag, KB, nullptr);
+    else k_quant_frag<float, false><<<grid, 256, 0, st>>>((const float *)Z, m, n, frag, KB, packed);
+  }
+  return hipGetLastError();
+}
+
+hipError_t launch_act_transform(const void *X, bool bf16, int64_t N, int64_t Np, int64_t n, int d,
+                                const float *A, const float *b, void *Xp, int64_t ldp, float *s,
+                                hipStream_t st) {
+  dim3 grid((unsigned)Np);
+  if (bf16) {
+    if (d == 8) k_act_transform<uint16_t, uint16_t, 8><<<grid, 256, 0, st>>>((const uint16_t *)X, N, n, A, b, (uint16_t *)Xp, ldp, s);
+    else k_act_transform<uint16_t, uint16_t, 4><<<grid, 256, 0, st>>>((const uint16_t *)X, N, n, A, b, (uint16_t *)Xp, ldp, s);
+  } else {
+    if (d == 8) k_act_transform<float, float, 8><<<grid, 256, 0, st>>>((const float *)X, N, n, A, b, (float *)Xp, ldp, s);
+    else k_act_transform<float, float, 4><<<grid, 256, 0, st>>>((const float *)X, N, n, A, b, (float *)Xp, ldp, s);
+  }
+  return hipGetLastError();
+}
+
+hipError_t launch_rowsum(const void *dY, bool bf16, int64_t N, int64_t Np, int64_t m, float *rs, float *dA,
+                         float *db, int d, hipStream_t st) {
+  dim3 grid((unsigned)Np);
+  if (bf16) {
+    if (m % 8 == 0) k_rowsum<uint16_t, true><<<grid, 256, 0, st>>>((const uint16_t *)dY, N, m, rs, dA, db, d);
+    else k_rowsum<uint16_t, false><<<grid, 256, 0, st>>>((const uint16_t *)dY, N, m, rs, dA, db, d);
+  } else {
+    if (m % 8 == 0) k_rowsum<float, true><<<grid, 256, 0, st>>>((const float *)dY, N, m, rs, dA, db, d);
+    else k_rowsum<float, false><<<grid, 256, 0, st>>>((const float *)dY, N, m, rs, dA, db, d);
+  }
+  return hipGetLastError();
+}
+
+hipError_t launch_pack2bit(const void *src, int kind, bool bf16, int64_t m, int64_t n, uint8_t *packed,
+                           hipStream_t st) {
+  const int64_t total = m * n;
+  const int grid = grid_for(total / 16, 256);
+  if (kind == 1) k_pack2bit<uint8_t, true><<<grid, 256, 0, st>>>((const uint8_t *)src, total, packed);
+  else if (bf16) k_pack2bit<uint16_t, false><<<grid, 256, 0, st>>>((const uint16_t *)src, total, packed);
+  else k_pack2bit<float, false><<<grid, 256, 0, st>>>((const float *)src, total, packed);
+  return hipGetLastError();
+}
+
+template <int D, typename OT>
+static void dequant_dispatch(int kind, bool zbf16, const void *src, int64_t groups, const float *A,
+                             const float *b, void *W, int grid, hipStream_t st) {
+  OT *w = (OT *)W;
+  if (kind == 0) {
+    if (zbf16) k_dequant<D, 0, uint16_t, OT><<<grid, 256, 0, st>>>(src, groups, A, b, w);
+    else k_dequant<D, 0, float, OT><<<grid, 256, 0, st>>>(src, groups, A, b, w);
+  } else if (kind == 1) {
+    k_dequant<D, 1, uint8_t, OT><<<grid, 256, 0, st>>>(src, groups, A, b, w);
+  } else {
+    k_dequant<D, 2, uint8_t, OT><<<grid, 256, 0, st>>>(src, groups, A, b, w);
+  }
+}
+
+hipError_t launch_dequant(const void *src, int kind, bool z_bf16, int64_t m, int64_t n, int d,
+                          const float *A, const float *b, void *W, bool out_bf16, hipStream_t st) {
+  const int64_t groups = m * n / d;
+  const int grid = grid_for(groups, 256);
+  if (d == 8) {
+    if (out_bf16) dequant_dispatch<8, uint16_t>(kind, z_bf16, src, groups, A, b, W, grid, st);
+    else dequant_dispatch<8, float>(kind, z_bf16, src, groups, A, b, W, grid, st);
+  } else {
+    if (out_bf16) dequant_dispatch<4, uint16_t>(kind, z_bf16, src, groups, A, b, W, grid, st);
+    else dequant_dispatch<4, float>(kind, z_bf16, src, groups, A, b, W, grid, st);
+  }
+  return hipGetLastError();
+}
+
+}  // namespace lcvq

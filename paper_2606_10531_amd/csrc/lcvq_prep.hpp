@@ -1,0 +1,40 @@
+// Internal launchers of the LC-VQ kernels (host side).
+#pragma once
+
+#include "lcvq_common.hpp"
+
+namespace lcvq {
+
+// streaming kernels (lcvq_prep.hip)
+hipError_t launch_quant_frag(const void *Z, bool z_bf16, int64_t m, int64_t n, bool trans,
+                             uint32_t *frag, uint8_t *packed, hipStream_t st);
+hipError_t launch_act_transform(const void *X, bool bf16, int64_t N, int64_t Np, int64_t n, int d,
+                                const float *A, const float *b, void *Xp, int64_t ldp, float *s,
+                                hipStream_t st);
+hipError_t launch_rowsum(const void *dY, bool bf16, int64_t N, int64_t Np, int64_t m, float *rs, float *dA,
+                         float *db, int d, hipStream_t st);
+hipError_t launch_pack2bit(const void *src, int kind, bool bf16, int64_t m, int64_t n, uint8_t *packed,
+                           hipStream_t st);
+hipError_t launch_dequant(const void *src, int kind, bool z_bf16, int64_t m, int64_t n, int d,
+                          const float *A, const float *b, void *W, bool out_bf16, hipStream_t st);
+
+// bf16 matrix-core products (lcvq_gemm.hip)
+hipError_t launch_fwd_bf16(const uint32_t *frag, const uint16_t *Xp, int64_t ldp, const float *s,
+                           uint16_t *Y, int64_t N, int64_t m, int64_t n, hipStream_t st);
+hipError_t launch_dx_bf16(const uint32_t *frag, const uint16_t *dY, const float *rs, const float *A,
+                          const float *b, int d, uint16_t *dX, int64_t N, int64_t m, int64_t n,
+                          hipStream_t st);
+hipError_t launch_dz_bf16(const uint16_t *X, const uint16_t *dY, const uint16_t *Z, const float *A, int d,
+                          int mask_mode, int accumulate, void *dZ, bool dz_bf16, float *dA, float *db,
+                          int64_t N, int64_t m, int64_t n, hipStream_t st);
+
+// fp32 products on the vector ALUs (lcvq_f32.hip)
+hipError_t launch_fwd_f32(const float *Z, const float *Xp, const float *s, float *Y, int64_t N, int64_t m,
+                          int64_t n, hipStream_t st);
+hipError_t launch_dx_f32(const float *Z, const float *dY, const float *rs, const float *A, const float *b,
+                         int d, float *dX, int64_t N, int64_t m, int64_t n, hipStream_t st);
+hipError_t launch_dz_f32(const float *X, const float *dY, const float *Z, const float *A, int d,
+                         int mask_mode, int accumulate, float *dZ, float *dA, float *db, int64_t N,
+                         int64_t m, int64_t n, hipStream_t st);
+
+}  // namespace lcvq

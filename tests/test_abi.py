@@ -1,0 +1,117 @@
+"""The C ABI boundary without a GPU: the library loads, exports every entry
+point declared in include/lcvq.h, and rejects bad arguments on the host before
+anything is enqueued (so no call here reaches the HIP runtime)."""
+import ctypes
+import os
+import re
+
+import pytest
+
+from paper_2606_10531_amd import _lib as L
+
+HEADER = os.path.join(os.path.dirname(os.path.dirname(os.path.abspath(__file__))), "include", "lcvq.h")
+FAKE = 0x10000            # 16-byte aligned, never dereferenced: validation fails first
+MIS = 0x10002             # misaligned
+
+
+@pytest.fixture(scope="module")
+def lib():
+    return L.load()
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    return sorted(set(re.findall(r"^\s*(?:const\s+)?\w+\s*\*?\s*(lcvq_\w+)\s*\(", text, flags=re.M)))
+
+
+def test_every_declared_symbol_is_exported(lib):
+    names = declared_functions()
+    assert set(names) >= {"lcvq_dequant", "lcvq_linear_fwd", "lcvq_linear_bwd", "lcvq_pack2bit",
+                          "lcvq_workspace_bytes", "lcvq_status_string", "lcvq_last_error"}
+    for name in names:
+        assert hasattr(lib, name), name
+    assert set(names) == set(L.SIGNATURES)
+
+
+def test_status_strings(lib):
+    for s in range(6):
+        assert L.status_string(s)
+    assert L.status_string(99) == "unknown status"
+
+
+def test_workspace_bytes(lib):
+    f = lib.lcvq_workspace_bytes
+    assert f(L.OP_FWD, 16, 256, 256, 8, L.F32) > 0
+    assert f(L.OP_FWD, 4096, 4096, 4096, 8, L.BF16) >= 4096 * 4096 * 2      # transformed activations
+    assert f(L.OP_BWD, 4096, 4096, 4096, 8, L.BF16) >= 4096 * 4096 // 2     # codes, 4 bits each
+    assert f(L.OP_FWD, 16, 256, 256, 5, L.F32) == 0
+    assert f(L.OP_FWD, -1, 256, 256, 8, L.F32) == 0
+    assert f(7, 16, 256, 256, 8, L.F32) == 0
+    assert f(L.OP_FWD, 300, 264, 328, 8, L.BF16) >= f(L.OP_FWD, 256, 264, 328, 8, L.BF16)
+
+
+def fwd(lib, N=16, m=64, n=64, d=8, dt=L.BF16, Z=FAKE, A=FAKE, b=FAKE, X=FAKE, Y=FAKE, packed=None,
+        ws=FAKE, wsb=1 << 40):
+    return lib.lcvq_linear_fwd(N, m, n, d, dt, Z, A, b, X, Y, packed, ws, wsb, None)
+
+
+def bwd(lib, N=16, m=64, n=64, d=8, dt=L.BF16, mask=0, acc=0, dX=FAKE, dZ=FAKE, dzt=L.BF16, dA=FAKE,
+        db=FAKE, ws=FAKE, wsb=1 << 40, X=FAKE, dY=FAKE):
+    return lib.lcvq_linear_bwd(N, m, n, d, dt, FAKE, FAKE, FAKE, X, dY, mask, acc, dX, dZ, dzt, dA, db, ws,
+                               wsb, None)
+
+
+def test_fwd_validation(lib):
+    assert fwd(lib, d=5) == L.EUNSUPPORTED
+    assert fwd(lib, n=60, d=8) == L.EINVAL                 # n % d
+    assert fwd(lib, N=-1) == L.EINVAL
+    assert fwd(lib, dt=7) == L.EINVAL
+    assert fwd(lib, m=60, n=64) == L.EUNSUPPORTED          # bf16 path: m % 8
+    assert fwd(lib, m=60, n=64, dt=L.F32) != L.EUNSUPPORTED
+    assert fwd(lib, Z=None) == L.EINVAL
+    assert fwd(lib, X=None) == L.EINVAL
+    assert fwd(lib, Y=MIS) == L.EALIGN
+    assert fwd(lib, packed=MIS) == L.EALIGN
+    assert fwd(lib, wsb=16) == L.EWORKSPACE
+    assert fwd(lib, ws=None) == L.EWORKSPACE
+    assert "workspace" in L.last_error()
+    # an empty product is valid and enqueues nothing
+    assert fwd(lib, N=0, Y=None, X=None) == L.OK
+    assert fwd(lib, m=0, Y=None) == L.OK
+
+
+def test_bwd_validation(lib):
+    assert bwd(lib, d=3) == L.EUNSUPPORTED
+    assert bwd(lib, mask=2) == L.EINVAL
+    assert bwd(lib, acc=2) == L.EINVAL
+    assert bwd(lib, dA=None) == L.EINVAL                   # dA and db go together
+    assert bwd(lib, dt=L.F32, dzt=L.BF16) == L.EINVAL     # bf16 dZ needs the bf16 path
+    assert bwd(lib, X=None) == L.EINVAL
+    assert bwd(lib, dY=MIS) == L.EALIGN
+    assert bwd(lib, dZ=MIS) == L.EALIGN
+    assert bwd(lib, wsb=8) == L.EWORKSPACE
+    assert bwd(lib, N=0, acc=1) == L.OK                    # accumulate into nothing: no work
+
+
+def test_pack_and_dequant_validation(lib):
+    p = lib.lcvq_pack2bit
+    assert p(FAKE, L.SRC_LATENT, L.BF16, 4, 6, FAKE, None) == L.EINVAL        # n % 4
+    assert p(FAKE, L.SRC_PACKED2, L.BF16, 4, 8, FAKE, None) == L.EINVAL      # not a pack source
+    assert p(FAKE, L.SRC_LATENT, 9, 4, 8, FAKE, None) == L.EINVAL
+    assert p(None, L.SRC_LATENT, L.BF16, 4, 8, FAKE, None) == L.EINVAL
+    assert p(MIS, L.SRC_LATENT, L.BF16, 4, 8, FAKE, None) == L.EALIGN
+    assert p(None, L.SRC_LATENT, L.BF16, 0, 8, None, None) == L.OK
+    q = lib.lcvq_dequant
+    assert q(4, 8, 3, L.SRC_LATENT, L.BF16, FAKE, FAKE, FAKE, FAKE, L.BF16, None) == L.EUNSUPPORTED
+    assert q(4, 12, 8, L.SRC_LATENT, L.BF16, FAKE, FAKE, FAKE, FAKE, L.BF16, None) == L.EINVAL
+    assert q(4, 8, 8, 5, L.BF16, FAKE, FAKE, FAKE, FAKE, L.BF16, None) == L.EINVAL
+    assert q(4, 8, 8, L.SRC_LATENT, L.BF16, FAKE, None, FAKE, FAKE, L.BF16, None) == L.EINVAL
+    assert q(4, 8, 8, L.SRC_LATENT, L.BF16, FAKE, FAKE, FAKE, MIS, L.BF16, None) == L.EALIGN
+
+
+def test_binding_refuses_cpu_tensors():
+    torch = pytest.importorskip("torch")
+    import paper_2606_10531_amd as lc
+    Z = torch.zeros(8, 8)
+    with pytest.raises(ValueError, match="GPU"):
+        lc.pack2bit(Z)
