@@ -1,0 +1,273 @@
+#!/usr/bin/env python3
+"""Benchmark of the LC-VQ linear layer training step on one MI355X.
+
+A step is one forward (quantise + 2-bit pack, activation transform, matrix-core
+product) plus one straight-through backward (dX, dZ, dA, db) of one LC-VQ
+weight matrix, on seeded synthetic inputs already resident in HBM.  The
+reported value is the work of the three products, 6 N m n flop, divided by the
+step time.  Prints one JSON line.
+
+  python bench.py [--steps K] [--warmup W] [--workload NAME] [--no-cpu-baseline]
+"""
+from __future__ import annotations
+
+import argparse
+import ctypes
+import hashlib
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "LC-VQ linear fwd+bwd TFLOP/s (frac of MFMA peak) at 4096x4096; codes bit-exact"
+PEAK_MFMA_BF16 = 2500.0      # TFLOP/s, MI355X dense bf16 matrix cores (published)
+PEAK_HBM = 8000.0            # GB/s, MI355X HBM3E (published)
+DEFAULT_WORKLOAD = "lcvq_4096x4096_n4096_bf16"
+MATRIX_KERNELS = ("fwd", "dx", "dw")
+
+
+def kernel_source_digest() -> str:
+    h = hashlib.sha256()
+    for f in sorted(os.listdir(os.path.join(ROOT, "paper_2606_10531_amd", "csrc"))):
+        with open(os.path.join(ROOT, "paper_2606_10531_amd", "csrc", f), "rb") as fh:
+            h.update(f.encode() + fh.read())
+    return h.hexdigest()[:16]
+
+
+def measured_traffic(kernel: str, workload: str):
+    """HBM bytes per launch from the committed rocprofv3 counter summary, if it
+    was taken on the current kernel sources; else None."""
+    path = os.path.join(ROOT, "profiles", "traffic.json")
+    if not os.path.exists(path):
+        return None
+    try:
+        rec = json.load(open(path))
+    except ValueError:
+        return None
+    entry = rec.get(workload, {}).get(kernel)
+    if not entry or entry.get("source_digest") != kernel_source_digest():
+        return None
+    return entry.get("bytes_per_launch")
+
+
+class Layer:
+    """Device buffers and the fwd+bwd step of one LC-VQ weight matrix."""
+
+    def __init__(self, lc, torch, N, m, n, d, k):
+        import numpy as np
+
+        import synth
+        inp = synth.layer_inputs(N, m, n, d, "bf16", k=k)
+        self.inp = inp
+        self.lc, self.N, self.m, self.n, self.d = lc, N, m, n, d
+
+        def dev(bits):
+            return torch.from_numpy(np.ascontiguousarray(bits).view(np.int16)).view(torch.bfloat16).cuda()
+
+        self.Z, self.X, self.dY = dev(inp["Z"]), dev(inp["X"]), dev(inp["dY"])
+        self.A, self.b = torch.from_numpy(inp["A"]).cuda(), torch.from_numpy(inp["b"]).cuda()
+        bf = torch.bfloat16
+        self.Y = torch.empty((N, m), dtype=bf, device="cuda")
+        self.packed = torch.empty((m, n // 4), dtype=torch.uint8, device="cuda")
+        self.dX = torch.empty((N, n), dtype=bf, device="cuda")
+        self.dZ = torch.empty((m, n), dtype=bf, device="cuda")
+        self.dA = torch.empty((d, d), dtype=torch.float32, device="cuda")
+        self.db = torch.empty((d,), dtype=torch.float32, device="cuda")
+        self.wsf = torch.empty(lc.workspace_bytes(lc.OP_FWD, N, m, n, d, bf), dtype=torch.uint8, device="cuda")
+        self.wsb = torch.empty(lc.workspace_bytes(lc.OP_BWD, N, m, n, d, bf), dtype=torch.uint8, device="cuda")
+
+    def step(self):
+        lc = self.lc
+        lc.linear_fwd(self.Z, self.A, self.b, self.X, self.d, packed_out=self.packed, workspace=self.wsf,
+                      out=self.Y)
+        lc.linear_bwd(self.Z, self.A, self.b, self.X, self.dY, self.d, dX=self.dX, dZ=self.dZ, dA=self.dA,
+                      db=self.db, workspace=self.wsb)
+
+    def flops(self):
+        return 6.0 * self.N * self.m * self.n
+
+
+def timer_read(lib, kernel_id):
+    ms, cnt = ctypes.c_double(), ctypes.c_int64()
+    lib.lcvq_timer_read(kernel_id, ctypes.byref(ms), ctypes.byref(cnt))
+    return ms.value, cnt.value
+
+
+def hbm_kernels(lc, torch):
+    """Achieved bandwidth of the streaming kernels on a 28672 x 8192 matrix
+    (470 MB of bf16 latents, larger than the 256 MB last-level cache)."""
+    import numpy as np
+
+    import synth
+    m, n, d = 28672, 8192, 8
+    lib = lc._lib.load()
+    Z = torch.from_numpy(synth.draw_latent(m, n, 0, "bf16").view(np.int16)).view(torch.bfloat16).cuda()
+    A, b = torch.eye(d, device="cuda"), torch.zeros(d, device="cuda")
+    packed = torch.empty((m, n // 4), dtype=torch.uint8, device="cuda")
+    W = torch.empty((m, n), dtype=torch.bfloat16, device="cuda")
+    out = {}
+    cases = [("pack2bit_from_bf16", lambda: lc.pack2bit(Z, out=packed), 2.25, "pack"),
+             ("dequant_packed_to_bf16", lambda: lc.dequant(packed, A, b, d, n=n, src_kind=lc.SRC_PACKED2,
+                                                           out=W), 2.25, "dequant"),
+             ("dequant_bf16_latent_to_bf16", lambda: lc.dequant(Z, A, b, d, out=W), 4.0, "dequant")]
+    for name, fn, bpe, kname in cases:
+        for _ in range(3):
+            fn()
+        torch.cuda.synchronize()
+        kid = lc._lib.KERNELS.index(kname)
+        lib.lcvq_timer_enable(1 << kid)
+        for _ in range(20):
+            fn()
+        torch.cuda.synchronize()
+        ms, cnt = timer_read(lib, kid)
+        lib.lcvq_timer_enable(0)
+        us = 1e3 * ms / max(cnt, 1)
+        gbps = bpe * m * n / (us * 1e-6) / 1e9
+        out[name] = {"us": round(us, 2), "GB/s": round(gbps, 1), "frac_hbm": round(gbps / PEAK_HBM, 3),
+                     "bytes_per_elem": bpe, "shape": [m, n]}
+    del Z, packed, W
+    return out
+
+
+def cpu_baseline(layer, max_seconds: float):
+    """The fp64 oracle on the host, on the same inputs (a bounded number of full
+    fwd+bwd repetitions), with its parity check of the GPU results."""
+    import numpy as np
+    import torch
+
+    import oracle as orc
+    try:
+        from threadpoolctl import threadpool_info
+        cores = max([p.get("num_threads", 1) for p in threadpool_info() if p.get("user_api") == "blas"] or [1])
+    except Exception:  # pragma: no cover
+        cores = os.cpu_count()
+    inp, d = layer.inp, layer.d
+    v = {k: orc.widen(inp[k], "bf16") for k in ("Z", "X", "dY")}
+    A64, b64 = inp["A"].astype(np.float64), inp["b"].astype(np.float64)
+    reps, t0 = 0, time.perf_counter()
+    while True:
+        Yref, codes = orc.linear_forward(v["Z"], A64, b64, v["X"], d)
+        ref = orc.linear_backward(v["Z"], A64, b64, v["X"], v["dY"], d)
+        reps += 1
+        el = time.perf_counter() - t0
+        if el >= max_seconds or reps >= 5:
+            break
+    per = el / reps
+
+    def host(t):
+        t = t.detach().cpu()
+        if t.dtype == torch.bfloat16:
+            return orc.widen(t.view(torch.int16).numpy().view(np.uint16), "bf16")
+        return t.numpy().astype(np.float64)
+
+    def rel(a, r):
+        return float(np.linalg.norm(a - r) / np.linalg.norm(r))
+
+    layer.step()
+    torch.cuda.synchronize()
+    parity = {"codes_bit_exact": bool(np.array_equal(layer.packed.cpu().numpy(), orc.pack2bit(codes))),
+              "rel_fro": {"Y": rel(host(layer.Y), Yref), "dX": rel(host(layer.dX), ref["dX"]),
+                          "dZ": rel(host(layer.dZ), ref["dZ"]), "dA": rel(host(layer.dA), ref["dA"]),
+                          "db": rel(host(layer.db), ref["db"])},
+              "tolerance": 2e-2}
+    return {"value": round(layer.flops() / per / 1e12, 5), "unit": "TFLOP/s", "cores": cores, "kind": "oracle",
+            "sample": f"full {layer.m}x{layer.n} layer, {layer.N} tokens, fwd+bwd in fp64 (numpy/OpenBLAS), "
+                      f"{reps} repetition(s), {per:.2f} s each",
+            "parity": parity}
+
+
+def main():
+    ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=50)
+    ap.add_argument("--warmup", type=int, default=10)
+    ap.add_argument("--workload", default=DEFAULT_WORKLOAD)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-hbm", action="store_true")
+    ap.add_argument("--cpu-seconds", type=float, default=10.0)
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print(f"bench.py: this build runs on one GPU only (asked for --gpus {args.gpus}); the multi-GPU "
+              "sharding of the layer is described in DESIGN.md but not built.", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+
+    import paper_2606_10531_amd as lc
+    import synth
+    assert torch.cuda.is_available(), "bench.py needs a GPU"
+    lib = lc._lib.load()
+    wl = synth.WORKLOADS[args.workload]
+    if wl["dtype"] != "bf16":
+        sys.exit("bench.py times the bf16 matrix-core path; pick a bf16 workload")
+    layers = [Layer(lc, torch, wl["N"], m, n, wl["d"], k) for k, (m, n) in enumerate(wl["mats"])]
+
+    def step():
+        for L in layers:
+            L.step()
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+
+    # per-kernel breakdown (separate, untimed pass) to pick the dominant kernel
+    lib.lcvq_timer_enable((1 << len(lc._lib.KERNELS)) - 1)
+    for _ in range(3):
+        step()
+    torch.cuda.synchronize()
+    breakdown = {}
+    for kid, name in enumerate(lc._lib.KERNELS):
+        ms, cnt = timer_read(lib, kid)
+        if cnt:
+            breakdown[name] = round(1e3 * ms / 3, 2)      # us per step
+    lib.lcvq_timer_enable(0)
+    dominant = max(MATRIX_KERNELS, key=lambda k: breakdown.get(k, 0.0))
+    dom_id = lc._lib.KERNELS.index(dominant)
+
+    # timed region: K steps between two events; the dominant kernel is also
+    # bracketed by its own events on the same stream
+    lib.lcvq_timer_enable(1 << dom_id)
+    start, stop = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    start.record()
+    for _ in range(args.steps):
+        step()
+    stop.record()
+    torch.cuda.synchronize()
+    ms_step = start.elapsed_time(stop) / args.steps
+    dom_ms, dom_cnt = timer_read(lib, dom_id)
+    lib.lcvq_timer_enable(0)
+    dom_us = 1e3 * dom_ms / max(dom_cnt, 1)
+
+    flops = sum(L.flops() for L in layers)
+    value = flops / (ms_step * 1e-3) / 1e12
+    per_launch_flop = 2.0 * sum(L.N * L.m * L.n for L in layers) / len(layers)
+    achieved = per_launch_flop / (dom_us * 1e-6) / 1e12
+    traffic = measured_traffic(dominant, args.workload)
+
+    res = {
+        "metric": METRIC, "value": round(value, 2), "unit": "TFLOP/s", "n_gpus": 1, "steps": args.steps,
+        "warmup": args.warmup, "ms_per_step": round(ms_step, 4), "higher_is_better": True, "scaling": "weak",
+        "vs_baseline": None, "dtype": "bf16", "data": "synthetic",
+        "config": {"workload": args.workload, "N": wl["N"], "matrices": [list(x) for x in wl["mats"]],
+                   "d": wl["d"], "step": "fwd (+2-bit pack) + straight-through bwd (dX, dZ, dA, db)"},
+        "frac_of_peak": round(value / PEAK_MFMA_BF16, 4),
+        "roofline": {"kernel": dominant, "bound": "mfma", "achieved": round(achieved, 2),
+                     "peak": PEAK_MFMA_BF16, "unit": "TFLOP/s", "frac": round(achieved / PEAK_MFMA_BF16, 4),
+                     "traffic": traffic, "avg_launch_us": round(dom_us, 2),
+                     "flop_per_launch": per_launch_flop},
+        "kernels_us_per_step": breakdown,
+    }
+    if not args.no_hbm:
+        res["hbm_kernels"] = hbm_kernels(lc, torch)
+    if not args.no_cpu_baseline:
+        res["cpu_baseline"] = cpu_baseline(layers[0], args.cpu_seconds)
+        res["cpu_baseline"]["note"] = "first matrix of the workload" if len(layers) > 1 else "whole workload"
+    print(json.dumps(res), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -19,7 +19,8 @@
  *
  * Conventions shared by every call
  *  - All tensors are dense, row-major, caller-owned DEVICE pointers; the
- *    library allocates nothing and keeps no mutable global state.
+ *    library allocates no device memory and keeps no mutable global state
+ *    apart from the optional kernel timer below.
  *  - `stream` is a hipStream_t passed as void* (NULL = the null stream).
  *    Every call only enqueues work on it and returns; device-side results are
  *    visible after the caller synchronises that stream.
@@ -149,6 +150,32 @@ lcvq_status_t lcvq_linear_bwd(int64_t N, int64_t m, int64_t n, int32_t d, int32_
                               const void *X, const void *dY, int32_t mask_mode, int32_t accumulate,
                               void *dX, void *dZ, int32_t dz_dtype, float *dA, float *db,
                               void *workspace, size_t workspace_bytes, void *stream);
+
+/*
+ * Instrumentation: device time of individual kernels, measured with HIP events.
+ * lcvq_timer_enable(mask) makes every later launch of a kernel whose bit
+ * (1 << lcvq_kernel_t) is set in `mask`, by any thread, record a start event
+ * immediately before and a stop event immediately after it on the launch's
+ * stream; mask 0 switches recording off and discards pending records.
+ * lcvq_timer_read(kernel, &total_ms, &launches) waits for the recorded launches
+ * of `kernel`, returns their summed duration and count, and clears them.  Not
+ * for use while the stream is being captured into a graph.
+ */
+typedef enum {
+  LCVQ_K_QUANT = 0,     /* latents -> codes in the forward operand layout (+ 2-bit pack) */
+  LCVQ_K_ACT = 1,       /* X' = X blockdiag(A), s = X b~ */
+  LCVQ_K_FWD = 2,       /* Y = X' codes^T + s 1^T (matrix cores) */
+  LCVQ_K_ROWSUM = 3,    /* per-token sums of dY */
+  LCVQ_K_QUANT_T = 4,   /* latents -> codes in the input-gradient operand layout */
+  LCVQ_K_DX = 5,        /* dX (matrix cores + A^T map) */
+  LCVQ_K_DW = 6,        /* dW = dY^T X with dZ, dA, db epilogue (matrix cores) */
+  LCVQ_K_PACK = 7,      /* lcvq_pack2bit */
+  LCVQ_K_DEQUANT = 8,   /* lcvq_dequant */
+  LCVQ_K_FILL = 9,      /* zero fills of degenerate shapes */
+  LCVQ_K_COUNT = 10
+} lcvq_kernel_t;
+lcvq_status_t lcvq_timer_enable(uint32_t mask);
+lcvq_status_t lcvq_timer_read(int32_t kernel, double *total_ms, int64_t *launches);
 
 /* Static description of a status code. */
 const char *lcvq_status_string(lcvq_status_t status);

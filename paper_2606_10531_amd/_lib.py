@@ -16,6 +16,8 @@ SRC_LATENT, SRC_CODES_U8, SRC_PACKED2 = 0, 1, 2
 MASK_ROUNDED, MASK_LATENT = 0, 1
 # lcvq_op_t
 OP_FWD, OP_BWD = 0, 1
+# lcvq_kernel_t
+KERNELS = ["quant", "act", "fwd", "rowsum", "quant_t", "dx", "dw", "pack", "dequant", "fill"]
 
 _P = ctypes.c_void_p
 _I64 = ctypes.c_int64
@@ -29,6 +31,8 @@ SIGNATURES = {
     "lcvq_linear_fwd": (_I32, [_I64, _I64, _I64, _I32, _I32, _P, _P, _P, _P, _P, _P, _P, _SZ, _P]),
     "lcvq_linear_bwd": (_I32, [_I64, _I64, _I64, _I32, _I32, _P, _P, _P, _P, _P, _I32, _I32,
                                _P, _P, _I32, _P, _P, _P, _SZ, _P]),
+    "lcvq_timer_enable": (_I32, [ctypes.c_uint32]),
+    "lcvq_timer_read": (_I32, [_I32, ctypes.POINTER(ctypes.c_double), ctypes.POINTER(ctypes.c_int64)]),
     "lcvq_status_string": (ctypes.c_char_p, [_I32]),
     "lcvq_last_error": (ctypes.c_char_p, []),
 }

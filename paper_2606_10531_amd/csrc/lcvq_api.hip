@@ -4,6 +4,11 @@
 #include <stdarg.h>
 #include <stdio.h>
 
+#include <atomic>
+#include <mutex>
+#include <utility>
+#include <vector>
+
 #include "../../include/lcvq.h"
 #include "lcvq_prep.hpp"
 
@@ -80,6 +85,47 @@ BwdLayout bwd_layout(int64_t N, int64_t m, int64_t n, bool bf16) {
   return L;
 }
 
+// ---- per-kernel event timing (instrumentation, off by default) ------------
+struct Timer {
+  std::atomic<uint32_t> mask{0};
+  std::mutex mu;
+  std::vector<hipEvent_t> pool;
+  std::vector<std::pair<hipEvent_t, hipEvent_t>> rec[LCVQ_K_COUNT];
+  hipEvent_t get() {  // caller holds mu
+    if (!pool.empty()) {
+      hipEvent_t e = pool.back();
+      pool.pop_back();
+      return e;
+    }
+    hipEvent_t e = nullptr;
+    if (hipEventCreate(&e) != hipSuccess) return nullptr;
+    return e;
+  }
+};
+Timer g_timer;
+
+// Brackets one launch with start/stop events when its kernel is being timed.
+struct Timed {
+  int k;
+  hipStream_t st;
+  hipEvent_t e0 = nullptr, e1 = nullptr;
+  Timed(int kernel, hipStream_t s) : k(kernel), st(s) {
+    if (!(g_timer.mask.load(std::memory_order_relaxed) & (1u << k))) return;
+    std::lock_guard<std::mutex> lock(g_timer.mu);
+    e0 = g_timer.get();
+    e1 = g_timer.get();
+    if (e0 && e1) hipEventRecord(e0, st);
+  }
+  hipError_t done(hipError_t e) {
+    if (e0 && e1) {
+      hipEventRecord(e1, st);
+      std::lock_guard<std::mutex> lock(g_timer.mu);
+      g_timer.rec[k].emplace_back(e0, e1);
+    }
+    return e;
+  }
+};
+
 // Zero-fill without hipMemsetAsync (safe to capture in a graph).
 __global__ void k_fill_zero(uint32_t *p, int64_t words) {
   for (int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x; i < words; i += (int64_t)gridDim.x * 256) p[i] = 0u;
@@ -90,8 +136,9 @@ hipError_t fill_zero(void *p, size_t bytes, hipStream_t st) {
   int64_t g = (words + 255) / 256;
   if (g > 65536) g = 65536;
   if (g < 1) g = 1;
+  Timed tm(LCVQ_K_FILL, st);
   k_fill_zero<<<(unsigned)g, 256, 0, st>>>((uint32_t *)p, words);
-  return hipGetLastError();
+  return tm.done(hipGetLastError());
 }
 
 lcvq_status_t check_common(int64_t N, int64_t m, int64_t n, int32_t d, int32_t dtype) {
@@ -125,6 +172,52 @@ const char *lcvq_status_string(lcvq_status_t s) {
 
 const char *lcvq_last_error(void) { return g_err; }
 
+lcvq_status_t lcvq_timer_enable(uint32_t mask) {
+  if (mask >> LCVQ_K_COUNT) return fail(LCVQ_EINVAL, "timer mask 0x%x has unknown kernel bits", mask);
+  g_timer.mask.store(mask);
+  if (mask == 0) {
+    std::lock_guard<std::mutex> lock(g_timer.mu);
+    for (auto &v : g_timer.rec) {
+      for (auto &p : v) {
+        hipEventSynchronize(p.second);
+        g_timer.pool.push_back(p.first);
+        g_timer.pool.push_back(p.second);
+      }
+      v.clear();
+    }
+  }
+  return ok();
+}
+
+lcvq_status_t lcvq_timer_read(int32_t kernel, double *total_ms, int64_t *launches) {
+  if (kernel < 0 || kernel >= LCVQ_K_COUNT || total_ms == nullptr || launches == nullptr)
+    return fail(LCVQ_EINVAL, "timer_read(kernel=%d)", kernel);
+  std::vector<std::pair<hipEvent_t, hipEvent_t>> recs;
+  {
+    std::lock_guard<std::mutex> lock(g_timer.mu);
+    recs.swap(g_timer.rec[kernel]);
+  }
+  double tot = 0.0;
+  hipError_t err = hipSuccess;
+  for (auto &p : recs) {
+    float ms = 0.0f;
+    hipError_t e = hipEventSynchronize(p.second);
+    if (e == hipSuccess) e = hipEventElapsedTime(&ms, p.first, p.second);
+    if (e != hipSuccess && err == hipSuccess) err = e;
+    tot += ms;
+  }
+  {
+    std::lock_guard<std::mutex> lock(g_timer.mu);
+    for (auto &p : recs) {
+      g_timer.pool.push_back(p.first);
+      g_timer.pool.push_back(p.second);
+    }
+  }
+  *total_ms = tot;
+  *launches = (int64_t)recs.size();
+  return err == hipSuccess ? ok() : hip_fail(err, "timer events");
+}
+
 size_t lcvq_workspace_bytes(int32_t op, int64_t N, int64_t m, int64_t n, int32_t d, int32_t dtype) {
   if (N < 0 || m < 0 || n < 0 || (d != 4 && d != 8) || (dtype != LCVQ_F32 && dtype != LCVQ_BF16)) return 0;
   const bool bf16 = dtype == LCVQ_BF16;
@@ -144,7 +237,8 @@ lcvq_status_t lcvq_pack2bit(const void *src, int32_t src_kind, int32_t src_dtype
   if (m == 0 || n == 0) return ok();
   if (src == nullptr || packed == nullptr) return fail(LCVQ_EINVAL, "null pointer");
   if (!aligned16(src) || !aligned16(packed)) return fail(LCVQ_EALIGN, "src/packed must be 16-byte aligned");
-  hipError_t e = lcvq::launch_pack2bit(src, src_kind, src_dtype == LCVQ_BF16, m, n, packed, (hipStream_t)stream);
+  Timed tm(LCVQ_K_PACK, (hipStream_t)stream);
+  hipError_t e = tm.done(lcvq::launch_pack2bit(src, src_kind, src_dtype == LCVQ_BF16, m, n, packed, (hipStream_t)stream));
   return e == hipSuccess ? ok() : hip_fail(e, "pack2bit launch");
 }
 
@@ -161,8 +255,9 @@ lcvq_status_t lcvq_dequant(int64_t m, int64_t n, int32_t d, int32_t src_kind, in
   if (m == 0 || n == 0) return ok();
   if (src == nullptr || A == nullptr || b == nullptr || W_hat == nullptr) return fail(LCVQ_EINVAL, "null pointer");
   if (!aligned16(src) || !aligned16(W_hat)) return fail(LCVQ_EALIGN, "src/W_hat must be 16-byte aligned");
-  hipError_t e = lcvq::launch_dequant(src, src_kind, src_dtype == LCVQ_BF16, m, n, d, A, b, W_hat,
-                                      out_dtype == LCVQ_BF16, (hipStream_t)stream);
+  Timed tm(LCVQ_K_DEQUANT, (hipStream_t)stream);
+  hipError_t e = tm.done(lcvq::launch_dequant(src, src_kind, src_dtype == LCVQ_BF16, m, n, d, A, b, W_hat,
+                                              out_dtype == LCVQ_BF16, (hipStream_t)stream));
   return e == hipSuccess ? ok() : hip_fail(e, "dequant launch");
 }
 
@@ -198,19 +293,20 @@ lcvq_status_t lcvq_linear_fwd(int64_t N, int64_t m, int64_t n, int32_t d, int32_
   hipError_t e;
   if (bf16) {
     uint32_t *frag = (uint32_t *)(ws + L.frag);
-    e = lcvq::launch_quant_frag(Z, true, m, n, false, frag, packed_codes_out, st);
+    { Timed tm(LCVQ_K_QUANT, st); e = tm.done(lcvq::launch_quant_frag(Z, true, m, n, false, frag, packed_codes_out, st)); }
     if (e != hipSuccess) return hip_fail(e, "quantise launch");
-    e = lcvq::launch_act_transform(X, true, N, L.Np, n, d, A, b, ws + L.xp, L.ldp, svec, st);
+    { Timed tm(LCVQ_K_ACT, st); e = tm.done(lcvq::launch_act_transform(X, true, N, L.Np, n, d, A, b, ws + L.xp, L.ldp, svec, st)); }
     if (e != hipSuccess) return hip_fail(e, "activation transform launch");
-    e = lcvq::launch_fwd_bf16(frag, (const uint16_t *)(ws + L.xp), L.ldp, svec, (uint16_t *)Y, N, m, n, st);
+    { Timed tm(LCVQ_K_FWD, st); e = tm.done(lcvq::launch_fwd_bf16(frag, (const uint16_t *)(ws + L.xp), L.ldp, svec, (uint16_t *)Y, N, m, n, st)); }
     if (e != hipSuccess) return hip_fail(e, "forward product launch");
   } else {
-    e = lcvq::launch_act_transform(X, false, N, N, n, d, A, b, ws + L.xp, n, svec, st);
+    { Timed tm(LCVQ_K_ACT, st); e = tm.done(lcvq::launch_act_transform(X, false, N, N, n, d, A, b, ws + L.xp, n, svec, st)); }
     if (e != hipSuccess) return hip_fail(e, "activation transform launch");
-    e = lcvq::launch_fwd_f32((const float *)Z, (const float *)(ws + L.xp), svec, (float *)Y, N, m, n, st);
+    { Timed tm(LCVQ_K_FWD, st); e = tm.done(lcvq::launch_fwd_f32((const float *)Z, (const float *)(ws + L.xp), svec, (float *)Y, N, m, n, st)); }
     if (e != hipSuccess) return hip_fail(e, "forward product launch");
     if (packed_codes_out != nullptr) {
-      e = lcvq::launch_pack2bit(Z, LCVQ_SRC_LATENT, false, m, n, packed_codes_out, st);
+      Timed tm(LCVQ_K_PACK, st);
+      e = tm.done(lcvq::launch_pack2bit(Z, LCVQ_SRC_LATENT, false, m, n, packed_codes_out, st));
       if (e != hipSuccess) return hip_fail(e, "pack launch");
     }
   }
@@ -265,16 +361,18 @@ lcvq_status_t lcvq_linear_bwd(int64_t N, int64_t m, int64_t n, int32_t d, int32_
   float *zb = (want_map && !accumulate) ? db : nullptr;
 
   if (dX != nullptr) {
-    e = lcvq::launch_rowsum(dY, bf16, N, N, m, rs, zA, zb, d, st);
+    { Timed tm(LCVQ_K_ROWSUM, st); e = tm.done(lcvq::launch_rowsum(dY, bf16, N, N, m, rs, zA, zb, d, st)); }
     if (e != hipSuccess) return hip_fail(e, "row-sum launch");
     zA = zb = nullptr;  // cleared by the row-sum launch
     if (bf16) {
       uint32_t *frag = (uint32_t *)(ws + L.frag);
-      e = lcvq::launch_quant_frag(Z, true, m, n, true, frag, nullptr, st);
+      { Timed tm(LCVQ_K_QUANT_T, st); e = tm.done(lcvq::launch_quant_frag(Z, true, m, n, true, frag, nullptr, st)); }
       if (e != hipSuccess) return hip_fail(e, "quantise launch");
-      e = lcvq::launch_dx_bf16(frag, (const uint16_t *)dY, rs, A, b, d, (uint16_t *)dX, N, m, n, st);
+      Timed tm(LCVQ_K_DX, st);
+      e = tm.done(lcvq::launch_dx_bf16(frag, (const uint16_t *)dY, rs, A, b, d, (uint16_t *)dX, N, m, n, st));
     } else {
-      e = lcvq::launch_dx_f32((const float *)Z, (const float *)dY, rs, A, b, d, (float *)dX, N, m, n, st);
+      Timed tm(LCVQ_K_DX, st);
+      e = tm.done(lcvq::launch_dx_f32((const float *)Z, (const float *)dY, rs, A, b, d, (float *)dX, N, m, n, st));
     }
     if (e != hipSuccess) return hip_fail(e, "input-gradient launch");
   }
@@ -283,12 +381,14 @@ lcvq_status_t lcvq_linear_bwd(int64_t N, int64_t m, int64_t n, int32_t d, int32_
     if ((e = fill_zero(zb, (size_t)d * 4, st)) != hipSuccess) return hip_fail(e, "zero fill");
   }
   if (dZ != nullptr || want_map) {
+    Timed tm(LCVQ_K_DW, st);
     if (bf16)
       e = lcvq::launch_dz_bf16((const uint16_t *)X, (const uint16_t *)dY, (const uint16_t *)Z, A, d, mask_mode,
                                accumulate, dZ, dz_dtype == LCVQ_BF16, dA, db, N, m, n, st);
     else
       e = lcvq::launch_dz_f32((const float *)X, (const float *)dY, (const float *)Z, A, d, mask_mode, accumulate,
                               (float *)dZ, dA, db, N, m, n, st);
+    e = tm.done(e);
     if (e != hipSuccess) return hip_fail(e, "weight-gradient launch");
   }
   return ok();
