@@ -9,7 +9,7 @@
 #include <utility>
 #include <vector>
 
-#include "../../include/lcvq.h"
+#include "lcvq.h"
 #include "lcvq_prep.hpp"
 
 namespace {
@@ -43,15 +43,15 @@ struct FwdLayout {
   int64_t Np, ldp;
 };
 struct BwdLayout {
-  size_t rs, frag, total;
-  int64_t Np;
+  size_t rs, frag, xt, dyt, total;
 };
 
 FwdLayout fwd_layout(int64_t N, int64_t m, int64_t n, bool bf16) {
   FwdLayout L{};
   if (bf16) {
+    // K padded to an even number of 64-wide steps (the product loop takes two per trip)
     L.Np = lcvq::round_up(N, 256);
-    L.ldp = lcvq::round_up(n, 64);
+    L.ldp = lcvq::round_up(n, 128);
     const size_t xp = (size_t)L.Np * L.ldp * 2, s = (size_t)L.Np * 4;
     const size_t frag = (size_t)(lcvq::round_up(m, 256) / 32) * (L.ldp / 64) * 1024;
     L.xp = 0;
@@ -71,16 +71,19 @@ FwdLayout fwd_layout(int64_t N, int64_t m, int64_t n, bool bf16) {
 
 BwdLayout bwd_layout(int64_t N, int64_t m, int64_t n, bool bf16) {
   BwdLayout L{};
-  L.Np = N;
   L.rs = 0;
-  const size_t rs = up256((size_t)N * 4);
   if (bf16) {
-    const size_t frag = (size_t)(lcvq::round_up(n, 256) / 32) * (lcvq::round_up(m, 64) / 64) * 1024;
+    // per-token sums; codes in the input-gradient operand layout; X' and dY in
+    // the token-K fragment layout (tokens padded to 128, features to 256)
+    const size_t rs = up256((size_t)lcvq::round_up(N, 256) * 4);
+    const size_t frag = (size_t)(lcvq::round_up(n, 256) / 32) * (lcvq::round_up(m, 128) / 64) * 1024;
+    const size_t Nt = (size_t)lcvq::round_up(N, 128);
     L.frag = rs;
-    L.total = rs + up256(frag);
+    L.xt = L.frag + up256(frag);
+    L.dyt = L.xt + up256((size_t)lcvq::round_up(n, 256) * Nt * 2);
+    L.total = L.dyt + up256((size_t)lcvq::round_up(m, 256) * Nt * 2);
   } else {
-    L.frag = rs;
-    L.total = rs;
+    L.frag = L.xt = L.dyt = L.total = up256((size_t)N * 4);
   }
   return L;
 }
@@ -357,23 +360,52 @@ lcvq_status_t lcvq_linear_bwd(int64_t N, int64_t m, int64_t n, int32_t d, int32_
   char *ws = (char *)workspace;
   float *rs = (float *)(ws + L.rs);
   const bool want_map = dA != nullptr;
-  float *zA = (want_map && !accumulate) ? dA : nullptr;
-  float *zb = (want_map && !accumulate) ? db : nullptr;
+  const bool clear_map = want_map && !accumulate;
 
+  if (bf16) {
+    // 1. codes (input-gradient operand layout); its first block clears rs and,
+    //    when overwriting, dA/db, which later kernels accumulate into
+    // 2. X' = X blockdiag(A) and dY transposed into fragments, rs = row sums of dY
+    // 3. dX = (dY codes) A-map + rs b (+ dA, db)      4. dZ = mask * dY^T X'
+    const bool run_dx = dX != nullptr || want_map;
+    uint32_t *frag = (uint32_t *)(ws + L.frag);
+    uint16_t *xt = (uint16_t *)(ws + L.xt), *dyt = (uint16_t *)(ws + L.dyt);
+    if (run_dx) {
+      Timed tm(LCVQ_K_QUANT_T, st);
+      e = tm.done(lcvq::launch_quant_frag(Z, true, m, n, true, frag, nullptr, st, rs, lcvq::round_up(N, 256),
+                                          clear_map ? dA : nullptr, clear_map ? d * d : 0,
+                                          clear_map ? db : nullptr, clear_map ? d : 0));
+      if (e != hipSuccess) return hip_fail(e, "quantise launch");
+    }
+    {
+      Timed tm(LCVQ_K_ROWSUM, st);
+      e = tm.done(lcvq::launch_bwd_prep((const uint16_t *)X, (const uint16_t *)dY, A, d, N, m, n, xt, dyt, rs, st));
+      if (e != hipSuccess) return hip_fail(e, "backward operand launch");
+    }
+    if (run_dx) {
+      Timed tm(LCVQ_K_DX, st);
+      e = tm.done(lcvq::launch_dx_bf16(frag, (const uint16_t *)dY, rs, A, b, d, (uint16_t *)dX, (const uint16_t *)X,
+                                       dA, db, N, m, n, st));
+      if (e != hipSuccess) return hip_fail(e, "input-gradient launch");
+    }
+    if (dZ != nullptr) {
+      Timed tm(LCVQ_K_DW, st);
+      e = tm.done(lcvq::launch_dw_bf16(xt, dyt, (const uint16_t *)Z, mask_mode, accumulate, dZ,
+                                       dz_dtype == LCVQ_BF16, N, m, n, st));
+      if (e != hipSuccess) return hip_fail(e, "weight-gradient launch");
+    }
+    return ok();
+  }
+
+  // fp32 mode
+  float *zA = clear_map ? dA : nullptr;
+  float *zb = clear_map ? db : nullptr;
   if (dX != nullptr) {
-    { Timed tm(LCVQ_K_ROWSUM, st); e = tm.done(lcvq::launch_rowsum(dY, bf16, N, N, m, rs, zA, zb, d, st)); }
+    { Timed tm(LCVQ_K_ROWSUM, st); e = tm.done(lcvq::launch_rowsum(dY, false, N, N, m, rs, zA, zb, d, st)); }
     if (e != hipSuccess) return hip_fail(e, "row-sum launch");
     zA = zb = nullptr;  // cleared by the row-sum launch
-    if (bf16) {
-      uint32_t *frag = (uint32_t *)(ws + L.frag);
-      { Timed tm(LCVQ_K_QUANT_T, st); e = tm.done(lcvq::launch_quant_frag(Z, true, m, n, true, frag, nullptr, st)); }
-      if (e != hipSuccess) return hip_fail(e, "quantise launch");
-      Timed tm(LCVQ_K_DX, st);
-      e = tm.done(lcvq::launch_dx_bf16(frag, (const uint16_t *)dY, rs, A, b, d, (uint16_t *)dX, N, m, n, st));
-    } else {
-      Timed tm(LCVQ_K_DX, st);
-      e = tm.done(lcvq::launch_dx_f32((const float *)Z, (const float *)dY, rs, A, b, d, (float *)dX, N, m, n, st));
-    }
+    Timed tm(LCVQ_K_DX, st);
+    e = tm.done(lcvq::launch_dx_f32((const float *)Z, (const float *)dY, rs, A, b, d, (float *)dX, N, m, n, st));
     if (e != hipSuccess) return hip_fail(e, "input-gradient launch");
   }
   if (zA != nullptr) {
@@ -382,13 +414,8 @@ lcvq_status_t lcvq_linear_bwd(int64_t N, int64_t m, int64_t n, int32_t d, int32_
   }
   if (dZ != nullptr || want_map) {
     Timed tm(LCVQ_K_DW, st);
-    if (bf16)
-      e = lcvq::launch_dz_bf16((const uint16_t *)X, (const uint16_t *)dY, (const uint16_t *)Z, A, d, mask_mode,
-                               accumulate, dZ, dz_dtype == LCVQ_BF16, dA, db, N, m, n, st);
-    else
-      e = lcvq::launch_dz_f32((const float *)X, (const float *)dY, (const float *)Z, A, d, mask_mode, accumulate,
-                              (float *)dZ, dA, db, N, m, n, st);
-    e = tm.done(e);
+    e = tm.done(lcvq::launch_dz_f32((const float *)X, (const float *)dY, (const float *)Z, A, d, mask_mode, accumulate,
+                                    (float *)dZ, dA, db, N, m, n, st));
     if (e != hipSuccess) return hip_fail(e, "weight-gradient launch");
   }
   return ok();

@@ -30,8 +30,11 @@ __device__ __forceinline__ uint32_t f32_to_bf16(float f) {
   if ((u & 0x7fffffffu) > 0x7f800000u) return (u >> 16) | 0x40u;
   return (u + 0x7fffu + ((u >> 16) & 1u)) >> 16;
 }
+typedef float float2_t __attribute__((ext_vector_type(2)));
+// Two fp32 -> packed bf16 (round to nearest even, v_cvt_pk_bf16_f32).
 __device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
-  return f32_to_bf16(lo) | (f32_to_bf16(hi) << 16);
+  const float2_t f = {lo, hi};
+  return __builtin_bit_cast(uint32_t, __builtin_convertvector(f, bf16x2));
 }
 
 // ---- the quantiser of eq. quant_param ------------------------------------
@@ -62,6 +65,29 @@ __host__ __device__ __forceinline__ int perm32(int m) { return (m & 3) + 4 * (m 
 // Slabs are stored M-slab-major: slab (mb, kb) at byte ((mb * KB) + kb) * 1024.
 __device__ __forceinline__ uint32_t frag_dword_index(int mb, int kb, int KB, int lane, int kk) {
   return ((uint32_t)(mb * KB + kb) * 64u + (uint32_t)lane) * 4u + (uint32_t)kk;
+}
+
+// Activations in the B-operand layout of v_mfma_f32_32x32x16_bf16: a block of
+// 32 tokens x 64 K (4 KiB) holds, for K substep kk, 1 KiB in which lane L owns
+// the 16 bytes of token 32 tb + L % 32, K = 64 kb + 16 kk + 8 (L / 32) + 0..7.
+// Blocks are token-block-major: element index of (t, k) with KB K steps is
+// (((t / 32) * KB + k / 64) * 4 + (k % 64) / 16) * 512 + ((t % 32) + 32 ((k % 16) / 8)) * 8 + k % 8.
+__host__ __device__ __forceinline__ int64_t bfrag_index(int64_t t, int64_t k, int64_t KB) {
+  return (((t >> 5) * KB + (k >> 6)) * 4 + ((k & 63) >> 4)) * 512 + ((t & 31) + 32 * ((k & 15) >> 3)) * 8 + (k & 7);
+}
+
+// Inverse of perm32.
+__host__ __device__ __forceinline__ int perm32_inv(int m) { return (m & 3) + 4 * (m >> 4) + 8 * ((m >> 2) & 3); }
+
+// Token-K operand fragments of the weight-gradient product (features f on the
+// MFMA M or N axis, tokens t on K): block (f / 32, t / 64) holds 4 KiB; for
+// K substep kk (16 tokens) 1 KiB in which lane L owns the 16 bytes of feature
+// 32 (f / 32) + sel(L % 32), tokens 64 kb + 16 kk + 8 (L / 32) + 0..7, with
+// sel = perm32 on the M side (in-features) and the identity on the N side.
+// KBt = number of 64-token steps.  Returns the element index of (f, t).
+__host__ __device__ __forceinline__ int64_t tfrag_index(int64_t f, int64_t t, int64_t KBt, bool mside) {
+  const int l = mside ? perm32_inv((int)(f & 31)) : (int)(f & 31);
+  return (((f >> 5) * KBt + (t >> 6)) * 4 + ((t & 63) >> 4)) * 512 + (l + 32 * ((t & 15) >> 3)) * 8 + (t & 7);
 }
 
 // Eight 4-bit codes (0..3) -> eight exact bf16 values via the fp4 (e2m1)

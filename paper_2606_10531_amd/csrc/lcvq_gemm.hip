@@ -25,6 +25,17 @@ constexpr int kKStep = 64;   // K per main-loop step
 
 // s_waitcnt with every counter at zero.
 #define LCVQ_WAIT_ALL() __builtin_amdgcn_s_waitcnt(0)
+// s_waitcnt vmcnt(N) lgkmcnt(0) (gfx9 encoding; expcnt left at its maximum).
+#define LCVQ_WAIT_VM_LGKM0(N) __builtin_amdgcn_s_waitcnt(((N) & 15) | (((N) >> 4) << 14) | (7 << 4))
+// Workgroup barrier without the release fence of __syncthreads() (which would
+// drain the prefetch loads); the asm statements keep the compiler from moving
+// memory operations across it.  LDS visibility is ensured by the waits above.
+#define LCVQ_BARRIER()                   \
+  do {                                   \
+    asm volatile("" ::: "memory");       \
+    __builtin_amdgcn_s_barrier();        \
+    asm volatile("" ::: "memory");       \
+  } while (0)
 
 // Blocks are dispatched round-robin over the eight XCDs.  Give each XCD a
 // contiguous run of tile ids, and walk tiles in bands of four M-tiles, so the
@@ -43,369 +54,436 @@ __device__ __forceinline__ void tile_of_block(int tiles_m, int tiles_n, int &tm,
 }
 
 __device__ __forceinline__ float as_f(uint32_t u) { return __uint_as_float(u); }
+// Copy a (uniform) value into a vector register.
+__device__ __forceinline__ float to_vgpr(float x) {
+  float v;
+  asm volatile("v_mov_b32 %0, %1" : "=v"(v) : "s"(x));
+  return v;
+}
 __device__ __forceinline__ uint32_t as_u(float f) { return __float_as_uint(f); }
 
 // ============================================================================
 // Products with codes as the A operand (forward, input gradient).
-// B operand tile in LDS: 256 token rows x 64 K (bf16), 128 B per row; 16-byte
-// chunk q of row r lives at physical chunk q ^ ((r >> 1) & 7).
+// No LDS: wave w of a block owns the 256 weight-side rows x 64 tokens
+// [64 w, 64 w + 64) of the block tile and streams both operands straight into
+// registers: the codes of the block's eight 32-row slabs (operand layout; the
+// four waves share them through the L1) and its own activations, either in the
+// matrix-core B layout (forward: X' as written by the activation transform) or
+// row-major (input gradient: dY as the caller holds it).  K is padded to an
+// even number of 64-wide steps.
 // ============================================================================
 
-__device__ __forceinline__ uint32_t btile_off(int row, int chunk) {
-  return (uint32_t)(row * 128 + ((chunk ^ ((row >> 1) & 7)) << 4));
-}
-
-template <int kMode, int D, bool kMaskK>  // kMode 0: forward, 1: input gradient
+// Input-gradient mode also forms the map gradients from the same accumulator
+// P = dY codes: dA[j, k] = sum_{t,g} X[t, g*D + j] P[t, g*D + k] and
+// db[j] = sum_{t,g} X[t, g*D + j] rs[t] (the chain rule through X' = X blockdiag(A)
+// and s = X b~), reduced lanes -> wave -> block and added with one atomic per
+// block per entry.  X is N x Mvalid row-major; dA == nullptr skips this.
+template <int kMode, int D>  // kMode 0: forward (B = X' fragments), 1: input gradient (B = dY rows)
 __global__ __launch_bounds__(256, 1) void k_gemm_codes(
     const uint32_t *__restrict__ frag, int KB, const uint16_t *__restrict__ Bsrc, int ldb,
     int64_t brows, int kvalid, int tiles_m, int tiles_n, const float *__restrict__ vecT,
     const float *__restrict__ A, const float *__restrict__ bvec, uint16_t *__restrict__ out,
-    int64_t ldo, int64_t Mvalid, int64_t Tvalid) {
-  __shared__ __attribute__((aligned(1024))) char lds[2 * kTile * 128];  // two stages
-
+    int64_t ldo, int64_t Mvalid, int64_t Tvalid, const uint16_t *__restrict__ X,
+    float *__restrict__ dA, float *__restrict__ db) {
   const int tid = threadIdx.x, lane = tid & 63, h = lane >> 5;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
-  const int wm = wave >> 1, wn = wave & 1;
   int tm, tn;
   tile_of_block(tiles_m, tiles_n, tm, tn);
   const int64_t tok0 = (int64_t)tn * kTile;
+  const int64_t tw = tok0 + 64 * wave;  // this wave's first token
 
-  // B tile loads: instruction j of wave w fills rows 32 j + 8 w .. + 7; the
-  // lane part of the byte offset is fixed, the K step moves the buffer base.
-  const int brow0 = 8 * wave + (lane >> 3);
-  const int bchunk = (lane & 7) ^ ((brow0 >> 1) & 7);
-  const uint32_t boff0 = (uint32_t)(brow0 * ldb + bchunk * 8) * 2u;
-  const uint32_t bstep = (uint32_t)ldb * 64u;  // 32 rows
-  const uint16_t *Bt = Bsrc + tok0 * ldb;
-  const int64_t bbytes = (brows - tok0) * (int64_t)ldb * 2;
-
-  // codes: this wave's four 32-row slabs, 1 KiB per (slab, K step)
-  const uint32_t *fw = frag + (size_t)(tm * 8 + wm * 4) * KB * 256;
-  const __amdgpu_buffer_rsrc_t rsA = make_rsrc(fw, (int64_t)4 * KB * 1024);
-
-  // B fragment reads: row wn*128 + ni*32 + lane%32, logical chunk 2 kk + h
-  const int bx = ((lane & 31) >> 1) & 7;
-  const uint32_t brow = (uint32_t)(wn * 128 + (lane & 31)) * 128u;
-  uint32_t brd[4];
+  // codes: slabs tm * 8 + mi, 1 KiB per (slab, step), lane owns 16 bytes
+  const __amdgpu_buffer_rsrc_t rsA = make_rsrc(frag + (size_t)(tm * 8) * KB * 256, (int64_t)8 * KB * 1024);
+  // activations of tokens tw .. tw + 63
+  __amdgpu_buffer_rsrc_t rsB;
+  uint32_t boff[2][4];  // per (ni, kk): byte offset of this lane's 16 bytes at step 0
+  uint32_t kofs[4];     // per kk: this lane's K index at step 0 (input gradient K tail)
+  if constexpr (kMode == 0) {
+    rsB = make_rsrc(Bsrc + (tw >> 5) * (int64_t)KB * 2048, (int64_t)2 * KB * 4096);
 #pragma unroll
-  for (int kk = 0; kk < 4; ++kk) brd[kk] = brow + ((uint32_t)((2 * kk + h) ^ bx) << 4);
-
-  floatx16 acc[4][4];
+    for (int ni = 0; ni < 2; ++ni)
 #pragma unroll
-  for (int i = 0; i < 4; ++i)
-#pragma unroll
-    for (int j = 0; j < 4; ++j) acc[i][j] = floatx16{};
-
-  auto issue_b = [&](char *stage, int kb) {
-    const __amdgpu_buffer_rsrc_t rs = make_rsrc(Bt + kb * kKStep, bbytes - (int64_t)kb * 128);
-    uint32_t base = boff0;
-    if constexpr (kMaskK) base = (kb * kKStep + bchunk * 8 < kvalid) ? boff0 : kOffNone;
-#pragma unroll
-    for (int j = 0; j < 8; ++j)
-      buffer_to_lds16(rs, (lds_void *)(stage + (j * 4 + wave) * 1024), base + (uint32_t)j * bstep);
-  };
-  auto load_a = [&](u32x4 *dst, int kb) {
-#pragma unroll
-    for (int mi = 0; mi < 4; ++mi)
-      dst[mi] = __builtin_amdgcn_raw_buffer_load_b128(rsA, lane * 16, (mi * KB + kb) * 1024, 0);
-  };
-  auto compute = [&](const char *stage, const u32x4 *ca) {
+      for (int kk = 0; kk < 4; ++kk) boff[ni][kk] = (uint32_t)((ni * KB * 4 + kk) * 1024 + lane * 16);
+  } else {
+    rsB = make_rsrc(Bsrc + tw * ldb, (brows - tw) * (int64_t)ldb * 2);
 #pragma unroll
     for (int kk = 0; kk < 4; ++kk) {
-      bf16x8 a[4], b[4];
+      kofs[kk] = (uint32_t)(16 * kk + 8 * h);
 #pragma unroll
-      for (int ni = 0; ni < 4; ++ni) b[ni] = *reinterpret_cast<const bf16x8 *>(stage + brd[kk] + ni * 4096);
+      for (int ni = 0; ni < 2; ++ni) boff[ni][kk] = (uint32_t)(((32 * ni + (lane & 31)) * ldb + 16 * kk + 8 * h) * 2);
+    }
+  }
+
+  floatx16 acc[8][2];
 #pragma unroll
-      for (int mi = 0; mi < 4; ++mi) a[mi] = nibbles_to_bf16x8(ca[mi][kk]);
+  for (int i = 0; i < 8; ++i)
 #pragma unroll
-      for (int mi = 0; mi < 4; ++mi)
+    for (int j = 0; j < 2; ++j) acc[i][j] = floatx16{};
+
+  // Two register buffers of one 64-wide step each; the loads of step k + 2 are
+  // issued as soon as step k's MFMAs have been issued.  (Deeper prefetch with
+  // four 32-wide buffers measured slower.)
+  u32x4 ca[2][8], cb[2][2][4];
+  auto load = [&](int buf, int kb) {
+    const bool live = kb < KB;
 #pragma unroll
-        for (int ni = 0; ni < 4; ++ni)
-          acc[mi][ni] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[mi], b[ni], acc[mi][ni], 0, 0, 0);
+    for (int mi = 0; mi < 8; ++mi)
+      ca[buf][mi] = __builtin_amdgcn_raw_buffer_load_b128(rsA, live ? lane * 16 : (int)kOffNone,
+                                                          (mi * KB + kb) * 1024, 0);
+#pragma unroll
+    for (int ni = 0; ni < 2; ++ni)
+#pragma unroll
+      for (int kk = 0; kk < 4; ++kk) {
+        uint32_t off;
+        bool ok = live;
+        if constexpr (kMode == 0) {
+          off = boff[ni][kk] + (uint32_t)kb * 4096u;
+        } else {
+          off = (uint32_t)kb * 128u + boff[ni][kk];
+          ok = ok && (uint32_t)kb * 64u + kofs[kk] < (uint32_t)kvalid;
+        }
+        cb[buf][ni][kk] = __builtin_amdgcn_raw_buffer_load_b128(rsB, (int)(ok ? off : kOffNone), 0, 0);
+      }
+  };
+  auto compute = [&](int buf) {
+#pragma unroll
+    for (int kk = 0; kk < 4; ++kk) {
+      bf16x8 a[8];
+#pragma unroll
+      for (int mi = 0; mi < 8; ++mi) a[mi] = nibbles_to_bf16x8(ca[buf][mi][kk]);
+#pragma unroll
+      for (int mi = 0; mi < 8; ++mi)
+#pragma unroll
+        for (int ni = 0; ni < 2; ++ni)
+          acc[mi][ni] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
+              a[mi], __builtin_bit_cast(bf16x8, cb[buf][ni][kk]), acc[mi][ni], 0, 0, 0);
     }
   };
 
-  u32x4 ca[4], cn[4];
-  issue_b(lds, 0);
-  load_a(cn, 0);
-  for (int kb = 0; kb < KB; ++kb) {
-    LCVQ_WAIT_ALL();
-    __syncthreads();
-#pragma unroll
-    for (int mi = 0; mi < 4; ++mi) ca[mi] = cn[mi];
-    if (kb + 1 < KB) {
-      issue_b(lds + ((kb + 1) & 1) * (kTile * 128), kb + 1);
-      load_a(cn, kb + 1);
-    }
-    compute(lds + (kb & 1) * (kTile * 128), ca);
+  // The scheduling fences keep every load of buffer 0 ahead of every load of
+  // buffer 1, so the compiler can wait for one buffer while the other is still
+  // in flight (without them it sinks both groups to the end of the trip and
+  // waits for all loads before the next MFMA).
+  load(0, 0);
+  __builtin_amdgcn_sched_barrier(0);
+  load(1, 1);
+  __builtin_amdgcn_sched_barrier(0);
+  for (int kb = 0; kb < KB; kb += 2) {
+    compute(0);
+    __builtin_amdgcn_sched_barrier(0);
+    load(0, kb + 2);
+    __builtin_amdgcn_sched_barrier(0);
+    compute(1);
+    __builtin_amdgcn_sched_barrier(0);
+    load(1, kb + 3);
+    __builtin_amdgcn_sched_barrier(0);
   }
 
   // ---------------------------------------------------------------- epilogue
   // Lane L holds, for each (mi, ni), the 16 consecutive weight-side columns
   // cb .. cb + 15 of token row t.  Branch-free: rows beyond the tensor fall
   // outside the buffer (loads give 0, stores are dropped) and columns beyond it
-  // get an out-of-range offset.
-  const __amdgpu_buffer_rsrc_t ro = make_rsrc(out + tok0 * ldo, (Tvalid - tok0) * ldo * 2);
-  const __amdgpu_buffer_rsrc_t rv = make_rsrc(vecT + tok0, (Tvalid - tok0) * 4);
-  const int64_t cb0 = (int64_t)tm * kTile + wm * 128 + 16 * h;
-  float am[D][D], bm[D];
-  if constexpr (kMode == 1) {
+  // get an out-of-range offset.  Every load is issued before the first store:
+  // the store and load counters are shared, so a load behind stores would wait
+  // for all of them.
+  const __amdgpu_buffer_rsrc_t ro = make_rsrc(out + tw * ldo, out == nullptr ? 0 : (Tvalid - tw) * ldo * 2);
+  const __amdgpu_buffer_rsrc_t rv = make_rsrc(vecT + tw, (Tvalid - tw) * 4);
+  const int64_t cb0 = (int64_t)tm * kTile + 16 * h;
+  float vt[2];
 #pragma unroll
-    for (int j = 0; j < D; ++j) {
-      bm[j] = bvec[j];
+  for (int ni = 0; ni < 2; ++ni) vt[ni] = as_f(__builtin_amdgcn_raw_buffer_load_b32(rv, (ni * 32 + (lane & 31)) * 4, 0, 0));
+  if constexpr (kMode == 0) {
 #pragma unroll
-      for (int k = 0; k < D; ++k) am[j][k] = A[j * D + k];
+    for (int ni = 0; ni < 2; ++ni) {
+      const int tl = ni * 32 + (lane & 31);
+#pragma unroll
+      for (int mi = 0; mi < 8; ++mi)
+#pragma unroll
+        for (int half = 0; half < 2; ++half) {
+          const int64_t c = cb0 + mi * 32 + 8 * half;
+          const uint32_t off = c < Mvalid ? (uint32_t)(tl * ldo + c) * 2u : kOffNone;
+          u32x4 w;
+#pragma unroll
+          for (int e = 0; e < 4; ++e)
+            w[e] = pack_bf16x2(acc[mi][ni][8 * half + 2 * e] + vt[ni], acc[mi][ni][8 * half + 2 * e + 1] + vt[ni]);
+          __builtin_amdgcn_raw_buffer_store_b128(w, ro, off, 0, 0);
+        }
     }
-  }
-#pragma unroll
-  for (int ni = 0; ni < 4; ++ni) {
-    const int tl = wn * 128 + ni * 32 + (lane & 31);
-    const float vt = as_f(__builtin_amdgcn_raw_buffer_load_b32(rv, tl * 4, 0, 0));
-#pragma unroll
-    for (int mi = 0; mi < 4; ++mi) {
-      float y[16];
-      if constexpr (kMode == 0) {
-        // forward: Y[t, r] = D + s[t]
-#pragma unroll
-        for (int i = 0; i < 16; ++i) y[i] = acc[mi][ni][i] + vt;
-      } else {
-        // input gradient: dX[t, g*D + j] = sum_k A[j, k] P[t, g*D + k] + rs[t] b[j]
-#pragma unroll
-        for (int g = 0; g < 16 / D; ++g)
-#pragma unroll
-          for (int j = 0; j < D; ++j) {
-            float v = vt * bm[j];
-#pragma unroll
-            for (int k = 0; k < D; ++k) v = fmaf(am[j][k], acc[mi][ni][g * D + k], v);
-            y[g * D + j] = v;
-          }
-      }
+  } else {
+    const bool want_map = dA != nullptr;
+    // X[t, cb .. cb + 15] of (ni, mi) pair p = ni * 8 + mi, fetched two pairs
+    // ahead (three rotating 32-byte buffers)
+    const __amdgpu_buffer_rsrc_t rx = make_rsrc(X + tw * Mvalid, want_map ? (Tvalid - tw) * Mvalid * 2 : 0);
+    u32x4 xv[3][2];
+    auto xload = [&](int p) {
+      const int ni = p >> 3, mi = p & 7, tl = ni * 32 + (lane & 31);
 #pragma unroll
       for (int half = 0; half < 2; ++half) {
+        const int64_t c = cb0 + mi * 32 + 8 * half;
+        const uint32_t off = c < Mvalid ? (uint32_t)(tl * Mvalid + c) * 2u : kOffNone;
+        xv[p % 3][half] = __builtin_amdgcn_raw_buffer_load_b128(rx, off, 0, 0);
+      }
+    };
+    // the map in vector registers (in scalar ones it would not fit beside the
+    // buffer descriptors and would spill)
+    float am[D][D], bm[D], gA[D][D], gb[D];
+#pragma unroll
+    for (int j = 0; j < D; ++j) {
+      bm[j] = to_vgpr(bvec[j]);
+      gb[j] = 0.0f;
+#pragma unroll
+      for (int k = 0; k < D; ++k) {
+        am[j][k] = to_vgpr(A[j * D + k]);
+        gA[j][k] = 0.0f;
+      }
+    }
+    xload(0);
+    xload(1);
+#pragma unroll
+    for (int p = 0; p < 16; ++p) {
+      const int ni = p >> 3, mi = p & 7, tl = ni * 32 + (lane & 31);
+      if (p + 2 < 16) xload(p + 2);
+#pragma unroll
+      for (int half = 0; half < 2; ++half) {
+        float y[8], x[8];
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          x[2 * e] = bf16_lo(xv[p % 3][half][e]);
+          x[2 * e + 1] = bf16_hi(xv[p % 3][half][e]);
+        }
+#pragma unroll
+        for (int g = 0; g < 8 / D; ++g) {
+          float pv[D];
+#pragma unroll
+          for (int k = 0; k < D; ++k) pv[k] = acc[mi][ni][8 * half + g * D + k];
+#pragma unroll
+          for (int j = 0; j < D; ++j) {
+            float v = vt[ni] * bm[j];
+#pragma unroll
+            for (int k = 0; k < D; ++k) {
+              v = fmaf(am[j][k], pv[k], v);
+              gA[j][k] = fmaf(x[g * D + j], pv[k], gA[j][k]);
+            }
+            y[g * D + j] = v;
+            gb[j] = fmaf(x[g * D + j], vt[ni], gb[j]);
+          }
+        }
         const int64_t c = cb0 + mi * 32 + 8 * half;
         const uint32_t off = c < Mvalid ? (uint32_t)(tl * ldo + c) * 2u : kOffNone;
         u32x4 w;
 #pragma unroll
-        for (int e = 0; e < 4; ++e) w[e] = pack_bf16x2(y[8 * half + 2 * e], y[8 * half + 2 * e + 1]);
+        for (int e = 0; e < 4; ++e) w[e] = pack_bf16x2(y[2 * e], y[2 * e + 1]);
         __builtin_amdgcn_raw_buffer_store_b128(w, ro, off, 0, 0);
+      }
+    }
+    if (want_map) {
+      // lanes -> wave (shuffles), waves -> block (LDS), one atomic per entry
+      __shared__ float red[4][D * D + D];
+#pragma unroll
+      for (int j = 0; j < D; ++j) {
+#pragma unroll
+        for (int k = 0; k < D; ++k)
+#pragma unroll
+          for (int o = 32; o >= 1; o >>= 1) gA[j][k] += __shfl_xor(gA[j][k], o, 64);
+#pragma unroll
+        for (int o = 32; o >= 1; o >>= 1) gb[j] += __shfl_xor(gb[j], o, 64);
+      }
+      if (lane == 0) {
+#pragma unroll
+        for (int j = 0; j < D; ++j) {
+          red[wave][D * D + j] = gb[j];
+#pragma unroll
+          for (int k = 0; k < D; ++k) red[wave][j * D + k] = gA[j][k];
+        }
+      }
+      __syncthreads();
+      if (tid < D * D + D) {
+        const float v = red[0][tid] + red[1][tid] + red[2][tid] + red[3][tid];
+        if (tid < D * D) unsafeAtomicAdd(dA + tid, v);
+        else unsafeAtomicAdd(db + (tid - D * D), v);
       }
     }
   }
 }
 
 // ============================================================================
-// Weight-gradient product with the straight-through epilogue.
-// Both operands are K(token)-major in memory; tiles of 64 token rows x 256
-// columns (512 B per row) go to LDS, and ds_read_b64_tr_b16 hands each lane
-// eight consecutive tokens of one column.  16-byte chunk q of row t lives at
-// physical chunk q ^ (4 * (t & 3)).
+// Weight-gradient product with the straight-through epilogue:
+//   D[c, r] = sum_t X'[t, c] dY[t, r] = (dW blockdiag(A))[r, c],  dZ = mask * D
+// (X' = X blockdiag(A), so the map is already applied).  Both operands come
+// pre-transposed in the token-K fragment layout.  Wave w owns in-features
+// [64 w, 64 w + 64) of the block tile (two 32-row slabs, A operand, streamed
+// straight into registers) against all 256 out-features (eight 32-column
+// blocks, B operand, shared by the four waves through three LDS stages filled
+// by direct-to-LDS loads).
 // ============================================================================
 
-template <int D>
-__global__ __launch_bounds__(256, 1) void k_gemm_dz(
-    const uint16_t *__restrict__ X, const uint16_t *__restrict__ dY, const uint16_t *__restrict__ Z,
-    const float *__restrict__ A, int mask_mode, int accumulate, void *__restrict__ dZ, int dz_bf16,
-    float *__restrict__ dA, float *__restrict__ db, int64_t N, int m, int n, int tiles_m,
-    int tiles_n, int KB) {
-  // two stages, each an X tile then a dY tile of 64 token rows x 512 B
-  __shared__ __attribute__((aligned(1024))) char lds[4 * 64 * 512];
-  __shared__ float red[4][D * D + D];
+__global__ __launch_bounds__(256, 1) void k_gemm_dw(const uint16_t *__restrict__ xt, const uint16_t *__restrict__ dyt,
+                                                    int KBt, const uint16_t *__restrict__ Z, int mask_mode,
+                                                    int accumulate, void *__restrict__ dZ, int dz_bf16, int m, int n,
+                                                    int tiles_m, int tiles_n) {
+  constexpr int kStage = 32 * 1024;  // eight 4 KiB B blocks
+  __shared__ __attribute__((aligned(1024))) char lds[3 * kStage];
 
   const int tid = threadIdx.x, lane = tid & 63, h = lane >> 5;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
-  const int wm = wave >> 1, wn = wave & 1;
   int tm, tn;
   tile_of_block(tiles_m, tiles_n, tm, tn);
   const int c0 = tm * kTile, r0 = tn * kTile;
 
-  // tile loads: instruction j of wave w fills token rows 8 j + 2 w + {0, 1};
-  // columns outside the tensor get an out-of-range offset (zero fill).
-  const int lrow = 2 * wave + h;
-  const int lchunk = (lane & 31) ^ (4 * (lrow & 3));
-  const uint32_t xoff0 = c0 + lchunk * 8 < n ? (uint32_t)(lrow * n + lchunk * 8) * 2u : kOffNone;
-  const uint32_t yoff0 = r0 + lchunk * 8 < m ? (uint32_t)(lrow * m + lchunk * 8) * 2u : kOffNone;
-  const uint32_t xstep = (uint32_t)n * 16u, ystep = (uint32_t)m * 16u;  // 8 rows
+  // A: slabs tm * 8 + 2 * wave + mi; 4 KiB per (slab, step)
+  const __amdgpu_buffer_rsrc_t rsA =
+      make_rsrc(xt + (size_t)(tm * 8 + 2 * wave) * KBt * 2048, (int64_t)2 * KBt * 4096);
+  // B: blocks tn * 8 + j; wave w copies blocks 2w, 2w + 1 (4 KiB each per step)
+  const __amdgpu_buffer_rsrc_t rsB = make_rsrc(dyt + (size_t)(tn * 8) * KBt * 2048, (int64_t)8 * KBt * 4096);
 
-  // transposed fragment reads: per-lane offsets for the four 32-column blocks
-  const int g = lane >> 4, s = lane & 15;
-  const int trow = 8 * (g >> 1) + (s >> 2), tsw = 4 * (trow & 3);
-  // A operand rows follow perm32: source lane s of group g reads the four
-  // columns perm32(16 (g & 1) + 4 (s & 3)) .. + 3.
-  uint32_t ra[4], rb[4];
+  floatx16 acc[2][8];
 #pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    const int ca = wm * 128 + i * 32 + perm32(16 * (g & 1) + 4 * (s & 3));
-    const int cb = wn * 128 + i * 32 + 16 * (g & 1) + 4 * (s & 3);
-    ra[i] = (uint32_t)(trow * 512 + (((ca >> 3) ^ tsw) << 4) + (ca & 7) * 2);
-    rb[i] = (uint32_t)(trow * 512 + (((cb >> 3) ^ tsw) << 4) + (cb & 7) * 2);
-  }
+  for (int i = 0; i < 2; ++i)
+#pragma unroll
+    for (int j = 0; j < 8; ++j) acc[i][j] = floatx16{};
 
-  floatx16 acc[4][4];
+  auto issue = [&](int st, int kb, bool live) {  // 8 direct-to-LDS loads per wave
+    char *stage = lds + st * kStage;
 #pragma unroll
-  for (int i = 0; i < 4; ++i)
+    for (int j = 0; j < 2; ++j) {
+      const int blk = 2 * wave + j;
 #pragma unroll
-    for (int j = 0; j < 4; ++j) acc[i][j] = floatx16{};
-
-  auto issue = [&](char *sx, char *sy, int kb) {
-    const int64_t t0 = (int64_t)kb * 64;
-    const __amdgpu_buffer_rsrc_t rx = make_rsrc(X + t0 * n + c0, (N - t0) * n * 2 - (int64_t)c0 * 2);
-    const __amdgpu_buffer_rsrc_t ry = make_rsrc(dY + t0 * m + r0, (N - t0) * m * 2 - (int64_t)r0 * 2);
-#pragma unroll
-    for (int j = 0; j < 8; ++j) {
-      buffer_to_lds16(rx, (lds_void *)(sx + (j * 4 + wave) * 1024), xoff0 + (uint32_t)j * xstep);
-      buffer_to_lds16(ry, (lds_void *)(sy + (j * 4 + wave) * 1024), yoff0 + (uint32_t)j * ystep);
+      for (int kk = 0; kk < 4; ++kk) {
+        const uint32_t off = live ? (uint32_t)(((blk * KBt + kb) * 4 + kk) * 1024 + lane * 16) : kOffNone;
+        buffer_to_lds16(rsB, (lds_void *)(stage + (blk * 4 + kk) * 1024), off);
+      }
     }
   };
-  auto frag_tr = [&](const char *tile, uint32_t off) {
-    const bf16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4 *)(tile + off));
-    const bf16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4 *)(tile + off + 2048));
-    return (bf16x8)__builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
+  u32x4 ca[2][2][4];
+  auto load_a = [&](int buf, int kb, bool live) {  // 8 loads per wave
+#pragma unroll
+    for (int mi = 0; mi < 2; ++mi)
+#pragma unroll
+      for (int kk = 0; kk < 4; ++kk)
+        ca[buf][mi][kk] = __builtin_amdgcn_raw_buffer_load_b128(
+            rsA, live ? (int)(((mi * KBt + kb) * 4 + kk) * 1024 + lane * 16) : (int)kOffNone, 0, 0);
   };
-  auto compute = [&](const char *sx, const char *sy) {
+  auto compute = [&](int buf, int st) {
+    const char *stage = lds + st * kStage;
 #pragma unroll
     for (int kk = 0; kk < 4; ++kk) {
-      bf16x8 a[4], b[4];
+      bf16x8 b[8];
 #pragma unroll
-      for (int i = 0; i < 4; ++i) a[i] = frag_tr(sx + kk * 8192, ra[i]);
+      for (int ni = 0; ni < 8; ++ni) b[ni] = *reinterpret_cast<const bf16x8 *>(stage + (ni * 4 + kk) * 1024 + lane * 16);
 #pragma unroll
-      for (int i = 0; i < 4; ++i) b[i] = frag_tr(sy + kk * 8192, rb[i]);
+      for (int mi = 0; mi < 2; ++mi)
 #pragma unroll
-      for (int mi = 0; mi < 4; ++mi)
-#pragma unroll
-        for (int ni = 0; ni < 4; ++ni)
-          acc[mi][ni] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[mi], b[ni], acc[mi][ni], 0, 0, 0);
+        for (int ni = 0; ni < 8; ++ni)
+          acc[mi][ni] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, ca[buf][mi][kk]), b[ni],
+                                                               acc[mi][ni], 0, 0, 0);
     }
   };
 
-  constexpr int kStage = 2 * 64 * 512;
-  issue(lds, lds + 64 * 512, 0);
-  for (int kb = 0; kb < KB; ++kb) {
-    LCVQ_WAIT_ALL();
-    __syncthreads();
-    if (kb + 1 < KB) {
-      char *nx = lds + ((kb + 1) & 1) * kStage;
-      issue(nx, nx + 64 * 512, kb + 1);
+  // Issue order per step kb (fixed by the scheduling fences):
+  //   wait(B of kb) + barrier, B loads of kb + 2, MFMAs of kb, A loads of kb + 2.
+  // B of step kb was issued before the A loads of kb, the B loads of kb + 1 and
+  // the A loads of kb + 1: 24 later loads may still be in flight.
+  issue(0, 0, true);
+  load_a(0, 0, true);
+  __builtin_amdgcn_sched_barrier(0);
+  issue(1, 1, KBt > 1);
+  load_a(1, 1, KBt > 1);
+  __builtin_amdgcn_sched_barrier(0);
+  int st = 0;
+  for (int kb = 0; kb < KBt; kb += 2) {
+#pragma unroll
+    for (int u = 0; u < 2; ++u) {
+      const int k = kb + u;
+      const int st2 = st == 0 ? 2 : st - 1;  // (st + 2) % 3
+      LCVQ_WAIT_VM_LGKM0(16);
+      LCVQ_BARRIER();
+      __builtin_amdgcn_sched_barrier(0);
+      issue(st2, k + 2, k + 2 < KBt);
+      __builtin_amdgcn_sched_barrier(0);
+      compute(u, st);
+      __builtin_amdgcn_sched_barrier(0);
+      load_a(u, k + 2, k + 2 < KBt);
+      __builtin_amdgcn_sched_barrier(0);
+      st = st == 2 ? 0 : st + 1;
     }
-    const char *cx = lds + (kb & 1) * kStage;
-    compute(cx, cx + 64 * 512);
   }
+  LCVQ_WAIT_VM_LGKM0(0);
 
   // ------------------------------------------------ straight-through epilogue
-  // Lane L holds dW[r, cb .. cb + 15] for each (mi, ni): whole groups, so the
-  // map A (uniform, in scalar registers) applies lane-locally.
-  float am[D][D];
-#pragma unroll
-  for (int j = 0; j < D; ++j)
-#pragma unroll
-    for (int k = 0; k < D; ++k) am[j][k] = A[j * D + k];
-  float gA[D][D], gb[D];
-#pragma unroll
-  for (int j = 0; j < D; ++j) {
-    gb[j] = 0.0f;
-#pragma unroll
-    for (int k = 0; k < D; ++k) gA[j][k] = 0.0f;
-  }
-
-  // rows r >= m fall outside these buffers; columns c >= n get an out-of-range index
+  // Lane L holds D[c .. c + 15, r] for each (mi, ni): dZ[r, c .. c + 15] =
+  // mask * D.  Rows r >= m fall outside the buffers; columns c >= n get an
+  // out-of-range offset.  The latents (and old dZ) of the next block row are
+  // loaded before this one's stores: loads and stores share one counter.
   const __amdgpu_buffer_rsrc_t rz = make_rsrc(Z + (int64_t)r0 * n, (int64_t)(m - r0) * n * 2);
   const int es = dz_bf16 ? 2 : 4;
-  const __amdgpu_buffer_rsrc_t rg =
-      make_rsrc((char *)dZ + (int64_t)r0 * n * es, dZ == nullptr ? 0 : (int64_t)(m - r0) * n * es);
+  const __amdgpu_buffer_rsrc_t rg = make_rsrc((char *)dZ + (int64_t)r0 * n * es, (int64_t)(m - r0) * n * es);
+  u32x4 zv[2][2][2], ov[2][2][2][2];
+  auto eload = [&](int buf, int ni) {
+    const int rl = ni * 32 + (lane & 31);
 #pragma unroll
-  for (int ni = 0; ni < 4; ++ni) {
-    const int rl = wn * 128 + ni * 32 + (lane & 31);
-#pragma unroll
-    for (int mi = 0; mi < 4; ++mi)
+    for (int mi = 0; mi < 2; ++mi)
 #pragma unroll
       for (int half = 0; half < 2; ++half) {
-        const int c = c0 + wm * 128 + mi * 32 + 16 * h + 8 * half;
+        const int c = c0 + 64 * wave + 32 * mi + 16 * h + 8 * half;
         const bool cv = c < n;
-        const uint32_t e2 = cv ? (uint32_t)(rl * n + c) * 2u : kOffNone;  // byte offsets, bf16
-        const uint32_t e4 = cv ? (uint32_t)(rl * n + c) * 4u : kOffNone;  // and fp32
-        const u32x4 zw = __builtin_amdgcn_raw_buffer_load_b128(rz, e2, 0, 0);
-        float z[8];
-#pragma unroll
-        for (int e = 0; e < 4; ++e) {
-          z[2 * e] = bf16_lo(zw[e]);
-          z[2 * e + 1] = bf16_hi(zw[e]);
+        const uint32_t e = (uint32_t)(rl * n + c);
+        zv[buf][mi][half] = __builtin_amdgcn_raw_buffer_load_b128(rz, cv ? e * 2u : kOffNone, 0, 0);
+        if (accumulate) {
+          if (dz_bf16) {
+            ov[buf][mi][half][0] = __builtin_amdgcn_raw_buffer_load_b128(rg, cv ? e * 2u : kOffNone, 0, 0);
+          } else {
+            ov[buf][mi][half][0] = __builtin_amdgcn_raw_buffer_load_b128(rg, cv ? e * 4u : kOffNone, 0, 0);
+            ov[buf][mi][half][1] = __builtin_amdgcn_raw_buffer_load_b128(rg, cv ? e * 4u + 16u : kOffNone, 0, 0);
+          }
         }
-        float gz[8];
+      }
+  };
+  eload(0, 0);
 #pragma unroll
-        for (int g = 0; g < 8 / D; ++g) {
-          float w[D], code[D];
+  for (int ni = 0; ni < 8; ++ni) {
+    const int buf = ni & 1;
+    if (ni + 1 < 8) eload(buf ^ 1, ni + 1);
+    const int rl = ni * 32 + (lane & 31);
 #pragma unroll
-          for (int j = 0; j < D; ++j) {
-            w[j] = acc[mi][ni][8 * half + g * D + j];
-            code[j] = (float)quant_code(z[g * D + j]);
-            gb[j] += w[j];
-          }
+    for (int mi = 0; mi < 2; ++mi)
 #pragma unroll
-          for (int k = 0; k < D; ++k) {
-            float v = 0.0f;
+      for (int half = 0; half < 2; ++half) {
+        const int c = c0 + 64 * wave + 32 * mi + 16 * h + 8 * half;
+        const bool cv = c < n;
+        const uint32_t e = (uint32_t)(rl * n + c);
+        float g[8];
 #pragma unroll
-            for (int j = 0; j < D; ++j) {
-              v = fmaf(w[j], am[j][k], v);
-              gA[j][k] = fmaf(w[j], code[k], gA[j][k]);
-            }
-            gz[g * D + k] = ste_pass(z[g * D + k], mask_mode) ? v : 0.0f;
-          }
+        for (int q = 0; q < 4; ++q) {
+          const uint32_t zw = zv[buf][mi][half][q];
+          g[2 * q] = ste_pass(bf16_lo(zw), mask_mode) ? acc[mi][ni][8 * half + 2 * q] : 0.0f;
+          g[2 * q + 1] = ste_pass(bf16_hi(zw), mask_mode) ? acc[mi][ni][8 * half + 2 * q + 1] : 0.0f;
         }
         if (dz_bf16) {
           if (accumulate) {
-            const u32x4 o = __builtin_amdgcn_raw_buffer_load_b128(rg, e2, 0, 0);
 #pragma unroll
-            for (int e = 0; e < 4; ++e) {
-              gz[2 * e] += bf16_lo(o[e]);
-              gz[2 * e + 1] += bf16_hi(o[e]);
+            for (int q = 0; q < 4; ++q) {
+              g[2 * q] += bf16_lo(ov[buf][mi][half][0][q]);
+              g[2 * q + 1] += bf16_hi(ov[buf][mi][half][0][q]);
             }
           }
-          u32x4 wv;
+          u32x4 w;
 #pragma unroll
-          for (int e = 0; e < 4; ++e) wv[e] = pack_bf16x2(gz[2 * e], gz[2 * e + 1]);
-          __builtin_amdgcn_raw_buffer_store_b128(wv, rg, e2, 0, 0);
+          for (int q = 0; q < 4; ++q) w[q] = pack_bf16x2(g[2 * q], g[2 * q + 1]);
+          __builtin_amdgcn_raw_buffer_store_b128(w, rg, cv ? e * 2u : kOffNone, 0, 0);
         } else {
 #pragma unroll
-          for (int q = 0; q < 2; ++q) {
-            u32x4 wv;
-            if (accumulate) {
-              const u32x4 o = __builtin_amdgcn_raw_buffer_load_b128(rg, e4 + 16u * q, 0, 0);
+          for (int p = 0; p < 2; ++p) {
+            u32x4 w;
 #pragma unroll
-              for (int e = 0; e < 4; ++e) gz[4 * q + e] += as_f(o[e]);
+            for (int q = 0; q < 4; ++q) {
+              float v = g[4 * p + q];
+              if (accumulate) v += as_f(ov[buf][mi][half][p][q]);
+              w[q] = as_u(v);
             }
-#pragma unroll
-            for (int e = 0; e < 4; ++e) wv[e] = as_u(gz[4 * q + e]);
-            __builtin_amdgcn_raw_buffer_store_b128(wv, rg, e4 + 16u * q, 0, 0);
+            __builtin_amdgcn_raw_buffer_store_b128(w, rg, cv ? e * 4u + 16u * p : kOffNone, 0, 0);
           }
         }
-        // keep the scheduler from hoisting every block's loads (register pressure)
-        __builtin_amdgcn_sched_barrier(0);
       }
-  }
-
-  // reduce the map gradients: lanes -> wave (shuffles), waves -> block (LDS),
-  // then one atomic per block per entry.
-#pragma unroll
-  for (int j = 0; j < D; ++j) {
-#pragma unroll
-    for (int k = 0; k < D; ++k)
-#pragma unroll
-      for (int o = 32; o >= 1; o >>= 1) gA[j][k] += __shfl_xor(gA[j][k], o, 64);
-#pragma unroll
-    for (int o = 32; o >= 1; o >>= 1) gb[j] += __shfl_xor(gb[j], o, 64);
-  }
-  if (lane == 0) {
-#pragma unroll
-    for (int j = 0; j < D; ++j) {
-      red[wave][D * D + j] = gb[j];
-#pragma unroll
-      for (int k = 0; k < D; ++k) red[wave][j * D + k] = gA[j][k];
-    }
-  }
-  __syncthreads();
-  if (tid < D * D + D) {
-    const float v = red[0][tid] + red[1][tid] + red[2][tid] + red[3][tid];
-    if (tid < D * D) unsafeAtomicAdd(dA + tid, v);
-    else unsafeAtomicAdd(db + (tid - D * D), v);
   }
 }
 
@@ -415,38 +493,34 @@ hipError_t launch_fwd_bf16(const uint32_t *frag, const uint16_t *Xp, int64_t ldp
                            uint16_t *Y, int64_t N, int64_t m, int64_t n, hipStream_t st) {
   (void)n;
   const int tiles_m = (int)ceil_div(m, kTile), tiles_n = (int)ceil_div(N, kTile);
-  const int KB = (int)(ldp / kKStep);
+  const int KB = (int)(ldp / kKStep);  // even: ldp is a multiple of 128
   const int64_t Np = (int64_t)tiles_n * kTile;
-  k_gemm_codes<0, 8, false><<<tiles_m * tiles_n, 256, 0, st>>>(frag, KB, Xp, (int)ldp, Np, (int)ldp, tiles_m,
-                                                               tiles_n, s, nullptr, nullptr, Y, m, m, N);
+  k_gemm_codes<0, 8><<<tiles_m * tiles_n, 256, 0, st>>>(frag, KB, Xp, (int)ldp, Np, (int)ldp, tiles_m, tiles_n, s,
+                                                        nullptr, nullptr, Y, m, m, N, nullptr, nullptr, nullptr);
   return hipGetLastError();
 }
 
 hipError_t launch_dx_bf16(const uint32_t *frag, const uint16_t *dY, const float *rs, const float *A,
-                          const float *b, int d, uint16_t *dX, int64_t N, int64_t m, int64_t n,
-                          hipStream_t st) {
+                          const float *b, int d, uint16_t *dX, const uint16_t *X, float *dA, float *db, int64_t N,
+                          int64_t m, int64_t n, hipStream_t st) {
   const int tiles_m = (int)ceil_div(n, kTile), tiles_n = (int)ceil_div(N, kTile);
-  const int KB = (int)ceil_div(m, kKStep);
+  const int KB = (int)(round_up(m, 128) / kKStep);  // even, matches the operand layout
+  // dX == nullptr: the product still runs for dA/db; its stores are dropped.
   if (d == 8)
-    k_gemm_codes<1, 8, true><<<tiles_m * tiles_n, 256, 0, st>>>(frag, KB, dY, (int)m, N, (int)m, tiles_m,
-                                                                tiles_n, rs, A, b, dX, n, n, N);
+    k_gemm_codes<1, 8><<<tiles_m * tiles_n, 256, 0, st>>>(frag, KB, dY, (int)m, N, (int)m, tiles_m, tiles_n, rs, A,
+                                                          b, dX, n, n, N, X, dA, db);
   else
-    k_gemm_codes<1, 4, true><<<tiles_m * tiles_n, 256, 0, st>>>(frag, KB, dY, (int)m, N, (int)m, tiles_m,
-                                                                tiles_n, rs, A, b, dX, n, n, N);
+    k_gemm_codes<1, 4><<<tiles_m * tiles_n, 256, 0, st>>>(frag, KB, dY, (int)m, N, (int)m, tiles_m, tiles_n, rs, A,
+                                                          b, dX, n, n, N, X, dA, db);
   return hipGetLastError();
 }
 
-hipError_t launch_dz_bf16(const uint16_t *X, const uint16_t *dY, const uint16_t *Z, const float *A, int d,
-                          int mask_mode, int accumulate, void *dZ, bool dz_bf16, float *dA, float *db,
-                          int64_t N, int64_t m, int64_t n, hipStream_t st) {
+hipError_t launch_dw_bf16(const uint16_t *xt, const uint16_t *dyt, const uint16_t *Z, int mask_mode, int accumulate,
+                          void *dZ, bool dz_bf16, int64_t N, int64_t m, int64_t n, hipStream_t st) {
   const int tiles_m = (int)ceil_div(n, kTile), tiles_n = (int)ceil_div(m, kTile);
-  const int KB = (int)ceil_div(N, 64);
-  if (d == 8)
-    k_gemm_dz<8><<<tiles_m * tiles_n, 256, 0, st>>>(X, dY, Z, A, mask_mode, accumulate, dZ, dz_bf16 ? 1 : 0,
-                                                    dA, db, N, (int)m, (int)n, tiles_m, tiles_n, KB);
-  else
-    k_gemm_dz<4><<<tiles_m * tiles_n, 256, 0, st>>>(X, dY, Z, A, mask_mode, accumulate, dZ, dz_bf16 ? 1 : 0,
-                                                    dA, db, N, (int)m, (int)n, tiles_m, tiles_n, KB);
+  const int KBt = (int)(round_up(N, 128) / 64);  // even
+  k_gemm_dw<<<tiles_m * tiles_n, 256, 0, st>>>(xt, dyt, KBt, Z, mask_mode, accumulate, dZ, dz_bf16 ? 1 : 0, (int)m,
+                                               (int)n, tiles_m, tiles_n);
   return hipGetLastError();
 }
 

@@ -70,12 +70,21 @@ __device__ __forceinline__ float block_sum256(float v, float *red /* >= 4 floats
 // One block per 64 x 64 tile of Z (rows r, columns c).  kTrans = false: the
 // operand's M axis is r and its K axis c (forward product); kTrans = true: M is
 // c and K is r (input-gradient product).  Tiles beyond Z hold code 0.
+// The first block also clears up to three float buffers, used by the backward
+// for the per-token sums and the map gradients that later kernels accumulate into.
 template <typename ZT, bool kTrans>
 __global__ __launch_bounds__(256) void k_quant_frag(const ZT *__restrict__ Z, int64_t m, int64_t n,
                                                      uint32_t *__restrict__ frag, int KB,
-                                                     uint8_t *__restrict__ packed) {
+                                                     uint8_t *__restrict__ packed, float *__restrict__ zero,
+                                                     int64_t nz, float *__restrict__ zero2, int nz2,
+                                                     float *__restrict__ zero3, int nz3) {
   __shared__ uint8_t codes[64][64 + 4];
   const int tid = threadIdx.x;
+  if (blockIdx.x == 0 && blockIdx.y == 0) {
+    for (int64_t i = tid; i < nz; i += 256) zero[i] = 0.0f;
+    for (int i = tid; i < nz2; i += 256) zero2[i] = 0.0f;
+    for (int i = tid; i < nz3; i += 256) zero3[i] = 0.0f;
+  }
   const int64_t r0 = (int64_t)blockIdx.y * 64, c0 = (int64_t)blockIdx.x * 64;
 #pragma unroll
   for (int i = 0; i < 2; ++i) {
@@ -130,7 +139,9 @@ __global__ __launch_bounds__(256) void k_quant_frag(const ZT *__restrict__ Z, in
 // One block per (padded) token row: X'[t, g*D + k] = sum_j X[t, g*D + j] A[j, k]
 // and s[t] = sum_c X[t, c] b[c % D].  Rows t >= N and columns >= n of X' are
 // written as zero.
-template <typename XT, typename OT, int D>
+// kFrag: X' goes to the matrix-core B-operand layout (bfrag_index, ldp / 64 K
+// steps) instead of row-major with row length ldp.
+template <typename XT, typename OT, int D, bool kFrag>
 __global__ __launch_bounds__(256) void k_act_transform(const XT *__restrict__ X, int64_t N, int64_t n,
                                                         const float *__restrict__ A,
                                                         const float *__restrict__ b,
@@ -164,7 +175,8 @@ __global__ __launch_bounds__(256) void k_act_transform(const XT *__restrict__ X,
     }
 #pragma unroll
     for (int j = 0; j < D; ++j) acc_s = fmaf(x[j], bb[j], acc_s);
-    storeD<D>(Xp + t * ldp + g * D, y);
+    if constexpr (kFrag) storeD<D>(Xp + bfrag_index(t, g * D, ldp / 64), y);
+    else storeD<D>(Xp + t * ldp + g * D, y);
   }
   const float tot = block_sum256(acc_s, red);
   if (threadIdx.x == 0) s[t] = tot;
@@ -299,6 +311,84 @@ __global__ __launch_bounds__(256) void k_dequant(const void *__restrict__ src, i
   }
 }
 
+// ---- backward operands of the weight-gradient product ----------------------
+// One block per 64 tokens x 64 features of either X (blockIdx.y < nfx) or dY.
+// X rows become X' = X blockdiag(A) (so the product yields dW blockdiag(A)
+// directly); both are written transposed into the token-K fragment layout
+// (X' on the M side, dY on the N side), zero-padded to KBt steps and to whole
+// 256-feature tiles.  dY rows are also summed into rs[t] (atomics; rs cleared
+// beforehand).
+template <int D>
+__global__ __launch_bounds__(256) void k_bwd_prep(const uint16_t *__restrict__ X, const uint16_t *__restrict__ dY,
+                                                   const float *__restrict__ A, int64_t N, int64_t n, int64_t m,
+                                                   int KBt, int nfx, uint16_t *__restrict__ xt,
+                                                   uint16_t *__restrict__ dyt, float *__restrict__ rs) {
+  __shared__ __attribute__((aligned(16))) uint16_t tile[64][64 + 8];
+  const int tid = threadIdx.x;
+  const bool isx = (int)blockIdx.y < nfx;
+  const int64_t t0 = (int64_t)blockIdx.x * 64;
+  const int64_t f0 = (int64_t)(isx ? blockIdx.y : blockIdx.y - nfx) * 64;
+  const int64_t F = isx ? n : m;
+  const uint16_t *src = isx ? X : dY;
+  float a[D][D];
+#pragma unroll
+  for (int j = 0; j < D; ++j)
+#pragma unroll
+    for (int k = 0; k < D; ++k) a[j][k] = A[j * D + k];
+#pragma unroll
+  for (int i = 0; i < 2; ++i) {
+    const int id = tid + 256 * i, row = id >> 3, ch = id & 7;
+    const int64_t t = t0 + row, f = f0 + ch * 8;
+    float v[8];
+    if (t < N && f < F) {
+      load8(src + t * F + f, v);
+    } else {
+#pragma unroll
+      for (int e = 0; e < 8; ++e) v[e] = 0.0f;
+    }
+    float o[8];
+    if (isx) {
+#pragma unroll
+      for (int g = 0; g < 8 / D; ++g)
+#pragma unroll
+        for (int k = 0; k < D; ++k) {
+          float y = 0.0f;
+#pragma unroll
+          for (int j = 0; j < D; ++j) y = fmaf(v[g * D + j], a[j][k], y);
+          o[g * D + k] = y;
+        }
+    } else {
+#pragma unroll
+      for (int e = 0; e < 8; ++e) o[e] = v[e];
+      // row sum over this chunk, then over the row's eight chunks (lanes id .. id + 7)
+      float sum = 0.0f;
+#pragma unroll
+      for (int e = 0; e < 8; ++e) sum += v[e];
+      sum += __shfl_xor(sum, 1, 64);
+      sum += __shfl_xor(sum, 2, 64);
+      sum += __shfl_xor(sum, 4, 64);
+      if (ch == 0 && t < N) unsafeAtomicAdd(rs + t, sum);
+    }
+    u32x4 w;
+#pragma unroll
+    for (int e = 0; e < 4; ++e) w[e] = pack_bf16x2(o[2 * e], o[2 * e + 1]);
+    *reinterpret_cast<u32x4 *>(&tile[row][ch * 8]) = w;
+  }
+  __syncthreads();
+  uint16_t *dst = isx ? xt : dyt;
+#pragma unroll
+  for (int i = 0; i < 2; ++i) {
+    const int id = tid + 256 * i, fb = id >> 8, kk = (id >> 6) & 3, L = id & 63;
+    const int fl = fb * 32 + (isx ? perm32(L & 31) : (L & 31));
+    const int tl = kk * 16 + 8 * (L >> 5);
+    u32x4 w;
+#pragma unroll
+    for (int e = 0; e < 4; ++e) w[e] = (uint32_t)tile[tl + 2 * e][fl] | ((uint32_t)tile[tl + 2 * e + 1][fl] << 16);
+    const int64_t blk = (f0 >> 5) + fb;
+    *reinterpret_cast<u32x4 *>(dst + (((blk * KBt + (t0 >> 6)) * 4 + kk) * 64 + L) * 8) = w;
+  }
+}
+
 // ---- launchers -------------------------------------------------------------
 
 static inline int grid_for(int64_t items, int64_t per_block) {
@@ -308,17 +398,18 @@ static inline int grid_for(int64_t items, int64_t per_block) {
 }
 
 hipError_t launch_quant_frag(const void *Z, bool z_bf16, int64_t m, int64_t n, bool trans,
-                             uint32_t *frag, uint8_t *packed, hipStream_t st) {
+                             uint32_t *frag, uint8_t *packed, hipStream_t st, float *zero, int64_t nz,
+                             float *zero2, int nz2, float *zero3, int nz3) {
   // forward: M = r padded to 256, K = c padded to 64; transposed: M = c, K = r
-  const int64_t Mp = round_up(trans ? n : m, 256), Kp = round_up(trans ? m : n, 64);
+  const int64_t Mp = round_up(trans ? n : m, 256), Kp = round_up(trans ? m : n, 128);
   const int KB = (int)(Kp / 64);
   dim3 grid(trans ? (unsigned)(Mp / 64) : (unsigned)(Kp / 64), trans ? (unsigned)(Kp / 64) : (unsigned)(Mp / 64));
   if (z_bf16) {
-    if (trans) k_quant_frag<uint16_t, true><<<grid, 256, 0, st>>>((const uint16_t *)Z, m, n, frag, KB, nullptr);
-    else k_quant_frag<uint16_t, false><<<grid, 256, 0, st>>>((const uint16_t *)Z, m, n, frag, KB, packed);
+    if (trans) k_quant_frag<uint16_t, true><<<grid, 256, 0, st>>>((const uint16_t *)Z, m, n, frag, KB, nullptr, zero, nz, zero2, nz2, zero3, nz3);
+    else k_quant_frag<uint16_t, false><<<grid, 256, 0, st>>>((const uint16_t *)Z, m, n, frag, KB, packed, zero, nz, zero2, nz2, zero3, nz3);
   } else {
-    if (trans) k_quant_frag<float, true><<<grid, 256, 0, st>>>((const float *)Z, m, n, frag, KB, nullptr);
-    else k_quant_frag<float, false><<<grid, 256, 0, st>>>((const float *)Z, m, n, frag, KB, packed);
+    if (trans) k_quant_frag<float, true><<<grid, 256, 0, st>>>((const float *)Z, m, n, frag, KB, nullptr, zero, nz, zero2, nz2, zero3, nz3);
+    else k_quant_frag<float, false><<<grid, 256, 0, st>>>((const float *)Z, m, n, frag, KB, packed, zero, nz, zero2, nz2, zero3, nz3);
   }
   return hipGetLastError();
 }
@@ -327,12 +418,12 @@ hipError_t launch_act_transform(const void *X, bool bf16, int64_t N, int64_t Np,
                                 const float *A, const float *b, void *Xp, int64_t ldp, float *s,
                                 hipStream_t st) {
   dim3 grid((unsigned)Np);
-  if (bf16) {
-    if (d == 8) k_act_transform<uint16_t, uint16_t, 8><<<grid, 256, 0, st>>>((const uint16_t *)X, N, n, A, b, (uint16_t *)Xp, ldp, s);
-    else k_act_transform<uint16_t, uint16_t, 4><<<grid, 256, 0, st>>>((const uint16_t *)X, N, n, A, b, (uint16_t *)Xp, ldp, s);
-  } else {
-    if (d == 8) k_act_transform<float, float, 8><<<grid, 256, 0, st>>>((const float *)X, N, n, A, b, (float *)Xp, ldp, s);
-    else k_act_transform<float, float, 4><<<grid, 256, 0, st>>>((const float *)X, N, n, A, b, (float *)Xp, ldp, s);
+  if (bf16) {  // matrix-core layout
+    if (d == 8) k_act_transform<uint16_t, uint16_t, 8, true><<<grid, 256, 0, st>>>((const uint16_t *)X, N, n, A, b, (uint16_t *)Xp, ldp, s);
+    else k_act_transform<uint16_t, uint16_t, 4, true><<<grid, 256, 0, st>>>((const uint16_t *)X, N, n, A, b, (uint16_t *)Xp, ldp, s);
+  } else {  // row-major
+    if (d == 8) k_act_transform<float, float, 8, false><<<grid, 256, 0, st>>>((const float *)X, N, n, A, b, (float *)Xp, ldp, s);
+    else k_act_transform<float, float, 4, false><<<grid, 256, 0, st>>>((const float *)X, N, n, A, b, (float *)Xp, ldp, s);
   }
   return hipGetLastError();
 }
@@ -388,4 +479,16 @@ hipError_t launch_dequant(const void *src, int kind, bool z_bf16, int64_t m, int
   return hipGetLastError();
 }
 
+}  // namespace lcvq
+
+namespace lcvq {
+hipError_t launch_bwd_prep(const uint16_t *X, const uint16_t *dY, const float *A, int d, int64_t N, int64_t m,
+                           int64_t n, uint16_t *xt, uint16_t *dyt, float *rs, hipStream_t st) {
+  const int KBt = (int)(round_up(N, 128) / 64);
+  const int nfx = (int)(round_up(n, 256) / 64), nfy = (int)(round_up(m, 256) / 64);
+  dim3 grid((unsigned)KBt, (unsigned)(nfx + nfy));
+  if (d == 8) k_bwd_prep<8><<<grid, 256, 0, st>>>(X, dY, A, N, n, m, KBt, nfx, xt, dyt, rs);
+  else k_bwd_prep<4><<<grid, 256, 0, st>>>(X, dY, A, N, n, m, KBt, nfx, xt, dyt, rs);
+  return hipGetLastError();
+}
 }  // namespace lcvq

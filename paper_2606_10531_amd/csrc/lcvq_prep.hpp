@@ -7,7 +7,11 @@ namespace lcvq {
 
 // streaming kernels (lcvq_prep.hip)
 hipError_t launch_quant_frag(const void *Z, bool z_bf16, int64_t m, int64_t n, bool trans,
-                             uint32_t *frag, uint8_t *packed, hipStream_t st);
+                             uint32_t *frag, uint8_t *packed, hipStream_t st, float *zero = nullptr,
+                             int64_t nz = 0, float *zero2 = nullptr, int nz2 = 0, float *zero3 = nullptr,
+                             int nz3 = 0);
+hipError_t launch_bwd_prep(const uint16_t *X, const uint16_t *dY, const float *A, int d, int64_t N, int64_t m,
+                           int64_t n, uint16_t *xt, uint16_t *dyt, float *rs, hipStream_t st);
 hipError_t launch_act_transform(const void *X, bool bf16, int64_t N, int64_t Np, int64_t n, int d,
                                 const float *A, const float *b, void *Xp, int64_t ldp, float *s,
                                 hipStream_t st);
@@ -22,11 +26,10 @@ hipError_t launch_dequant(const void *src, int kind, bool z_bf16, int64_t m, int
 hipError_t launch_fwd_bf16(const uint32_t *frag, const uint16_t *Xp, int64_t ldp, const float *s,
                            uint16_t *Y, int64_t N, int64_t m, int64_t n, hipStream_t st);
 hipError_t launch_dx_bf16(const uint32_t *frag, const uint16_t *dY, const float *rs, const float *A,
-                          const float *b, int d, uint16_t *dX, int64_t N, int64_t m, int64_t n,
-                          hipStream_t st);
-hipError_t launch_dz_bf16(const uint16_t *X, const uint16_t *dY, const uint16_t *Z, const float *A, int d,
-                          int mask_mode, int accumulate, void *dZ, bool dz_bf16, float *dA, float *db,
-                          int64_t N, int64_t m, int64_t n, hipStream_t st);
+                          const float *b, int d, uint16_t *dX, const uint16_t *X, float *dA, float *db, int64_t N,
+                          int64_t m, int64_t n, hipStream_t st);
+hipError_t launch_dw_bf16(const uint16_t *xt, const uint16_t *dyt, const uint16_t *Z, int mask_mode, int accumulate,
+                          void *dZ, bool dz_bf16, int64_t N, int64_t m, int64_t n, hipStream_t st);
 
 // fp32 products on the vector ALUs (lcvq_f32.hip)
 hipError_t launch_fwd_f32(const float *Z, const float *Xp, const float *s, float *Y, int64_t N, int64_t m,
