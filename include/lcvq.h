@@ -165,7 +165,7 @@ typedef enum {
   LCVQ_K_QUANT = 0,     /* latents -> codes in the forward operand layout (+ 2-bit pack) */
   LCVQ_K_ACT = 1,       /* X' = X blockdiag(A), s = X b~ */
   LCVQ_K_FWD = 2,       /* Y = X' codes^T + s 1^T (matrix cores) */
-  LCVQ_K_ROWSUM = 3,    /* per-token sums of dY */
+  LCVQ_K_BWD_PREP = 3,  /* backward prepass: per-token sums of dY (+ weight-gradient operands) */
   LCVQ_K_QUANT_T = 4,   /* latents -> codes in the input-gradient operand layout */
   LCVQ_K_DX = 5,        /* dX (matrix cores + A^T map) */
   LCVQ_K_DW = 6,        /* dW = dY^T X with dZ, dA, db epilogue (matrix cores) */

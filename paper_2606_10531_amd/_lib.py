@@ -17,7 +17,7 @@ MASK_ROUNDED, MASK_LATENT = 0, 1
 # lcvq_op_t
 OP_FWD, OP_BWD = 0, 1
 # lcvq_kernel_t
-KERNELS = ["quant", "act", "fwd", "rowsum", "quant_t", "dx", "dw", "pack", "dequant", "fill"]
+KERNELS = ["quant", "act", "fwd", "bwd_prep", "quant_t", "dx", "dw", "pack", "dequant", "fill"]
 
 _P = ctypes.c_void_p
 _I64 = ctypes.c_int64

@@ -378,7 +378,7 @@ lcvq_status_t lcvq_linear_bwd(int64_t N, int64_t m, int64_t n, int32_t d, int32_
       if (e != hipSuccess) return hip_fail(e, "quantise launch");
     }
     {
-      Timed tm(LCVQ_K_ROWSUM, st);
+      Timed tm(LCVQ_K_BWD_PREP, st);
       e = tm.done(lcvq::launch_bwd_prep((const uint16_t *)X, (const uint16_t *)dY, A, d, N, m, n, xt, dyt, rs, st));
       if (e != hipSuccess) return hip_fail(e, "backward operand launch");
     }
@@ -401,7 +401,7 @@ lcvq_status_t lcvq_linear_bwd(int64_t N, int64_t m, int64_t n, int32_t d, int32_
   float *zA = clear_map ? dA : nullptr;
   float *zb = clear_map ? db : nullptr;
   if (dX != nullptr) {
-    { Timed tm(LCVQ_K_ROWSUM, st); e = tm.done(lcvq::launch_rowsum(dY, false, N, N, m, rs, zA, zb, d, st)); }
+    { Timed tm(LCVQ_K_BWD_PREP, st); e = tm.done(lcvq::launch_rowsum(dY, false, N, N, m, rs, zA, zb, d, st)); }
     if (e != hipSuccess) return hip_fail(e, "row-sum launch");
     zA = zb = nullptr;  // cleared by the row-sum launch
     Timed tm(LCVQ_K_DX, st);
