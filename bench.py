@@ -108,11 +108,19 @@ def hbm_kernels(lc, torch):
     A, b = torch.eye(d, device="cuda"), torch.zeros(d, device="cuda")
     packed = torch.empty((m, n // 4), dtype=torch.uint8, device="cuda")
     W = torch.empty((m, n), dtype=torch.bfloat16, device="cuda")
+    # AdamW on the same matrix: fp32 master, moments; bf16 gradient and bf16 latent copy
+    theta = Z.float().reshape(-1)
+    m1, m2 = torch.zeros_like(theta), torch.zeros_like(theta)
+    gZ = W.reshape(-1)
+    shadow = torch.empty_like(gZ)
     out = {}
     cases = [("pack2bit_from_bf16", lambda: lc.pack2bit(Z, out=packed), 2.25, "pack"),
              ("dequant_packed_to_bf16", lambda: lc.dequant(packed, A, b, d, n=n, src_kind=lc.SRC_PACKED2,
                                                            out=W), 2.25, "dequant"),
-             ("dequant_bf16_latent_to_bf16", lambda: lc.dequant(Z, A, b, d, out=W), 4.0, "dequant")]
+             ("dequant_bf16_latent_to_bf16", lambda: lc.dequant(Z, A, b, d, out=W), 4.0, "dequant"),
+             # per parameter: theta, m1, m2 read + written (24 B), bf16 gradient read, bf16 copy written
+             ("adamw_step_fp32_master_bf16_grad",
+              lambda: lc.adamw_step(theta, gZ, m1, m2, 1, 1e-4, shadow=shadow), 28.0, "adam")]
     for name, fn, bpe, kname in cases:
         for _ in range(3):
             fn()
@@ -128,7 +136,7 @@ def hbm_kernels(lc, torch):
         gbps = bpe * m * n / (us * 1e-6) / 1e9
         out[name] = {"us": round(us, 2), "GB/s": round(gbps, 1), "frac_hbm": round(gbps / PEAK_HBM, 3),
                      "bytes_per_elem": bpe, "shape": [m, n]}
-    del Z, packed, W
+    del Z, packed, W, theta, m1, m2, shadow
     return out
 
 

@@ -152,6 +152,27 @@ lcvq_status_t lcvq_linear_bwd(int64_t N, int64_t m, int64_t n, int32_t d, int32_
                               void *workspace, size_t workspace_bytes, void *stream);
 
 /*
+ * lcvq_adamw_step -- one AdamW update of a flat fp32 parameter array: the
+ * optimiser the paper trains Z, A and b with (Sec. 4.4), with bias correction
+ * and decoupled weight decay, all arithmetic in fp32:
+ *   m1 = beta1 m1 + (1 - beta1) g;   m2 = beta2 m2 + (1 - beta2) g^2
+ *   theta = theta - lr weight_decay theta
+ *           - lr (m1 / (1 - beta1^step)) / (sqrt(m2 / (1 - beta2^step)) + eps)
+ *   theta, m1, m2  numel fp32 each, updated in place (caller zeroes m1, m2
+ *                  before step 1)
+ *   grad           numel gradients of element type grad_dtype (F32 or BF16)
+ *   shadow         NULL, or numel elements of shadow_dtype (F32 or BF16) that
+ *                  receive the updated theta (bf16: rounded to nearest even);
+ *                  the latent copy the layer calls read
+ *   step           1-based step count (>= 1)
+ * Requires beta1, beta2 in [0, 1), eps > 0, lr >= 0; pointers 16-byte aligned;
+ * theta, m1, m2, grad and shadow must not overlap.  numel == 0 returns LCVQ_OK.
+ */
+lcvq_status_t lcvq_adamw_step(float *theta, const void *grad, int32_t grad_dtype, float *m1, float *m2,
+                              void *shadow, int32_t shadow_dtype, int64_t numel, float lr, float beta1,
+                              float beta2, float eps, float weight_decay, int32_t step, void *stream);
+
+/*
  * Instrumentation: device time of individual kernels, measured with HIP events.
  * lcvq_timer_enable(mask) makes every later launch of a kernel whose bit
  * (1 << lcvq_kernel_t) is set in `mask`, by any thread, record a start event
@@ -172,7 +193,8 @@ typedef enum {
   LCVQ_K_PACK = 7,      /* lcvq_pack2bit */
   LCVQ_K_DEQUANT = 8,   /* lcvq_dequant */
   LCVQ_K_FILL = 9,      /* zero fills of degenerate shapes */
-  LCVQ_K_COUNT = 10
+  LCVQ_K_ADAM = 10,     /* lcvq_adamw_step */
+  LCVQ_K_COUNT = 11
 } lcvq_kernel_t;
 lcvq_status_t lcvq_timer_enable(uint32_t mask);
 lcvq_status_t lcvq_timer_read(int32_t kernel, double *total_ms, int64_t *launches);

@@ -15,7 +15,7 @@ from . import _lib
 from ._lib import (BF16, F32, MASK_LATENT, MASK_ROUNDED, OP_BWD, OP_FWD,  # noqa: F401
                    SRC_CODES_U8, SRC_LATENT, SRC_PACKED2, LcvqError)
 
-__all__ = ["linear_fwd", "linear_bwd", "pack2bit", "dequant", "workspace_bytes", "LcvqError",
+__all__ = ["linear_fwd", "linear_bwd", "pack2bit", "dequant", "adamw_step", "workspace_bytes", "LcvqError",
            "MASK_ROUNDED", "MASK_LATENT", "SRC_LATENT", "SRC_CODES_U8", "SRC_PACKED2"]
 
 _DT = {torch.float32: F32, torch.bfloat16: BF16}
@@ -87,6 +87,25 @@ def dequant(src: torch.Tensor, A: torch.Tensor, b: torch.Tensor, d: int, n: int 
     _lib.check(_lib.load().lcvq_dequant(m, n, d, src_kind, sdt, _dev(src, "src"), _dev(A, "A"), _dev(b, "b"),
                                         _dev(out, "out"), _DT[out.dtype], _stream(src.device)), "lcvq_dequant")
     return out
+
+
+def adamw_step(theta: torch.Tensor, grad: torch.Tensor, m1: torch.Tensor, m2: torch.Tensor, step: int,
+               lr: float, beta1: float = 0.9, beta2: float = 0.999, eps: float = 1e-8,
+               weight_decay: float = 0.0, shadow: torch.Tensor | None = None) -> None:
+    """One in-place AdamW update of fp32 `theta`, `m1`, `m2` from `grad` (fp32 or bf16);
+    `shadow` (fp32 or bf16, optional) receives the updated theta."""
+    for t, nm in ((theta, "theta"), (m1, "m1"), (m2, "m2")):
+        if t.dtype != torch.float32:
+            raise TypeError(f"{nm} must be float32")
+    numel = theta.numel()
+    for t, nm in ((grad, "grad"), (m1, "m1"), (m2, "m2")) + (((shadow, "shadow"),) if shadow is not None else ()):
+        if t.numel() != numel:
+            raise ValueError(f"{nm} has {t.numel()} elements, theta has {numel}")
+    sdt = _dtype_code(shadow) if shadow is not None else F32
+    _lib.check(_lib.load().lcvq_adamw_step(_dev(theta, "theta"), _dev(grad, "grad"), _dtype_code(grad),
+                                           _dev(m1, "m1"), _dev(m2, "m2"), _opt(shadow, "shadow"), sdt, numel,
+                                           lr, beta1, beta2, eps, weight_decay, step, _stream(theta.device)),
+               "lcvq_adamw_step")
 
 
 def linear_fwd(Z: torch.Tensor, A: torch.Tensor, b: torch.Tensor, X: torch.Tensor, d: int,

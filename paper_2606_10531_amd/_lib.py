@@ -17,7 +17,7 @@ MASK_ROUNDED, MASK_LATENT = 0, 1
 # lcvq_op_t
 OP_FWD, OP_BWD = 0, 1
 # lcvq_kernel_t
-KERNELS = ["quant", "act", "fwd", "bwd_prep", "quant_t", "dx", "dw", "pack", "dequant", "fill"]
+KERNELS = ["quant", "act", "fwd", "bwd_prep", "quant_t", "dx", "dw", "pack", "dequant", "fill", "adam"]
 
 _P = ctypes.c_void_p
 _I64 = ctypes.c_int64
@@ -31,6 +31,8 @@ SIGNATURES = {
     "lcvq_linear_fwd": (_I32, [_I64, _I64, _I64, _I32, _I32, _P, _P, _P, _P, _P, _P, _P, _SZ, _P]),
     "lcvq_linear_bwd": (_I32, [_I64, _I64, _I64, _I32, _I32, _P, _P, _P, _P, _P, _I32, _I32,
                                _P, _P, _I32, _P, _P, _P, _SZ, _P]),
+    "lcvq_adamw_step": (_I32, [_P, _P, _I32, _P, _P, _P, _I32, _I64, ctypes.c_float, ctypes.c_float,
+                                ctypes.c_float, ctypes.c_float, ctypes.c_float, _I32, _P]),
     "lcvq_timer_enable": (_I32, [ctypes.c_uint32]),
     "lcvq_timer_read": (_I32, [_I32, ctypes.POINTER(ctypes.c_double), ctypes.POINTER(ctypes.c_int64)]),
     "lcvq_status_string": (ctypes.c_char_p, [_I32]),

@@ -52,7 +52,8 @@ FwdLayout fwd_layout(int64_t N, int64_t m, int64_t n, bool bf16) {
     // K padded to an even number of 64-wide steps (the product loop takes two per trip)
     L.Np = lcvq::round_up(N, 256);
     L.ldp = lcvq::round_up(n, 128);
-    const size_t xp = (size_t)L.Np * L.ldp * 2, s = (size_t)L.Np * 4;
+    // s is held as one partial row of Np floats per K chunk of the transform
+    const size_t xp = (size_t)L.Np * L.ldp * 2, s = (size_t)lcvq::act_chunks(L.ldp) * L.Np * 4;
     const size_t frag = (size_t)(lcvq::round_up(m, 256) / 32) * (L.ldp / 64) * 1024;
     L.xp = 0;
     L.s = up256(xp);
@@ -243,6 +244,28 @@ lcvq_status_t lcvq_pack2bit(const void *src, int32_t src_kind, int32_t src_dtype
   Timed tm(LCVQ_K_PACK, (hipStream_t)stream);
   hipError_t e = tm.done(lcvq::launch_pack2bit(src, src_kind, src_dtype == LCVQ_BF16, m, n, packed, (hipStream_t)stream));
   return e == hipSuccess ? ok() : hip_fail(e, "pack2bit launch");
+}
+
+lcvq_status_t lcvq_adamw_step(float *theta, const void *grad, int32_t grad_dtype, float *m1, float *m2,
+                              void *shadow, int32_t shadow_dtype, int64_t numel, float lr, float beta1,
+                              float beta2, float eps, float weight_decay, int32_t step, void *stream) {
+  if (numel < 0) return fail(LCVQ_EINVAL, "negative numel");
+  if (grad_dtype != LCVQ_F32 && grad_dtype != LCVQ_BF16) return fail(LCVQ_EINVAL, "grad_dtype=%d", grad_dtype);
+  if (shadow != nullptr && shadow_dtype != LCVQ_F32 && shadow_dtype != LCVQ_BF16)
+    return fail(LCVQ_EINVAL, "shadow_dtype=%d", shadow_dtype);
+  if (step < 1) return fail(LCVQ_EINVAL, "step=%d (1-based)", step);
+  if (!(beta1 >= 0.0f && beta1 < 1.0f) || !(beta2 >= 0.0f && beta2 < 1.0f) || !(eps > 0.0f) || !(lr >= 0.0f) ||
+      !(weight_decay >= 0.0f))
+    return fail(LCVQ_EINVAL, "hyper-parameters out of range");
+  if (numel == 0) return ok();
+  if (theta == nullptr || grad == nullptr || m1 == nullptr || m2 == nullptr) return fail(LCVQ_EINVAL, "null pointer");
+  if (!aligned16(theta) || !aligned16(grad) || !aligned16(m1) || !aligned16(m2) || (shadow && !aligned16(shadow)))
+    return fail(LCVQ_EALIGN, "theta/grad/m1/m2/shadow must be 16-byte aligned");
+  const int shadow_kind = shadow == nullptr ? 0 : (shadow_dtype == LCVQ_F32 ? 1 : 2);
+  Timed tm(LCVQ_K_ADAM, (hipStream_t)stream);
+  hipError_t e = tm.done(lcvq::launch_adamw(theta, grad, grad_dtype == LCVQ_BF16, m1, m2, shadow, shadow_kind, numel,
+                                            lr, beta1, beta2, eps, weight_decay, step, (hipStream_t)stream));
+  return e == hipSuccess ? ok() : hip_fail(e, "adamw launch");
 }
 
 lcvq_status_t lcvq_dequant(int64_t m, int64_t n, int32_t d, int32_t src_kind, int32_t src_dtype,

@@ -81,8 +81,8 @@ __device__ __forceinline__ uint32_t as_u(float f) { return __float_as_uint(f); }
 template <int kMode, int D>  // kMode 0: forward (B = X' fragments), 1: input gradient (B = dY rows)
 __global__ __launch_bounds__(256, 1) void k_gemm_codes(
     const uint32_t *__restrict__ frag, int KB, const uint16_t *__restrict__ Bsrc, int ldb,
-    int64_t brows, int kvalid, int tiles_m, int tiles_n, const float *__restrict__ vecT,
-    const float *__restrict__ A, const float *__restrict__ bvec, uint16_t *__restrict__ out,
+    int64_t brows, int kvalid, int tiles_m, int tiles_n, const float *__restrict__ vecT, int vparts,
+    int64_t vstride, const float *__restrict__ A, const float *__restrict__ bvec, uint16_t *__restrict__ out,
     int64_t ldo, int64_t Mvalid, int64_t Tvalid, const uint16_t *__restrict__ X,
     float *__restrict__ dA, float *__restrict__ db) {
   const int tid = threadIdx.x, lane = tid & 63, h = lane >> 5;
@@ -187,11 +187,24 @@ __global__ __launch_bounds__(256, 1) void k_gemm_codes(
   // the store and load counters are shared, so a load behind stores would wait
   // for all of them.
   const __amdgpu_buffer_rsrc_t ro = make_rsrc(out + tw * ldo, out == nullptr ? 0 : (Tvalid - tw) * ldo * 2);
-  const __amdgpu_buffer_rsrc_t rv = make_rsrc(vecT + tw, (Tvalid - tw) * 4);
   const int64_t cb0 = (int64_t)tm * kTile + 16 * h;
-  float vt[2];
+  // Per-token term: s of the forward (up to kMaxParts partial rows vstride
+  // apart, summed here) or rowsum(dY) of the input gradient.
+  constexpr int kMaxParts = kMode == 0 ? 8 : 1;
+  const __amdgpu_buffer_rsrc_t rv = make_rsrc(vecT + tw, ((int64_t)(vparts - 1) * vstride + Tvalid - tw) * 4);
+  float vp[kMaxParts][2], vt[2];
 #pragma unroll
-  for (int ni = 0; ni < 2; ++ni) vt[ni] = as_f(__builtin_amdgcn_raw_buffer_load_b32(rv, (ni * 32 + (lane & 31)) * 4, 0, 0));
+  for (int p = 0; p < kMaxParts; ++p)
+#pragma unroll
+    for (int ni = 0; ni < 2; ++ni)
+      vp[p][ni] = as_f(__builtin_amdgcn_raw_buffer_load_b32(
+          rv, p < vparts ? (int)((p * vstride + ni * 32 + (lane & 31)) * 4) : (int)kOffNone, 0, 0));
+#pragma unroll
+  for (int ni = 0; ni < 2; ++ni) {
+    vt[ni] = vp[0][ni];
+#pragma unroll
+    for (int p = 1; p < kMaxParts; ++p) vt[ni] += vp[p][ni];
+  }
   if constexpr (kMode == 0) {
 #pragma unroll
     for (int ni = 0; ni < 2; ++ni) {
@@ -496,7 +509,7 @@ hipError_t launch_fwd_bf16(const uint32_t *frag, const uint16_t *Xp, int64_t ldp
   const int KB = (int)(ldp / kKStep);  // even: ldp is a multiple of 128
   const int64_t Np = (int64_t)tiles_n * kTile;
   k_gemm_codes<0, 8><<<tiles_m * tiles_n, 256, 0, st>>>(frag, KB, Xp, (int)ldp, Np, (int)ldp, tiles_m, tiles_n, s,
-                                                        nullptr, nullptr, Y, m, m, N, nullptr, nullptr, nullptr);
+                                                        act_chunks(ldp), Np, nullptr, nullptr, Y, m, m, N, nullptr, nullptr, nullptr);
   return hipGetLastError();
 }
 
@@ -507,11 +520,11 @@ hipError_t launch_dx_bf16(const uint32_t *frag, const uint16_t *dY, const float 
   const int KB = (int)(round_up(m, 128) / kKStep);  // even, matches the operand layout
   // dX == nullptr: the product still runs for dA/db; its stores are dropped.
   if (d == 8)
-    k_gemm_codes<1, 8><<<tiles_m * tiles_n, 256, 0, st>>>(frag, KB, dY, (int)m, N, (int)m, tiles_m, tiles_n, rs, A,
-                                                          b, dX, n, n, N, X, dA, db);
+    k_gemm_codes<1, 8><<<tiles_m * tiles_n, 256, 0, st>>>(frag, KB, dY, (int)m, N, (int)m, tiles_m, tiles_n, rs, 1,
+                                                          0, A, b, dX, n, n, N, X, dA, db);
   else
-    k_gemm_codes<1, 4><<<tiles_m * tiles_n, 256, 0, st>>>(frag, KB, dY, (int)m, N, (int)m, tiles_m, tiles_n, rs, A,
-                                                          b, dX, n, n, N, X, dA, db);
+    k_gemm_codes<1, 4><<<tiles_m * tiles_n, 256, 0, st>>>(frag, KB, dY, (int)m, N, (int)m, tiles_m, tiles_n, rs, 1,
+                                                          0, A, b, dX, n, n, N, X, dA, db);
   return hipGetLastError();
 }
 

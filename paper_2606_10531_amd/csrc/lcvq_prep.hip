@@ -135,13 +135,10 @@ __global__ __launch_bounds__(256) void k_quant_frag(const ZT *__restrict__ Z, in
   }
 }
 
-// ---- activation transform (def. forward_x) ---------------------------------
-// One block per (padded) token row: X'[t, g*D + k] = sum_j X[t, g*D + j] A[j, k]
-// and s[t] = sum_c X[t, c] b[c % D].  Rows t >= N and columns >= n of X' are
-// written as zero.
-// kFrag: X' goes to the matrix-core B-operand layout (bfrag_index, ldp / 64 K
-// steps) instead of row-major with row length ldp.
-template <typename XT, typename OT, int D, bool kFrag>
+// ---- activation transform (def. forward_x), fp32 row-major -----------------
+// One block per token row: X'[t, g*D + k] = sum_j X[t, g*D + j] A[j, k] and
+// s[t] = sum_c X[t, c] b[c % D], X' row-major with row length ldp.
+template <typename XT, typename OT, int D>
 __global__ __launch_bounds__(256) void k_act_transform(const XT *__restrict__ X, int64_t N, int64_t n,
                                                         const float *__restrict__ A,
                                                         const float *__restrict__ b,
@@ -175,11 +172,78 @@ __global__ __launch_bounds__(256) void k_act_transform(const XT *__restrict__ X,
     }
 #pragma unroll
     for (int j = 0; j < D; ++j) acc_s = fmaf(x[j], bb[j], acc_s);
-    if constexpr (kFrag) storeD<D>(Xp + bfrag_index(t, g * D, ldp / 64), y);
-    else storeD<D>(Xp + t * ldp + g * D, y);
+    storeD<D>(Xp + t * ldp + g * D, y);
   }
   const float tot = block_sum256(acc_s, red);
   if (threadIdx.x == 0) s[t] = tot;
+}
+
+// ---- activation transform, bf16, straight into the B-operand fragments -----
+// Block (tb, kc): tokens 32 tb .. 32 tb + 31, 64-wide K steps of chunk kc;
+// wave w takes steps kb0 + w, kb0 + w + 4, ...  For (step kb, sub-step kk) lane
+// L owns token 32 tb + L % 32 and K = 64 kb + 16 kk + 8 (L / 32) + 0..7 -- one
+// whole group (d = 8) or two (d = 4) -- so it loads the 16 bytes it will store,
+// and each wave writes one whole 1 KiB fragment per sub-step.  Tokens >= N and
+// K >= n give zeros.  sp[kc * Np + t] = this chunk's part of s[t].
+template <int D>
+__global__ __launch_bounds__(256) void k_act_frag(const uint16_t *__restrict__ X, int64_t N, int64_t n,
+                                                   const float *__restrict__ A, const float *__restrict__ b,
+                                                   uint16_t *__restrict__ Xp, int KB, int spc, int64_t Np,
+                                                   float *__restrict__ sp) {
+  __shared__ float red[4][32];
+  const int tid = threadIdx.x, lane = tid & 63, h = lane >> 5;
+  const int wave = tid >> 6;
+  const int64_t tb = blockIdx.x;
+  const int kc = blockIdx.y;
+  const int64_t rows = N - tb * 32;  // > 0 only for blocks that hold real tokens
+  const __amdgpu_buffer_rsrc_t rx = make_rsrc(X + tb * 32 * n, rows > 0 ? (rows < 32 ? rows : 32) * n * 2 : 0);
+  float a[D][D], bb[D];
+#pragma unroll
+  for (int j = 0; j < D; ++j) {
+    bb[j] = b[j];
+#pragma unroll
+    for (int k = 0; k < D; ++k) a[j][k] = A[j * D + k];
+  }
+  const int kb0 = kc * spc, kb1 = min(kb0 + spc, KB);
+  float acc_s = 0.0f;
+  for (int kb = kb0 + wave; kb < kb1; kb += 4) {
+    u32x4 xv[4];
+#pragma unroll
+    for (int kk = 0; kk < 4; ++kk) {
+      const int64_t k = (int64_t)kb * 64 + 16 * kk + 8 * h;
+      const uint32_t off = k < n ? (uint32_t)(((lane & 31) * n + k) * 2) : kOffNone;
+      xv[kk] = __builtin_amdgcn_raw_buffer_load_b128(rx, off, 0, 0);
+    }
+    uint16_t *dst = Xp + ((tb * KB + kb) * 4) * 512 + lane * 8;
+#pragma unroll
+    for (int kk = 0; kk < 4; ++kk) {
+      float x[8], y[8];
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        x[2 * e] = bf16_lo(xv[kk][e]);
+        x[2 * e + 1] = bf16_hi(xv[kk][e]);
+      }
+#pragma unroll
+      for (int g = 0; g < 8 / D; ++g)
+#pragma unroll
+        for (int k = 0; k < D; ++k) {
+          float v = 0.0f;
+#pragma unroll
+          for (int j = 0; j < D; ++j) v = fmaf(x[g * D + j], a[j][k], v);
+          y[g * D + k] = v;
+        }
+#pragma unroll
+      for (int e = 0; e < 8; ++e) acc_s = fmaf(x[e], bb[e % D], acc_s);
+      u32x4 w;
+#pragma unroll
+      for (int e = 0; e < 4; ++e) w[e] = pack_bf16x2(y[2 * e], y[2 * e + 1]);
+      *reinterpret_cast<u32x4 *>(dst + kk * 512) = w;
+    }
+  }
+  acc_s += __shfl_xor(acc_s, 32, 64);
+  if (lane < 32) red[wave][lane] = acc_s;
+  __syncthreads();
+  if (tid < 32) sp[(int64_t)kc * Np + tb * 32 + tid] = red[0][tid] + red[1][tid] + red[2][tid] + red[3][tid];
 }
 
 // ---- per-token sums of dY (dX offset term) ---------------------------------
@@ -418,12 +482,14 @@ hipError_t launch_act_transform(const void *X, bool bf16, int64_t N, int64_t Np,
                                 const float *A, const float *b, void *Xp, int64_t ldp, float *s,
                                 hipStream_t st) {
   dim3 grid((unsigned)Np);
-  if (bf16) {  // matrix-core layout
-    if (d == 8) k_act_transform<uint16_t, uint16_t, 8, true><<<grid, 256, 0, st>>>((const uint16_t *)X, N, n, A, b, (uint16_t *)Xp, ldp, s);
-    else k_act_transform<uint16_t, uint16_t, 4, true><<<grid, 256, 0, st>>>((const uint16_t *)X, N, n, A, b, (uint16_t *)Xp, ldp, s);
+  if (bf16) {  // matrix-core layout, one partial s per K chunk
+    const int KB = (int)(ldp / 64), spc = act_steps_per_chunk(ldp);
+    dim3 g2((unsigned)(Np / 32), (unsigned)act_chunks(ldp));
+    if (d == 8) k_act_frag<8><<<g2, 256, 0, st>>>((const uint16_t *)X, N, n, A, b, (uint16_t *)Xp, KB, spc, Np, s);
+    else k_act_frag<4><<<g2, 256, 0, st>>>((const uint16_t *)X, N, n, A, b, (uint16_t *)Xp, KB, spc, Np, s);
   } else {  // row-major
-    if (d == 8) k_act_transform<float, float, 8, false><<<grid, 256, 0, st>>>((const float *)X, N, n, A, b, (float *)Xp, ldp, s);
-    else k_act_transform<float, float, 4, false><<<grid, 256, 0, st>>>((const float *)X, N, n, A, b, (float *)Xp, ldp, s);
+    if (d == 8) k_act_transform<float, float, 8><<<grid, 256, 0, st>>>((const float *)X, N, n, A, b, (float *)Xp, ldp, s);
+    else k_act_transform<float, float, 4><<<grid, 256, 0, st>>>((const float *)X, N, n, A, b, (float *)Xp, ldp, s);
   }
   return hipGetLastError();
 }

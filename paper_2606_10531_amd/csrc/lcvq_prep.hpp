@@ -5,6 +5,18 @@
 
 namespace lcvq {
 
+// The bf16 activation transform splits K into at most eight chunks and writes
+// one partial s per chunk (rows of Np floats); the forward product sums them.
+// Both are at least 1 (ldp may be 0 for an empty problem).
+inline int act_steps_per_chunk(int64_t ldp) {
+  const int64_t spc = (ldp / 64 + 7) / 8;
+  return spc < 1 ? 1 : (int)spc;
+}
+inline int act_chunks(int64_t ldp) {
+  const int64_t c = (ldp / 64 + act_steps_per_chunk(ldp) - 1) / act_steps_per_chunk(ldp);
+  return c < 1 ? 1 : (int)c;
+}
+
 // streaming kernels (lcvq_prep.hip)
 hipError_t launch_quant_frag(const void *Z, bool z_bf16, int64_t m, int64_t n, bool trans,
                              uint32_t *frag, uint8_t *packed, hipStream_t st, float *zero = nullptr,
@@ -21,6 +33,11 @@ hipError_t launch_pack2bit(const void *src, int kind, bool bf16, int64_t m, int6
                            hipStream_t st);
 hipError_t launch_dequant(const void *src, int kind, bool z_bf16, int64_t m, int64_t n, int d,
                           const float *A, const float *b, void *W, bool out_bf16, hipStream_t st);
+
+// optimiser (lcvq_adam.hip); shadow_kind 0 none, 1 fp32, 2 bf16
+hipError_t launch_adamw(float *theta, const void *grad, bool grad_bf16, float *m1, float *m2, void *shadow,
+                        int shadow_kind, int64_t numel, float lr, float beta1, float beta2, float eps,
+                        float weight_decay, int step, hipStream_t st);
 
 // bf16 matrix-core products (lcvq_gemm.hip)
 hipError_t launch_fwd_bf16(const uint32_t *frag, const uint16_t *Xp, int64_t ldp, const float *s,

@@ -50,6 +50,15 @@ def test_workspace_bytes(lib):
     assert f(L.OP_FWD, 300, 264, 328, 8, L.BF16) >= f(L.OP_FWD, 256, 264, 328, 8, L.BF16)
 
 
+def test_workspace_bytes_of_empty_problems(lib):
+    """Zero sizes must not trip the host-side layout arithmetic (no division by zero)."""
+    f = lib.lcvq_workspace_bytes
+    for op in (L.OP_FWD, L.OP_BWD):
+        for dt in (L.F32, L.BF16):
+            for N, m, n in ((0, 64, 64), (16, 0, 64), (16, 64, 0), (0, 0, 0)):
+                assert f(op, N, m, n, 8, dt) >= 0
+
+
 def fwd(lib, N=16, m=64, n=64, d=8, dt=L.BF16, Z=FAKE, A=FAKE, b=FAKE, X=FAKE, Y=FAKE, packed=None,
         ws=FAKE, wsb=1 << 40):
     return lib.lcvq_linear_fwd(N, m, n, d, dt, Z, A, b, X, Y, packed, ws, wsb, None)
@@ -107,6 +116,25 @@ def test_pack_and_dequant_validation(lib):
     assert q(4, 8, 8, 5, L.BF16, FAKE, FAKE, FAKE, FAKE, L.BF16, None) == L.EINVAL
     assert q(4, 8, 8, L.SRC_LATENT, L.BF16, FAKE, None, FAKE, FAKE, L.BF16, None) == L.EINVAL
     assert q(4, 8, 8, L.SRC_LATENT, L.BF16, FAKE, FAKE, FAKE, MIS, L.BF16, None) == L.EALIGN
+
+
+def test_adamw_validation(lib):
+    def a(theta=FAKE, grad=FAKE, gdt=L.BF16, m1=FAKE, m2=FAKE, sh=None, sdt=L.BF16, numel=64, lr=1e-3,
+          b1=0.9, b2=0.999, eps=1e-8, wd=0.0, step=1):
+        return lib.lcvq_adamw_step(theta, grad, gdt, m1, m2, sh, sdt, numel, lr, b1, b2, eps, wd, step, None)
+    assert a(numel=-1) == L.EINVAL
+    assert a(gdt=7) == L.EINVAL
+    assert a(sh=FAKE, sdt=7) == L.EINVAL
+    assert a(step=0) == L.EINVAL
+    assert a(b1=1.0) == L.EINVAL
+    assert a(b2=-0.1) == L.EINVAL
+    assert a(eps=0.0) == L.EINVAL
+    assert a(lr=-1.0) == L.EINVAL
+    assert a(wd=float("nan")) == L.EINVAL
+    assert a(m2=None) == L.EINVAL
+    assert a(grad=MIS) == L.EALIGN
+    assert a(sh=MIS) == L.EALIGN
+    assert a(numel=0, theta=None) == L.OK        # empty: nothing to do
 
 
 def test_binding_refuses_cpu_tensors():
