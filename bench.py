@@ -140,6 +140,26 @@ def hbm_kernels(lc, torch):
     return out
 
 
+def library_gemm(torch, N, m, n):
+    """Context: one plain bf16 product of the same shape (Y = X W^T, N(0,1) data)
+    through torch.matmul, i.e. the vendor GEMM library, with no quantisation."""
+    g = torch.Generator(device="cuda").manual_seed(0)
+    X = torch.randn(N, n, device="cuda", generator=g).to(torch.bfloat16)
+    W = torch.randn(m, n, device="cuda", generator=g).to(torch.bfloat16)
+    for _ in range(5):
+        torch.matmul(X, W.t())
+    start, stop = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    start.record()
+    for _ in range(20):
+        torch.matmul(X, W.t())
+    stop.record()
+    torch.cuda.synchronize()
+    us = 1e3 * start.elapsed_time(stop) / 20
+    return {"op": "torch.matmul bf16 X[N,n] @ W[m,n]^T", "shape": [N, m, n], "us": round(us, 2),
+            "TFLOP/s": round(2.0 * N * m * n / (us * 1e-6) / 1e12, 1)}
+
+
 def cpu_baseline(layer, max_seconds: float):
     """The fp64 oracle on the host, on the same inputs (a bounded number of full
     fwd+bwd repetitions), with its parity check of the GPU results."""
@@ -232,13 +252,14 @@ def main():
         step()
     torch.cuda.synchronize()
 
-    # per-kernel breakdown (separate, untimed pass) to pick the dominant kernel
-    lib.lcvq_timer_enable((1 << len(lc._lib.KERNELS)) - 1)
-    for _ in range(3):
-        step()
-    torch.cuda.synchronize()
+    # per-kernel breakdown (untimed passes, one kernel's events at a time) to
+    # pick the dominant kernel
     breakdown = {}
     for kid, name in enumerate(lc._lib.KERNELS):
+        lib.lcvq_timer_enable(1 << kid)
+        for _ in range(3):
+            step()
+        torch.cuda.synchronize()
         ms, cnt = timer_read(lib, kid)
         if cnt:
             breakdown[name] = round(1e3 * ms / 3, 2)      # us per step
@@ -246,9 +267,7 @@ def main():
     dominant = max(MATRIX_KERNELS, key=lambda k: breakdown.get(k, 0.0))
     dom_id = lc._lib.KERNELS.index(dominant)
 
-    # timed region: K steps between two events; the dominant kernel is also
-    # bracketed by its own events on the same stream
-    lib.lcvq_timer_enable(1 << dom_id)
+    # timed region: K steps between two events, nothing else recorded
     start, stop = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     torch.cuda.synchronize()
     start.record()
@@ -257,6 +276,18 @@ def main():
     stop.record()
     torch.cuda.synchronize()
     ms_step = start.elapsed_time(stop) / args.steps
+
+    # the same K steps again with every launch of the dominant kernel bracketed
+    # by HIP events on its stream (the extra event records lengthen the step, so
+    # the step time above comes from the run without them)
+    lib.lcvq_timer_enable(1 << dom_id)
+    torch.cuda.synchronize()
+    start.record()
+    for _ in range(args.steps):
+        step()
+    stop.record()
+    torch.cuda.synchronize()
+    ms_step_ev = start.elapsed_time(stop) / args.steps
     dom_ms, dom_cnt = timer_read(lib, dom_id)
     lib.lcvq_timer_enable(0)
     dom_us = 1e3 * dom_ms / max(dom_cnt, 1)
@@ -276,10 +307,12 @@ def main():
         "frac_of_peak": round(value / PEAK_MFMA_BF16, 4),
         "roofline": {"kernel": dominant, "bound": "mfma", "achieved": round(achieved, 2),
                      "peak": PEAK_MFMA_BF16, "unit": "TFLOP/s", "frac": round(achieved / PEAK_MFMA_BF16, 4),
-                     "traffic": traffic, "avg_launch_us": round(dom_us, 2),
-                     "flop_per_launch": per_launch_flop},
+                     "traffic": traffic, "avg_launch_us": round(dom_us, 2), "launches": dom_cnt,
+                     "flop_per_launch": per_launch_flop, "ms_per_step_with_kernel_events": round(ms_step_ev, 4)},
         "kernels_us_per_step": breakdown,
     }
+    L0 = layers[0]
+    res["library_gemm_same_shape"] = library_gemm(torch, L0.N, L0.m, L0.n)
     if not args.no_hbm:
         res["hbm_kernels"] = hbm_kernels(lc, torch)
     if not args.no_cpu_baseline:
