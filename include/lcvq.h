@@ -183,18 +183,18 @@ lcvq_status_t lcvq_adamw_step(float *theta, const void *grad, int32_t grad_dtype
  * for use while the stream is being captured into a graph.
  */
 typedef enum {
-  LCVQ_K_QUANT = 0,     /* latents -> codes in the forward operand layout (+ 2-bit pack) */
-  LCVQ_K_ACT = 1,       /* X' = X blockdiag(A), s = X b~ */
-  LCVQ_K_FWD = 2,       /* Y = X' codes^T + s 1^T (matrix cores) */
-  LCVQ_K_BWD_PREP = 3,  /* backward prepass: per-token sums of dY (+ weight-gradient operands) */
-  LCVQ_K_QUANT_T = 4,   /* latents -> codes in the input-gradient operand layout */
-  LCVQ_K_DX = 5,        /* dX (matrix cores + A^T map) */
-  LCVQ_K_DW = 6,        /* dW = dY^T X with dZ, dA, db epilogue (matrix cores) */
-  LCVQ_K_PACK = 7,      /* lcvq_pack2bit */
-  LCVQ_K_DEQUANT = 8,   /* lcvq_dequant */
-  LCVQ_K_FILL = 9,      /* zero fills of degenerate shapes */
-  LCVQ_K_ADAM = 10,     /* lcvq_adamw_step */
-  LCVQ_K_COUNT = 11
+  LCVQ_K_FWD_PREP = 0,  /* forward prepass: codes in the product's operand layout (+ 2-bit pack)
+                           and X' = X blockdiag(A), s = X b~ */
+  LCVQ_K_FWD = 1,       /* Y = X' codes^T + s 1^T */
+  LCVQ_K_BWD_PREP = 2,  /* backward prepass: codes in the input-gradient operand layout, X' and dY
+                           in the weight-gradient operand layout (fp32: row sums of dY) */
+  LCVQ_K_DX = 3,        /* dX (with dA, db in bf16 mode) */
+  LCVQ_K_DW = 4,        /* dZ = mask * (dY^T X') (with dA, db in fp32 mode) */
+  LCVQ_K_PACK = 5,      /* lcvq_pack2bit */
+  LCVQ_K_DEQUANT = 6,   /* lcvq_dequant */
+  LCVQ_K_FILL = 7,      /* zero fills of degenerate shapes */
+  LCVQ_K_ADAM = 8,      /* lcvq_adamw_step */
+  LCVQ_K_COUNT = 9
 } lcvq_kernel_t;
 lcvq_status_t lcvq_timer_enable(uint32_t mask);
 lcvq_status_t lcvq_timer_read(int32_t kernel, double *total_ms, int64_t *launches);

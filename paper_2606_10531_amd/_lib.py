@@ -17,7 +17,7 @@ MASK_ROUNDED, MASK_LATENT = 0, 1
 # lcvq_op_t
 OP_FWD, OP_BWD = 0, 1
 # lcvq_kernel_t
-KERNELS = ["quant", "act", "fwd", "bwd_prep", "quant_t", "dx", "dw", "pack", "dequant", "fill", "adam"]
+KERNELS = ["fwd_prep", "fwd", "bwd_prep", "dx", "dw", "pack", "dequant", "fill", "adam"]
 
 _P = ctypes.c_void_p
 _I64 = ctypes.c_int64

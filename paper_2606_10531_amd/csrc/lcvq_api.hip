@@ -74,11 +74,11 @@ BwdLayout bwd_layout(int64_t N, int64_t m, int64_t n, bool bf16) {
   BwdLayout L{};
   L.rs = 0;
   if (bf16) {
-    // per-token sums; codes in the input-gradient operand layout; X' and dY in
-    // the token-K fragment layout (tokens padded to 128, features to 256)
-    const size_t rs = up256((size_t)lcvq::round_up(N, 256) * 4);
-    const size_t frag = (size_t)(lcvq::round_up(n, 256) / 32) * (lcvq::round_up(m, 128) / 64) * 1024;
+    // partial row sums of dY; codes in the input-gradient operand layout; X'
+    // and dY in the token-K fragment layout (tokens padded to 128, features to 256)
     const size_t Nt = (size_t)lcvq::round_up(N, 128);
+    const size_t rs = up256((size_t)lcvq::rowsum_parts(m) * Nt * 4);
+    const size_t frag = (size_t)(lcvq::round_up(n, 256) / 32) * (lcvq::round_up(m, 128) / 64) * 1024;
     L.frag = rs;
     L.xt = L.frag + up256(frag);
     L.dyt = L.xt + up256((size_t)lcvq::round_up(n, 256) * Nt * 2);
@@ -321,14 +321,16 @@ lcvq_status_t lcvq_linear_fwd(int64_t N, int64_t m, int64_t n, int32_t d, int32_
   hipError_t e;
   if (bf16) {
     uint32_t *frag = (uint32_t *)(ws + L.frag);
-    { Timed tm(LCVQ_K_QUANT, st); e = tm.done(lcvq::launch_quant_frag(Z, true, m, n, false, frag, packed_codes_out, st)); }
-    if (e != hipSuccess) return hip_fail(e, "quantise launch");
-    { Timed tm(LCVQ_K_ACT, st); e = tm.done(lcvq::launch_act_transform(X, true, N, L.Np, n, d, A, b, ws + L.xp, L.ldp, svec, st)); }
-    if (e != hipSuccess) return hip_fail(e, "activation transform launch");
+    {
+      Timed tm(LCVQ_K_FWD_PREP, st);
+      e = tm.done(lcvq::launch_fwd_prep_bf16((const uint16_t *)Z, m, n, frag, packed_codes_out, (const uint16_t *)X, N,
+                                             L.Np, L.ldp, d, A, b, (uint16_t *)(ws + L.xp), svec, st));
+    }
+    if (e != hipSuccess) return hip_fail(e, "forward prepass launch");
     { Timed tm(LCVQ_K_FWD, st); e = tm.done(lcvq::launch_fwd_bf16(frag, (const uint16_t *)(ws + L.xp), L.ldp, svec, (uint16_t *)Y, N, m, n, st)); }
     if (e != hipSuccess) return hip_fail(e, "forward product launch");
   } else {
-    { Timed tm(LCVQ_K_ACT, st); e = tm.done(lcvq::launch_act_transform(X, false, N, N, n, d, A, b, ws + L.xp, n, svec, st)); }
+    { Timed tm(LCVQ_K_FWD_PREP, st); e = tm.done(lcvq::launch_act_transform(X, false, N, N, n, d, A, b, ws + L.xp, n, svec, st)); }
     if (e != hipSuccess) return hip_fail(e, "activation transform launch");
     { Timed tm(LCVQ_K_FWD, st); e = tm.done(lcvq::launch_fwd_f32((const float *)Z, (const float *)(ws + L.xp), svec, (float *)Y, N, m, n, st)); }
     if (e != hipSuccess) return hip_fail(e, "forward product launch");
@@ -388,24 +390,22 @@ lcvq_status_t lcvq_linear_bwd(int64_t N, int64_t m, int64_t n, int32_t d, int32_
   const bool clear_map = want_map && !accumulate;
 
   if (bf16) {
-    // 1. codes (input-gradient operand layout); its first block clears rs and,
-    //    when overwriting, dA/db, which later kernels accumulate into
-    // 2. X' = X blockdiag(A) and dY transposed into fragments, rs = row sums of dY
-    // 3. dX = (dY codes) A-map + rs b (+ dA, db)      4. dZ = mask * dY^T X'
+    // 1. one prepass launch: codes in the input-gradient operand layout (when
+    //    dX or dA/db are wanted), X' = X blockdiag(A) and dY in the weight-
+    //    gradient fragments (when dZ is wanted); its first block clears dA/db
+    //    when overwriting them
+    //    and the partial row sums of dY
+    // 2. dX = (dY codes) A-map + rowsum(dY) b (+ dA, db)    3. dZ = mask * dY^T X'
     const bool run_dx = dX != nullptr || want_map;
     uint32_t *frag = (uint32_t *)(ws + L.frag);
     uint16_t *xt = (uint16_t *)(ws + L.xt), *dyt = (uint16_t *)(ws + L.dyt);
-    if (run_dx) {
-      Timed tm(LCVQ_K_QUANT_T, st);
-      e = tm.done(lcvq::launch_quant_frag(Z, true, m, n, true, frag, nullptr, st, rs, lcvq::round_up(N, 256),
-                                          clear_map ? dA : nullptr, clear_map ? d * d : 0,
-                                          clear_map ? db : nullptr, clear_map ? d : 0));
-      if (e != hipSuccess) return hip_fail(e, "quantise launch");
-    }
     {
       Timed tm(LCVQ_K_BWD_PREP, st);
-      e = tm.done(lcvq::launch_bwd_prep((const uint16_t *)X, (const uint16_t *)dY, A, d, N, m, n, xt, dyt, rs, st));
-      if (e != hipSuccess) return hip_fail(e, "backward operand launch");
+      e = tm.done(lcvq::launch_bwd_prep_bf16((const uint16_t *)Z, m, n, run_dx ? frag : nullptr, (const uint16_t *)X,
+                                             (const uint16_t *)dY, A, d, N, dZ != nullptr ? xt : nullptr,
+                                             dZ != nullptr ? dyt : nullptr, rs, clear_map ? dA : nullptr,
+                                             clear_map ? d * d : 0, clear_map ? db : nullptr, clear_map ? d : 0, st));
+      if (e != hipSuccess) return hip_fail(e, "backward prepass launch");
     }
     if (run_dx) {
       Timed tm(LCVQ_K_DX, st);

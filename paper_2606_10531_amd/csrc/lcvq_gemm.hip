@@ -188,9 +188,9 @@ __global__ __launch_bounds__(256, 1) void k_gemm_codes(
   // for all of them.
   const __amdgpu_buffer_rsrc_t ro = make_rsrc(out + tw * ldo, out == nullptr ? 0 : (Tvalid - tw) * ldo * 2);
   const int64_t cb0 = (int64_t)tm * kTile + 16 * h;
-  // Per-token term: s of the forward (up to kMaxParts partial rows vstride
-  // apart, summed here) or rowsum(dY) of the input gradient.
-  constexpr int kMaxParts = kMode == 0 ? 8 : 1;
+  // Per-token term, held as up to kMaxParts partial rows vstride apart and
+  // summed here: s of the forward, rowsum(dY) of the input gradient.
+  constexpr int kMaxParts = 8;
   const __amdgpu_buffer_rsrc_t rv = make_rsrc(vecT + tw, ((int64_t)(vparts - 1) * vstride + Tvalid - tw) * 4);
   float vp[kMaxParts][2], vt[2];
 #pragma unroll
@@ -513,18 +513,20 @@ hipError_t launch_fwd_bf16(const uint32_t *frag, const uint16_t *Xp, int64_t ldp
   return hipGetLastError();
 }
 
-hipError_t launch_dx_bf16(const uint32_t *frag, const uint16_t *dY, const float *rs, const float *A,
-                          const float *b, int d, uint16_t *dX, const uint16_t *X, float *dA, float *db, int64_t N,
-                          int64_t m, int64_t n, hipStream_t st) {
+hipError_t launch_dx_bf16(const uint32_t *frag, const uint16_t *dY, const float *rsp, const float *A, const float *b,
+                          int d, uint16_t *dX, const uint16_t *X, float *dA, float *db, int64_t N, int64_t m, int64_t n,
+                          hipStream_t st) {
+  const int parts = rowsum_parts(m);
+  const int64_t Nt = round_up(N, 128);  // row stride of the partial row sums
   const int tiles_m = (int)ceil_div(n, kTile), tiles_n = (int)ceil_div(N, kTile);
   const int KB = (int)(round_up(m, 128) / kKStep);  // even, matches the operand layout
   // dX == nullptr: the product still runs for dA/db; its stores are dropped.
   if (d == 8)
-    k_gemm_codes<1, 8><<<tiles_m * tiles_n, 256, 0, st>>>(frag, KB, dY, (int)m, N, (int)m, tiles_m, tiles_n, rs, 1,
-                                                          0, A, b, dX, n, n, N, X, dA, db);
+    k_gemm_codes<1, 8><<<tiles_m * tiles_n, 256, 0, st>>>(frag, KB, dY, (int)m, N, (int)m, tiles_m, tiles_n, rsp,
+                                                          parts, Nt, A, b, dX, n, n, N, X, dA, db);
   else
-    k_gemm_codes<1, 4><<<tiles_m * tiles_n, 256, 0, st>>>(frag, KB, dY, (int)m, N, (int)m, tiles_m, tiles_n, rs, 1,
-                                                          0, A, b, dX, n, n, N, X, dA, db);
+    k_gemm_codes<1, 4><<<tiles_m * tiles_n, 256, 0, st>>>(frag, KB, dY, (int)m, N, (int)m, tiles_m, tiles_n, rsp,
+                                                          parts, Nt, A, b, dX, n, n, N, X, dA, db);
   return hipGetLastError();
 }
 

@@ -67,25 +67,17 @@ __device__ __forceinline__ float block_sum256(float v, float *red /* >= 4 floats
 }
 
 // ---- quantise into the operand layout --------------------------------------
-// One block per 64 x 64 tile of Z (rows r, columns c).  kTrans = false: the
-// operand's M axis is r and its K axis c (forward product); kTrans = true: M is
-// c and K is r (input-gradient product).  Tiles beyond Z hold code 0.
-// The first block also clears up to three float buffers, used by the backward
-// for the per-token sums and the map gradients that later kernels accumulate into.
+// One 64 x 64 tile (tile row by, tile column bx) of Z (rows r, columns c).
+// kTrans = false: the operand's M axis is r and its K axis c (forward product);
+// kTrans = true: M is c and K is r (input-gradient product).  Elements beyond Z
+// hold code 0.  With `packed`, the forward also writes the tile's 2-bit codes.
+typedef uint8_t CodeTile[64][64 + 4];
 template <typename ZT, bool kTrans>
-__global__ __launch_bounds__(256) void k_quant_frag(const ZT *__restrict__ Z, int64_t m, int64_t n,
-                                                     uint32_t *__restrict__ frag, int KB,
-                                                     uint8_t *__restrict__ packed, float *__restrict__ zero,
-                                                     int64_t nz, float *__restrict__ zero2, int nz2,
-                                                     float *__restrict__ zero3, int nz3) {
-  __shared__ uint8_t codes[64][64 + 4];
+__device__ __forceinline__ void quant_tile(int bx, int by, const ZT *__restrict__ Z, int64_t m, int64_t n,
+                                           uint32_t *__restrict__ frag, int KB, uint8_t *__restrict__ packed,
+                                           CodeTile &codes) {
   const int tid = threadIdx.x;
-  if (blockIdx.x == 0 && blockIdx.y == 0) {
-    for (int64_t i = tid; i < nz; i += 256) zero[i] = 0.0f;
-    for (int i = tid; i < nz2; i += 256) zero2[i] = 0.0f;
-    for (int i = tid; i < nz3; i += 256) zero3[i] = 0.0f;
-  }
-  const int64_t r0 = (int64_t)blockIdx.y * 64, c0 = (int64_t)blockIdx.x * 64;
+  const int64_t r0 = (int64_t)by * 64, c0 = (int64_t)bx * 64;
 #pragma unroll
   for (int i = 0; i < 2; ++i) {
     const int id = tid + 256 * i, rr = id >> 3, cc = (id & 7) * 8;
@@ -111,28 +103,54 @@ __global__ __launch_bounds__(256) void k_quant_frag(const ZT *__restrict__ Z, in
       const uint32_t c = kTrans ? codes[kloc + j][mloc] : codes[mloc][kloc + j];
       w |= c << (4 * j);
     }
-    const int mb = (kTrans ? (int)blockIdx.x : (int)blockIdx.y) * 2 + slab;
-    const int kb = kTrans ? (int)blockIdx.y : (int)blockIdx.x;
+    const int mb = (kTrans ? bx : by) * 2 + slab;
+    const int kb = kTrans ? by : bx;
     frag[frag_dword_index(mb, kb, KB, lane, kk)] = w;
   }
-  if (!kTrans && packed != nullptr) {
-    // 2-bit packing of the same tile: thread -> (row, 16 codes), stored as two
-    // 16-bit words (n % 8 == 0 keeps them aligned).
-    const int rr = tid >> 2, w = tid & 3;
-    const int64_t r = r0 + rr;
+  if (!kTrans && packed != nullptr && tid < 64) {
+    // 2-bit packing of the same tile: thread -> one row's 64 codes = 16 bytes
+    // (n % 8 == 0 keeps every 8-code half aligned)
+    const int64_t r = r0 + tid;
     if (r < m) {
 #pragma unroll
-      for (int h = 0; h < 2; ++h) {
-        const int64_t c = c0 + 16 * w + 8 * h;
-        if (c < n) {
-          uint32_t bits = 0;
+      for (int hq = 0; hq < 2; ++hq) {
+        const int64_t c = c0 + 32 * hq;
+        uint32_t bits[2];
 #pragma unroll
-          for (int j = 0; j < 8; ++j) bits |= (uint32_t)codes[rr][16 * w + 8 * h + j] << (2 * j);
-          *reinterpret_cast<uint16_t *>(packed + r * (n / 4) + c / 4) = (uint16_t)bits;
+        for (int w = 0; w < 2; ++w) {
+          bits[w] = 0;
+#pragma unroll
+          for (int j = 0; j < 16; ++j) bits[w] |= (uint32_t)codes[tid][32 * hq + 16 * w + j] << (2 * j);
+        }
+        uint8_t *dst = packed + r * (n / 4) + c / 4;
+        if (c + 32 <= n && ((n / 4) & 7) == 0) {  // whole, 8-byte aligned
+          *reinterpret_cast<uint2 *>(dst) = make_uint2(bits[0], bits[1]);
+        } else {  // 16-bit pieces: n % 8 == 0 keeps them 2-byte aligned
+          const int64_t end = c + 32 < n ? c + 32 : n;
+          for (int64_t q = c; q < end; q += 8)
+            *reinterpret_cast<uint16_t *>(dst + (q - c) / 4) = (uint16_t)(bits[(q - c) / 16] >> (2 * ((q - c) % 16)));
         }
       }
     }
   }
+}
+
+// Stand-alone quantiser (the fp32 path and the packing-only forward).  The
+// first block also clears up to three float buffers.
+template <typename ZT, bool kTrans>
+__global__ __launch_bounds__(256) void k_quant_frag(const ZT *__restrict__ Z, int64_t m, int64_t n,
+                                                     uint32_t *__restrict__ frag, int KB,
+                                                     uint8_t *__restrict__ packed, float *__restrict__ zero,
+                                                     int64_t nz, float *__restrict__ zero2, int nz2,
+                                                     float *__restrict__ zero3, int nz3) {
+  __shared__ CodeTile codes;
+  const int tid = threadIdx.x;
+  if (blockIdx.x == 0 && blockIdx.y == 0) {
+    for (int64_t i = tid; i < nz; i += 256) zero[i] = 0.0f;
+    for (int i = tid; i < nz2; i += 256) zero2[i] = 0.0f;
+    for (int i = tid; i < nz3; i += 256) zero3[i] = 0.0f;
+  }
+  quant_tile<ZT, kTrans>((int)blockIdx.x, (int)blockIdx.y, Z, m, n, frag, KB, packed, codes);
 }
 
 // ---- activation transform (def. forward_x), fp32 row-major -----------------
@@ -186,15 +204,12 @@ __global__ __launch_bounds__(256) void k_act_transform(const XT *__restrict__ X,
 // and each wave writes one whole 1 KiB fragment per sub-step.  Tokens >= N and
 // K >= n give zeros.  sp[kc * Np + t] = this chunk's part of s[t].
 template <int D>
-__global__ __launch_bounds__(256) void k_act_frag(const uint16_t *__restrict__ X, int64_t N, int64_t n,
-                                                   const float *__restrict__ A, const float *__restrict__ b,
-                                                   uint16_t *__restrict__ Xp, int KB, int spc, int64_t Np,
-                                                   float *__restrict__ sp) {
-  __shared__ float red[4][32];
+__device__ __forceinline__ void act_block(int64_t tb, int kc, const uint16_t *__restrict__ X, int64_t N, int64_t n,
+                                          const float *__restrict__ A, const float *__restrict__ b,
+                                          uint16_t *__restrict__ Xp, int KB, int spc, int64_t Np,
+                                          float *__restrict__ sp, float (&red)[4][32]) {
   const int tid = threadIdx.x, lane = tid & 63, h = lane >> 5;
   const int wave = tid >> 6;
-  const int64_t tb = blockIdx.x;
-  const int kc = blockIdx.y;
   const int64_t rows = N - tb * 32;  // > 0 only for blocks that hold real tokens
   const __amdgpu_buffer_rsrc_t rx = make_rsrc(X + tb * 32 * n, rows > 0 ? (rows < 32 ? rows : 32) * n * 2 : 0);
   float a[D][D], bb[D];
@@ -244,6 +259,28 @@ __global__ __launch_bounds__(256) void k_act_frag(const uint16_t *__restrict__ X
   if (lane < 32) red[wave][lane] = acc_s;
   __syncthreads();
   if (tid < 32) sp[(int64_t)kc * Np + tb * 32 + tid] = red[0][tid] + red[1][tid] + red[2][tid] + red[3][tid];
+}
+
+// ---- forward prepass, bf16: one launch for both operands ---------------------
+// Blocks [0, nq): quantise tiles of Z (tile (id % gq, id / gq), K = columns),
+// with the 2-bit pack when `packed` is set; blocks [nq, nq + ntb * nkc): the
+// activation transform, block (tb, kc) = ((id - nq) % ntb, (id - nq) / ntb).
+template <int D>
+__global__ __launch_bounds__(256) void k_fwd_prep(const uint16_t *__restrict__ Z, int64_t m, int64_t n,
+                                                   uint32_t *__restrict__ frag, uint8_t *__restrict__ packed, int gq,
+                                                   int nq, const uint16_t *__restrict__ X, int64_t N,
+                                                   const float *__restrict__ A, const float *__restrict__ b,
+                                                   uint16_t *__restrict__ Xp, int KB, int spc, int64_t Np,
+                                                   float *__restrict__ sp) {
+  __shared__ CodeTile codes;
+  __shared__ float red[4][32];
+  const int id = blockIdx.x;
+  if (id < nq) {
+    quant_tile<uint16_t, false>(id % gq, id / gq, Z, m, n, frag, KB, packed, codes);
+  } else {
+    const int j = id - nq, ntb = (int)(Np / 32);
+    act_block<D>(j % ntb, j / ntb, X, N, n, A, b, Xp, KB, spc, Np, sp, red);
+  }
 }
 
 // ---- per-token sums of dY (dX offset term) ---------------------------------
@@ -376,29 +413,20 @@ __global__ __launch_bounds__(256) void k_dequant(const void *__restrict__ src, i
 }
 
 // ---- backward operands of the weight-gradient product ----------------------
-// One block per 64 tokens x 64 features of either X (blockIdx.y < nfx) or dY.
-// X rows become X' = X blockdiag(A) (so the product yields dW blockdiag(A)
-// directly); both are written transposed into the token-K fragment layout
-// (X' on the M side, dY on the N side), zero-padded to KBt steps and to whole
-// 256-feature tiles.  dY rows are also summed into rs[t] (atomics; rs cleared
-// beforehand).
-template <int D>
-__global__ __launch_bounds__(256) void k_bwd_prep(const uint16_t *__restrict__ X, const uint16_t *__restrict__ dY,
-                                                   const float *__restrict__ A, int64_t N, int64_t n, int64_t m,
-                                                   int KBt, int nfx, uint16_t *__restrict__ xt,
-                                                   uint16_t *__restrict__ dyt, float *__restrict__ rs) {
-  __shared__ __attribute__((aligned(16))) uint16_t tile[64][64 + 8];
+// One 64-token (bt) x 64-feature (f0) sub-tile of X or dY.  X rows become
+// X' = X blockdiag(A) (so the product yields dW blockdiag(A) directly); both
+// are written transposed into the token-K fragment layout (X' on the M side,
+// dY on the N side), zero-padded to KBt steps and to whole 256-feature tiles.
+// For dY, each thread's two rows (row0 = tid / 8 and row0 + 32) get their
+// partial sums over the sub-tile added to rsum[0..1] (threads with tid % 8 == 0
+// hold the row totals).
+template <int D, bool kIsX>
+__device__ __forceinline__ void bwd_subtile(int bt, int64_t f0, const uint16_t *__restrict__ src, int64_t F,
+                                            const float (&a)[D][D], int64_t N, int KBt,
+                                            uint16_t *__restrict__ dst, uint16_t (&tile)[64][64 + 8],
+                                            float (&rsum)[2]) {
   const int tid = threadIdx.x;
-  const bool isx = (int)blockIdx.y < nfx;
-  const int64_t t0 = (int64_t)blockIdx.x * 64;
-  const int64_t f0 = (int64_t)(isx ? blockIdx.y : blockIdx.y - nfx) * 64;
-  const int64_t F = isx ? n : m;
-  const uint16_t *src = isx ? X : dY;
-  float a[D][D];
-#pragma unroll
-  for (int j = 0; j < D; ++j)
-#pragma unroll
-    for (int k = 0; k < D; ++k) a[j][k] = A[j * D + k];
+  const int64_t t0 = (int64_t)bt * 64;
 #pragma unroll
   for (int i = 0; i < 2; ++i) {
     const int id = tid + 256 * i, row = id >> 3, ch = id & 7;
@@ -411,7 +439,7 @@ __global__ __launch_bounds__(256) void k_bwd_prep(const uint16_t *__restrict__ X
       for (int e = 0; e < 8; ++e) v[e] = 0.0f;
     }
     float o[8];
-    if (isx) {
+    if constexpr (kIsX) {
 #pragma unroll
       for (int g = 0; g < 8 / D; ++g)
 #pragma unroll
@@ -422,16 +450,17 @@ __global__ __launch_bounds__(256) void k_bwd_prep(const uint16_t *__restrict__ X
           o[g * D + k] = y;
         }
     } else {
-#pragma unroll
-      for (int e = 0; e < 8; ++e) o[e] = v[e];
-      // row sum over this chunk, then over the row's eight chunks (lanes id .. id + 7)
       float sum = 0.0f;
 #pragma unroll
-      for (int e = 0; e < 8; ++e) sum += v[e];
+      for (int e = 0; e < 8; ++e) {
+        o[e] = v[e];
+        sum += v[e];
+      }
+      // over the row's eight 8-feature chunks (lanes id .. id + 7)
       sum += __shfl_xor(sum, 1, 64);
       sum += __shfl_xor(sum, 2, 64);
       sum += __shfl_xor(sum, 4, 64);
-      if (ch == 0 && t < N) unsafeAtomicAdd(rs + t, sum);
+      rsum[i] += sum;
     }
     u32x4 w;
 #pragma unroll
@@ -439,11 +468,10 @@ __global__ __launch_bounds__(256) void k_bwd_prep(const uint16_t *__restrict__ X
     *reinterpret_cast<u32x4 *>(&tile[row][ch * 8]) = w;
   }
   __syncthreads();
-  uint16_t *dst = isx ? xt : dyt;
 #pragma unroll
-  for (int i = 0; i < 2; ++i) {
+  for (int i = 0; i < 2 && dst != nullptr; ++i) {
     const int id = tid + 256 * i, fb = id >> 8, kk = (id >> 6) & 3, L = id & 63;
-    const int fl = fb * 32 + (isx ? perm32(L & 31) : (L & 31));
+    const int fl = fb * 32 + (kIsX ? perm32(L & 31) : (L & 31));
     const int tl = kk * 16 + 8 * (L >> 5);
     u32x4 w;
 #pragma unroll
@@ -451,6 +479,110 @@ __global__ __launch_bounds__(256) void k_bwd_prep(const uint16_t *__restrict__ X
     const int64_t blk = (f0 >> 5) + fb;
     *reinterpret_cast<u32x4 *>(dst + (((blk * KBt + (t0 >> 6)) * 4 + kk) * 64 + L) * 8) = w;
   }
+  __syncthreads();  // the tile is reused by the next sub-tile
+}
+
+// dY part (bt, p): sub-tiles [sf0, sf1) of 64 out-features for tokens
+// 64 bt .. 64 bt + 63, written transposed into dyt (when set) and summed per
+// row into rsum[0..1] (rows tid / 8 and tid / 8 + 32, totals in threads with
+// tid % 8 == 0).  The loads of sub-tile sf + 1 are issued before sub-tile sf is
+// transposed and stored.
+__device__ __forceinline__ void dy_part(int bt, int sf0, int sf1, const uint16_t *__restrict__ dY, int64_t m,
+                                        int64_t N, int KBt, uint16_t *__restrict__ dyt, uint16_t (&tile)[64][64 + 8],
+                                        float (&rsum)[2]) {
+  const int tid = threadIdx.x;
+  const int64_t t0 = (int64_t)bt * 64;
+  auto load = [&](int sf, u32x4 (&v)[2]) {
+#pragma unroll
+    for (int i = 0; i < 2; ++i) {
+      const int id = tid + 256 * i, row = id >> 3, ch = id & 7;
+      const int64_t t = t0 + row, f = (int64_t)sf * 64 + ch * 8;
+      if (t < N && f < m) v[i] = *reinterpret_cast<const u32x4 *>(dY + t * m + f);
+      else v[i] = u32x4{0u, 0u, 0u, 0u};
+    }
+  };
+  u32x4 nxt[2];
+  if (sf0 < sf1) load(sf0, nxt);
+  for (int sf = sf0; sf < sf1; ++sf) {
+    u32x4 cur[2] = {nxt[0], nxt[1]};
+    if (sf + 1 < sf1) load(sf + 1, nxt);
+#pragma unroll
+    for (int i = 0; i < 2; ++i) {
+      const int id = tid + 256 * i, row = id >> 3, ch = id & 7;
+      float sum = 0.0f;
+#pragma unroll
+      for (int e = 0; e < 4; ++e) sum += bf16_lo(cur[i][e]) + bf16_hi(cur[i][e]);
+      sum += __shfl_xor(sum, 1, 64);
+      sum += __shfl_xor(sum, 2, 64);
+      sum += __shfl_xor(sum, 4, 64);
+      rsum[i] += sum;
+      if (dyt != nullptr) *reinterpret_cast<u32x4 *>(&tile[row][ch * 8]) = cur[i];
+    }
+    if (dyt == nullptr) continue;
+    __syncthreads();
+#pragma unroll
+    for (int i = 0; i < 2; ++i) {
+      const int id = tid + 256 * i, fb = id >> 8, kk = (id >> 6) & 3, L = id & 63;
+      const int fl = fb * 32 + (L & 31);
+      const int tl = kk * 16 + 8 * (L >> 5);
+      u32x4 w;
+#pragma unroll
+      for (int e = 0; e < 4; ++e) w[e] = (uint32_t)tile[tl + 2 * e][fl] | ((uint32_t)tile[tl + 2 * e + 1][fl] << 16);
+      const int64_t blk = (int64_t)sf * 2 + fb;
+      *reinterpret_cast<u32x4 *>(dyt + (((blk * KBt + bt) * 4 + kk) * 64 + L) * 8) = w;
+    }
+    __syncthreads();  // the tile is rewritten by the next sub-tile
+  }
+}
+
+// ---- backward prepass, bf16: one launch for all operands --------------------
+// Blocks [0, KBt * nrp): dY parts, block (bt, p) = (id % KBt, id / KBt) covers
+// out-feature sub-tiles [p * spf, (p + 1) * spf) and writes its partial row
+// sums to rsp[p * Nt + t] (Nt = KBt * 64; no atomics); these are the longest
+// blocks and go first.  Then nq quantise tiles into the input-gradient operand
+// layout (tile (q % gq, q / gq), K = rows of Z), then KBt * nfx X' sub-tiles
+// (tile (bt, fx) = (x % KBt, x / KBt)).
+// Block 0 clears dA (nza floats) and db (nzb) when the backward overwrites them
+// (the input-gradient kernel, launched after this one, accumulates into them).
+template <int D>
+__global__ __launch_bounds__(256) void k_bwd_prep(const uint16_t *__restrict__ Z, int64_t m, int64_t n,
+                                                   uint32_t *__restrict__ frag, int KBq, int gq, int nq,
+                                                   const uint16_t *__restrict__ X, const uint16_t *__restrict__ dY,
+                                                   const float *__restrict__ A, int64_t N, int KBt, int nfx,
+                                                   int nfy, int spf, int nrp, uint16_t *__restrict__ xt,
+                                                   uint16_t *__restrict__ dyt, float *__restrict__ rsp,
+                                                   float *__restrict__ za, int nza, float *__restrict__ zb, int nzb) {
+  __shared__ CodeTile codes;
+  __shared__ __attribute__((aligned(16))) uint16_t tile[64][64 + 8];
+  const int id = blockIdx.x, tid = threadIdx.x;
+  if (id == 0) {
+    for (int i = tid; i < nza; i += 256) za[i] = 0.0f;
+    for (int i = tid; i < nzb; i += 256) zb[i] = 0.0f;
+  }
+  const int ndy = KBt * nrp;
+  float rsum[2] = {0.0f, 0.0f};
+  if (id < ndy) {
+    const int bt = id % KBt, p = id / KBt;
+    dy_part(bt, p * spf, min((p + 1) * spf, nfy), dY, m, N, KBt, dyt, tile, rsum);
+    if ((tid & 7) == 0) {
+      const int64_t Nt = (int64_t)KBt * 64, t = (int64_t)bt * 64 + (tid >> 3);
+      rsp[(int64_t)p * Nt + t] = rsum[0];
+      rsp[(int64_t)p * Nt + t + 32] = rsum[1];
+    }
+    return;
+  }
+  const int q = id - ndy;
+  if (q < nq) {
+    quant_tile<uint16_t, true>(q % gq, q / gq, Z, m, n, frag, KBq, nullptr, codes);
+    return;
+  }
+  const int x = q - nq;
+  float a[D][D];
+#pragma unroll
+  for (int jj = 0; jj < D; ++jj)
+#pragma unroll
+    for (int k = 0; k < D; ++k) a[jj][k] = A[jj * D + k];
+  bwd_subtile<D, true>(x % KBt, (int64_t)(x / KBt) * 64, X, n, a, N, KBt, xt, tile, rsum);
 }
 
 // ---- launchers -------------------------------------------------------------
@@ -481,16 +613,23 @@ hipError_t launch_quant_frag(const void *Z, bool z_bf16, int64_t m, int64_t n, b
 hipError_t launch_act_transform(const void *X, bool bf16, int64_t N, int64_t Np, int64_t n, int d,
                                 const float *A, const float *b, void *Xp, int64_t ldp, float *s,
                                 hipStream_t st) {
-  dim3 grid((unsigned)Np);
-  if (bf16) {  // matrix-core layout, one partial s per K chunk
-    const int KB = (int)(ldp / 64), spc = act_steps_per_chunk(ldp);
-    dim3 g2((unsigned)(Np / 32), (unsigned)act_chunks(ldp));
-    if (d == 8) k_act_frag<8><<<g2, 256, 0, st>>>((const uint16_t *)X, N, n, A, b, (uint16_t *)Xp, KB, spc, Np, s);
-    else k_act_frag<4><<<g2, 256, 0, st>>>((const uint16_t *)X, N, n, A, b, (uint16_t *)Xp, KB, spc, Np, s);
-  } else {  // row-major
-    if (d == 8) k_act_transform<float, float, 8><<<grid, 256, 0, st>>>((const float *)X, N, n, A, b, (float *)Xp, ldp, s);
-    else k_act_transform<float, float, 4><<<grid, 256, 0, st>>>((const float *)X, N, n, A, b, (float *)Xp, ldp, s);
-  }
+  (void)Np;
+  (void)bf16;  // fp32 only: the bf16 transform runs inside launch_fwd_prep_bf16
+  dim3 grid((unsigned)N);
+  if (d == 8) k_act_transform<float, float, 8><<<grid, 256, 0, st>>>((const float *)X, N, n, A, b, (float *)Xp, ldp, s);
+  else k_act_transform<float, float, 4><<<grid, 256, 0, st>>>((const float *)X, N, n, A, b, (float *)Xp, ldp, s);
+  return hipGetLastError();
+}
+
+hipError_t launch_fwd_prep_bf16(const uint16_t *Z, int64_t m, int64_t n, uint32_t *frag, uint8_t *packed,
+                                const uint16_t *X, int64_t N, int64_t Np, int64_t ldp, int d, const float *A,
+                                const float *b, uint16_t *Xp, float *sp, hipStream_t st) {
+  const int KB = (int)(ldp / 64);
+  const int gq = KB, nq = gq * (int)(round_up(m, 256) / 64);  // K = columns (ldp), M = rows padded to 256
+  const int ntb = (int)(Np / 32), nkc = act_chunks(ldp), spc = act_steps_per_chunk(ldp);
+  const unsigned grid = (unsigned)(nq + ntb * nkc);
+  if (d == 8) k_fwd_prep<8><<<grid, 256, 0, st>>>(Z, m, n, frag, packed, gq, nq, X, N, A, b, Xp, KB, spc, Np, sp);
+  else k_fwd_prep<4><<<grid, 256, 0, st>>>(Z, m, n, frag, packed, gq, nq, X, N, A, b, Xp, KB, spc, Np, sp);
   return hipGetLastError();
 }
 
@@ -548,13 +687,24 @@ hipError_t launch_dequant(const void *src, int kind, bool z_bf16, int64_t m, int
 }  // namespace lcvq
 
 namespace lcvq {
-hipError_t launch_bwd_prep(const uint16_t *X, const uint16_t *dY, const float *A, int d, int64_t N, int64_t m,
-                           int64_t n, uint16_t *xt, uint16_t *dyt, float *rs, hipStream_t st) {
+hipError_t launch_bwd_prep_bf16(const uint16_t *Z, int64_t m, int64_t n, uint32_t *frag, const uint16_t *X,
+                                const uint16_t *dY, const float *A, int d, int64_t N, uint16_t *xt, uint16_t *dyt,
+                                float *rsp, float *za, int nza, float *zb, int nzb, hipStream_t st) {
+  // codes: M = columns of Z padded to 256, K = rows padded to 128 (skipped when frag == nullptr)
+  const int gq = (int)(round_up(n, 256) / 64), KBq = (int)(round_up(m, 128) / 64);
+  const int nq = frag != nullptr ? gq * KBq : 0;
+  // X' sub-tiles (only when xt is wanted) and dY parts (always: they give the
+  // row sums; their transposed copy is written only when dyt is set)
   const int KBt = (int)(round_up(N, 128) / 64);
-  const int nfx = (int)(round_up(n, 256) / 64), nfy = (int)(round_up(m, 256) / 64);
-  dim3 grid((unsigned)KBt, (unsigned)(nfx + nfy));
-  if (d == 8) k_bwd_prep<8><<<grid, 256, 0, st>>>(X, dY, A, N, n, m, KBt, nfx, xt, dyt, rs);
-  else k_bwd_prep<4><<<grid, 256, 0, st>>>(X, dY, A, N, n, m, KBt, nfx, xt, dyt, rs);
+  const int nfx = xt != nullptr ? (int)(round_up(n, 256) / 64) : 0;
+  const int nfy = (int)(round_up(m, 256) / 64), spf = rowsum_subtiles_per_part(m), nrp = rowsum_parts(m);
+  const unsigned grid = (unsigned)(nq + KBt * (nfx + nrp));
+  if (d == 8)
+    k_bwd_prep<8><<<grid, 256, 0, st>>>(Z, m, n, frag, KBq, gq, nq, X, dY, A, N, KBt, nfx, nfy, spf, nrp, xt, dyt,
+                                        rsp, za, nza, zb, nzb);
+  else
+    k_bwd_prep<4><<<grid, 256, 0, st>>>(Z, m, n, frag, KBq, gq, nq, X, dY, A, N, KBt, nfx, nfy, spf, nrp, xt, dyt,
+                                        rsp, za, nza, zb, nzb);
   return hipGetLastError();
 }
 }  // namespace lcvq

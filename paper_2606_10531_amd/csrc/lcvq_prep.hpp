@@ -22,8 +22,30 @@ hipError_t launch_quant_frag(const void *Z, bool z_bf16, int64_t m, int64_t n, b
                              uint32_t *frag, uint8_t *packed, hipStream_t st, float *zero = nullptr,
                              int64_t nz = 0, float *zero2 = nullptr, int nz2 = 0, float *zero3 = nullptr,
                              int nz3 = 0);
-hipError_t launch_bwd_prep(const uint16_t *X, const uint16_t *dY, const float *A, int d, int64_t N, int64_t m,
-                           int64_t n, uint16_t *xt, uint16_t *dyt, float *rs, hipStream_t st);
+// bf16 forward prepass: codes (+ 2-bit pack) and X' = X A, partial s, in one launch
+hipError_t launch_fwd_prep_bf16(const uint16_t *Z, int64_t m, int64_t n, uint32_t *frag, uint8_t *packed,
+                                const uint16_t *X, int64_t N, int64_t Np, int64_t ldp, int d, const float *A,
+                                const float *b, uint16_t *Xp, float *sp, hipStream_t st);
+// The bf16 backward prepass sums each dY row in at most eight parts (runs of
+// 64-feature sub-tiles of the out-features, padded to 256); the input-gradient
+// product adds the parts.
+inline int rowsum_subtiles_per_part(int64_t m) {
+  const int64_t nfy = (m + 255) / 256 * 4;
+  const int64_t spf = (nfy + 7) / 8;
+  return spf < 1 ? 1 : (int)spf;
+}
+inline int rowsum_parts(int64_t m) {
+  const int64_t nfy = (m + 255) / 256 * 4;
+  const int64_t p = (nfy + rowsum_subtiles_per_part(m) - 1) / rowsum_subtiles_per_part(m);
+  return p < 1 ? 1 : (int)p;
+}
+// bf16 backward prepass in one launch: codes of the input-gradient product
+// (frag, optional), the weight-gradient operands (xt, dyt; skipped when xt is
+// nullptr) and the partial row sums of dY (rsp: rowsum_parts(m) rows of
+// round_up(N, 128) floats)
+hipError_t launch_bwd_prep_bf16(const uint16_t *Z, int64_t m, int64_t n, uint32_t *frag, const uint16_t *X,
+                                const uint16_t *dY, const float *A, int d, int64_t N, uint16_t *xt, uint16_t *dyt,
+                                float *rsp, float *za, int nza, float *zb, int nzb, hipStream_t st);
 hipError_t launch_act_transform(const void *X, bool bf16, int64_t N, int64_t Np, int64_t n, int d,
                                 const float *A, const float *b, void *Xp, int64_t ldp, float *s,
                                 hipStream_t st);
@@ -42,9 +64,9 @@ hipError_t launch_adamw(float *theta, const void *grad, bool grad_bf16, float *m
 // bf16 matrix-core products (lcvq_gemm.hip)
 hipError_t launch_fwd_bf16(const uint32_t *frag, const uint16_t *Xp, int64_t ldp, const float *s,
                            uint16_t *Y, int64_t N, int64_t m, int64_t n, hipStream_t st);
-hipError_t launch_dx_bf16(const uint32_t *frag, const uint16_t *dY, const float *rs, const float *A,
-                          const float *b, int d, uint16_t *dX, const uint16_t *X, float *dA, float *db, int64_t N,
-                          int64_t m, int64_t n, hipStream_t st);
+hipError_t launch_dx_bf16(const uint32_t *frag, const uint16_t *dY, const float *rsp, const float *A, const float *b,
+                          int d, uint16_t *dX, const uint16_t *X, float *dA, float *db, int64_t N, int64_t m, int64_t n,
+                          hipStream_t st);
 hipError_t launch_dw_bf16(const uint16_t *xt, const uint16_t *dyt, const uint16_t *Z, int mask_mode, int accumulate,
                           void *dZ, bool dz_bf16, int64_t N, int64_t m, int64_t n, hipStream_t st);
 
