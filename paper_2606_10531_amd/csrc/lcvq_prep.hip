@@ -67,90 +67,86 @@ __device__ __forceinline__ float block_sum256(float v, float *red /* >= 4 floats
 }
 
 // ---- quantise into the operand layout --------------------------------------
-// One 64 x 64 tile (tile row by, tile column bx) of Z (rows r, columns c).
-// kTrans = false: the operand's M axis is r and its K axis c (forward product);
-// kTrans = true: M is c and K is r (input-gradient product).  Elements beyond Z
-// hold code 0.  With `packed`, the forward also writes the tile's 2-bit codes.
-typedef uint8_t CodeTile[64][64 + 4];
-template <typename ZT, bool kTrans>
-__device__ __forceinline__ void quant_tile(int bx, int by, const ZT *__restrict__ Z, int64_t m, int64_t n,
-                                           uint32_t *__restrict__ frag, int KB, uint8_t *__restrict__ packed,
-                                           CodeTile &codes) {
+// One block quantises four 64 x 64 tiles of bf16 Z side by side: tile row by
+// (rows r), tile columns 4 bq .. 4 bq + 3 (columns c; those at or past gx are
+// skipped).  kTrans = false: the operand's M axis is r and its K axis c
+// (forward product); kTrans = true: M is c and K is r (input-gradient
+// product).  Elements beyond Z hold code 0.  All loads of the four tiles are
+// issued before the first is used.  With `packed`, the forward also writes the
+// 2-bit codes.
+typedef uint8_t CodeTile[64][64 + 8];  // rows of 72 bytes keep 8-byte stores aligned
+template <bool kTrans>
+__device__ __forceinline__ void quant_block(int bq, int by, int gx, const uint16_t *__restrict__ Z, int64_t m,
+                                            int64_t n, uint32_t *__restrict__ frag, int KB,
+                                            uint8_t *__restrict__ packed, CodeTile (&codes)[4]) {
   const int tid = threadIdx.x;
-  const int64_t r0 = (int64_t)by * 64, c0 = (int64_t)bx * 64;
+  const int64_t r0 = (int64_t)by * 64;
+  u32x4 v[4][2];
 #pragma unroll
-  for (int i = 0; i < 2; ++i) {
-    const int id = tid + 256 * i, rr = id >> 3, cc = (id & 7) * 8;
-    const int64_t r = r0 + rr, c = c0 + cc;
-    float v[8];
-    if (r < m && c < n) {
-      load8(Z + r * n + c, v);
-    } else {
+  for (int q = 0; q < 4; ++q)
 #pragma unroll
-      for (int j = 0; j < 8; ++j) v[j] = 0.0f;
+    for (int i = 0; i < 2; ++i) {
+      const int id = tid + 256 * i, rr = id >> 3, cc = (id & 7) * 8;
+      const int64_t r = r0 + rr, c = (int64_t)(4 * bq + q) * 64 + cc;
+      v[q][i] = u32x4{0u, 0u, 0u, 0u};
+      if (r < m && c < n) v[q][i] = *reinterpret_cast<const u32x4 *>(Z + r * n + c);
     }
 #pragma unroll
-    for (int j = 0; j < 8; ++j) codes[rr][cc + j] = (uint8_t)quant_code(v[j]);
-  }
-  __syncthreads();
+  for (int q = 0; q < 4; ++q)
 #pragma unroll
-  for (int i = 0; i < 2; ++i) {
-    const int id = tid + 256 * i, slab = id >> 8, lane = (id >> 2) & 63, kk = id & 3;
-    const int mloc = slab * 32 + perm32(lane & 31), kloc = 16 * kk + 8 * (lane >> 5);
-    uint32_t w = 0;
+    for (int i = 0; i < 2; ++i) {
+      const int id = tid + 256 * i, rr = id >> 3, cc = (id & 7) * 8;
+      uint32_t lo = 0, hi = 0;
 #pragma unroll
-    for (int j = 0; j < 8; ++j) {
-      const uint32_t c = kTrans ? codes[kloc + j][mloc] : codes[mloc][kloc + j];
-      w |= c << (4 * j);
-    }
-    const int mb = (kTrans ? bx : by) * 2 + slab;
-    const int kb = kTrans ? by : bx;
-    frag[frag_dword_index(mb, kb, KB, lane, kk)] = w;
-  }
-  if (!kTrans && packed != nullptr && tid < 64) {
-    // 2-bit packing of the same tile: thread -> one row's 64 codes = 16 bytes
-    // (n % 8 == 0 keeps every 8-code half aligned)
-    const int64_t r = r0 + tid;
-    if (r < m) {
-#pragma unroll
-      for (int hq = 0; hq < 2; ++hq) {
-        const int64_t c = c0 + 32 * hq;
-        uint32_t bits[2];
-#pragma unroll
-        for (int w = 0; w < 2; ++w) {
-          bits[w] = 0;
-#pragma unroll
-          for (int j = 0; j < 16; ++j) bits[w] |= (uint32_t)codes[tid][32 * hq + 16 * w + j] << (2 * j);
-        }
-        uint8_t *dst = packed + r * (n / 4) + c / 4;
-        if (c + 32 <= n && ((n / 4) & 7) == 0) {  // whole, 8-byte aligned
-          *reinterpret_cast<uint2 *>(dst) = make_uint2(bits[0], bits[1]);
-        } else {  // 16-bit pieces: n % 8 == 0 keeps them 2-byte aligned
-          const int64_t end = c + 32 < n ? c + 32 : n;
-          for (int64_t q = c; q < end; q += 8)
-            *reinterpret_cast<uint16_t *>(dst + (q - c) / 4) = (uint16_t)(bits[(q - c) / 16] >> (2 * ((q - c) % 16)));
+      for (int e = 0; e < 2; ++e) {
+        lo |= (quant_code(bf16_lo(v[q][i][e])) | (quant_code(bf16_hi(v[q][i][e])) << 8)) << (16 * e);
+        hi |= (quant_code(bf16_lo(v[q][i][2 + e])) | (quant_code(bf16_hi(v[q][i][2 + e])) << 8)) << (16 * e);
+      }
+      *reinterpret_cast<uint2 *>(&codes[q][rr][cc]) = make_uint2(lo, hi);
+      if (!kTrans && packed != nullptr) {
+        // 2-bit codes of these 8 columns (16 bits, least significant first);
+        // the even thread of each pair stores its neighbour's 16 bits with its
+        // own (4 bytes, 16 codes; n % 16 == 0 keeps them aligned, else 2-byte
+        // pieces)
+        const uint32_t b2 = (lo & 3u) | ((lo >> 6) & 0xcu) | ((lo >> 12) & 0x30u) | ((lo >> 18) & 0xc0u) |
+                            ((hi & 3u) << 8) | ((hi << 2) & 0xc00u) | ((hi >> 4) & 0x3000u) | ((hi >> 10) & 0xc000u);
+        const uint32_t nb = (uint32_t)__shfl_xor((int)b2, 1, 64);
+        const int64_t r = r0 + rr, c = (int64_t)(4 * bq + q) * 64 + cc;
+        if (r < m && c < n) {
+          uint8_t *dst = packed + r * (n / 4) + c / 4;
+          if ((n & 15) == 0) {
+            if ((id & 1) == 0) *reinterpret_cast<uint32_t *>(dst) = b2 | (nb << 16);
+          } else {
+            *reinterpret_cast<uint16_t *>(dst) = (uint16_t)b2;
+          }
         }
       }
     }
+  __syncthreads();
+#pragma unroll
+  for (int q = 0; q < 4; ++q) {
+    const int bx = 4 * bq + q;
+    if (bx >= gx) break;
+#pragma unroll
+    for (int i = 0; i < 2; ++i) {
+      const int id = tid + 256 * i, slab = id >> 8, lane = (id >> 2) & 63, kk = id & 3;
+      const int mloc = slab * 32 + perm32(lane & 31), kloc = 16 * kk + 8 * (lane >> 5);
+      uint32_t w = 0;
+      if constexpr (kTrans) {
+#pragma unroll
+        for (int j = 0; j < 8; ++j) w |= (uint32_t)codes[q][kloc + j][mloc] << (4 * j);
+      } else {
+        // eight consecutive codes (bytes, each <= 3) -> eight nibbles
+        const uint2 c8 = *reinterpret_cast<const uint2 *>(&codes[q][mloc][kloc]);
+        w = (c8.x & 0xfu) | ((c8.x >> 4) & 0xf0u) | ((c8.x >> 8) & 0xf00u) | ((c8.x >> 12) & 0xf000u) |
+            ((c8.y & 0xfu) << 16) | ((c8.y << 12) & 0xf00000u) | ((c8.y << 8) & 0xf000000u) |
+            ((c8.y << 4) & 0xf0000000u);
+      }
+      const int mb = (kTrans ? bx : by) * 2 + slab;
+      const int kb = kTrans ? by : bx;
+      frag[frag_dword_index(mb, kb, KB, lane, kk)] = w;
+    }
   }
-}
-
-// Stand-alone quantiser (the fp32 path and the packing-only forward).  The
-// first block also clears up to three float buffers.
-template <typename ZT, bool kTrans>
-__global__ __launch_bounds__(256) void k_quant_frag(const ZT *__restrict__ Z, int64_t m, int64_t n,
-                                                     uint32_t *__restrict__ frag, int KB,
-                                                     uint8_t *__restrict__ packed, float *__restrict__ zero,
-                                                     int64_t nz, float *__restrict__ zero2, int nz2,
-                                                     float *__restrict__ zero3, int nz3) {
-  __shared__ CodeTile codes;
-  const int tid = threadIdx.x;
-  if (blockIdx.x == 0 && blockIdx.y == 0) {
-    for (int64_t i = tid; i < nz; i += 256) zero[i] = 0.0f;
-    for (int i = tid; i < nz2; i += 256) zero2[i] = 0.0f;
-    for (int i = tid; i < nz3; i += 256) zero3[i] = 0.0f;
-  }
-  quant_tile<ZT, kTrans>((int)blockIdx.x, (int)blockIdx.y, Z, m, n, frag, KB, packed, codes);
 }
 
 // ---- activation transform (def. forward_x), fp32 row-major -----------------
@@ -221,38 +217,49 @@ __device__ __forceinline__ void act_block(int64_t tb, int kc, const uint16_t *__
   }
   const int kb0 = kc * spc, kb1 = min(kb0 + spc, KB);
   float acc_s = 0.0f;
-  for (int kb = kb0 + wave; kb < kb1; kb += 4) {
-    u32x4 xv[4];
+  // batches of 8 steps: this wave's two (kb0 + 8 i + wave + 4 s), all 8
+  // loads issued before the first is used
+  for (int base = kb0 + wave; base < kb1; base += 8) {
+    u32x4 xv[2][4];
 #pragma unroll
-    for (int kk = 0; kk < 4; ++kk) {
-      const int64_t k = (int64_t)kb * 64 + 16 * kk + 8 * h;
-      const uint32_t off = k < n ? (uint32_t)(((lane & 31) * n + k) * 2) : kOffNone;
-      xv[kk] = __builtin_amdgcn_raw_buffer_load_b128(rx, off, 0, 0);
-    }
-    uint16_t *dst = Xp + ((tb * KB + kb) * 4) * 512 + lane * 8;
+    for (int st = 0; st < 2; ++st) {
+      const int kb = base + 4 * st;
 #pragma unroll
-    for (int kk = 0; kk < 4; ++kk) {
-      float x[8], y[8];
-#pragma unroll
-      for (int e = 0; e < 4; ++e) {
-        x[2 * e] = bf16_lo(xv[kk][e]);
-        x[2 * e + 1] = bf16_hi(xv[kk][e]);
+      for (int kk = 0; kk < 4; ++kk) {
+        const int64_t k = (int64_t)kb * 64 + 16 * kk + 8 * h;
+        const uint32_t off = (kb < kb1 && k < n) ? (uint32_t)(((lane & 31) * n + k) * 2) : kOffNone;
+        xv[st][kk] = __builtin_amdgcn_raw_buffer_load_b128(rx, off, 0, 0);
       }
+    }
 #pragma unroll
-      for (int g = 0; g < 8 / D; ++g)
+    for (int st = 0; st < 2; ++st) {
+      const int kb = base + 4 * st;
+      if (kb >= kb1) break;
+      uint16_t *dst = Xp + ((tb * KB + kb) * 4) * 512 + lane * 8;
 #pragma unroll
-        for (int k = 0; k < D; ++k) {
-          float v = 0.0f;
+      for (int kk = 0; kk < 4; ++kk) {
+        float x[8], y[8];
 #pragma unroll
-          for (int j = 0; j < D; ++j) v = fmaf(x[g * D + j], a[j][k], v);
-          y[g * D + k] = v;
+        for (int e = 0; e < 4; ++e) {
+          x[2 * e] = bf16_lo(xv[st][kk][e]);
+          x[2 * e + 1] = bf16_hi(xv[st][kk][e]);
         }
 #pragma unroll
-      for (int e = 0; e < 8; ++e) acc_s = fmaf(x[e], bb[e % D], acc_s);
-      u32x4 w;
+        for (int g = 0; g < 8 / D; ++g)
 #pragma unroll
-      for (int e = 0; e < 4; ++e) w[e] = pack_bf16x2(y[2 * e], y[2 * e + 1]);
-      *reinterpret_cast<u32x4 *>(dst + kk * 512) = w;
+          for (int k = 0; k < D; ++k) {
+            float v = 0.0f;
+#pragma unroll
+            for (int j = 0; j < D; ++j) v = fmaf(x[g * D + j], a[j][k], v);
+            y[g * D + k] = v;
+          }
+#pragma unroll
+        for (int e = 0; e < 8; ++e) acc_s = fmaf(x[e], bb[e % D], acc_s);
+        u32x4 w;
+#pragma unroll
+        for (int e = 0; e < 4; ++e) w[e] = pack_bf16x2(y[2 * e], y[2 * e + 1]);
+        *reinterpret_cast<u32x4 *>(dst + kk * 512) = w;
+      }
     }
   }
   acc_s += __shfl_xor(acc_s, 32, 64);
@@ -262,8 +269,8 @@ __device__ __forceinline__ void act_block(int64_t tb, int kc, const uint16_t *__
 }
 
 // ---- forward prepass, bf16: one launch for both operands ---------------------
-// Blocks [0, nq): quantise tiles of Z (tile (id % gq, id / gq), K = columns),
-// with the 2-bit pack when `packed` is set; blocks [nq, nq + ntb * nkc): the
+// Blocks [0, nq): quantise blocks of Z (four 64 x 64 tiles each, block
+// (id % gq, id / gq), K = columns), with the 2-bit pack when `packed` is set; blocks [nq, nq + ntb * nkc): the
 // activation transform, block (tb, kc) = ((id - nq) % ntb, (id - nq) / ntb).
 template <int D>
 __global__ __launch_bounds__(256) void k_fwd_prep(const uint16_t *__restrict__ Z, int64_t m, int64_t n,
@@ -272,11 +279,11 @@ __global__ __launch_bounds__(256) void k_fwd_prep(const uint16_t *__restrict__ Z
                                                    const float *__restrict__ A, const float *__restrict__ b,
                                                    uint16_t *__restrict__ Xp, int KB, int spc, int64_t Np,
                                                    float *__restrict__ sp) {
-  __shared__ CodeTile codes;
+  __shared__ CodeTile codes[4];
   __shared__ float red[4][32];
   const int id = blockIdx.x;
   if (id < nq) {
-    quant_tile<uint16_t, false>(id % gq, id / gq, Z, m, n, frag, KB, packed, codes);
+    quant_block<false>(id % gq, id / gq, KB, Z, m, n, frag, KB, packed, codes);
   } else {
     const int j = id - nq, ntb = (int)(Np / 32);
     act_block<D>(j % ntb, j / ntb, X, N, n, A, b, Xp, KB, spc, Np, sp, red);
@@ -413,125 +420,118 @@ __global__ __launch_bounds__(256) void k_dequant(const void *__restrict__ src, i
 }
 
 // ---- backward operands of the weight-gradient product ----------------------
-// One 64-token (bt) x 64-feature (f0) sub-tile of X or dY.  X rows become
-// X' = X blockdiag(A) (so the product yields dW blockdiag(A) directly); both
-// are written transposed into the token-K fragment layout (X' on the M side,
-// dY on the N side), zero-padded to KBt steps and to whole 256-feature tiles.
-// For dY, each thread's two rows (row0 = tid / 8 and row0 + 32) get their
-// partial sums over the sub-tile added to rsum[0..1] (threads with tid % 8 == 0
-// hold the row totals).
-template <int D, bool kIsX>
-__device__ __forceinline__ void bwd_subtile(int bt, int64_t f0, const uint16_t *__restrict__ src, int64_t F,
-                                            const float (&a)[D][D], int64_t N, int KBt,
-                                            uint16_t *__restrict__ dst, uint16_t (&tile)[64][64 + 8],
-                                            float (&rsum)[2]) {
+// Transposed store of one 64-token x 64-feature sub-tile from the LDS tile
+// into the token-K fragment layout (zero-padded to KBt steps and to whole
+// 256-feature tiles): block (f0 / 32 + fb, bt), sub-step kk, lane L holds
+// tokens kk * 16 + 8 (L / 32) + 0..7 of feature sel(L % 32), sel = perm32 for
+// in-features (M side) and the identity for out-features (N side).
+template <bool kMside>
+__device__ __forceinline__ void tile_store_t(int bt, int64_t f0, int KBt, uint16_t *__restrict__ dst,
+                                             const uint16_t (&tile)[64][64 + 8]) {
   const int tid = threadIdx.x;
-  const int64_t t0 = (int64_t)bt * 64;
 #pragma unroll
   for (int i = 0; i < 2; ++i) {
-    const int id = tid + 256 * i, row = id >> 3, ch = id & 7;
-    const int64_t t = t0 + row, f = f0 + ch * 8;
-    float v[8];
-    if (t < N && f < F) {
-      load8(src + t * F + f, v);
-    } else {
+    const int id = tid + 256 * i, fb = id >> 8, kk = (id >> 6) & 3, L = id & 63;
+    const int fl = fb * 32 + (kMside ? perm32(L & 31) : (L & 31));
+    const int tl = kk * 16 + 8 * (L >> 5);
+    u32x4 w;
 #pragma unroll
-      for (int e = 0; e < 8; ++e) v[e] = 0.0f;
+    for (int e = 0; e < 4; ++e) w[e] = (uint32_t)tile[tl + 2 * e][fl] | ((uint32_t)tile[tl + 2 * e + 1][fl] << 16);
+    const int64_t blk = (f0 >> 5) + fb;
+    *reinterpret_cast<u32x4 *>(dst + (((blk * KBt + bt) * 4 + kk) * 64 + L) * 8) = w;
+  }
+}
+
+// Loads of up to four 64 x 64 sub-tiles (columns 64 (sf0 + q), q < nsub) of a
+// row-major bf16 matrix with F columns, rows t0 .. t0 + 63 (only rows < `rows`
+// are read): thread -> rows tid / 8 and tid / 8 + 32, 8 columns at (tid % 8) * 8.
+__device__ __forceinline__ void load_subtiles4(u32x4 (&v)[4][2], const uint16_t *__restrict__ src, int64_t F,
+                                               int64_t t0, int64_t rows, int sf0, int nsub) {
+  const int tid = threadIdx.x;
+#pragma unroll
+  for (int q = 0; q < 4; ++q)
+#pragma unroll
+    for (int i = 0; i < 2; ++i) {
+      const int id = tid + 256 * i, row = id >> 3, ch = id & 7;
+      const int64_t t = t0 + row, f = (int64_t)(sf0 + q) * 64 + ch * 8;
+      v[q][i] = u32x4{0u, 0u, 0u, 0u};
+      if (q < nsub && t < rows && f < F) v[q][i] = *reinterpret_cast<const u32x4 *>(src + t * F + f);
     }
-    float o[8];
-    if constexpr (kIsX) {
+}
+
+// X block (bt, fx4): tokens 64 bt .. + 63, in-features 256 fx4 .. + 255.  Rows
+// become X' = X blockdiag(A) (so the product yields dW blockdiag(A) directly)
+// and are written transposed into xt.
+template <int D>
+__device__ __forceinline__ void x_block(int bt, int fx4, const uint16_t *__restrict__ X, int64_t n, int64_t N,
+                                        const float (&a)[D][D], int KBt, uint16_t *__restrict__ xt,
+                                        uint16_t (&tile)[64][64 + 8]) {
+  const int tid = threadIdx.x;
+  u32x4 v[4][2];
+  load_subtiles4(v, X, n, (int64_t)bt * 64, N, 4 * fx4, 4);
+#pragma unroll
+  for (int q = 0; q < 4; ++q) {
+#pragma unroll
+    for (int i = 0; i < 2; ++i) {
+      const int id = tid + 256 * i;
+      float x[8], o[8];
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        x[2 * e] = bf16_lo(v[q][i][e]);
+        x[2 * e + 1] = bf16_hi(v[q][i][e]);
+      }
 #pragma unroll
       for (int g = 0; g < 8 / D; ++g)
 #pragma unroll
         for (int k = 0; k < D; ++k) {
           float y = 0.0f;
 #pragma unroll
-          for (int j = 0; j < D; ++j) y = fmaf(v[g * D + j], a[j][k], y);
+          for (int j = 0; j < D; ++j) y = fmaf(x[g * D + j], a[j][k], y);
           o[g * D + k] = y;
         }
-    } else {
-      float sum = 0.0f;
+      u32x4 w;
 #pragma unroll
-      for (int e = 0; e < 8; ++e) {
-        o[e] = v[e];
-        sum += v[e];
-      }
-      // over the row's eight 8-feature chunks (lanes id .. id + 7)
-      sum += __shfl_xor(sum, 1, 64);
-      sum += __shfl_xor(sum, 2, 64);
-      sum += __shfl_xor(sum, 4, 64);
-      rsum[i] += sum;
+      for (int e = 0; e < 4; ++e) w[e] = pack_bf16x2(o[2 * e], o[2 * e + 1]);
+      *reinterpret_cast<u32x4 *>(&tile[id >> 3][(id & 7) * 8]) = w;
     }
-    u32x4 w;
-#pragma unroll
-    for (int e = 0; e < 4; ++e) w[e] = pack_bf16x2(o[2 * e], o[2 * e + 1]);
-    *reinterpret_cast<u32x4 *>(&tile[row][ch * 8]) = w;
+    __syncthreads();
+    tile_store_t<true>(bt, (int64_t)(4 * fx4 + q) * 64, KBt, xt, tile);
+    __syncthreads();  // the tile is rewritten for the next sub-tile
   }
-  __syncthreads();
-#pragma unroll
-  for (int i = 0; i < 2 && dst != nullptr; ++i) {
-    const int id = tid + 256 * i, fb = id >> 8, kk = (id >> 6) & 3, L = id & 63;
-    const int fl = fb * 32 + (kIsX ? perm32(L & 31) : (L & 31));
-    const int tl = kk * 16 + 8 * (L >> 5);
-    u32x4 w;
-#pragma unroll
-    for (int e = 0; e < 4; ++e) w[e] = (uint32_t)tile[tl + 2 * e][fl] | ((uint32_t)tile[tl + 2 * e + 1][fl] << 16);
-    const int64_t blk = (f0 >> 5) + fb;
-    *reinterpret_cast<u32x4 *>(dst + (((blk * KBt + (t0 >> 6)) * 4 + kk) * 64 + L) * 8) = w;
-  }
-  __syncthreads();  // the tile is reused by the next sub-tile
 }
 
 // dY part (bt, p): sub-tiles [sf0, sf1) of 64 out-features for tokens
 // 64 bt .. 64 bt + 63, written transposed into dyt (when set) and summed per
 // row into rsum[0..1] (rows tid / 8 and tid / 8 + 32, totals in threads with
-// tid % 8 == 0).  The loads of sub-tile sf + 1 are issued before sub-tile sf is
-// transposed and stored.
+// tid % 8 == 0).  Sub-tiles are loaded four at a time.
 __device__ __forceinline__ void dy_part(int bt, int sf0, int sf1, const uint16_t *__restrict__ dY, int64_t m,
                                         int64_t N, int KBt, uint16_t *__restrict__ dyt, uint16_t (&tile)[64][64 + 8],
                                         float (&rsum)[2]) {
   const int tid = threadIdx.x;
-  const int64_t t0 = (int64_t)bt * 64;
-  auto load = [&](int sf, u32x4 (&v)[2]) {
+  for (int base = sf0; base < sf1; base += 4) {
+    u32x4 v[4][2];
+    load_subtiles4(v, dY, m, (int64_t)bt * 64, N, base, sf1 - base);
 #pragma unroll
-    for (int i = 0; i < 2; ++i) {
-      const int id = tid + 256 * i, row = id >> 3, ch = id & 7;
-      const int64_t t = t0 + row, f = (int64_t)sf * 64 + ch * 8;
-      if (t < N && f < m) v[i] = *reinterpret_cast<const u32x4 *>(dY + t * m + f);
-      else v[i] = u32x4{0u, 0u, 0u, 0u};
+    for (int q = 0; q < 4; ++q) {
+      if (base + q >= sf1) break;
+#pragma unroll
+      for (int i = 0; i < 2; ++i) {
+        const int id = tid + 256 * i;
+        float sum = 0.0f;
+#pragma unroll
+        for (int e = 0; e < 4; ++e) sum += bf16_lo(v[q][i][e]) + bf16_hi(v[q][i][e]);
+        // over the row's eight 8-feature chunks (lanes id .. id + 7)
+        sum += __shfl_xor(sum, 1, 64);
+        sum += __shfl_xor(sum, 2, 64);
+        sum += __shfl_xor(sum, 4, 64);
+        rsum[i] += sum;
+        if (dyt != nullptr) *reinterpret_cast<u32x4 *>(&tile[id >> 3][(id & 7) * 8]) = v[q][i];
+      }
+      if (dyt == nullptr) continue;
+      __syncthreads();
+      tile_store_t<false>(bt, (int64_t)(base + q) * 64, KBt, dyt, tile);
+      __syncthreads();  // the tile is rewritten by the next sub-tile
     }
-  };
-  u32x4 nxt[2];
-  if (sf0 < sf1) load(sf0, nxt);
-  for (int sf = sf0; sf < sf1; ++sf) {
-    u32x4 cur[2] = {nxt[0], nxt[1]};
-    if (sf + 1 < sf1) load(sf + 1, nxt);
-#pragma unroll
-    for (int i = 0; i < 2; ++i) {
-      const int id = tid + 256 * i, row = id >> 3, ch = id & 7;
-      float sum = 0.0f;
-#pragma unroll
-      for (int e = 0; e < 4; ++e) sum += bf16_lo(cur[i][e]) + bf16_hi(cur[i][e]);
-      sum += __shfl_xor(sum, 1, 64);
-      sum += __shfl_xor(sum, 2, 64);
-      sum += __shfl_xor(sum, 4, 64);
-      rsum[i] += sum;
-      if (dyt != nullptr) *reinterpret_cast<u32x4 *>(&tile[row][ch * 8]) = cur[i];
-    }
-    if (dyt == nullptr) continue;
-    __syncthreads();
-#pragma unroll
-    for (int i = 0; i < 2; ++i) {
-      const int id = tid + 256 * i, fb = id >> 8, kk = (id >> 6) & 3, L = id & 63;
-      const int fl = fb * 32 + (L & 31);
-      const int tl = kk * 16 + 8 * (L >> 5);
-      u32x4 w;
-#pragma unroll
-      for (int e = 0; e < 4; ++e) w[e] = (uint32_t)tile[tl + 2 * e][fl] | ((uint32_t)tile[tl + 2 * e + 1][fl] << 16);
-      const int64_t blk = (int64_t)sf * 2 + fb;
-      *reinterpret_cast<u32x4 *>(dyt + (((blk * KBt + bt) * 4 + kk) * 64 + L) * 8) = w;
-    }
-    __syncthreads();  // the tile is rewritten by the next sub-tile
   }
 }
 
@@ -539,20 +539,20 @@ __device__ __forceinline__ void dy_part(int bt, int sf0, int sf1, const uint16_t
 // Blocks [0, KBt * nrp): dY parts, block (bt, p) = (id % KBt, id / KBt) covers
 // out-feature sub-tiles [p * spf, (p + 1) * spf) and writes its partial row
 // sums to rsp[p * Nt + t] (Nt = KBt * 64; no atomics); these are the longest
-// blocks and go first.  Then nq quantise tiles into the input-gradient operand
-// layout (tile (q % gq, q / gq), K = rows of Z), then KBt * nfx X' sub-tiles
-// (tile (bt, fx) = (x % KBt, x / KBt)).
+// blocks and go first.  Then nq quantise blocks into the input-gradient operand
+// layout (four tiles each, block (q % gq, q / gq), K = rows of Z), then
+// KBt * nfx4 X' blocks of 64 tokens x 256 in-features (block (x % KBt, x / KBt)).
 // Block 0 clears dA (nza floats) and db (nzb) when the backward overwrites them
 // (the input-gradient kernel, launched after this one, accumulates into them).
 template <int D>
 __global__ __launch_bounds__(256) void k_bwd_prep(const uint16_t *__restrict__ Z, int64_t m, int64_t n,
                                                    uint32_t *__restrict__ frag, int KBq, int gq, int nq,
                                                    const uint16_t *__restrict__ X, const uint16_t *__restrict__ dY,
-                                                   const float *__restrict__ A, int64_t N, int KBt, int nfx,
+                                                   const float *__restrict__ A, int64_t N, int KBt, int nfx4,
                                                    int nfy, int spf, int nrp, uint16_t *__restrict__ xt,
                                                    uint16_t *__restrict__ dyt, float *__restrict__ rsp,
                                                    float *__restrict__ za, int nza, float *__restrict__ zb, int nzb) {
-  __shared__ CodeTile codes;
+  __shared__ CodeTile codes[4];
   __shared__ __attribute__((aligned(16))) uint16_t tile[64][64 + 8];
   const int id = blockIdx.x, tid = threadIdx.x;
   if (id == 0) {
@@ -573,7 +573,7 @@ __global__ __launch_bounds__(256) void k_bwd_prep(const uint16_t *__restrict__ Z
   }
   const int q = id - ndy;
   if (q < nq) {
-    quant_tile<uint16_t, true>(q % gq, q / gq, Z, m, n, frag, KBq, nullptr, codes);
+    quant_block<true>(q % gq, q / gq, 4 * gq, Z, m, n, frag, KBq, nullptr, codes);
     return;
   }
   const int x = q - nq;
@@ -582,7 +582,7 @@ __global__ __launch_bounds__(256) void k_bwd_prep(const uint16_t *__restrict__ Z
   for (int jj = 0; jj < D; ++jj)
 #pragma unroll
     for (int k = 0; k < D; ++k) a[jj][k] = A[jj * D + k];
-  bwd_subtile<D, true>(x % KBt, (int64_t)(x / KBt) * 64, X, n, a, N, KBt, xt, tile, rsum);
+  x_block<D>(x % KBt, x / KBt, X, n, N, a, KBt, xt, tile);
 }
 
 // ---- launchers -------------------------------------------------------------
@@ -591,23 +591,6 @@ static inline int grid_for(int64_t items, int64_t per_block) {
   int64_t g = ceil_div(items, per_block);
   if (g > 65536) g = 65536;
   return (int)(g < 1 ? 1 : g);
-}
-
-hipError_t launch_quant_frag(const void *Z, bool z_bf16, int64_t m, int64_t n, bool trans,
-                             uint32_t *frag, uint8_t *packed, hipStream_t st, float *zero, int64_t nz,
-                             float *zero2, int nz2, float *zero3, int nz3) {
-  // forward: M = r padded to 256, K = c padded to 64; transposed: M = c, K = r
-  const int64_t Mp = round_up(trans ? n : m, 256), Kp = round_up(trans ? m : n, 128);
-  const int KB = (int)(Kp / 64);
-  dim3 grid(trans ? (unsigned)(Mp / 64) : (unsigned)(Kp / 64), trans ? (unsigned)(Kp / 64) : (unsigned)(Mp / 64));
-  if (z_bf16) {
-    if (trans) k_quant_frag<uint16_t, true><<<grid, 256, 0, st>>>((const uint16_t *)Z, m, n, frag, KB, nullptr, zero, nz, zero2, nz2, zero3, nz3);
-    else k_quant_frag<uint16_t, false><<<grid, 256, 0, st>>>((const uint16_t *)Z, m, n, frag, KB, packed, zero, nz, zero2, nz2, zero3, nz3);
-  } else {
-    if (trans) k_quant_frag<float, true><<<grid, 256, 0, st>>>((const float *)Z, m, n, frag, KB, nullptr, zero, nz, zero2, nz2, zero3, nz3);
-    else k_quant_frag<float, false><<<grid, 256, 0, st>>>((const float *)Z, m, n, frag, KB, packed, zero, nz, zero2, nz2, zero3, nz3);
-  }
-  return hipGetLastError();
 }
 
 hipError_t launch_act_transform(const void *X, bool bf16, int64_t N, int64_t Np, int64_t n, int d,
@@ -625,7 +608,8 @@ hipError_t launch_fwd_prep_bf16(const uint16_t *Z, int64_t m, int64_t n, uint32_
                                 const uint16_t *X, int64_t N, int64_t Np, int64_t ldp, int d, const float *A,
                                 const float *b, uint16_t *Xp, float *sp, hipStream_t st) {
   const int KB = (int)(ldp / 64);
-  const int gq = KB, nq = gq * (int)(round_up(m, 256) / 64);  // K = columns (ldp), M = rows padded to 256
+  // quantise blocks: K = columns (ldp / 64 tiles, four per block), M = rows padded to 256
+  const int gq = (KB + 3) / 4, nq = gq * (int)(round_up(m, 256) / 64);
   const int ntb = (int)(Np / 32), nkc = act_chunks(ldp), spc = act_steps_per_chunk(ldp);
   const unsigned grid = (unsigned)(nq + ntb * nkc);
   if (d == 8) k_fwd_prep<8><<<grid, 256, 0, st>>>(Z, m, n, frag, packed, gq, nq, X, N, A, b, Xp, KB, spc, Np, sp);
@@ -690,20 +674,21 @@ namespace lcvq {
 hipError_t launch_bwd_prep_bf16(const uint16_t *Z, int64_t m, int64_t n, uint32_t *frag, const uint16_t *X,
                                 const uint16_t *dY, const float *A, int d, int64_t N, uint16_t *xt, uint16_t *dyt,
                                 float *rsp, float *za, int nza, float *zb, int nzb, hipStream_t st) {
-  // codes: M = columns of Z padded to 256, K = rows padded to 128 (skipped when frag == nullptr)
-  const int gq = (int)(round_up(n, 256) / 64), KBq = (int)(round_up(m, 128) / 64);
+  // codes: M = columns of Z padded to 256 (four 64-column tiles per block), K = rows
+  // padded to 128 (skipped when frag == nullptr)
+  const int gq = (int)(round_up(n, 256) / 256), KBq = (int)(round_up(m, 128) / 64);
   const int nq = frag != nullptr ? gq * KBq : 0;
   // X' sub-tiles (only when xt is wanted) and dY parts (always: they give the
   // row sums; their transposed copy is written only when dyt is set)
   const int KBt = (int)(round_up(N, 128) / 64);
-  const int nfx = xt != nullptr ? (int)(round_up(n, 256) / 64) : 0;
+  const int nfx4 = xt != nullptr ? (int)(round_up(n, 256) / 256) : 0;
   const int nfy = (int)(round_up(m, 256) / 64), spf = rowsum_subtiles_per_part(m), nrp = rowsum_parts(m);
-  const unsigned grid = (unsigned)(nq + KBt * (nfx + nrp));
+  const unsigned grid = (unsigned)(nq + KBt * (nfx4 + nrp));
   if (d == 8)
-    k_bwd_prep<8><<<grid, 256, 0, st>>>(Z, m, n, frag, KBq, gq, nq, X, dY, A, N, KBt, nfx, nfy, spf, nrp, xt, dyt,
+    k_bwd_prep<8><<<grid, 256, 0, st>>>(Z, m, n, frag, KBq, gq, nq, X, dY, A, N, KBt, nfx4, nfy, spf, nrp, xt, dyt,
                                         rsp, za, nza, zb, nzb);
   else
-    k_bwd_prep<4><<<grid, 256, 0, st>>>(Z, m, n, frag, KBq, gq, nq, X, dY, A, N, KBt, nfx, nfy, spf, nrp, xt, dyt,
+    k_bwd_prep<4><<<grid, 256, 0, st>>>(Z, m, n, frag, KBq, gq, nq, X, dY, A, N, KBt, nfx4, nfy, spf, nrp, xt, dyt,
                                         rsp, za, nza, zb, nzb);
   return hipGetLastError();
 }

@@ -7,10 +7,11 @@ namespace lcvq {
 
 // The bf16 activation transform splits K into at most eight chunks and writes
 // one partial s per chunk (rows of Np floats); the forward product sums them.
-// Both are at least 1 (ldp may be 0 for an empty problem).
+// Both are at least 1 (ldp may be 0 for an empty problem).  A chunk is a
+// whole number of 8-step batches (two steps per wave, loads issued together).
 inline int act_steps_per_chunk(int64_t ldp) {
   const int64_t spc = (ldp / 64 + 7) / 8;
-  return spc < 1 ? 1 : (int)spc;
+  return spc <= 8 ? 8 : (int)((spc + 7) / 8 * 8);
 }
 inline int act_chunks(int64_t ldp) {
   const int64_t c = (ldp / 64 + act_steps_per_chunk(ldp) - 1) / act_steps_per_chunk(ldp);
@@ -18,10 +19,6 @@ inline int act_chunks(int64_t ldp) {
 }
 
 // streaming kernels (lcvq_prep.hip)
-hipError_t launch_quant_frag(const void *Z, bool z_bf16, int64_t m, int64_t n, bool trans,
-                             uint32_t *frag, uint8_t *packed, hipStream_t st, float *zero = nullptr,
-                             int64_t nz = 0, float *zero2 = nullptr, int nz2 = 0, float *zero3 = nullptr,
-                             int nz3 = 0);
 // bf16 forward prepass: codes (+ 2-bit pack) and X' = X A, partial s, in one launch
 hipError_t launch_fwd_prep_bf16(const uint16_t *Z, int64_t m, int64_t n, uint32_t *frag, uint8_t *packed,
                                 const uint16_t *X, int64_t N, int64_t Np, int64_t ldp, int d, const float *A,
