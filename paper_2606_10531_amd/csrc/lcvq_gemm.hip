@@ -78,10 +78,10 @@ __device__ __forceinline__ uint32_t as_u(float f) { return __float_as_uint(f); }
 // db[j] = sum_{t,g} X[t, g*D + j] rs[t] (the chain rule through X' = X blockdiag(A)
 // and s = X b~), reduced lanes -> wave -> block and added with one atomic per
 // block per entry.  X is N x Mvalid row-major; dA == nullptr skips this.
-template <int kMode, int D>  // kMode 0: forward (B = X' fragments), 1: input gradient (B = dY rows)
+template <int kMode, int D>  // kMode 0: forward (B = X' fragments), 1: input gradient (B = dY fragments)
 __global__ __launch_bounds__(256, 1) void k_gemm_codes(
-    const uint32_t *__restrict__ frag, int KB, const uint16_t *__restrict__ Bsrc, int ldb,
-    int64_t brows, int kvalid, int tiles_m, int tiles_n, const float *__restrict__ vecT, int vparts,
+    const uint32_t *__restrict__ frag, int KB, const uint16_t *__restrict__ Bsrc,
+    int tiles_m, int tiles_n, const float *__restrict__ vecT, int vparts,
     int64_t vstride, const float *__restrict__ A, const float *__restrict__ bvec, uint16_t *__restrict__ out,
     int64_t ldo, int64_t Mvalid, int64_t Tvalid, const uint16_t *__restrict__ X,
     float *__restrict__ dA, float *__restrict__ db) {
@@ -94,25 +94,14 @@ __global__ __launch_bounds__(256, 1) void k_gemm_codes(
 
   // codes: slabs tm * 8 + mi, 1 KiB per (slab, step), lane owns 16 bytes
   const __amdgpu_buffer_rsrc_t rsA = make_rsrc(frag + (size_t)(tm * 8) * KB * 256, (int64_t)8 * KB * 1024);
-  // activations of tokens tw .. tw + 63
-  __amdgpu_buffer_rsrc_t rsB;
+  // B operand of tokens tw .. tw + 63 (X' for the forward, dY for the input
+  // gradient), both in the B-operand fragment layout with KB K steps
+  const __amdgpu_buffer_rsrc_t rsB = make_rsrc(Bsrc + (tw >> 5) * (int64_t)KB * 2048, (int64_t)2 * KB * 4096);
   uint32_t boff[2][4];  // per (ni, kk): byte offset of this lane's 16 bytes at step 0
-  uint32_t kofs[4];     // per kk: this lane's K index at step 0 (input gradient K tail)
-  if constexpr (kMode == 0) {
-    rsB = make_rsrc(Bsrc + (tw >> 5) * (int64_t)KB * 2048, (int64_t)2 * KB * 4096);
 #pragma unroll
-    for (int ni = 0; ni < 2; ++ni)
+  for (int ni = 0; ni < 2; ++ni)
 #pragma unroll
-      for (int kk = 0; kk < 4; ++kk) boff[ni][kk] = (uint32_t)((ni * KB * 4 + kk) * 1024 + lane * 16);
-  } else {
-    rsB = make_rsrc(Bsrc + tw * ldb, (brows - tw) * (int64_t)ldb * 2);
-#pragma unroll
-    for (int kk = 0; kk < 4; ++kk) {
-      kofs[kk] = (uint32_t)(16 * kk + 8 * h);
-#pragma unroll
-      for (int ni = 0; ni < 2; ++ni) boff[ni][kk] = (uint32_t)(((32 * ni + (lane & 31)) * ldb + 16 * kk + 8 * h) * 2);
-    }
-  }
+    for (int kk = 0; kk < 4; ++kk) boff[ni][kk] = (uint32_t)((ni * KB * 4 + kk) * 1024 + lane * 16);
 
   floatx16 acc[8][2];
 #pragma unroll
@@ -133,17 +122,9 @@ __global__ __launch_bounds__(256, 1) void k_gemm_codes(
 #pragma unroll
     for (int ni = 0; ni < 2; ++ni)
 #pragma unroll
-      for (int kk = 0; kk < 4; ++kk) {
-        uint32_t off;
-        bool ok = live;
-        if constexpr (kMode == 0) {
-          off = boff[ni][kk] + (uint32_t)kb * 4096u;
-        } else {
-          off = (uint32_t)kb * 128u + boff[ni][kk];
-          ok = ok && (uint32_t)kb * 64u + kofs[kk] < (uint32_t)kvalid;
-        }
-        cb[buf][ni][kk] = __builtin_amdgcn_raw_buffer_load_b128(rsB, (int)(ok ? off : kOffNone), 0, 0);
-      }
+      for (int kk = 0; kk < 4; ++kk)
+        cb[buf][ni][kk] = __builtin_amdgcn_raw_buffer_load_b128(
+            rsB, live ? (int)(boff[ni][kk] + (uint32_t)kb * 4096u) : (int)kOffNone, 0, 0);
   };
   auto compute = [&](int buf) {
 #pragma unroll
@@ -508,24 +489,24 @@ hipError_t launch_fwd_bf16(const uint32_t *frag, const uint16_t *Xp, int64_t ldp
   const int tiles_m = (int)ceil_div(m, kTile), tiles_n = (int)ceil_div(N, kTile);
   const int KB = (int)(ldp / kKStep);  // even: ldp is a multiple of 128
   const int64_t Np = (int64_t)tiles_n * kTile;
-  k_gemm_codes<0, 8><<<tiles_m * tiles_n, 256, 0, st>>>(frag, KB, Xp, (int)ldp, Np, (int)ldp, tiles_m, tiles_n, s,
+  k_gemm_codes<0, 8><<<tiles_m * tiles_n, 256, 0, st>>>(frag, KB, Xp, tiles_m, tiles_n, s,
                                                         act_chunks(ldp), Np, nullptr, nullptr, Y, m, m, N, nullptr, nullptr, nullptr);
   return hipGetLastError();
 }
 
-hipError_t launch_dx_bf16(const uint32_t *frag, const uint16_t *dY, const float *rsp, const float *A, const float *b,
+hipError_t launch_dx_bf16(const uint32_t *frag, const uint16_t *dyb, const float *rsp, const float *A, const float *b,
                           int d, uint16_t *dX, const uint16_t *X, float *dA, float *db, int64_t N, int64_t m, int64_t n,
                           hipStream_t st) {
   const int parts = rowsum_parts(m);
-  const int64_t Nt = round_up(N, 128);  // row stride of the partial row sums
+  const int64_t Nt = bwd_tokens(N);  // row stride of the partial row sums
   const int tiles_m = (int)ceil_div(n, kTile), tiles_n = (int)ceil_div(N, kTile);
   const int KB = (int)(round_up(m, 128) / kKStep);  // even, matches the operand layout
   // dX == nullptr: the product still runs for dA/db; its stores are dropped.
   if (d == 8)
-    k_gemm_codes<1, 8><<<tiles_m * tiles_n, 256, 0, st>>>(frag, KB, dY, (int)m, N, (int)m, tiles_m, tiles_n, rsp,
+    k_gemm_codes<1, 8><<<tiles_m * tiles_n, 256, 0, st>>>(frag, KB, dyb, tiles_m, tiles_n, rsp,
                                                           parts, Nt, A, b, dX, n, n, N, X, dA, db);
   else
-    k_gemm_codes<1, 4><<<tiles_m * tiles_n, 256, 0, st>>>(frag, KB, dY, (int)m, N, (int)m, tiles_m, tiles_n, rsp,
+    k_gemm_codes<1, 4><<<tiles_m * tiles_n, 256, 0, st>>>(frag, KB, dyb, tiles_m, tiles_n, rsp,
                                                           parts, Nt, A, b, dX, n, n, N, X, dA, db);
   return hipGetLastError();
 }
@@ -533,7 +514,7 @@ hipError_t launch_dx_bf16(const uint32_t *frag, const uint16_t *dY, const float 
 hipError_t launch_dw_bf16(const uint16_t *xt, const uint16_t *dyt, const uint16_t *Z, int mask_mode, int accumulate,
                           void *dZ, bool dz_bf16, int64_t N, int64_t m, int64_t n, hipStream_t st) {
   const int tiles_m = (int)ceil_div(n, kTile), tiles_n = (int)ceil_div(m, kTile);
-  const int KBt = (int)(round_up(N, 128) / 64);  // even
+  const int KBt = (int)(bwd_tokens(N) / 64);  // even
   k_gemm_dw<<<tiles_m * tiles_n, 256, 0, st>>>(xt, dyt, KBt, Z, mask_mode, accumulate, dZ, dz_bf16 ? 1 : 0, (int)m,
                                                (int)n, tiles_m, tiles_n);
   return hipGetLastError();

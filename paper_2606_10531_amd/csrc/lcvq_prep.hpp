@@ -23,6 +23,11 @@ inline int act_chunks(int64_t ldp) {
 hipError_t launch_fwd_prep_bf16(const uint16_t *Z, int64_t m, int64_t n, uint32_t *frag, uint8_t *packed,
                                 const uint16_t *X, int64_t N, int64_t Np, int64_t ldp, int d, const float *A,
                                 const float *b, uint16_t *Xp, float *sp, hipStream_t st);
+// Tokens of the bf16 backward are padded to whole 256-token tiles of the
+// input-gradient product (the weight-gradient operands and row sums use the
+// same padding).
+inline int64_t bwd_tokens(int64_t N) { return (N + 255) / 256 * 256; }
+
 // The bf16 backward prepass sums each dY row in at most eight parts (runs of
 // 64-feature sub-tiles of the out-features, padded to 256); the input-gradient
 // product adds the parts.
@@ -37,12 +42,12 @@ inline int rowsum_parts(int64_t m) {
   return p < 1 ? 1 : (int)p;
 }
 // bf16 backward prepass in one launch: codes of the input-gradient product
-// (frag, optional), the weight-gradient operands (xt, dyt; skipped when xt is
-// nullptr) and the partial row sums of dY (rsp: rowsum_parts(m) rows of
-// round_up(N, 128) floats)
+// (frag, optional), dY in that product's B-operand layout (dyb, optional), the
+// weight-gradient operands (xt, dyt; skipped when xt is nullptr) and the
+// partial row sums of dY (rsp: rowsum_parts(m) rows of bwd_tokens(N) floats)
 hipError_t launch_bwd_prep_bf16(const uint16_t *Z, int64_t m, int64_t n, uint32_t *frag, const uint16_t *X,
-                                const uint16_t *dY, const float *A, int d, int64_t N, uint16_t *xt, uint16_t *dyt,
-                                float *rsp, float *za, int nza, float *zb, int nzb, hipStream_t st);
+                                const uint16_t *dY, const float *A, int d, int64_t N, uint16_t *dyb, uint16_t *xt,
+                                uint16_t *dyt, float *rsp, float *za, int nza, float *zb, int nzb, hipStream_t st);
 hipError_t launch_act_transform(const void *X, bool bf16, int64_t N, int64_t Np, int64_t n, int d,
                                 const float *A, const float *b, void *Xp, int64_t ldp, float *s,
                                 hipStream_t st);
@@ -61,7 +66,7 @@ hipError_t launch_adamw(float *theta, const void *grad, bool grad_bf16, float *m
 // bf16 matrix-core products (lcvq_gemm.hip)
 hipError_t launch_fwd_bf16(const uint32_t *frag, const uint16_t *Xp, int64_t ldp, const float *s,
                            uint16_t *Y, int64_t N, int64_t m, int64_t n, hipStream_t st);
-hipError_t launch_dx_bf16(const uint32_t *frag, const uint16_t *dY, const float *rsp, const float *A, const float *b,
+hipError_t launch_dx_bf16(const uint32_t *frag, const uint16_t *dyb, const float *rsp, const float *A, const float *b,
                           int d, uint16_t *dX, const uint16_t *X, float *dA, float *db, int64_t N, int64_t m, int64_t n,
                           hipStream_t st);
 hipError_t launch_dw_bf16(const uint16_t *xt, const uint16_t *dyt, const uint16_t *Z, int mask_mode, int accumulate,
