@@ -43,7 +43,7 @@ struct FwdLayout {
   int64_t Np, ldp;
 };
 struct BwdLayout {
-  size_t rs, frag, dyb, xt, dyt, total;
+  size_t rs, frag, dyb, xt, dyt, mask, total;
 };
 
 FwdLayout fwd_layout(int64_t N, int64_t m, int64_t n, bool bf16) {
@@ -84,9 +84,11 @@ BwdLayout bwd_layout(int64_t N, int64_t m, int64_t n, bool bf16) {
     L.dyb = L.frag + up256(frag);
     L.xt = L.dyb + up256(Nt * (size_t)lcvq::round_up(m, 128) * 2);
     L.dyt = L.xt + up256((size_t)lcvq::round_up(n, 256) * Nt * 2);
-    L.total = L.dyt + up256((size_t)lcvq::round_up(m, 256) * Nt * 2);
+    // straight-through mask of Z, one bit per element (rows of whole 64-bit words)
+    L.mask = L.dyt + up256((size_t)lcvq::round_up(m, 256) * Nt * 2);
+    L.total = L.mask + up256((size_t)m * lcvq::mask_words_per_row(n) * 8);
   } else {
-    L.frag = L.dyb = L.xt = L.dyt = L.total = up256((size_t)N * 4);
+    L.frag = L.dyb = L.xt = L.dyt = L.mask = L.total = up256((size_t)N * 4);
   }
   return L;
 }
@@ -400,13 +402,15 @@ lcvq_status_t lcvq_linear_bwd(int64_t N, int64_t m, int64_t n, int32_t d, int32_
     const bool run_dx = dX != nullptr || want_map;
     uint32_t *frag = (uint32_t *)(ws + L.frag);
     uint16_t *dyb = (uint16_t *)(ws + L.dyb), *xt = (uint16_t *)(ws + L.xt), *dyt = (uint16_t *)(ws + L.dyt);
+    uint64_t *maskbits = (uint64_t *)(ws + L.mask);
     {
+      // the quantise blocks (which write the mask bitmap) run whenever dX, dA or dZ is wanted
       Timed tm(LCVQ_K_BWD_PREP, st);
-      e = tm.done(lcvq::launch_bwd_prep_bf16((const uint16_t *)Z, m, n, run_dx ? frag : nullptr, (const uint16_t *)X,
+      e = tm.done(lcvq::launch_bwd_prep_bf16((const uint16_t *)Z, m, n, frag, (const uint16_t *)X,
                                              (const uint16_t *)dY, A, d, N, run_dx ? dyb : nullptr,
                                              dZ != nullptr ? xt : nullptr, dZ != nullptr ? dyt : nullptr, rs,
-                                             clear_map ? dA : nullptr, clear_map ? d * d : 0,
-                                             clear_map ? db : nullptr, clear_map ? d : 0, st));
+                                             dZ != nullptr ? maskbits : nullptr, mask_mode, clear_map ? dA : nullptr,
+                                             clear_map ? d * d : 0, clear_map ? db : nullptr, clear_map ? d : 0, st));
       if (e != hipSuccess) return hip_fail(e, "backward prepass launch");
     }
     if (run_dx) {
@@ -417,8 +421,7 @@ lcvq_status_t lcvq_linear_bwd(int64_t N, int64_t m, int64_t n, int32_t d, int32_
     }
     if (dZ != nullptr) {
       Timed tm(LCVQ_K_DW, st);
-      e = tm.done(lcvq::launch_dw_bf16(xt, dyt, (const uint16_t *)Z, mask_mode, accumulate, dZ,
-                                       dz_dtype == LCVQ_BF16, N, m, n, st));
+      e = tm.done(lcvq::launch_dw_bf16(xt, dyt, maskbits, accumulate, dZ, dz_dtype == LCVQ_BF16, N, m, n, st));
       if (e != hipSuccess) return hip_fail(e, "weight-gradient launch");
     }
     return ok();

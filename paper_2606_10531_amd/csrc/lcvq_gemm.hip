@@ -312,7 +312,7 @@ __global__ __launch_bounds__(256, 1) void k_gemm_codes(
 // ============================================================================
 
 __global__ __launch_bounds__(256, 1) void k_gemm_dw(const uint16_t *__restrict__ xt, const uint16_t *__restrict__ dyt,
-                                                    int KBt, const uint16_t *__restrict__ Z, int mask_mode,
+                                                    int KBt, const uint64_t *__restrict__ maskbits, int64_t ldm8,
                                                     int accumulate, void *__restrict__ dZ, int dz_bf16, int m, int n,
                                                     int tiles_m, int tiles_n) {
   constexpr int kStage = 32 * 1024;  // eight 4 KiB B blocks
@@ -405,14 +405,24 @@ __global__ __launch_bounds__(256, 1) void k_gemm_dw(const uint16_t *__restrict__
 
   // ------------------------------------------------ straight-through epilogue
   // Lane L holds D[c .. c + 15, r] for each (mi, ni): dZ[r, c .. c + 15] =
-  // mask * D.  Rows r >= m fall outside the buffers; columns c >= n get an
-  // out-of-range offset.  The latents (and old dZ) of the next block row are
-  // loaded before this one's stores: loads and stores share one counter.
-  const __amdgpu_buffer_rsrc_t rz = make_rsrc(Z + (int64_t)r0 * n, (int64_t)(m - r0) * n * 2);
+  // mask * D, the mask read from the bitmap the backward prepass wrote (one
+  // 64-bit word per row and wave: columns c0 + 64 w .. + 63).  Rows r >= m fall
+  // outside the buffers; columns c >= n get an out-of-range offset.  Every load
+  // (mask words, and old dZ when accumulating) of a block row is issued before
+  // the stores of the previous one: loads and stores share one counter.
+  const __amdgpu_buffer_rsrc_t rmk = make_rsrc(maskbits + (int64_t)r0 * ldm8, (int64_t)(m - r0) * ldm8 * 8);
+  const int64_t mw = (int64_t)tm * 4 + wave;  // this wave's word of each bitmap row
   const int es = dz_bf16 ? 2 : 4;
   const __amdgpu_buffer_rsrc_t rg = make_rsrc((char *)dZ + (int64_t)r0 * n * es, (int64_t)(m - r0) * n * es);
-  u32x4 zv[2][2][2], ov[2][2][2][2];
+  u32x2 mk[8];
+#pragma unroll
+  for (int ni = 0; ni < 8; ++ni) {
+    const int rl = ni * 32 + (lane & 31);
+    mk[ni] = __builtin_amdgcn_raw_buffer_load_b64(rmk, mw < ldm8 ? (int)((rl * ldm8 + mw) * 8) : (int)kOffNone, 0, 0);
+  }
+  u32x4 ov[2][2][2][2];
   auto eload = [&](int buf, int ni) {
+    if (!accumulate) return;
     const int rl = ni * 32 + (lane & 31);
 #pragma unroll
     for (int mi = 0; mi < 2; ++mi)
@@ -421,14 +431,11 @@ __global__ __launch_bounds__(256, 1) void k_gemm_dw(const uint16_t *__restrict__
         const int c = c0 + 64 * wave + 32 * mi + 16 * h + 8 * half;
         const bool cv = c < n;
         const uint32_t e = (uint32_t)(rl * n + c);
-        zv[buf][mi][half] = __builtin_amdgcn_raw_buffer_load_b128(rz, cv ? e * 2u : kOffNone, 0, 0);
-        if (accumulate) {
-          if (dz_bf16) {
-            ov[buf][mi][half][0] = __builtin_amdgcn_raw_buffer_load_b128(rg, cv ? e * 2u : kOffNone, 0, 0);
-          } else {
-            ov[buf][mi][half][0] = __builtin_amdgcn_raw_buffer_load_b128(rg, cv ? e * 4u : kOffNone, 0, 0);
-            ov[buf][mi][half][1] = __builtin_amdgcn_raw_buffer_load_b128(rg, cv ? e * 4u + 16u : kOffNone, 0, 0);
-          }
+        if (dz_bf16) {
+          ov[buf][mi][half][0] = __builtin_amdgcn_raw_buffer_load_b128(rg, cv ? e * 2u : kOffNone, 0, 0);
+        } else {
+          ov[buf][mi][half][0] = __builtin_amdgcn_raw_buffer_load_b128(rg, cv ? e * 4u : kOffNone, 0, 0);
+          ov[buf][mi][half][1] = __builtin_amdgcn_raw_buffer_load_b128(rg, cv ? e * 4u + 16u : kOffNone, 0, 0);
         }
       }
   };
@@ -445,13 +452,10 @@ __global__ __launch_bounds__(256, 1) void k_gemm_dw(const uint16_t *__restrict__
         const int c = c0 + 64 * wave + 32 * mi + 16 * h + 8 * half;
         const bool cv = c < n;
         const uint32_t e = (uint32_t)(rl * n + c);
+        const uint32_t mb = mk[ni][mi] >> (16 * h + 8 * half);
         float g[8];
 #pragma unroll
-        for (int q = 0; q < 4; ++q) {
-          const uint32_t zw = zv[buf][mi][half][q];
-          g[2 * q] = ste_pass(bf16_lo(zw), mask_mode) ? acc[mi][ni][8 * half + 2 * q] : 0.0f;
-          g[2 * q + 1] = ste_pass(bf16_hi(zw), mask_mode) ? acc[mi][ni][8 * half + 2 * q + 1] : 0.0f;
-        }
+        for (int q = 0; q < 8; ++q) g[q] = ((mb >> q) & 1u) ? acc[mi][ni][8 * half + q] : 0.0f;
         if (dz_bf16) {
           if (accumulate) {
 #pragma unroll
@@ -511,13 +515,12 @@ hipError_t launch_dx_bf16(const uint32_t *frag, const uint16_t *dyb, const float
   return hipGetLastError();
 }
 
-hipError_t launch_dw_bf16(const uint16_t *xt, const uint16_t *dyt, const uint16_t *Z, int mask_mode, int accumulate,
+hipError_t launch_dw_bf16(const uint16_t *xt, const uint16_t *dyt, const uint64_t *maskbits, int accumulate,
                           void *dZ, bool dz_bf16, int64_t N, int64_t m, int64_t n, hipStream_t st) {
   const int tiles_m = (int)ceil_div(n, kTile), tiles_n = (int)ceil_div(m, kTile);
   const int KBt = (int)(bwd_tokens(N) / 64);  // even
-  k_gemm_dw<<<tiles_m * tiles_n, 256, 0, st>>>(xt, dyt, KBt, Z, mask_mode, accumulate, dZ, dz_bf16 ? 1 : 0, (int)m,
-                                               (int)n, tiles_m, tiles_n);
+  k_gemm_dw<<<tiles_m * tiles_n, 256, 0, st>>>(xt, dyt, KBt, maskbits, mask_words_per_row(n), accumulate, dZ,
+                                               dz_bf16 ? 1 : 0, (int)m, (int)n, tiles_m, tiles_n);
   return hipGetLastError();
 }
-
 }  // namespace lcvq

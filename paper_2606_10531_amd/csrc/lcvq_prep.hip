@@ -78,7 +78,9 @@ typedef uint8_t CodeTile[64][64 + 8];  // rows of 72 bytes keep 8-byte stores al
 template <bool kTrans>
 __device__ __forceinline__ void quant_block(int bq, int by, int gx, const uint16_t *__restrict__ Z, int64_t m,
                                             int64_t n, uint32_t *__restrict__ frag, int KB,
-                                            uint8_t *__restrict__ packed, CodeTile (&codes)[4]) {
+                                            uint8_t *__restrict__ packed, CodeTile (&codes)[4],
+                                            uint64_t *__restrict__ maskbits = nullptr, int64_t ldm8 = 0,
+                                            int mask_mode = 0) {
   const int tid = threadIdx.x;
   const int64_t r0 = (int64_t)by * 64;
   u32x4 v[4][2];
@@ -103,6 +105,24 @@ __device__ __forceinline__ void quant_block(int bq, int by, int gx, const uint16
         hi |= (quant_code(bf16_lo(v[q][i][2 + e])) | (quant_code(bf16_hi(v[q][i][2 + e])) << 8)) << (16 * e);
       }
       *reinterpret_cast<uint2 *>(&codes[q][rr][cc]) = make_uint2(lo, hi);
+      if (kTrans && maskbits != nullptr) {
+        // straight-through mask of these 8 latents -> byte (cc / 8) of the
+        // row's 64-bit word; threads cc / 8 = 0 and 4 store the two halves
+        const int64_t r = r0 + rr, c = (int64_t)(4 * bq + q) * 64 + cc;
+        uint32_t mb = 0;
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          const bool in = r < m && c + 2 * e < n;
+          mb |= (in && ste_pass(bf16_lo(v[q][i][e]), mask_mode) ? 1u : 0u) << (2 * e);
+          mb |= (in && ste_pass(bf16_hi(v[q][i][e]), mask_mode) ? 1u : 0u) << (2 * e + 1);
+        }
+        mb <<= 8 * ((id >> 0) & 3);
+        mb |= (uint32_t)__shfl_xor((int)mb, 1, 64);
+        mb |= (uint32_t)__shfl_xor((int)mb, 2, 64);
+        const int64_t wc = c / 64;
+        if ((id & 3) == 0 && r < m && wc < ldm8)
+          reinterpret_cast<uint32_t *>(maskbits + r * ldm8 + wc)[(id >> 2) & 1] = mb;
+      }
       if (!kTrans && packed != nullptr) {
         // 2-bit codes of these 8 columns (16 bits, least significant first);
         // the even thread of each pair stores its neighbour's 16 bits with its
@@ -556,7 +576,8 @@ __global__ __launch_bounds__(256) void k_bwd_prep(const uint16_t *__restrict__ Z
                                                    const float *__restrict__ A, int64_t N, int KBt, int nfx4,
                                                    int nfy, int spf, int nrp, uint16_t *__restrict__ dyb, int KBm,
                                                    uint16_t *__restrict__ xt, uint16_t *__restrict__ dyt,
-                                                   float *__restrict__ rsp,
+                                                   float *__restrict__ rsp, uint64_t *__restrict__ maskbits,
+                                                   int64_t ldm8, int mask_mode,
                                                    float *__restrict__ za, int nza, float *__restrict__ zb, int nzb) {
   __shared__ CodeTile codes[4];
   __shared__ __attribute__((aligned(16))) uint16_t tile[64][64 + 8];
@@ -579,7 +600,7 @@ __global__ __launch_bounds__(256) void k_bwd_prep(const uint16_t *__restrict__ Z
   }
   const int q = id - ndy;
   if (q < nq) {
-    quant_block<true>(q % gq, q / gq, 4 * gq, Z, m, n, frag, KBq, nullptr, codes);
+    quant_block<true>(q % gq, q / gq, 4 * gq, Z, m, n, frag, KBq, nullptr, codes, maskbits, ldm8, mask_mode);
     return;
   }
   const int x = q - nq;
@@ -679,7 +700,9 @@ hipError_t launch_dequant(const void *src, int kind, bool z_bf16, int64_t m, int
 namespace lcvq {
 hipError_t launch_bwd_prep_bf16(const uint16_t *Z, int64_t m, int64_t n, uint32_t *frag, const uint16_t *X,
                                 const uint16_t *dY, const float *A, int d, int64_t N, uint16_t *dyb, uint16_t *xt,
-                                uint16_t *dyt, float *rsp, float *za, int nza, float *zb, int nzb, hipStream_t st) {
+                                uint16_t *dyt, float *rsp, uint64_t *maskbits, int mask_mode, float *za, int nza,
+                                float *zb, int nzb, hipStream_t st) {
+  const int64_t ldm8 = mask_words_per_row(n);
   // codes: M = columns of Z padded to 256 (four 64-column tiles per block), K = rows
   // padded to 128 (skipped when frag == nullptr)
   const int gq = (int)(round_up(n, 256) / 256), KBq = (int)(round_up(m, 128) / 64);
@@ -692,10 +715,10 @@ hipError_t launch_bwd_prep_bf16(const uint16_t *Z, int64_t m, int64_t n, uint32_
   const unsigned grid = (unsigned)(nq + KBt * (nfx4 + nrp));
   if (d == 8)
     k_bwd_prep<8><<<grid, 256, 0, st>>>(Z, m, n, frag, KBq, gq, nq, X, dY, A, N, KBt, nfx4, nfy, spf, nrp, dyb, KBq,
-                                        xt, dyt, rsp, za, nza, zb, nzb);
+                                        xt, dyt, rsp, maskbits, ldm8, mask_mode, za, nza, zb, nzb);
   else
     k_bwd_prep<4><<<grid, 256, 0, st>>>(Z, m, n, frag, KBq, gq, nq, X, dY, A, N, KBt, nfx4, nfy, spf, nrp, dyb, KBq,
-                                        xt, dyt, rsp, za, nza, zb, nzb);
+                                        xt, dyt, rsp, maskbits, ldm8, mask_mode, za, nza, zb, nzb);
   return hipGetLastError();
 }
 }  // namespace lcvq

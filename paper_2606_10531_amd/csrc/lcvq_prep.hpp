@@ -41,13 +41,20 @@ inline int rowsum_parts(int64_t m) {
   const int64_t p = (nfy + rowsum_subtiles_per_part(m) - 1) / rowsum_subtiles_per_part(m);
   return p < 1 ? 1 : (int)p;
 }
+// Row stride, in 64-bit words, of the straight-through mask bitmap of an m x n
+// matrix (bit c % 64 of word r * stride + c / 64 is the mask of Z[r, c]).
+inline int64_t mask_words_per_row(int64_t n) { return (n + 63) / 64; }
+
 // bf16 backward prepass in one launch: codes of the input-gradient product
 // (frag, optional), dY in that product's B-operand layout (dyb, optional), the
-// weight-gradient operands (xt, dyt; skipped when xt is nullptr) and the
-// partial row sums of dY (rsp: rowsum_parts(m) rows of bwd_tokens(N) floats)
+// weight-gradient operands (xt, dyt; skipped when xt is nullptr), the partial
+// row sums of dY (rsp: rowsum_parts(m) rows of bwd_tokens(N) floats) and the
+// mask bitmap of the straight-through estimator (maskbits, optional; written by
+// the quantise blocks, so only together with frag)
 hipError_t launch_bwd_prep_bf16(const uint16_t *Z, int64_t m, int64_t n, uint32_t *frag, const uint16_t *X,
                                 const uint16_t *dY, const float *A, int d, int64_t N, uint16_t *dyb, uint16_t *xt,
-                                uint16_t *dyt, float *rsp, float *za, int nza, float *zb, int nzb, hipStream_t st);
+                                uint16_t *dyt, float *rsp, uint64_t *maskbits, int mask_mode, float *za, int nza,
+                                float *zb, int nzb, hipStream_t st);
 hipError_t launch_act_transform(const void *X, bool bf16, int64_t N, int64_t Np, int64_t n, int d,
                                 const float *A, const float *b, void *Xp, int64_t ldp, float *s,
                                 hipStream_t st);
@@ -69,7 +76,7 @@ hipError_t launch_fwd_bf16(const uint32_t *frag, const uint16_t *Xp, int64_t ldp
 hipError_t launch_dx_bf16(const uint32_t *frag, const uint16_t *dyb, const float *rsp, const float *A, const float *b,
                           int d, uint16_t *dX, const uint16_t *X, float *dA, float *db, int64_t N, int64_t m, int64_t n,
                           hipStream_t st);
-hipError_t launch_dw_bf16(const uint16_t *xt, const uint16_t *dyt, const uint16_t *Z, int mask_mode, int accumulate,
+hipError_t launch_dw_bf16(const uint16_t *xt, const uint16_t *dyt, const uint64_t *maskbits, int accumulate,
                           void *dZ, bool dz_bf16, int64_t N, int64_t m, int64_t n, hipStream_t st);
 
 // fp32 products on the vector ALUs (lcvq_f32.hip)
