@@ -38,13 +38,14 @@ constexpr int kKStep = 64;   // K per main-loop step
   } while (0)
 
 // Blocks are dispatched round-robin over the eight XCDs.  Give each XCD a
-// contiguous run of tile ids, and walk tiles in bands of four M-tiles, so the
-// blocks sharing an XCD's L2 share operand tiles.
+// contiguous run of tile ids, and walk tiles in bands of eight M-tiles, so the
+// blocks sharing an XCD's L2 share operand tiles (with 256 tiles: 8 M-tiles x
+// 4 token tiles per XCD, the fewest operand bytes per L2 for these products).
 __device__ __forceinline__ void tile_of_block(int tiles_m, int tiles_n, int &tm, int &tn) {
   const int nblocks = (int)gridDim.x;
   int id = (int)blockIdx.x;
   if (nblocks % 8 == 0) id = (id % 8) * (nblocks / 8) + id / 8;
-  constexpr int GM = 4;
+  constexpr int GM = 8;
   const int band = id / (GM * tiles_n);
   const int first = band * GM;
   const int gm = min(tiles_m - first, GM);
