@@ -445,18 +445,23 @@ __global__ __launch_bounds__(256) void k_dequant(const void *__restrict__ src, i
 // 256-feature tiles): block (f0 / 32 + fb, bt), sub-step kk, lane L holds
 // tokens kk * 16 + 8 (L / 32) + 0..7 of feature sel(L % 32), sel = perm32 for
 // in-features (M side) and the identity for out-features (N side).
+// The column reads use the transposing LDS read: in each 16-lane group, lane
+// 4 e + q addresses token e (+ 4 for the second read) and four consecutive
+// features F(q) .. F(q) + 3, and output lane 4 q + w receives feature F(q) + w
+// of the four tokens.  F places those features where sel puts them.
 template <bool kMside>
 __device__ __forceinline__ void tile_store_t(int bt, int64_t f0, int KBt, uint16_t *__restrict__ dst,
-                                             const uint16_t (&tile)[64][64 + 8]) {
+                                             uint16_t (&tile)[64][64 + 8]) {
   const int tid = threadIdx.x;
+  const int L = tid & 63, g = L >> 4, e = (L >> 2) & 3, q = L & 3;
+  const int F = kMside ? 8 * (g & 1) + 4 * (q >> 1) + 16 * (q & 1) : 16 * (g & 1) + 4 * q;
 #pragma unroll
   for (int i = 0; i < 2; ++i) {
-    const int id = tid + 256 * i, fb = id >> 8, kk = (id >> 6) & 3, L = id & 63;
-    const int fl = fb * 32 + (kMside ? perm32(L & 31) : (L & 31));
-    const int tl = kk * 16 + 8 * (L >> 5);
-    u32x4 w;
-#pragma unroll
-    for (int e = 0; e < 4; ++e) w[e] = (uint32_t)tile[tl + 2 * e][fl] | ((uint32_t)tile[tl + 2 * e + 1][fl] << 16);
+    const int id = tid + 256 * i, fb = id >> 8, kk = (id >> 6) & 3;
+    const int t = kk * 16 + 8 * (g >> 1) + e;
+    const bf16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4 *)&tile[t][fb * 32 + F]);
+    const bf16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4 *)&tile[t + 4][fb * 32 + F]);
+    const u32x4 w = __builtin_bit_cast(u32x4, __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7));
     const int64_t blk = (f0 >> 5) + fb;
     *reinterpret_cast<u32x4 *>(dst + (((blk * KBt + bt) * 4 + kk) * 64 + L) * 8) = w;
   }
