@@ -24,6 +24,14 @@ Readings of the paper where it is silent or inconsistent:
     mask = [0 <= round(Z) <= 3] ("rounded").  The alternative
     mask = [0 <= Z <= 3] ("latent") is also provided.
   * NaN latents quantise to code 0 with mask 0; +-inf clip to 3 / 0, mask 0.
+  * Differentiable gradient estimator (eq. dge, Sec. 3.3): the paper gives f on
+    one rounding interval of width delta = 1 (the interval of round() on the
+    code-domain latent).  It is extended periodically, F(z) = floor(z) +
+    f(z - floor(z)), which is continuous and steps at the half-integers like
+    round().  Its slope f' is unbounded at the middle of each interval, so it
+    is capped at a caller-given value.  clip() keeps its ordinary derivative;
+    through clip(F(Z), 0, 3) that is the "latent" mask [0 <= Z <= 3] (F is
+    increasing with F(0) = 0 and F(3) = 3); the "rounded" mask stays available.
 """
 from __future__ import annotations
 
@@ -71,6 +79,29 @@ def ste_mask(Z: np.ndarray, mode: int = MASK_ROUNDED) -> np.ndarray:
     if mode == MASK_LATENT:
         return (Z >= 0.0) & (Z <= CODE_MAX)
     raise ValueError(mode)
+
+
+# ---------------------------------- differentiable gradient estimator ------
+
+def dge_surrogate(Z: np.ndarray, k: float) -> np.ndarray:
+    """Smooth stand-in for round() (eq. dge, Sec. 3.3) with delta = 1:
+        f(x) = 1/2 (1 + sign(2x - 1) |2x - 1|^(1/k))   on one interval x in [0, 1],
+    extended periodically: F(z) = floor(z) + f(z - floor(z))."""
+    Z = np.asarray(Z, dtype=np.float64)
+    fl = np.floor(Z)
+    v = 2.0 * (Z - fl) - 1.0
+    return fl + 0.5 * (1.0 + np.sign(v) * np.abs(v) ** (1.0 / k))
+
+
+def dge_slope(Z: np.ndarray, k: float, cap: float) -> np.ndarray:
+    """Slope of the surrogate, f'(x) = (1/k) |2x - 1|^(1/k - 1) at the position x
+    of Z within its rounding interval (Sec. 3.3, delta = 1), capped at `cap`
+    (f' is unbounded where x = 1/2)."""
+    Z = np.asarray(Z, dtype=np.float64)
+    w = np.abs(2.0 * (Z - np.floor(Z)) - 1.0)
+    with np.errstate(divide="ignore"):
+        fp = (1.0 / k) * w ** (1.0 / k - 1.0)
+    return np.minimum(fp, cap)
 
 
 # --------------------------------------------------------------- decode -----
@@ -158,13 +189,18 @@ def linear_forward(Z, A, b, X, d):
     return forward(X, decode(codes, A, b, d)), codes
 
 
-def linear_backward(Z, A, b, X, dY, d, mask_mode: int = MASK_ROUNDED):
-    """(dX, dZ, dA, db, dW_hat) of one LC-VQ linear call (all inputs fp64 values)."""
+def linear_backward(Z, A, b, X, dY, d, mask_mode: int = MASK_ROUNDED, dge=None):
+    """(dX, dZ, dA, db, dW_hat) of one LC-VQ linear call (all inputs fp64 values).
+
+    dge = None: straight-through estimator.  dge = (k, cap): the differentiable
+    gradient estimator (Sec. 3.3), dZ = mask * dge_slope(Z) * dL/dcode."""
     codes = quantize(Z)
     W_hat = decode(codes, A, b, d)
     dW = grad_weight(dY, X)
     dX = grad_input(dY, W_hat)
     dZ = grad_latent(dW, A, d, ste_mask(Z, mask_mode))
+    if dge is not None:
+        dZ = dZ * dge_slope(Z, *dge)
     dA, db = grad_map(dW, codes, d)
     return dict(dX=dX, dZ=dZ, dA=dA, db=db, dW=dW)
 

@@ -250,6 +250,99 @@ def test_mask_latent_mode_in_backward():
     assert np.all(out_l["dZ"][:, [0, 4]] == 0)          # but lie outside it
 
 
+# ------------------------------------ differentiable gradient estimator -----
+
+def test_dge_surrogate_hand_values():
+    # eq. dge with delta = 1, k = 5: f(1/4) = (1 - 2^-1/5) / 2, f(3/4) = (1 + 2^-1/5) / 2
+    F = orc.dge_surrogate(np.array([0.0, 0.25, 0.5, 0.75, 1.0, 2.25, -0.75]), 5.0)
+    t = 2.0 ** -0.2
+    want = [0.0, (1 - t) / 2, 0.5, (1 + t) / 2, 1.0, 2 + (1 - t) / 2, -1 + (1 - t) / 2]
+    assert np.allclose(F, want, rtol=0, atol=1e-15)
+
+
+def test_dge_surrogate_limits():
+    z = np.random.default_rng(3).uniform(-2.0, 5.0, 1000)
+    assert np.allclose(orc.dge_surrogate(z, 1.0), z, rtol=0, atol=1e-12)        # k = 1: identity
+    far = np.abs(z - np.floor(z) - 0.5) > 0.05                                  # k -> inf: round()
+    assert np.allclose(orc.dge_surrogate(z[far], 1e6), np.rint(z[far]), rtol=0, atol=1e-4)
+    ints = np.arange(-3.0, 6.0)
+    assert np.array_equal(orc.dge_surrogate(ints, 5.0), ints)                    # fixed at integers
+    assert np.array_equal(orc.dge_surrogate(ints + 0.5, 5.0), ints + 0.5)        # and at the steps
+
+
+def test_dge_slope_hand_values():
+    s = orc.dge_slope(np.array([0.0, 0.25, 0.5, 0.75, 1.0, 3.25, -0.75]), 5.0, 3.0)
+    q = 0.2 * 2.0 ** 0.8                    # (1/5) |2/4 - 1|^(1/5 - 1)
+    assert np.allclose(s, [0.2, q, 3.0, q, 0.2, q, q], rtol=1e-15, atol=0)
+    assert np.array_equal(orc.dge_slope(np.array([0.5, 1.5, -2.5]), 5.0, 7.25), [7.25] * 3)
+    # k = 1: slope 1 everywhere, the middle of the interval included
+    assert np.array_equal(orc.dge_slope(np.array([0.0, 0.3, 0.5, 2.9]), 1.0, 3.0), [1.0] * 4)
+
+
+def test_dge_slope_is_derivative_of_surrogate():
+    r = np.random.default_rng(11)
+    z = r.uniform(-2.0, 5.0, 4000)
+    z = z[np.abs(z - np.floor(z) - 0.5) > 0.02]
+    for k in (2.0, 5.0, 9.0):
+        h = 1e-6
+        fd = (orc.dge_surrogate(z + h, k) - orc.dge_surrogate(z - h, k)) / (2 * h)
+        assert np.allclose(orc.dge_slope(z, k, 1e30), fd, rtol=1e-6, atol=0)
+
+
+@pytest.mark.parametrize("k,cap", [(5.0, 3.0), (5.0, 10.0), (3.0, 2.0)])
+def test_dge_capped_slope_mean_closed_form(k, cap):
+    # With w = |2x - 1| uniform on [0, 1] for x uniform, the slope is (1/k) w^(1/k-1),
+    # whose integral is w^(1/k); it exceeds the cap below w_c = (k cap)^(1/(1/k-1)).
+    # Mean of the capped slope = cap w_c + 1 - w_c^(1/k).  The uncapped mean is 1.
+    wc = (k * cap) ** (1.0 / (1.0 / k - 1.0))
+    want = cap * wc + 1.0 - wc ** (1.0 / k)
+    n = 2_000_000
+    x = (np.arange(n) + 0.5) / n                    # midpoint rule over one interval
+    got = orc.dge_slope(x, k, cap).mean()
+    assert abs(got - want) < 2e-6
+    assert want < 1.0
+
+
+@pytest.mark.parametrize("d", [4, 8])
+def test_dge_backward_matches_finite_differences_of_surrogate(d):
+    # Through the surrogate F of eq. dge the loss L(Z) = <dY, X decode(clip(F(Z), 0, 3))^T>
+    # is differentiable wherever F is (off the half-integers) and clip is (off 0 and 3):
+    # there dL/dZ is the estimator's dZ with the latent mask and an inactive cap.
+    r = np.random.default_rng(50 + d)
+    N, m, n = 3, 4, 2 * d
+    X, dY = r.standard_normal((N, n)), r.standard_normal((N, m))
+    A, b = r.standard_normal((d, d)), r.standard_normal(d)
+    frac = r.uniform(0.05, 0.45, size=(m, n)) + 0.5 * r.integers(0, 2, size=(m, n))
+    Z = r.integers(-2, 5, size=(m, n)) + frac      # latents in (-2, 5), clear of the kinks
+    k = 5.0
+    out = orc.linear_backward(Z, A, b, X, dY, d, orc.MASK_LATENT, dge=(k, 1e30))
+
+    def loss(Z_):
+        c = np.clip(orc.dge_surrogate(Z_, k), 0.0, 3.0)
+        return float(np.sum(dY * orc.forward(X, orc.decode(c, A, b, d))))
+
+    g = np.array([_fd(loss, Z, idx, 1e-6) for idx in np.ndindex(Z.shape)]).reshape(Z.shape)
+    assert np.allclose(out["dZ"], g, rtol=1e-6, atol=1e-8)
+    inside = (Z >= 0) & (Z <= 3)
+    assert inside.any() and (~inside).any()
+    assert np.all(out["dZ"][~inside] == 0.0)
+
+
+def test_dge_with_k_one_is_straight_through():
+    r = np.random.default_rng(12)
+    d, N, m, n = 8, 4, 5, 16
+    Z = r.uniform(-2.0, 5.0, (m, n))
+    Z[0, :4] = [0.5, 1.5, 2.5, -0.5]                # middles of the rounding intervals
+    X, dY = r.standard_normal((N, n)), r.standard_normal((N, m))
+    A, b = r.standard_normal((d, d)), r.standard_normal(d)
+    for mode in (orc.MASK_ROUNDED, orc.MASK_LATENT):
+        ste = orc.linear_backward(Z, A, b, X, dY, d, mode)
+        dge = orc.linear_backward(Z, A, b, X, dY, d, mode, dge=(1.0, 3.0))
+        assert np.array_equal(ste["dZ"], dge["dZ"])
+        for key in ("dX", "dA", "db"):
+            assert np.array_equal(ste[key], dge[key])
+
+
 # ------------------------------------------------------------- packing ------
 
 def test_pack_hand_values():
