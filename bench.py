@@ -86,6 +86,14 @@ class Layer:
         lc.linear_bwd(self.Z, self.A, self.b, self.X, self.dY, self.d, dX=self.dX, dZ=self.dZ, dA=self.dA,
                       db=self.db, workspace=self.wsb)
 
+    def step_dge(self, k=5.0, cap=3.0):
+        """The same step with the differentiable gradient estimator in the backward."""
+        lc = self.lc
+        lc.linear_fwd(self.Z, self.A, self.b, self.X, self.d, packed_out=self.packed, workspace=self.wsf,
+                      out=self.Y)
+        lc.linear_bwd_dge(self.Z, self.A, self.b, self.X, self.dY, self.d, k=k, cap=cap, dX=self.dX, dZ=self.dZ,
+                          dA=self.dA, db=self.db, workspace=self.wsb)
+
     def flops(self):
         return 6.0 * self.N * self.m * self.n
 
@@ -138,6 +146,35 @@ def hbm_kernels(lc, torch):
                      "bytes_per_elem": bpe, "shape": [m, n]}
     del Z, packed, W, theta, m1, m2, shadow
     return out
+
+
+def dge_step(lc, torch, layers, steps):
+    """fwd + backward with the differentiable gradient estimator (k = 5, slope cap 3,
+    latent mask), timed like the main step, with its weight-gradient kernel."""
+    lib = lc._lib.load()
+    for _ in range(3):
+        for L in layers:
+            L.step_dge()
+    start, stop = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    start.record()
+    for _ in range(steps):
+        for L in layers:
+            L.step_dge()
+    stop.record()
+    torch.cuda.synchronize()
+    ms = start.elapsed_time(stop) / steps
+    kid = lc._lib.KERNELS.index("dw")
+    lib.lcvq_timer_enable(1 << kid)
+    for _ in range(5):
+        for L in layers:
+            L.step_dge()
+    torch.cuda.synchronize()
+    dw_ms, cnt = timer_read(lib, kid)
+    lib.lcvq_timer_enable(0)
+    flops = sum(L.flops() for L in layers)
+    return {"estimator": "dge k=5 cap=3 latent mask", "ms_per_step": round(ms, 4),
+            "TFLOP/s": round(flops / (ms * 1e-3) / 1e12, 2), "dw_us": round(1e3 * dw_ms / max(cnt, 1), 2)}
 
 
 def library_gemm(torch, N, m, n):
@@ -311,6 +348,7 @@ def main():
                      "flop_per_launch": per_launch_flop, "ms_per_step_with_kernel_events": round(ms_step_ev, 4)},
         "kernels_us_per_step": breakdown,
     }
+    res["dge_step"] = dge_step(lc, torch, layers, args.steps)
     L0 = layers[0]
     res["library_gemm_same_shape"] = library_gemm(torch, L0.N, L0.m, L0.n)
     if not args.no_hbm:

@@ -152,6 +152,30 @@ lcvq_status_t lcvq_linear_bwd(int64_t N, int64_t m, int64_t n, int32_t d, int32_
                               void *workspace, size_t workspace_bytes, void *stream);
 
 /*
+ * lcvq_linear_bwd_dge -- lcvq_linear_bwd with the differentiable gradient
+ * estimator of Sec. 3.3 (eq. dge) in place of the straight-through one.  round()
+ * is stood in for by f(x) = 1/2 (1 + sign(2x - 1) |2x - 1|^(1/k)) on each
+ * rounding interval (quantisation interval delta = 1 on the code-domain
+ * latent), so the latent's gradient gains the slope f' at Z's position
+ * x = Z - floor(Z) within its interval:
+ *   dZ[r, c] = mask[r, c] * min(cap, (1/k) |2x - 1|^(1/k - 1)) * sum_j dW[r, g*d + j] A[j, k]
+ * f' is unbounded at x = 1/2, hence the cap (the slope there is `cap` for
+ * k > 1; k = 1 gives slope 1 everywhere, i.e. the straight-through result).
+ * Through clip(f(Z), 0, 3) the chain rule gives the LCVQ_MASK_LATENT mask;
+ * mask_mode selects it as in lcvq_linear_bwd.  dX, dA and db are those of
+ * lcvq_linear_bwd.  The paper trains with k = 5.
+ *   k    finite, >= 1 (else LCVQ_EINVAL)
+ *   cap  finite, > 0 (else LCVQ_EINVAL)
+ * All other arguments, the workspace size and the error behaviour are those
+ * of lcvq_linear_bwd.
+ */
+lcvq_status_t lcvq_linear_bwd_dge(int64_t N, int64_t m, int64_t n, int32_t d, int32_t dtype,
+                                  const void *Z, const float *A, const float *b,
+                                  const void *X, const void *dY, int32_t mask_mode, float k, float cap,
+                                  int32_t accumulate, void *dX, void *dZ, int32_t dz_dtype, float *dA, float *db,
+                                  void *workspace, size_t workspace_bytes, void *stream);
+
+/*
  * lcvq_adamw_step -- one AdamW update of a flat fp32 parameter array: the
  * optimiser the paper trains Z, A and b with (Sec. 4.4), with bias correction
  * and decoupled weight decay, all arithmetic in fp32:

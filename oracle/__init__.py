@@ -98,8 +98,8 @@ def dge_slope(Z: np.ndarray, k: float, cap: float) -> np.ndarray:
     of Z within its rounding interval (Sec. 3.3, delta = 1), capped at `cap`
     (f' is unbounded where x = 1/2)."""
     Z = np.asarray(Z, dtype=np.float64)
-    w = np.abs(2.0 * (Z - np.floor(Z)) - 1.0)
-    with np.errstate(divide="ignore"):
+    with np.errstate(divide="ignore", invalid="ignore"):     # w = 0 at x = 1/2; NaN for non-finite Z
+        w = np.abs(2.0 * (Z - np.floor(Z)) - 1.0)
         fp = (1.0 / k) * w ** (1.0 / k - 1.0)
     return np.minimum(fp, cap)
 
@@ -198,9 +198,12 @@ def linear_backward(Z, A, b, X, dY, d, mask_mode: int = MASK_ROUNDED, dge=None):
     W_hat = decode(codes, A, b, d)
     dW = grad_weight(dY, X)
     dX = grad_input(dY, W_hat)
-    dZ = grad_latent(dW, A, d, ste_mask(Z, mask_mode))
-    if dge is not None:
-        dZ = dZ * dge_slope(Z, *dge)
+    mask = ste_mask(Z, mask_mode)
+    if dge is None:
+        dZ = grad_latent(dW, A, d, mask)
+    else:
+        with np.errstate(invalid="ignore"):
+            dZ = np.where(mask, grad_codes(dW, A, d) * dge_slope(Z, *dge), 0.0)
     dA, db = grad_map(dW, codes, d)
     return dict(dX=dX, dZ=dZ, dA=dA, db=db, dW=dW)
 

@@ -15,7 +15,7 @@ from . import _lib
 from ._lib import (BF16, F32, MASK_LATENT, MASK_ROUNDED, OP_BWD, OP_FWD,  # noqa: F401
                    SRC_CODES_U8, SRC_LATENT, SRC_PACKED2, LcvqError)
 
-__all__ = ["linear_fwd", "linear_bwd", "pack2bit", "dequant", "adamw_step", "workspace_bytes", "LcvqError",
+__all__ = ["linear_fwd", "linear_bwd", "linear_bwd_dge", "pack2bit", "dequant", "adamw_step", "workspace_bytes", "LcvqError",
            "MASK_ROUNDED", "MASK_LATENT", "SRC_LATENT", "SRC_CODES_U8", "SRC_PACKED2"]
 
 _DT = {torch.float32: F32, torch.bfloat16: BF16}
@@ -132,6 +132,26 @@ def linear_bwd(Z: torch.Tensor, A: torch.Tensor, b: torch.Tensor, X: torch.Tenso
                dX: torch.Tensor | None = None, dZ: torch.Tensor | None = None, dA: torch.Tensor | None = None,
                db: torch.Tensor | None = None, workspace: torch.Tensor | None = None):
     """Straight-through backward: returns (dX, dZ, dA, db); skipped outputs are None."""
+    return _linear_bwd(None, Z, A, b, X, dY, d, mask_mode, accumulate, need_dX, need_dZ, need_map, dz_dtype,
+                       dX, dZ, dA, db, workspace)
+
+
+def linear_bwd_dge(Z: torch.Tensor, A: torch.Tensor, b: torch.Tensor, X: torch.Tensor, dY: torch.Tensor,
+                   d: int, k: float = 5.0, cap: float = 3.0, mask_mode: int = MASK_LATENT,
+                   accumulate: bool = False, need_dX: bool = True, need_dZ: bool = True, need_map: bool = True,
+                   dz_dtype: torch.dtype | None = None, dX: torch.Tensor | None = None,
+                   dZ: torch.Tensor | None = None, dA: torch.Tensor | None = None, db: torch.Tensor | None = None,
+                   workspace: torch.Tensor | None = None):
+    """Backward with the differentiable gradient estimator (k, slope cap): returns (dX, dZ, dA, db).
+
+    The default mask is the latent one, [0 <= Z <= 3], which the chain rule
+    gives through clip(f(Z), 0, 3)."""
+    return _linear_bwd((float(k), float(cap)), Z, A, b, X, dY, d, mask_mode, accumulate, need_dX, need_dZ,
+                       need_map, dz_dtype, dX, dZ, dA, db, workspace)
+
+
+def _linear_bwd(dge, Z, A, b, X, dY, d, mask_mode, accumulate, need_dX, need_dZ, need_map, dz_dtype, dX, dZ, dA,
+                db, workspace):
     m, n = Z.shape
     N = X.shape[0]
     dt = _dtype_code(X)
@@ -146,10 +166,13 @@ def linear_bwd(Z: torch.Tensor, A: torch.Tensor, b: torch.Tensor, X: torch.Tenso
         dA = torch.zeros((d, d), dtype=torch.float32, device=dev)
         db = torch.zeros((d,), dtype=torch.float32, device=dev)
     ws = _workspace(OP_BWD, N, m, n, d, X.dtype, dev, workspace)
-    _lib.check(_lib.load().lcvq_linear_bwd(
-        N, m, n, d, dt, _dev(Z, "Z"), _dev(A, "A"), _dev(b, "b"), _dev(X, "X"), _dev(dY, "dY"), mask_mode,
-        1 if accumulate else 0, _opt(dX if need_dX else None, "dX"), _opt(dZ if need_dZ else None, "dZ"),
-        _DT[dz_dtype], _opt(dA if need_map else None, "dA"), _opt(db if need_map else None, "db"),
-        _dev(ws, "workspace"), ws.numel(), _stream(dev)), "lcvq_linear_bwd")
+    head = (N, m, n, d, dt, _dev(Z, "Z"), _dev(A, "A"), _dev(b, "b"), _dev(X, "X"), _dev(dY, "dY"), mask_mode)
+    tail = (1 if accumulate else 0, _opt(dX if need_dX else None, "dX"), _opt(dZ if need_dZ else None, "dZ"),
+            _DT[dz_dtype], _opt(dA if need_map else None, "dA"), _opt(db if need_map else None, "db"),
+            _dev(ws, "workspace"), ws.numel(), _stream(dev))
+    if dge is None:
+        _lib.check(_lib.load().lcvq_linear_bwd(*head, *tail), "lcvq_linear_bwd")
+    else:
+        _lib.check(_lib.load().lcvq_linear_bwd_dge(*head, *dge, *tail), "lcvq_linear_bwd_dge")
     return (dX if need_dX else None, dZ if need_dZ else None, dA if need_map else None,
             db if need_map else None)

@@ -31,6 +31,8 @@ SIGNATURES = {
     "lcvq_linear_fwd": (_I32, [_I64, _I64, _I64, _I32, _I32, _P, _P, _P, _P, _P, _P, _P, _SZ, _P]),
     "lcvq_linear_bwd": (_I32, [_I64, _I64, _I64, _I32, _I32, _P, _P, _P, _P, _P, _I32, _I32,
                                _P, _P, _I32, _P, _P, _P, _SZ, _P]),
+    "lcvq_linear_bwd_dge": (_I32, [_I64, _I64, _I64, _I32, _I32, _P, _P, _P, _P, _P, _I32, ctypes.c_float,
+                                   ctypes.c_float, _I32, _P, _P, _I32, _P, _P, _P, _SZ, _P]),
     "lcvq_adamw_step": (_I32, [_P, _P, _I32, _P, _P, _P, _I32, _I64, ctypes.c_float, ctypes.c_float,
                                 ctypes.c_float, ctypes.c_float, ctypes.c_float, _I32, _P]),
     "lcvq_timer_enable": (_I32, [ctypes.c_uint32]),

@@ -5,6 +5,7 @@
 #include <stdio.h>
 
 #include <atomic>
+#include <cmath>
 #include <mutex>
 #include <utility>
 #include <vector>
@@ -347,10 +348,13 @@ lcvq_status_t lcvq_linear_fwd(int64_t N, int64_t m, int64_t n, int32_t d, int32_
   return ok();
 }
 
-lcvq_status_t lcvq_linear_bwd(int64_t N, int64_t m, int64_t n, int32_t d, int32_t dtype, const void *Z,
-                              const float *A, const float *b, const void *X, const void *dY, int32_t mask_mode,
-                              int32_t accumulate, void *dX, void *dZ, int32_t dz_dtype, float *dA, float *db,
-                              void *workspace, size_t workspace_bytes, void *stream) {
+}  // extern "C"
+
+// Both backward entry points: `est` selects the estimator of the latent's gradient.
+static lcvq_status_t linear_bwd(int64_t N, int64_t m, int64_t n, int32_t d, int32_t dtype, const void *Z,
+                                const float *A, const float *b, const void *X, const void *dY, int32_t mask_mode,
+                                const lcvq::GradEst &est, int32_t accumulate, void *dX, void *dZ, int32_t dz_dtype,
+                                float *dA, float *db, void *workspace, size_t workspace_bytes, void *stream) {
   lcvq_status_t s = check_common(N, m, n, d, dtype);
   if (s != LCVQ_OK) return s;
   if (mask_mode != LCVQ_MASK_ROUNDED && mask_mode != LCVQ_MASK_LATENT) return fail(LCVQ_EINVAL, "mask_mode=%d", mask_mode);
@@ -402,15 +406,17 @@ lcvq_status_t lcvq_linear_bwd(int64_t N, int64_t m, int64_t n, int32_t d, int32_
     const bool run_dx = dX != nullptr || want_map;
     uint32_t *frag = (uint32_t *)(ws + L.frag);
     uint16_t *dyb = (uint16_t *)(ws + L.dyb), *xt = (uint16_t *)(ws + L.xt), *dyt = (uint16_t *)(ws + L.dyt);
-    uint64_t *maskbits = (uint64_t *)(ws + L.mask);
+    // the straight-through mask as a bitmap (the differentiable estimator reads Z itself)
+    uint64_t *maskbits = dZ != nullptr && !est.dge ? (uint64_t *)(ws + L.mask) : nullptr;
     {
-      // the quantise blocks (which write the mask bitmap) run whenever dX, dA or dZ is wanted
+      // the quantise blocks run when the input-gradient product or the bitmap needs them
       Timed tm(LCVQ_K_BWD_PREP, st);
-      e = tm.done(lcvq::launch_bwd_prep_bf16((const uint16_t *)Z, m, n, frag, (const uint16_t *)X,
-                                             (const uint16_t *)dY, A, d, N, run_dx ? dyb : nullptr,
-                                             dZ != nullptr ? xt : nullptr, dZ != nullptr ? dyt : nullptr, rs,
-                                             dZ != nullptr ? maskbits : nullptr, mask_mode, clear_map ? dA : nullptr,
-                                             clear_map ? d * d : 0, clear_map ? db : nullptr, clear_map ? d : 0, st));
+      e = tm.done(lcvq::launch_bwd_prep_bf16((const uint16_t *)Z, m, n, run_dx || maskbits ? frag : nullptr,
+                                             (const uint16_t *)X, (const uint16_t *)dY, A, d, N,
+                                             run_dx ? dyb : nullptr, dZ != nullptr ? xt : nullptr,
+                                             dZ != nullptr ? dyt : nullptr, rs, maskbits, mask_mode,
+                                             clear_map ? dA : nullptr, clear_map ? d * d : 0,
+                                             clear_map ? db : nullptr, clear_map ? d : 0, st));
       if (e != hipSuccess) return hip_fail(e, "backward prepass launch");
     }
     if (run_dx) {
@@ -421,7 +427,8 @@ lcvq_status_t lcvq_linear_bwd(int64_t N, int64_t m, int64_t n, int32_t d, int32_
     }
     if (dZ != nullptr) {
       Timed tm(LCVQ_K_DW, st);
-      e = tm.done(lcvq::launch_dw_bf16(xt, dyt, maskbits, accumulate, dZ, dz_dtype == LCVQ_BF16, N, m, n, st));
+      e = tm.done(lcvq::launch_dw_bf16(xt, dyt, maskbits, (const uint16_t *)Z, mask_mode, est, accumulate, dZ,
+                                       dz_dtype == LCVQ_BF16, N, m, n, st));
       if (e != hipSuccess) return hip_fail(e, "weight-gradient launch");
     }
     return ok();
@@ -444,11 +451,32 @@ lcvq_status_t lcvq_linear_bwd(int64_t N, int64_t m, int64_t n, int32_t d, int32_
   }
   if (dZ != nullptr || want_map) {
     Timed tm(LCVQ_K_DW, st);
-    e = tm.done(lcvq::launch_dz_f32((const float *)X, (const float *)dY, (const float *)Z, A, d, mask_mode, accumulate,
-                                    (float *)dZ, dA, db, N, m, n, st));
+    e = tm.done(lcvq::launch_dz_f32((const float *)X, (const float *)dY, (const float *)Z, A, d, mask_mode, est,
+                                    accumulate, (float *)dZ, dA, db, N, m, n, st));
     if (e != hipSuccess) return hip_fail(e, "weight-gradient launch");
   }
   return ok();
+}
+
+extern "C" {
+
+lcvq_status_t lcvq_linear_bwd(int64_t N, int64_t m, int64_t n, int32_t d, int32_t dtype, const void *Z,
+                              const float *A, const float *b, const void *X, const void *dY, int32_t mask_mode,
+                              int32_t accumulate, void *dX, void *dZ, int32_t dz_dtype, float *dA, float *db,
+                              void *workspace, size_t workspace_bytes, void *stream) {
+  return linear_bwd(N, m, n, d, dtype, Z, A, b, X, dY, mask_mode, lcvq::GradEst{0, 0.0f, 1.0f, 1.0f}, accumulate,
+                    dX, dZ, dz_dtype, dA, db, workspace, workspace_bytes, stream);
+}
+
+lcvq_status_t lcvq_linear_bwd_dge(int64_t N, int64_t m, int64_t n, int32_t d, int32_t dtype, const void *Z,
+                                  const float *A, const float *b, const void *X, const void *dY, int32_t mask_mode,
+                                  float k, float cap, int32_t accumulate, void *dX, void *dZ, int32_t dz_dtype,
+                                  float *dA, float *db, void *workspace, size_t workspace_bytes, void *stream) {
+  if (!(k >= 1.0f) || !std::isfinite(k)) return fail(LCVQ_EINVAL, "dge k=%g (need a finite k >= 1)", (double)k);
+  if (!(cap > 0.0f) || !std::isfinite(cap)) return fail(LCVQ_EINVAL, "dge cap=%g (need a finite cap > 0)", (double)cap);
+  const lcvq::GradEst est{1, (float)(1.0 / (double)k - 1.0), (float)(1.0 / (double)k), cap};
+  return linear_bwd(N, m, n, d, dtype, Z, A, b, X, dY, mask_mode, est, accumulate, dX, dZ, dz_dtype, dA, db,
+                    workspace, workspace_bytes, stream);
 }
 
 }  // extern "C"

@@ -52,6 +52,24 @@ __device__ __forceinline__ bool ste_pass(float z, int mode) {
   return v >= 0.0f && v <= (float)kMaxCode;
 }
 
+// Gradient estimator of the latent: straight-through (dge = 0), or the
+// differentiable estimator of eq. dge (Sec. 3.3) with delta = 1, slope
+// s |2x - 1|^e capped at `cap`, where s = 1/k and e = 1/k - 1.
+struct GradEst {
+  int dge;
+  float e, s, cap;
+};
+// The slope at the position x = z - floor(z) of z within its rounding
+// interval.  At x = 1/2 (w = 0) it is unbounded for k > 1 and 1 for k = 1; the
+// hardware log/exp would give NaN there for k = 1, so that point is set
+// explicitly.  A NaN or infinite z gives the (finite) cap; the mask is 0 there.
+__device__ __forceinline__ float dge_slope(float z, const GradEst &g) {
+  const float w = fabsf(2.0f * (z - floorf(z)) - 1.0f);
+  float f = g.s * __builtin_amdgcn_exp2f(g.e * __builtin_amdgcn_logf(w));
+  if (w == 0.0f) f = g.e < 0.0f ? g.cap : g.s;
+  return fminf(f, g.cap);
+}
+
 // ---- codes in the matrix-core operand layout -----------------------------
 // Row permutation of a 32-row MFMA block.  In a 32x32 accumulator, lane L
 // holds rows 8 (i / 4) + 4 (L / 32) + (i % 4), i = 0..15.  Feeding weight-side

@@ -33,8 +33,9 @@ __global__ __launch_bounds__(256) void k_f32(const float *__restrict__ P, int64_
                                              int64_t ldq, int64_t I, int64_t J, int64_t K,
                                              const float *__restrict__ vecI, const float *__restrict__ A,
                                              const float *__restrict__ bvec, const float *__restrict__ Z,
-                                             int mask_mode, int accumulate, float *__restrict__ out,
-                                             int64_t ldo, float *__restrict__ dA, float *__restrict__ db) {
+                                             int mask_mode, GradEst est, int accumulate,
+                                             float *__restrict__ out, int64_t ldo, float *__restrict__ dA,
+                                             float *__restrict__ db) {
   __shared__ float Ps[kFK][kF + 1];
   __shared__ float Qs[kFK][kF + 4];
   __shared__ float sred[D * D + D];
@@ -108,7 +109,8 @@ __global__ __launch_bounds__(256) void k_f32(const float *__restrict__ P, int64_
         }
     }
   } else {
-    // dW[r, c] = acc; dZ = mask * (dW-group A); dA, db summed over (r, g)
+    // dW[r, c] = acc; dZ = mask * (dW-group A) (times the estimator's slope);
+    // dA, db summed over (r, g)
     float gA[D * D], gb[D];
 #pragma unroll
     for (int x = 0; x < D * D; ++x) gA[x] = 0.0f;
@@ -131,7 +133,7 @@ __global__ __launch_bounds__(256) void k_f32(const float *__restrict__ P, int64_
 #pragma unroll
           for (int j = 0; j < D; ++j) v = fmaf(acc[a][g * D + j], A[j * D + k], v);
           if (valid && out != nullptr) {
-            const float gz = ste_pass(z, mask_mode) ? v : 0.0f;
+            const float gz = ste_pass(z, mask_mode) ? (est.dge ? v * dge_slope(z, est) : v) : 0.0f;
             float *p = out + r * ldo + cg + k;
             *p = accumulate ? *p + gz : gz;
           }
@@ -163,30 +165,30 @@ static inline dim3 grid2(int64_t J, int64_t I) {
 
 hipError_t launch_fwd_f32(const float *Z, const float *Xp, const float *s, float *Y, int64_t N, int64_t m,
                           int64_t n, hipStream_t st) {
-  k_f32<0, 8><<<grid2(m, N), 256, 0, st>>>(Xp, n, Z, n, N, m, n, s, nullptr, nullptr, nullptr, 0, 0, Y, m,
-                                           nullptr, nullptr);
+  k_f32<0, 8><<<grid2(m, N), 256, 0, st>>>(Xp, n, Z, n, N, m, n, s, nullptr, nullptr, nullptr, 0, GradEst{},
+                                           0, Y, m, nullptr, nullptr);
   return hipGetLastError();
 }
 
 hipError_t launch_dx_f32(const float *Z, const float *dY, const float *rs, const float *A, const float *b,
                          int d, float *dX, int64_t N, int64_t m, int64_t n, hipStream_t st) {
   if (d == 8)
-    k_f32<1, 8><<<grid2(n, N), 256, 0, st>>>(dY, m, Z, n, N, n, m, rs, A, b, nullptr, 0, 0, dX, n, nullptr,
-                                             nullptr);
+    k_f32<1, 8><<<grid2(n, N), 256, 0, st>>>(dY, m, Z, n, N, n, m, rs, A, b, nullptr, 0, GradEst{}, 0, dX,
+                                             n, nullptr, nullptr);
   else
-    k_f32<1, 4><<<grid2(n, N), 256, 0, st>>>(dY, m, Z, n, N, n, m, rs, A, b, nullptr, 0, 0, dX, n, nullptr,
-                                             nullptr);
+    k_f32<1, 4><<<grid2(n, N), 256, 0, st>>>(dY, m, Z, n, N, n, m, rs, A, b, nullptr, 0, GradEst{}, 0, dX,
+                                             n, nullptr, nullptr);
   return hipGetLastError();
 }
 
 hipError_t launch_dz_f32(const float *X, const float *dY, const float *Z, const float *A, int d,
-                         int mask_mode, int accumulate, float *dZ, float *dA, float *db, int64_t N,
-                         int64_t m, int64_t n, hipStream_t st) {
+                         int mask_mode, const GradEst &est, int accumulate, float *dZ, float *dA, float *db,
+                         int64_t N, int64_t m, int64_t n, hipStream_t st) {
   if (d == 8)
-    k_f32<2, 8><<<grid2(n, m), 256, 0, st>>>(dY, m, X, n, m, n, N, nullptr, A, nullptr, Z, mask_mode,
+    k_f32<2, 8><<<grid2(n, m), 256, 0, st>>>(dY, m, X, n, m, n, N, nullptr, A, nullptr, Z, mask_mode, est,
                                              accumulate, dZ, n, dA, db);
   else
-    k_f32<2, 4><<<grid2(n, m), 256, 0, st>>>(dY, m, X, n, m, n, N, nullptr, A, nullptr, Z, mask_mode,
+    k_f32<2, 4><<<grid2(n, m), 256, 0, st>>>(dY, m, X, n, m, n, N, nullptr, A, nullptr, Z, mask_mode, est,
                                              accumulate, dZ, n, dA, db);
   return hipGetLastError();
 }

@@ -302,8 +302,10 @@ __global__ __launch_bounds__(256, 1) void k_gemm_codes(
 }
 
 // ============================================================================
-// Weight-gradient product with the straight-through epilogue:
+// Weight-gradient product with the gradient-estimator epilogue:
 //   D[c, r] = sum_t X'[t, c] dY[t, r] = (dW blockdiag(A))[r, c],  dZ = mask * D
+// (straight-through), or dZ = mask * slope(Z) * D with mask and slope taken
+// from Z (differentiable estimator of eq. dge, kDge)
 // (X' = X blockdiag(A), so the map is already applied).  Both operands come
 // pre-transposed in the token-K fragment layout.  Wave w owns in-features
 // [64 w, 64 w + 64) of the block tile (two 32-row slabs, A operand, streamed
@@ -312,8 +314,10 @@ __global__ __launch_bounds__(256, 1) void k_gemm_codes(
 // by direct-to-LDS loads).
 // ============================================================================
 
+template <bool kDge>
 __global__ __launch_bounds__(256, 1) void k_gemm_dw(const uint16_t *__restrict__ xt, const uint16_t *__restrict__ dyt,
                                                     int KBt, const uint64_t *__restrict__ maskbits, int64_t ldm8,
+                                                    const uint16_t *__restrict__ Zb, int mask_mode, GradEst est,
                                                     int accumulate, void *__restrict__ dZ, int dz_bf16, int m, int n,
                                                     int tiles_m, int tiles_n) {
   constexpr int kStage = 32 * 1024;  // eight 4 KiB B blocks
@@ -404,27 +408,41 @@ __global__ __launch_bounds__(256, 1) void k_gemm_dw(const uint16_t *__restrict__
   }
   LCVQ_WAIT_VM_LGKM0(0);
 
-  // ------------------------------------------------ straight-through epilogue
+  // ------------------------------------------------ gradient-estimator epilogue
   // Lane L holds D[c .. c + 15, r] for each (mi, ni): dZ[r, c .. c + 15] =
   // mask * D, the mask read from the bitmap the backward prepass wrote (one
-  // 64-bit word per row and wave: columns c0 + 64 w .. + 63).  Rows r >= m fall
-  // outside the buffers; columns c >= n get an out-of-range offset.  Every load
-  // (mask words, and old dZ when accumulating) of a block row is issued before
+  // 64-bit word per row and wave: columns c0 + 64 w .. + 63); with kDge, mask
+  // and slope come from Z[r, c .. c + 15] instead.  Rows r >= m fall outside
+  // the buffers; columns c >= n get an out-of-range offset.  Every load (mask
+  // words or Z, and old dZ when accumulating) of a block row is issued before
   // the stores of the previous one: loads and stores share one counter.
-  const __amdgpu_buffer_rsrc_t rmk = make_rsrc(maskbits + (int64_t)r0 * ldm8, (int64_t)(m - r0) * ldm8 * 8);
+  const __amdgpu_buffer_rsrc_t rmk = make_rsrc(maskbits + (int64_t)r0 * ldm8, kDge ? 0 : (int64_t)(m - r0) * ldm8 * 8);
+  const __amdgpu_buffer_rsrc_t rz = make_rsrc(Zb + (int64_t)r0 * n, kDge ? (int64_t)(m - r0) * n * 2 : 0);
   const int64_t mw = (int64_t)tm * 4 + wave;  // this wave's word of each bitmap row
   const int es = dz_bf16 ? 2 : 4;
   const __amdgpu_buffer_rsrc_t rg = make_rsrc((char *)dZ + (int64_t)r0 * n * es, (int64_t)(m - r0) * n * es);
   u32x2 mk[8];
+  if constexpr (!kDge) {
 #pragma unroll
-  for (int ni = 0; ni < 8; ++ni) {
-    const int rl = ni * 32 + (lane & 31);
-    mk[ni] = __builtin_amdgcn_raw_buffer_load_b64(rmk, mw < ldm8 ? (int)((rl * ldm8 + mw) * 8) : (int)kOffNone, 0, 0);
+    for (int ni = 0; ni < 8; ++ni) {
+      const int rl = ni * 32 + (lane & 31);
+      mk[ni] = __builtin_amdgcn_raw_buffer_load_b64(rmk, mw < ldm8 ? (int)((rl * ldm8 + mw) * 8) : (int)kOffNone, 0, 0);
+    }
   }
   u32x4 ov[2][2][2][2];
+  u32x4 zv[2][2][2];  // kDge: Z[r, c .. c + 7] per (buffer, mi, half)
   auto eload = [&](int buf, int ni) {
-    if (!accumulate) return;
     const int rl = ni * 32 + (lane & 31);
+    if constexpr (kDge) {
+#pragma unroll
+      for (int mi = 0; mi < 2; ++mi)
+#pragma unroll
+        for (int half = 0; half < 2; ++half) {
+          const int c = c0 + 64 * wave + 32 * mi + 16 * h + 8 * half;
+          zv[buf][mi][half] = __builtin_amdgcn_raw_buffer_load_b128(rz, c < n ? (uint32_t)(rl * n + c) * 2u : kOffNone, 0, 0);
+        }
+    }
+    if (!accumulate) return;
 #pragma unroll
     for (int mi = 0; mi < 2; ++mi)
 #pragma unroll
@@ -453,10 +471,19 @@ __global__ __launch_bounds__(256, 1) void k_gemm_dw(const uint16_t *__restrict__
         const int c = c0 + 64 * wave + 32 * mi + 16 * h + 8 * half;
         const bool cv = c < n;
         const uint32_t e = (uint32_t)(rl * n + c);
-        const uint32_t mb = mk[ni][mi] >> (16 * h + 8 * half);
         float g[8];
+        if constexpr (kDge) {
 #pragma unroll
-        for (int q = 0; q < 8; ++q) g[q] = ((mb >> q) & 1u) ? acc[mi][ni][8 * half + q] : 0.0f;
+          for (int q = 0; q < 8; ++q) {
+            const uint32_t zw = zv[buf][mi][half][q >> 1];
+            const float z = (q & 1) ? bf16_hi(zw) : bf16_lo(zw);
+            g[q] = ste_pass(z, mask_mode) ? acc[mi][ni][8 * half + q] * dge_slope(z, est) : 0.0f;
+          }
+        } else {
+          const uint32_t mb = mk[ni][mi] >> (16 * h + 8 * half);
+#pragma unroll
+          for (int q = 0; q < 8; ++q) g[q] = ((mb >> q) & 1u) ? acc[mi][ni][8 * half + q] : 0.0f;
+        }
         if (dz_bf16) {
           if (accumulate) {
 #pragma unroll
@@ -516,12 +543,19 @@ hipError_t launch_dx_bf16(const uint32_t *frag, const uint16_t *dyb, const float
   return hipGetLastError();
 }
 
-hipError_t launch_dw_bf16(const uint16_t *xt, const uint16_t *dyt, const uint64_t *maskbits, int accumulate,
-                          void *dZ, bool dz_bf16, int64_t N, int64_t m, int64_t n, hipStream_t st) {
+hipError_t launch_dw_bf16(const uint16_t *xt, const uint16_t *dyt, const uint64_t *maskbits, const uint16_t *Z,
+                          int mask_mode, const GradEst &est, int accumulate, void *dZ, bool dz_bf16, int64_t N,
+                          int64_t m, int64_t n, hipStream_t st) {
   const int tiles_m = (int)ceil_div(n, kTile), tiles_n = (int)ceil_div(m, kTile);
   const int KBt = (int)(bwd_tokens(N) / 64);  // even
-  k_gemm_dw<<<tiles_m * tiles_n, 256, 0, st>>>(xt, dyt, KBt, maskbits, mask_words_per_row(n), accumulate, dZ,
-                                               dz_bf16 ? 1 : 0, (int)m, (int)n, tiles_m, tiles_n);
+  if (est.dge)
+    k_gemm_dw<true><<<tiles_m * tiles_n, 256, 0, st>>>(xt, dyt, KBt, nullptr, mask_words_per_row(n), Z, mask_mode,
+                                                       est, accumulate, dZ, dz_bf16 ? 1 : 0, (int)m, (int)n, tiles_m,
+                                                       tiles_n);
+  else
+    k_gemm_dw<false><<<tiles_m * tiles_n, 256, 0, st>>>(xt, dyt, KBt, maskbits, mask_words_per_row(n), nullptr,
+                                                        mask_mode, est, accumulate, dZ, dz_bf16 ? 1 : 0, (int)m,
+                                                        (int)n, tiles_m, tiles_n);
   return hipGetLastError();
 }
 }  // namespace lcvq

@@ -76,8 +76,11 @@ hipError_t launch_fwd_bf16(const uint32_t *frag, const uint16_t *Xp, int64_t ldp
 hipError_t launch_dx_bf16(const uint32_t *frag, const uint16_t *dyb, const float *rsp, const float *A, const float *b,
                           int d, uint16_t *dX, const uint16_t *X, float *dA, float *db, int64_t N, int64_t m, int64_t n,
                           hipStream_t st);
-hipError_t launch_dw_bf16(const uint16_t *xt, const uint16_t *dyt, const uint64_t *maskbits, int accumulate,
-                          void *dZ, bool dz_bf16, int64_t N, int64_t m, int64_t n, hipStream_t st);
+// maskbits: the straight-through mask; or, with est.dge set, nullptr and the
+// mask and slope are taken from Z (bf16, m x n) under mask_mode
+hipError_t launch_dw_bf16(const uint16_t *xt, const uint16_t *dyt, const uint64_t *maskbits, const uint16_t *Z,
+                          int mask_mode, const GradEst &est, int accumulate, void *dZ, bool dz_bf16, int64_t N,
+                          int64_t m, int64_t n, hipStream_t st);
 
 // fp32 products on the vector ALUs (lcvq_f32.hip)
 hipError_t launch_fwd_f32(const float *Z, const float *Xp, const float *s, float *Y, int64_t N, int64_t m,
@@ -85,7 +88,7 @@ hipError_t launch_fwd_f32(const float *Z, const float *Xp, const float *s, float
 hipError_t launch_dx_f32(const float *Z, const float *dY, const float *rs, const float *A, const float *b,
                          int d, float *dX, int64_t N, int64_t m, int64_t n, hipStream_t st);
 hipError_t launch_dz_f32(const float *X, const float *dY, const float *Z, const float *A, int d,
-                         int mask_mode, int accumulate, float *dZ, float *dA, float *db, int64_t N,
-                         int64_t m, int64_t n, hipStream_t st);
+                         int mask_mode, const GradEst &est, int accumulate, float *dZ, float *dA, float *db,
+                         int64_t N, int64_t m, int64_t n, hipStream_t st);
 
 }  // namespace lcvq

@@ -102,6 +102,30 @@ def test_bwd_validation(lib):
     assert bwd(lib, N=0, acc=1) == L.OK                    # accumulate into nothing: no work
 
 
+def bwd_dge(lib, k=5.0, cap=3.0, N=16, m=64, n=64, d=8, dt=L.BF16, mask=1, acc=0, dX=FAKE, dZ=FAKE, dzt=L.BF16,
+            dA=FAKE, db=FAKE, ws=FAKE, wsb=1 << 40, X=FAKE, dY=FAKE):
+    return lib.lcvq_linear_bwd_dge(N, m, n, d, dt, FAKE, FAKE, FAKE, X, dY, mask, k, cap, acc, dX, dZ, dzt, dA,
+                                   db, ws, wsb, None)
+
+
+def test_bwd_dge_validation(lib):
+    assert bwd_dge(lib, k=0.5) == L.EINVAL                 # k >= 1
+    assert bwd_dge(lib, k=float("nan")) == L.EINVAL
+    assert bwd_dge(lib, k=float("inf")) == L.EINVAL
+    assert bwd_dge(lib, cap=0.0) == L.EINVAL               # cap > 0
+    assert bwd_dge(lib, cap=-1.0) == L.EINVAL
+    assert bwd_dge(lib, cap=float("inf")) == L.EINVAL
+    assert "cap" in L.last_error()
+    # the remaining checks are those of the straight-through entry point
+    assert bwd_dge(lib, d=3) == L.EUNSUPPORTED
+    assert bwd_dge(lib, mask=2) == L.EINVAL
+    assert bwd_dge(lib, dA=None) == L.EINVAL
+    assert bwd_dge(lib, dY=MIS) == L.EALIGN
+    assert bwd_dge(lib, wsb=8) == L.EWORKSPACE
+    assert bwd_dge(lib, N=0, acc=1) == L.OK
+    assert bwd_dge(lib, k=1.0, N=0, acc=1) == L.OK
+
+
 def test_pack_and_dequant_validation(lib):
     p = lib.lcvq_pack2bit
     assert p(FAKE, L.SRC_LATENT, L.BF16, 4, 6, FAKE, None) == L.EINVAL        # n % 4

@@ -328,6 +328,15 @@ def test_dge_backward_matches_finite_differences_of_surrogate(d):
     assert np.all(out["dZ"][~inside] == 0.0)
 
 
+def test_dge_non_finite_latents_get_no_gradient():
+    d = 4
+    Z = np.array([[np.nan, np.inf, -np.inf, 1.25]])
+    out = orc.linear_backward(Z, np.eye(d), np.zeros(d), np.ones((2, 4)), np.ones((2, 1)), d, orc.MASK_LATENT,
+                              dge=(5.0, 3.0))
+    assert out["dZ"][0, :3].tolist() == [0.0, 0.0, 0.0]
+    assert out["dZ"][0, 3] == 2.0 * 0.2 * 2.0 ** 0.8      # dW = 2, slope at x = 1/4
+
+
 def test_dge_with_k_one_is_straight_through():
     r = np.random.default_rng(12)
     d, N, m, n = 8, 4, 5, 16
