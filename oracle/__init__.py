@@ -223,6 +223,24 @@ def pack2bit(codes: np.ndarray) -> np.ndarray:
     return byte.astype(np.uint8)
 
 
+def unpack2bit(packed: np.ndarray, n: int) -> np.ndarray:
+    """Codes of a packed m x n/4 array (inverse of pack2bit): code of column c =
+    bits 2*(c mod 4) .. 2*(c mod 4)+1 of byte c // 4."""
+    P = np.asarray(packed, dtype=np.uint8)
+    m = P.shape[0]
+    assert P.shape[1] * 4 == n
+    out = np.empty((m, n), dtype=np.uint8)
+    for i in range(4):
+        out[:, i::4] = (P >> (2 * i)) & 3
+    return out
+
+
+def linear_forward_packed(packed, A, b, X, d, n):
+    """Output of the layer from packed 2-bit codes (inference, Sec. 3.2 / App. A.2):
+    Y = X W_hat^T with W_hat decoded from the unpacked codes."""
+    return forward(X, decode(unpack2bit(packed, n), A, b, d))
+
+
 # ------------------------------------------------------------ optimiser -----
 
 def adamw_step(theta, grad, m1, m2, step: int, lr: float, beta1: float = 0.9,

@@ -365,12 +365,44 @@ def test_pack_hand_values():
         assert orc.pack2bit(row).tolist() == [expect]
 
 
+def test_unpack_hand_values():
+    assert orc.unpack2bit(np.array([[0x39]], np.uint8), 4).tolist() == [[1, 2, 3, 0]]
+    assert orc.unpack2bit(np.array([[0xFF, 0x00, 0x1B]], np.uint8), 12).tolist() == \
+        [[3, 3, 3, 3, 0, 0, 0, 0, 3, 2, 1, 0]]
+
+
+def test_forward_from_packed_codes_is_forward_from_latent():
+    r = np.random.default_rng(17)
+    for d in (4, 8):
+        N, m, n = 5, 7, 64
+        Z = r.uniform(-1.0, 4.0, (m, n))
+        X, A, b = r.standard_normal((N, n)), r.standard_normal((d, d)), r.standard_normal(d)
+        Y, codes = orc.linear_forward(Z, A, b, X, d)
+        # brute force: one output at a time from the bytes, no unpack helper
+        P = orc.pack2bit(codes)
+        Yb = np.zeros((N, m))
+        for t in range(N):
+            for rr in range(m):
+                acc = 0.0
+                for c in range(n):
+                    code = (int(P[rr, c // 4]) >> (2 * (c % 4))) & 3
+                    g, k = divmod(c, d)
+                    w = sum(A[k, kk] * ((int(P[rr, (g * d + kk) // 4]) >> (2 * ((g * d + kk) % 4))) & 3)
+                            for kk in range(d)) + b[k]
+                    acc += X[t, c] * w
+                    assert code == codes[rr, c]
+                Yb[t, rr] = acc
+        assert np.allclose(orc.linear_forward_packed(P, A, b, X, d, n), Yb, rtol=1e-12, atol=1e-12)
+        assert np.allclose(Y, Yb, rtol=1e-12, atol=1e-12)
+
+
 def test_pack_round_trip():
     codes = np.random.default_rng(2).integers(0, 4, size=(7, 64)).astype(np.uint8)
     p = orc.pack2bit(codes)
     assert p.shape == (7, 16)
     unpacked = np.stack([(p >> (2 * i)) & 3 for i in range(4)], axis=-1).reshape(7, 64)
     assert np.array_equal(unpacked, codes)
+    assert np.array_equal(orc.unpack2bit(p, 64), codes)
 
 
 # ------------------------------------------------------------ optimiser -----
