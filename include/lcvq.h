@@ -71,7 +71,7 @@ typedef enum {
   LCVQ_MASK_LATENT = 1    /* 0 <= Z <= 3 */
 } lcvq_mask_t;
 
-typedef enum { LCVQ_OP_FWD = 0, LCVQ_OP_BWD = 1 } lcvq_op_t;
+typedef enum { LCVQ_OP_FWD = 0, LCVQ_OP_BWD = 1, LCVQ_OP_FWD_PACKED = 2 } lcvq_op_t;
 
 /*
  * lcvq_pack2bit -- packed 2-bit codes, four per byte.
@@ -102,8 +102,9 @@ lcvq_status_t lcvq_dequant(int64_t m, int64_t n, int32_t d, int32_t src_kind, in
 
 /*
  * lcvq_workspace_bytes -- device workspace needed by lcvq_linear_fwd
- * (op = LCVQ_OP_FWD) or lcvq_linear_bwd (op = LCVQ_OP_BWD) for these sizes and
- * element type.  Returns 0 for invalid arguments.  The workspace holds
+ * (op = LCVQ_OP_FWD), lcvq_linear_bwd / lcvq_linear_bwd_dge (op = LCVQ_OP_BWD)
+ * or lcvq_linear_fwd_packed (op = LCVQ_OP_FWD_PACKED, dtype LCVQ_BF16; the
+ * size does not depend on N) for these sizes and element type.  Returns 0 for invalid arguments.  The workspace holds
  * transient, library-private data (transformed activations, codes in the
  * matrix-core operand layout, per-token sums); its contents are undefined
  * between calls.
@@ -128,6 +129,27 @@ lcvq_status_t lcvq_linear_fwd(int64_t N, int64_t m, int64_t n, int32_t d, int32_
                               const void *Z, const float *A, const float *b,
                               const void *X, void *Y, uint8_t *packed_codes_out,
                               void *workspace, size_t workspace_bytes, void *stream);
+
+/*
+ * lcvq_linear_fwd_packed -- Y = X W_hat^T with the codes read from their packed
+ * 2-bit form (lcvq_pack2bit layout): inference with the compressed weight
+ * (def. forward_x, Sec. 3.2, evaluated as in the paper's inference kernel of
+ * App. A.2 without ever forming W_hat).  For decode-sized batches: tokens are
+ * processed 16 at a time, and the packed codes (m * n / 4 bytes, the only
+ * large operand) are streamed once per 16 tokens.
+ *   N, m, n    tokens, out-features, in-features; d in {4, 8}
+ *   packed     m * n / 4 bytes of codes (device, 16-byte aligned)
+ *   A, b       map and offset, fp32 (device)
+ *   X          N x n bf16 activations;  Y  N x m output of element type y_dtype
+ *              (LCVQ_BF16 or LCVQ_F32), written
+ *   workspace  at least lcvq_workspace_bytes(LCVQ_OP_FWD_PACKED, N, m, n, d, LCVQ_BF16)
+ * Requires n % 64 == 0 and m % 8 == 0 (else LCVQ_EUNSUPPORTED).  X' = X
+ * blockdiag(A) is rounded to bf16 as in lcvq_linear_fwd.  Calls that share a
+ * workspace must not run concurrently (it holds per-call tile counters).
+ */
+lcvq_status_t lcvq_linear_fwd_packed(int64_t N, int64_t m, int64_t n, int32_t d, const uint8_t *packed,
+                                     const float *A, const float *b, const void *X, void *Y, int32_t y_dtype,
+                                     void *workspace, size_t workspace_bytes, void *stream);
 
 /*
  * lcvq_linear_bwd -- straight-through backward of lcvq_linear_fwd (Sec. 3.3):
@@ -218,7 +240,9 @@ typedef enum {
   LCVQ_K_DEQUANT = 6,   /* lcvq_dequant */
   LCVQ_K_FILL = 7,      /* zero fills of degenerate shapes */
   LCVQ_K_ADAM = 8,      /* lcvq_adamw_step */
-  LCVQ_K_COUNT = 9
+  LCVQ_K_PACKED_PREP = 9,  /* lcvq_linear_fwd_packed: X' and s of up to 16 tokens */
+  LCVQ_K_PACKED = 10,      /* lcvq_linear_fwd_packed: Y from the packed codes */
+  LCVQ_K_COUNT = 11
 } lcvq_kernel_t;
 lcvq_status_t lcvq_timer_enable(uint32_t mask);
 lcvq_status_t lcvq_timer_read(int32_t kernel, double *total_ms, int64_t *launches);

@@ -12,10 +12,10 @@ import ctypes
 import torch
 
 from . import _lib
-from ._lib import (BF16, F32, MASK_LATENT, MASK_ROUNDED, OP_BWD, OP_FWD,  # noqa: F401
+from ._lib import (BF16, F32, MASK_LATENT, MASK_ROUNDED, OP_BWD, OP_FWD, OP_FWD_PACKED,  # noqa: F401
                    SRC_CODES_U8, SRC_LATENT, SRC_PACKED2, LcvqError)
 
-__all__ = ["linear_fwd", "linear_bwd", "linear_bwd_dge", "pack2bit", "dequant", "adamw_step", "workspace_bytes", "LcvqError",
+__all__ = ["linear_fwd", "linear_fwd_packed", "linear_bwd", "linear_bwd_dge", "pack2bit", "dequant", "adamw_step", "workspace_bytes", "LcvqError",
            "MASK_ROUNDED", "MASK_LATENT", "SRC_LATENT", "SRC_CODES_U8", "SRC_PACKED2"]
 
 _DT = {torch.float32: F32, torch.bfloat16: BF16}
@@ -123,6 +123,26 @@ def linear_fwd(Z: torch.Tensor, A: torch.Tensor, b: torch.Tensor, X: torch.Tenso
     _lib.check(_lib.load().lcvq_linear_fwd(N, m, n, d, dt, _dev(Z, "Z"), _dev(A, "A"), _dev(b, "b"), _dev(X, "X"),
                                            _dev(out, "Y"), _opt(packed_out, "packed_out"), _dev(ws, "workspace"),
                                            ws.numel(), _stream(X.device)), "lcvq_linear_fwd")
+    return out
+
+
+def linear_fwd_packed(packed: torch.Tensor, A: torch.Tensor, b: torch.Tensor, X: torch.Tensor, d: int,
+                      out_dtype: torch.dtype = torch.bfloat16, workspace: torch.Tensor | None = None,
+                      out: torch.Tensor | None = None) -> torch.Tensor:
+    """Y = X W_hat^T (N x m, bf16 or fp32) from packed 2-bit codes (m x n/4 uint8) and bf16 X (N x n)."""
+    m, n = packed.shape[0], packed.shape[1] * 4
+    N = X.shape[0]
+    if packed.dtype != torch.uint8:
+        raise TypeError("packed codes must be uint8")
+    if X.dtype != torch.bfloat16:
+        raise TypeError("X must be bfloat16")
+    if out is None:
+        out = torch.empty((N, m), dtype=out_dtype, device=X.device)
+    ws = _workspace(OP_FWD_PACKED, N, m, n, d, torch.bfloat16, X.device, workspace)
+    _lib.check(_lib.load().lcvq_linear_fwd_packed(N, m, n, d, _dev(packed, "packed"), _dev(A, "A"), _dev(b, "b"),
+                                                  _dev(X, "X"), _dev(out, "Y"), _DT[out.dtype],
+                                                  _dev(ws, "workspace"), ws.numel(), _stream(X.device)),
+               "lcvq_linear_fwd_packed")
     return out
 
 

@@ -15,9 +15,10 @@ SRC_LATENT, SRC_CODES_U8, SRC_PACKED2 = 0, 1, 2
 # lcvq_mask_t
 MASK_ROUNDED, MASK_LATENT = 0, 1
 # lcvq_op_t
-OP_FWD, OP_BWD = 0, 1
+OP_FWD, OP_BWD, OP_FWD_PACKED = 0, 1, 2
 # lcvq_kernel_t
-KERNELS = ["fwd_prep", "fwd", "bwd_prep", "dx", "dw", "pack", "dequant", "fill", "adam"]
+KERNELS = ["fwd_prep", "fwd", "bwd_prep", "dx", "dw", "pack", "dequant", "fill", "adam", "packed_prep",
+           "packed"]
 
 _P = ctypes.c_void_p
 _I64 = ctypes.c_int64
@@ -29,6 +30,7 @@ SIGNATURES = {
     "lcvq_dequant": (_I32, [_I64, _I64, _I32, _I32, _I32, _P, _P, _P, _P, _I32, _P]),
     "lcvq_workspace_bytes": (_SZ, [_I32, _I64, _I64, _I64, _I32, _I32]),
     "lcvq_linear_fwd": (_I32, [_I64, _I64, _I64, _I32, _I32, _P, _P, _P, _P, _P, _P, _P, _SZ, _P]),
+    "lcvq_linear_fwd_packed": (_I32, [_I64, _I64, _I64, _I32, _P, _P, _P, _P, _P, _I32, _P, _SZ, _P]),
     "lcvq_linear_bwd": (_I32, [_I64, _I64, _I64, _I32, _I32, _P, _P, _P, _P, _P, _I32, _I32,
                                _P, _P, _I32, _P, _P, _P, _SZ, _P]),
     "lcvq_linear_bwd_dge": (_I32, [_I64, _I64, _I64, _I32, _I32, _P, _P, _P, _P, _P, _I32, ctypes.c_float,

@@ -4,6 +4,7 @@
 #include <stdarg.h>
 #include <stdio.h>
 
+#include <algorithm>
 #include <atomic>
 #include <cmath>
 #include <mutex>
@@ -91,6 +92,22 @@ BwdLayout bwd_layout(int64_t N, int64_t m, int64_t n, bool bf16) {
   } else {
     L.frag = L.dyb = L.xt = L.dyt = L.mask = L.total = up256((size_t)N * 4);
   }
+  return L;
+}
+
+// Layer output from packed codes: X' of 16 tokens, partial s, split-K
+// partials of the product and its tile counters.
+struct PackedLayout {
+  size_t xq, sp, part, counters, total;
+};
+PackedLayout packed_layout(int64_t m, int64_t n) {
+  const lcvq::PackedPlan p = lcvq::packed_plan(m, n);
+  PackedLayout L{};
+  L.xq = 0;
+  L.sp = up256((size_t)16 * p.nP * 2);
+  L.part = L.sp + up256((size_t)p.nchunks * 16 * 4);
+  L.counters = L.part + up256(p.KS > 1 ? (size_t)p.row_tiles * p.KS * 16 * 64 * 4 : 0);
+  L.total = L.counters + up256((size_t)p.row_tiles * 4);
   return L;
 }
 
@@ -234,6 +251,7 @@ size_t lcvq_workspace_bytes(int32_t op, int64_t N, int64_t m, int64_t n, int32_t
   const bool bf16 = dtype == LCVQ_BF16;
   if (op == LCVQ_OP_FWD) return fwd_layout(N, m, n, bf16).total;
   if (op == LCVQ_OP_BWD) return bwd_layout(N, m, n, bf16).total;
+  if (op == LCVQ_OP_FWD_PACKED) return bf16 ? packed_layout(m, n).total : 0;
   return 0;
 }
 
@@ -344,6 +362,49 @@ lcvq_status_t lcvq_linear_fwd(int64_t N, int64_t m, int64_t n, int32_t d, int32_
       e = tm.done(lcvq::launch_pack2bit(Z, LCVQ_SRC_LATENT, false, m, n, packed_codes_out, st));
       if (e != hipSuccess) return hip_fail(e, "pack launch");
     }
+  }
+  return ok();
+}
+
+lcvq_status_t lcvq_linear_fwd_packed(int64_t N, int64_t m, int64_t n, int32_t d, const uint8_t *packed,
+                                     const float *A, const float *b, const void *X, void *Y, int32_t y_dtype,
+                                     void *workspace, size_t workspace_bytes, void *stream) {
+  lcvq_status_t s = check_common(N, m, n, d, LCVQ_BF16);
+  if (s != LCVQ_OK) return s;
+  if (n % 64 != 0) return fail(LCVQ_EUNSUPPORTED, "packed forward needs n %% 64 == 0 (n=%lld)", (long long)n);
+  if (y_dtype != LCVQ_F32 && y_dtype != LCVQ_BF16) return fail(LCVQ_EINVAL, "y_dtype=%d", y_dtype);
+  const size_t ys = y_dtype == LCVQ_BF16 ? 2 : 4;
+  hipStream_t st = (hipStream_t)stream;
+  hipError_t e;
+  if (N == 0 || m == 0) return ok();
+  if (Y == nullptr) return fail(LCVQ_EINVAL, "null Y");
+  if (!aligned16(Y)) return fail(LCVQ_EALIGN, "Y must be 16-byte aligned");
+  if (n == 0) {  // empty sums: Y = 0
+    if ((e = fill_zero(Y, (size_t)N * m * ys, st)) != hipSuccess) return hip_fail(e, "zero fill");
+    return ok();
+  }
+  if (packed == nullptr || A == nullptr || b == nullptr || X == nullptr)
+    return fail(LCVQ_EINVAL, "null required pointer (packed, A, b, X)");
+  if (!aligned16(packed) || !aligned16(X) || !aligned16(workspace))
+    return fail(LCVQ_EALIGN, "packed, X and workspace must be 16-byte aligned");
+  const PackedLayout L = packed_layout(m, n);
+  if (workspace == nullptr || workspace_bytes < L.total)
+    return fail(LCVQ_EWORKSPACE, "workspace %zu bytes, need %zu", workspace_bytes, L.total);
+  char *ws = (char *)workspace;
+  uint16_t *xq = (uint16_t *)(ws + L.xq);
+  float *sp = (float *)(ws + L.sp), *part = (float *)(ws + L.part);
+  int *counters = (int *)(ws + L.counters);
+  for (int64_t t0 = 0; t0 < N; t0 += 16) {
+    const int Nc = (int)std::min<int64_t>(16, N - t0);
+    {
+      Timed tm(LCVQ_K_PACKED_PREP, st);
+      e = tm.done(lcvq::launch_packed_prep((const uint16_t *)X + t0 * n, Nc, m, n, d, A, b, xq, sp, counters, st));
+      if (e != hipSuccess) return hip_fail(e, "packed prepass launch");
+    }
+    Timed tm(LCVQ_K_PACKED, st);
+    e = tm.done(lcvq::launch_packed_gemv(packed, m, n, xq, sp, Nc, part, counters, (char *)Y + t0 * m * ys,
+                                         y_dtype == LCVQ_BF16, st));
+    if (e != hipSuccess) return hip_fail(e, "packed product launch");
   }
   return ok();
 }

@@ -65,6 +65,24 @@ hipError_t launch_pack2bit(const void *src, int kind, bool bf16, int64_t m, int6
 hipError_t launch_dequant(const void *src, int kind, bool z_bf16, int64_t m, int64_t n, int d,
                           const float *A, const float *b, void *W, bool out_bf16, hipStream_t st);
 
+// layer output from packed 2-bit codes, 16 tokens per pass (lcvq_packed.hip)
+struct PackedPlan {
+  int64_t nP;     // K padded to whole 256-column steps
+  int KT;         // steps
+  int row_tiles;  // 64-row tiles
+  int nchunks;    // 4096-column chunks of the prepass (partial sums of s)
+  int KS, spb;    // K splits over blocks, steps per split
+};
+PackedPlan packed_plan(int64_t m, int64_t n);
+// X' (16 x nP bf16, columns reordered per 16-column group), partial s
+// (nchunks x 16 fp32) and zeroed tile counters (row_tiles ints) for tokens
+// 0 .. Nc - 1 of X (Nc <= 16)
+hipError_t launch_packed_prep(const uint16_t *X, int Nc, int64_t m, int64_t n, int d, const float *A,
+                              const float *b, uint16_t *xq, float *sp, int *counters, hipStream_t st);
+// Y (Nc x m, bf16 or fp32) = codes X'^T + s; part holds row_tiles * KS * 16 * 64 fp32 split-K partials
+hipError_t launch_packed_gemv(const uint8_t *packed, int64_t m, int64_t n, const uint16_t *xq, const float *sp,
+                              int Nc, float *part, int *counters, void *Y, bool y_bf16, hipStream_t st);
+
 // optimiser (lcvq_adam.hip); shadow_kind 0 none, 1 fp32, 2 bf16
 hipError_t launch_adamw(float *theta, const void *grad, bool grad_bf16, float *m1, float *m2, void *shadow,
                         int shadow_kind, int64_t numel, float lr, float beta1, float beta2, float eps,

@@ -53,10 +53,12 @@ def test_workspace_bytes(lib):
 def test_workspace_bytes_of_empty_problems(lib):
     """Zero sizes must not trip the host-side layout arithmetic (no division by zero)."""
     f = lib.lcvq_workspace_bytes
-    for op in (L.OP_FWD, L.OP_BWD):
+    for op in (L.OP_FWD, L.OP_BWD, L.OP_FWD_PACKED):
         for dt in (L.F32, L.BF16):
             for N, m, n in ((0, 64, 64), (16, 0, 64), (16, 64, 0), (0, 0, 0)):
                 assert f(op, N, m, n, 8, dt) >= 0
+    assert f(L.OP_FWD_PACKED, 16, 64, 64, 8, L.BF16) > 0
+    assert f(L.OP_FWD_PACKED, 16, 64, 64, 8, L.F32) == 0          # bf16 only
 
 
 def fwd(lib, N=16, m=64, n=64, d=8, dt=L.BF16, Z=FAKE, A=FAKE, b=FAKE, X=FAKE, Y=FAKE, packed=None,
@@ -124,6 +126,27 @@ def test_bwd_dge_validation(lib):
     assert bwd_dge(lib, wsb=8) == L.EWORKSPACE
     assert bwd_dge(lib, N=0, acc=1) == L.OK
     assert bwd_dge(lib, k=1.0, N=0, acc=1) == L.OK
+
+
+def fwd_packed(lib, N=16, m=64, n=64, d=8, P=FAKE, X=FAKE, Y=FAKE, ydt=L.BF16, ws=FAKE, wsb=1 << 40):
+    return lib.lcvq_linear_fwd_packed(N, m, n, d, P, FAKE, FAKE, X, Y, ydt, ws, wsb, None)
+
+
+def test_fwd_packed_validation(lib):
+    assert fwd_packed(lib, d=5) == L.EUNSUPPORTED
+    assert fwd_packed(lib, n=32) == L.EUNSUPPORTED               # n % 64
+    assert "64" in L.last_error()
+    assert fwd_packed(lib, m=60) == L.EUNSUPPORTED               # m % 8
+    assert fwd_packed(lib, N=-1) == L.EINVAL
+    assert fwd_packed(lib, ydt=7) == L.EINVAL
+    assert fwd_packed(lib, P=None) == L.EINVAL
+    assert fwd_packed(lib, X=None) == L.EINVAL
+    assert fwd_packed(lib, Y=None) == L.EINVAL
+    assert fwd_packed(lib, P=MIS) == L.EALIGN
+    assert fwd_packed(lib, Y=MIS) == L.EALIGN
+    assert fwd_packed(lib, wsb=16) == L.EWORKSPACE
+    assert fwd_packed(lib, N=0, Y=None, X=None) == L.OK          # nothing to compute
+    assert fwd_packed(lib, m=0, Y=None) == L.OK
 
 
 def test_pack_and_dequant_validation(lib):
