@@ -177,6 +177,59 @@ def dge_step(lc, torch, layers, steps):
             "TFLOP/s": round(flops / (ms * 1e-3) / 1e12, 2), "dw_us": round(1e3 * dw_ms / max(cnt, 1), 2)}
 
 
+def packed_decode(lc, torch, token_counts=(1, 4, 16)):
+    """Layer output from packed 2-bit codes (inference) for decode-sized batches,
+    on 28672 x 8192 and 8192 x 28672 matrices, four of each (470 MB of codes,
+    more than the 256 MB last-level cache), called in turn.  Algorithmic bytes
+    per call: the codes (m n / 4), X (N n bf16) and Y (N m bf16)."""
+    import synth
+    d = 8
+    lib = lc._lib.load()
+    mats = [(28672, 8192), (8192, 28672)] * 4
+    g = torch.Generator(device="cuda").manual_seed(0)
+    P = [torch.randint(0, 256, (m, n // 4), dtype=torch.uint8, device="cuda", generator=g) for m, n in mats]
+    A, b = [torch.from_numpy(x).cuda() for x in synth.draw_map(d, 0)]
+    kp, kq = lc._lib.KERNELS.index("packed"), lc._lib.KERNELS.index("packed_prep")
+    out = {}
+    for N in token_counts:
+        X = {n: torch.randn(N, n, device="cuda", generator=g).to(torch.bfloat16) for n in (8192, 28672)}
+        Y = [torch.empty((N, m), dtype=torch.bfloat16, device="cuda") for m, _ in mats]
+        ws = [torch.empty(lc.workspace_bytes(lc.OP_FWD_PACKED, N, m, n, d, torch.bfloat16), dtype=torch.uint8,
+                          device="cuda") for m, n in mats]
+
+        def run():
+            for i, (m, n) in enumerate(mats):
+                lc.linear_fwd_packed(P[i], A, b, X[n], d, out=Y[i], workspace=ws[i])
+
+        for _ in range(3):
+            run()
+        start, stop = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        torch.cuda.synchronize()
+        start.record()
+        for _ in range(20):
+            run()
+        stop.record()
+        torch.cuda.synchronize()
+        call_us = 1e3 * start.elapsed_time(stop) / (20 * len(mats))
+        lib.lcvq_timer_enable((1 << kp) | (1 << kq))
+        for _ in range(10):
+            run()
+        torch.cuda.synchronize()
+        pm, pc = timer_read(lib, kp)
+        qm, qc = timer_read(lib, kq)
+        lib.lcvq_timer_enable(0)
+        pus, qus = 1e3 * pm / max(pc, 1), 1e3 * qm / max(qc, 1)
+        nbytes = sum(m * n / 4 + 2 * N * (n + m) for m, n in mats) / len(mats)
+        gbps = nbytes / (pus * 1e-6) / 1e9
+        out[f"N{N}"] = {"product_us": round(pus, 2), "prepass_us": round(qus, 2), "call_us": round(call_us, 2),
+                        "GB/s": round(gbps, 1), "frac_hbm": round(gbps / PEAK_HBM, 3),
+                        "bytes_per_call": int(nbytes)}
+    out["shapes"] = [[28672, 8192], [8192, 28672]]
+    out["note"] = "GB/s and frac_hbm over the product kernel's average duration; call_us includes the prepass"
+    del P
+    return out
+
+
 def library_gemm(torch, N, m, n):
     """Context: one plain bf16 product of the same shape (Y = X W^T, N(0,1) data)
     through torch.matmul, i.e. the vendor GEMM library, with no quantisation."""
@@ -353,6 +406,7 @@ def main():
     res["library_gemm_same_shape"] = library_gemm(torch, L0.N, L0.m, L0.n)
     if not args.no_hbm:
         res["hbm_kernels"] = hbm_kernels(lc, torch)
+        res["packed_decode"] = packed_decode(lc, torch)
     if not args.no_cpu_baseline:
         res["cpu_baseline"] = cpu_baseline(layers[0], args.cpu_seconds)
         res["cpu_baseline"]["note"] = "first matrix of the workload" if len(layers) > 1 else "whole workload"
