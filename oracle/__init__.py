@@ -24,6 +24,11 @@ Readings of the paper where it is silent or inconsistent:
     mask = [0 <= round(Z) <= 3] ("rounded").  The alternative
     mask = [0 <= Z <= 3] ("latent") is also provided.
   * NaN latents quantise to code 0 with mask 0; +-inf clip to 3 / 0, mask 0.
+  * Xavier reparameterisation (eq. xavier_preprocess, Sec. 3.4): with W_p =
+    s' (W_z - t), the quantiser acts on W_p / s' + t.  The kernels compute that
+    affine value as one fp32 fused multiply-add with fp32 scale 1/s' and shift
+    t, and the codes are decided on that fp32 value; the oracle takes the same
+    decision (fma_f32 below).  The latent's gradient gains the factor 1/s'.
   * Differentiable gradient estimator (eq. dge, Sec. 3.3): the paper gives f on
     one rounding interval of width delta = 1 (the interval of round() on the
     code-domain latent).  It is extended periodically, F(z) = floor(z) +
@@ -54,25 +59,73 @@ def widen(x, dtype: str) -> np.ndarray:
     raise ValueError(dtype)
 
 
+# -------------------------------------------------- quantiser domain -----
+
+def fma_f32(a, b, c) -> np.ndarray:
+    """a * b + c for fp32 values, rounded once to fp32 (binary32 fused multiply-add).
+
+    a * b is exact in fp64 (24 + 24 significant bits).  The sum is split into
+    its fp64 rounding s and the exact remainder e (TwoSum), and s is rounded to
+    fp32; that is the correctly rounded result unless s lies exactly halfway
+    between two fp32 values while e != 0, where e decides the direction."""
+    a, b, c = (np.asarray(x, dtype=np.float32).astype(np.float64) for x in (a, b, c))
+    p = a * b
+    with np.errstate(invalid="ignore", over="ignore"):
+        s = p + c
+        bv = s - p
+        e = (p - (s - bv)) + (c - bv)
+        r32 = s.astype(np.float32)
+        r = r32.astype(np.float64)
+        up = np.nextafter(r32, np.float32(np.inf)).astype(np.float64)
+        dn = np.nextafter(r32, np.float32(-np.inf)).astype(np.float64)
+        out = np.where((s > r) & (s == (r + up) / 2) & (e > 0), up, r)
+        out = np.where((s < r) & (s == (r + dn) / 2) & (e < 0), dn, out)
+    return out
+
+
+def code_domain(W: np.ndarray, scale: float = 1.0, shift: float = 0.0) -> np.ndarray:
+    """The value the quantiser rounds: W itself in the code domain (scale 1, shift
+    0), else fp32(W * scale + shift) with fp32 scale and shift (Sec. 3.4)."""
+    W = np.asarray(W, dtype=np.float64)
+    if scale == 1.0 and shift == 0.0:
+        return W
+    return fma_f32(W, scale, shift)
+
+
+def xavier_params(m: int, n: int, bits: int = 2):
+    """(s', t) of eq. xavier_preprocess: s' = 2a / (2^b - 1), t = (2^b - 1) / 2,
+    a = sqrt(6 / (m + n))."""
+    a = np.sqrt(6.0 / (m + n))
+    return 2.0 * a / (2 ** bits - 1), (2 ** bits - 1) / 2.0
+
+
+def xavier_init(codes: np.ndarray, m: int, n: int, bits: int = 2) -> np.ndarray:
+    """Initial proxy weights W_p = s' (W_z - t) of eq. xavier_preprocess."""
+    sp, t = xavier_params(m, n, bits)
+    return sp * (np.asarray(codes, dtype=np.float64) - t)
+
+
 # ------------------------------------------------------------ quantiser -----
 
-def quantize(Z: np.ndarray) -> np.ndarray:
-    """Integer weights W_z = clip(round(W_p), 0, 2^b - 1)  (eq. quant_param, Sec. 3.2).
+def quantize(Z: np.ndarray, scale: float = 1.0, shift: float = 0.0) -> np.ndarray:
+    """Integer weights W_z = clip(round(W_p), 0, 2^b - 1)  (eq. quant_param, Sec. 3.2),
+    with W_p taken through code_domain (Sec. 3.4) when scale / shift are given.
 
     Returns uint8 codes in {0, 1, 2, 3}."""
-    Z = np.asarray(Z, dtype=np.float64)
+    Z = code_domain(Z, scale, shift)
     u = np.rint(Z)                                  # round half to even
     codes = np.clip(u, 0.0, CODE_MAX)
     codes = np.where(np.isnan(Z), 0.0, codes)
     return codes.astype(np.uint8)
 
 
-def ste_mask(Z: np.ndarray, mode: int = MASK_ROUNDED) -> np.ndarray:
+def ste_mask(Z: np.ndarray, mode: int = MASK_ROUNDED, scale: float = 1.0, shift: float = 0.0) -> np.ndarray:
     """Where the straight-through gradient of eq. quant_param is passed (Sec. 3.3).
 
     rounded: derivative of clip() evaluated at round(Z): 1 iff 0 <= round(Z) <= 3.
-    latent : 1 iff 0 <= Z <= 3."""
-    Z = np.asarray(Z, dtype=np.float64)
+    latent : 1 iff 0 <= Z <= 3.
+    (Z in the code domain, code_domain(W, scale, shift).)"""
+    Z = code_domain(Z, scale, shift)
     if mode == MASK_ROUNDED:
         u = np.rint(Z)
         return (u >= 0.0) & (u <= CODE_MAX)
@@ -183,27 +236,33 @@ def grad_map(dW: np.ndarray, codes: np.ndarray, d: int):
 
 # ----------------------------------------------------------- whole layer ----
 
-def linear_forward(Z, A, b, X, d):
+def linear_forward(Z, A, b, X, d, scale: float = 1.0, shift: float = 0.0):
     """Y and the codes of one LC-VQ linear call (all inputs fp64 values)."""
-    codes = quantize(Z)
+    codes = quantize(Z, scale, shift)
     return forward(X, decode(codes, A, b, d)), codes
 
 
-def linear_backward(Z, A, b, X, dY, d, mask_mode: int = MASK_ROUNDED, dge=None):
+def linear_backward(Z, A, b, X, dY, d, mask_mode: int = MASK_ROUNDED, dge=None, scale: float = 1.0,
+                    shift: float = 0.0):
     """(dX, dZ, dA, db, dW_hat) of one LC-VQ linear call (all inputs fp64 values).
 
     dge = None: straight-through estimator.  dge = (k, cap): the differentiable
-    gradient estimator (Sec. 3.3), dZ = mask * dge_slope(Z) * dL/dcode."""
-    codes = quantize(Z)
+    gradient estimator (Sec. 3.3), dZ = mask * dge_slope(Z) * dL/dcode.  With a
+    quantiser scale / shift (Sec. 3.4) mask and slope are taken at the code-domain
+    value and the chain rule through it multiplies dZ by the scale."""
+    codes = quantize(Z, scale, shift)
     W_hat = decode(codes, A, b, d)
     dW = grad_weight(dY, X)
     dX = grad_input(dY, W_hat)
-    mask = ste_mask(Z, mask_mode)
+    u = code_domain(Z, scale, shift)
+    mask = ste_mask(u, mask_mode)
     if dge is None:
         dZ = grad_latent(dW, A, d, mask)
     else:
         with np.errstate(invalid="ignore"):
-            dZ = np.where(mask, grad_codes(dW, A, d) * dge_slope(Z, *dge), 0.0)
+            dZ = np.where(mask, grad_codes(dW, A, d) * dge_slope(u, *dge), 0.0)
+    if scale != 1.0:
+        dZ = dZ * np.float64(np.float32(scale))
     dA, db = grad_map(dW, codes, d)
     return dict(dX=dX, dZ=dZ, dA=dA, db=db, dW=dW)
 

@@ -352,6 +352,97 @@ def test_dge_with_k_one_is_straight_through():
             assert np.array_equal(ste[key], dge[key])
 
 
+# ------------------------------------------------- quantiser domain (3.4) ---
+
+def _fma_exact(a, b, c):
+    """Correctly rounded binary32 a*b + c by exact rational arithmetic (brute force)."""
+    from fractions import Fraction
+    v = Fraction(float(a)) * Fraction(float(b)) + Fraction(float(c))
+    f = np.float32(float(v))                       # nearest fp64, then fp32: may double-round
+    cands = [np.nextafter(f, np.float32(-np.inf)), f, np.nextafter(f, np.float32(np.inf))]
+    dist = [abs(Fraction(float(x)) - v) for x in cands]
+    best = min(dist)
+    ties = [x for x, dd in zip(cands, dist) if dd == best]
+    if len(ties) > 1:                              # exact tie: even significand
+        ties = [x for x in ties if (np.float32(x).view(np.uint32) & 1) == 0]
+    return float(ties[0])
+
+
+def test_fma_f32_against_exact_rounding():
+    r = np.random.default_rng(31)
+    a = r.standard_normal(3000).astype(np.float32) * np.float32(0.03)
+    b = np.float32(1.0 / 0.018)
+    c = np.float32(1.5)
+    got = orc.fma_f32(a, b, c)
+    want = np.array([_fma_exact(x, b, c) for x in a])
+    assert np.array_equal(got, want)
+    # Double-rounding cases: with a = +-2^-24 (1 + i 2^-23), b = 1 - i 2^-23 and
+    # c = 1 + 2^-23, a b + c = 1 + 3 2^-24 - i^2 2^-70 or 1 + 2^-24 + i^2 2^-70,
+    # i.e. i^2 2^-70 off an fp32 midpoint.  Rounding to fp64 first lands on the
+    # midpoint, whose tie goes the other way than the correct rounding.
+    naive_wrong = 0
+    for i in range(1, 40):
+        for sgn in (1.0, -1.0):
+            for e in (0, -7, 5):                   # same pattern at other exponents
+                x = np.float32(sgn * 2.0 ** (-24 + e) * (1.0 + i * 2.0 ** -23))
+                y = np.float32(1.0 - i * 2.0 ** -23)
+                z = np.float32(2.0 ** e * (1.0 + 2.0 ** -23))
+                want = _fma_exact(x, y, z)
+                assert orc.fma_f32(x, y, z) == want, (i, sgn, e)
+                naive_wrong += float(np.float32(float(x) * float(y) + float(z))) != want
+    assert naive_wrong > 0
+
+
+def test_xavier_params_hand_values():
+    sp, t = orc.xavier_params(4096, 4096)
+    a = np.sqrt(6.0 / 8192)
+    assert t == 1.5 and np.isclose(sp, 2 * a / 3, rtol=1e-15)
+    sp2, _ = orc.xavier_params(11008, 4096)
+    assert np.isclose(sp2, 2 * np.sqrt(6.0 / 15104) / 3, rtol=1e-15)
+
+
+@pytest.mark.parametrize("m,n", [(4096, 4096), (11008, 4096), (256, 256), (28672, 8192)])
+@pytest.mark.parametrize("store", ["bf16", "f32"])
+def test_xavier_init_quantises_back_to_its_codes(m, n, store):
+    # eq. xavier_preprocess preserves the codes: quantising W_p / s' + t returns W_z
+    codes = np.arange(4, dtype=np.uint8).repeat(64)
+    W = orc.xavier_init(codes, m, n).astype(np.float32)
+    if store == "bf16":
+        import synth
+        W = orc.widen(synth.bf16_bits(W), "bf16")
+    sp, t = orc.xavier_params(m, n)
+    assert np.array_equal(orc.quantize(W, np.float32(1.0 / sp), np.float32(t)), codes)
+
+
+def test_xavier_init_statistics():
+    # over uniform codes: mean exactly 0, range exactly [-a, a] (Xavier's uniform bound)
+    m, n = 4096, 11008
+    W = orc.xavier_init(np.arange(4), m, n)
+    a = np.sqrt(6.0 / (m + n))
+    assert abs(W.mean()) < 1e-18
+    assert np.isclose(W.max(), a, rtol=1e-15) and np.isclose(W.min(), -a, rtol=1e-15)
+
+
+def test_quantiser_scale_in_backward_matches_finite_differences():
+    # STE through code = W * scale + shift: relaxing round() to the identity, the loss
+    # <dY, X decode(W scale + shift)^T> has gradient scale * dL/dcode
+    r = np.random.default_rng(41)
+    d, N, m, n = 4, 3, 4, 8
+    scale, shift = np.float32(8.0), np.float32(1.5)      # exact in fp32
+    W = r.uniform(-0.15, 0.15, (m, n))                   # codes inside (0, 3): mask 1
+    X, dY = r.standard_normal((N, n)), r.standard_normal((N, m))
+    A, b = r.standard_normal((d, d)), r.standard_normal(d)
+    out = orc.linear_backward(W, A, b, X, dY, d, orc.MASK_LATENT, scale=scale, shift=shift)
+
+    def loss(W_):
+        return float(np.sum(dY * orc.forward(X, orc.decode(W_ * float(scale) + float(shift), A, b, d))))
+
+    g = np.array([_fd(loss, W, idx, 1e-3) for idx in np.ndindex(W.shape)]).reshape(W.shape)
+    assert np.allclose(out["dZ"], g, rtol=1e-9, atol=1e-9)
+    unit = orc.linear_backward(W * float(scale) + float(shift), A, b, X, dY, d, orc.MASK_LATENT)
+    assert np.allclose(out["dZ"], float(scale) * unit["dZ"], rtol=1e-12, atol=0)
+
+
 # ------------------------------------------------------------- packing ------
 
 def test_pack_hand_values():
