@@ -94,6 +94,16 @@ class Layer:
         lc.linear_bwd_dge(self.Z, self.A, self.b, self.X, self.dY, self.d, k=k, cap=cap, dX=self.dX, dZ=self.dZ,
                           dA=self.dA, db=self.db, workspace=self.wsb)
 
+    def step_xavier(self):
+        """The same step with the latent in the Xavier domain (Sec. 3.4): the same
+        latents read as W_p, quantised through W_p / s' + t."""
+        lc = self.lc
+        qs, qb = lc.xavier_quantizer(self.m, self.n)
+        lc.linear_fwd(self.Z, self.A, self.b, self.X, self.d, packed_out=self.packed, workspace=self.wsf,
+                      out=self.Y, q_scale=qs, q_shift=qb)
+        lc.linear_bwd(self.Z, self.A, self.b, self.X, self.dY, self.d, dX=self.dX, dZ=self.dZ, dA=self.dA,
+                      db=self.db, workspace=self.wsb, q_scale=qs, q_shift=qb)
+
     def flops(self):
         return 6.0 * self.N * self.m * self.n
 
@@ -148,33 +158,35 @@ def hbm_kernels(lc, torch):
     return out
 
 
-def dge_step(lc, torch, layers, steps):
-    """fwd + backward with the differentiable gradient estimator (k = 5, slope cap 3,
-    latent mask), timed like the main step, with its weight-gradient kernel."""
+def variant_step(lc, torch, layers, steps, which, label):
+    """fwd + bwd with a variant of the method (`which`: a Layer method), timed like
+    the main step, with its weight-gradient kernel."""
     lib = lc._lib.load()
-    for _ in range(3):
+
+    def step():
         for L in layers:
-            L.step_dge()
+            getattr(L, which)()
+
+    for _ in range(3):
+        step()
     start, stop = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     torch.cuda.synchronize()
     start.record()
     for _ in range(steps):
-        for L in layers:
-            L.step_dge()
+        step()
     stop.record()
     torch.cuda.synchronize()
     ms = start.elapsed_time(stop) / steps
     kid = lc._lib.KERNELS.index("dw")
     lib.lcvq_timer_enable(1 << kid)
     for _ in range(5):
-        for L in layers:
-            L.step_dge()
+        step()
     torch.cuda.synchronize()
     dw_ms, cnt = timer_read(lib, kid)
     lib.lcvq_timer_enable(0)
     flops = sum(L.flops() for L in layers)
-    return {"estimator": "dge k=5 cap=3 latent mask", "ms_per_step": round(ms, 4),
-            "TFLOP/s": round(flops / (ms * 1e-3) / 1e12, 2), "dw_us": round(1e3 * dw_ms / max(cnt, 1), 2)}
+    return {"variant": label, "ms_per_step": round(ms, 4), "TFLOP/s": round(flops / (ms * 1e-3) / 1e12, 2),
+            "dw_us": round(1e3 * dw_ms / max(cnt, 1), 2)}
 
 
 def packed_decode(lc, torch, token_counts=(1, 4, 16)):
@@ -401,7 +413,10 @@ def main():
                      "flop_per_launch": per_launch_flop, "ms_per_step_with_kernel_events": round(ms_step_ev, 4)},
         "kernels_us_per_step": breakdown,
     }
-    res["dge_step"] = dge_step(lc, torch, layers, args.steps)
+    res["dge_step"] = variant_step(lc, torch, layers, args.steps, "step_dge",
+                                   "differentiable gradient estimator, k=5, slope cap 3, latent mask")
+    res["xavier_step"] = variant_step(lc, torch, layers, args.steps, "step_xavier",
+                                      "latent in the Xavier domain: codes of W_p / s' + t, gradient / s'")
     L0 = layers[0]
     res["library_gemm_same_shape"] = library_gemm(torch, L0.N, L0.m, L0.n)
     if not args.no_hbm:

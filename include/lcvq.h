@@ -71,6 +71,12 @@ typedef enum {
   LCVQ_MASK_LATENT = 1    /* 0 <= Z <= 3 */
 } lcvq_mask_t;
 
+/* Gradient estimator of the latent through round() (Sec. 3.3). */
+typedef enum {
+  LCVQ_EST_STE = 0,  /* straight-through: slope 1 */
+  LCVQ_EST_DGE = 1   /* differentiable gradient estimator (eq. dge), see lcvq_linear_bwd_dge */
+} lcvq_estimator_t;
+
 typedef enum { LCVQ_OP_FWD = 0, LCVQ_OP_BWD = 1, LCVQ_OP_FWD_PACKED = 2 } lcvq_op_t;
 
 /*
@@ -129,6 +135,23 @@ lcvq_status_t lcvq_linear_fwd(int64_t N, int64_t m, int64_t n, int32_t d, int32_
                               const void *Z, const float *A, const float *b,
                               const void *X, void *Y, uint8_t *packed_codes_out,
                               void *workspace, size_t workspace_bytes, void *stream);
+
+/*
+ * lcvq_linear_fwd_ex -- lcvq_linear_fwd with the latent in another domain:
+ * the quantiser rounds the fp32 value fma(Z, q_scale, q_shift) (one rounding),
+ *   codes = clip(round(Z * q_scale + q_shift), 0, 3).
+ * This is the Xavier reparameterisation of Sec. 3.4 (eq. xavier_preprocess):
+ * with proxy weights W_p = s' (W_z - t), s' = 2a / 3, t = 3/2,
+ * a = sqrt(6 / (m + n)), pass Z = W_p, q_scale = 1 / s', q_shift = t.  Such
+ * W_p are made from codes by lcvq_dequant with A = s' I and b = -s' t.
+ * q_scale = 1, q_shift = 0 is lcvq_linear_fwd exactly.  q_scale must be finite
+ * and nonzero, q_shift finite (else LCVQ_EINVAL).  packed_codes_out receives
+ * these codes.  All else as lcvq_linear_fwd.
+ */
+lcvq_status_t lcvq_linear_fwd_ex(int64_t N, int64_t m, int64_t n, int32_t d, int32_t dtype,
+                                 const void *Z, float q_scale, float q_shift, const float *A, const float *b,
+                                 const void *X, void *Y, uint8_t *packed_codes_out,
+                                 void *workspace, size_t workspace_bytes, void *stream);
 
 /*
  * lcvq_linear_fwd_packed -- Y = X W_hat^T with the codes read from their packed
@@ -196,6 +219,24 @@ lcvq_status_t lcvq_linear_bwd_dge(int64_t N, int64_t m, int64_t n, int32_t d, in
                                   const void *X, const void *dY, int32_t mask_mode, float k, float cap,
                                   int32_t accumulate, void *dX, void *dZ, int32_t dz_dtype, float *dA, float *db,
                                   void *workspace, size_t workspace_bytes, void *stream);
+
+/*
+ * lcvq_linear_bwd_ex -- the general backward: latent domain as in
+ * lcvq_linear_fwd_ex (codes and mask taken at v = fma(Z, q_scale, q_shift);
+ * the chain rule through v multiplies dZ by q_scale) and the estimator
+ * (lcvq_estimator_t; dge_k and dge_cap as k and cap of lcvq_linear_bwd_dge,
+ * ignored for LCVQ_EST_STE):
+ *   dZ[r, c] = q_scale * mask(v) * slope(v) * sum_j dW[r, g*d + j] A[j, k].
+ * dX, dA and db are those of lcvq_linear_bwd for the codes of v.
+ * (q_scale, q_shift) = (1, 0) with LCVQ_EST_STE is lcvq_linear_bwd exactly.
+ * All else as lcvq_linear_bwd.
+ */
+lcvq_status_t lcvq_linear_bwd_ex(int64_t N, int64_t m, int64_t n, int32_t d, int32_t dtype,
+                                 const void *Z, float q_scale, float q_shift, const float *A, const float *b,
+                                 const void *X, const void *dY, int32_t mask_mode, int32_t estimator,
+                                 float dge_k, float dge_cap, int32_t accumulate, void *dX, void *dZ,
+                                 int32_t dz_dtype, float *dA, float *db,
+                                 void *workspace, size_t workspace_bytes, void *stream);
 
 /*
  * lcvq_adamw_step -- one AdamW update of a flat fp32 parameter array: the

@@ -8,15 +8,17 @@ library's HIP kernels; there is no CPU or PyTorch fallback.
 from __future__ import annotations
 
 import ctypes
+import math
 
 import torch
 
 from . import _lib
-from ._lib import (BF16, F32, MASK_LATENT, MASK_ROUNDED, OP_BWD, OP_FWD, OP_FWD_PACKED,  # noqa: F401
+from ._lib import (BF16, EST_DGE, EST_STE, F32, MASK_LATENT, MASK_ROUNDED, OP_BWD, OP_FWD, OP_FWD_PACKED,  # noqa: F401
                    SRC_CODES_U8, SRC_LATENT, SRC_PACKED2, LcvqError)
 
-__all__ = ["linear_fwd", "linear_fwd_packed", "linear_bwd", "linear_bwd_dge", "pack2bit", "dequant", "adamw_step", "workspace_bytes", "LcvqError",
-           "MASK_ROUNDED", "MASK_LATENT", "SRC_LATENT", "SRC_CODES_U8", "SRC_PACKED2"]
+__all__ = ["linear_fwd", "linear_fwd_packed", "linear_bwd", "linear_bwd_dge", "xavier_quantizer", "xavier_init",
+           "pack2bit", "dequant", "adamw_step", "workspace_bytes", "LcvqError", "MASK_ROUNDED", "MASK_LATENT",
+           "SRC_LATENT", "SRC_CODES_U8", "SRC_PACKED2", "EST_STE", "EST_DGE"]
 
 _DT = {torch.float32: F32, torch.bfloat16: BF16}
 
@@ -89,6 +91,25 @@ def dequant(src: torch.Tensor, A: torch.Tensor, b: torch.Tensor, d: int, n: int 
     return out
 
 
+def xavier_quantizer(m: int, n: int, bits: int = 2) -> tuple[float, float]:
+    """(q_scale, q_shift) = (1 / s', t) of the Xavier reparameterisation (eq. xavier_preprocess,
+    Sec. 3.4): s' = 2a / (2^b - 1), t = (2^b - 1) / 2, a = sqrt(6 / (m + n)); q_scale rounded to fp32."""
+    a = math.sqrt(6.0 / (m + n))
+    sp, t = 2.0 * a / (2 ** bits - 1), (2 ** bits - 1) / 2.0
+    return float(torch.tensor(1.0 / sp, dtype=torch.float32)), t
+
+
+def xavier_init(codes: torch.Tensor, m: int, n: int, d: int, src_kind: int | None = None,
+                out_dtype: torch.dtype = torch.float32, bits: int = 2) -> torch.Tensor:
+    """Initial proxy weights W_p = s' (W_z - t) (eq. xavier_preprocess) from uint8 or packed codes:
+    lcvq_dequant with A = s' I and b = -s' t."""
+    a = math.sqrt(6.0 / (m + n))
+    sp, t = 2.0 * a / (2 ** bits - 1), (2 ** bits - 1) / 2.0
+    A = torch.eye(d, dtype=torch.float32, device=codes.device) * sp
+    b = torch.full((d,), -sp * t, dtype=torch.float32, device=codes.device)
+    return dequant(codes, A, b, d, n=n, src_kind=src_kind, out_dtype=out_dtype)
+
+
 def adamw_step(theta: torch.Tensor, grad: torch.Tensor, m1: torch.Tensor, m2: torch.Tensor, step: int,
                lr: float, beta1: float = 0.9, beta2: float = 0.999, eps: float = 1e-8,
                weight_decay: float = 0.0, shadow: torch.Tensor | None = None) -> None:
@@ -110,8 +131,11 @@ def adamw_step(theta: torch.Tensor, grad: torch.Tensor, m1: torch.Tensor, m2: to
 
 def linear_fwd(Z: torch.Tensor, A: torch.Tensor, b: torch.Tensor, X: torch.Tensor, d: int,
                packed_out: torch.Tensor | None = None, workspace: torch.Tensor | None = None,
-               out: torch.Tensor | None = None) -> torch.Tensor:
-    """Y = X W_hat^T (N x m) for latents Z (m x n), map A (d x d fp32), offset b (d fp32)."""
+               out: torch.Tensor | None = None, q_scale: float = 1.0, q_shift: float = 0.0) -> torch.Tensor:
+    """Y = X W_hat^T (N x m) for latents Z (m x n), map A (d x d fp32), offset b (d fp32).
+
+    q_scale, q_shift: the quantiser rounds Z * q_scale + q_shift (see xavier_quantizer);
+    the default is the code domain."""
     m, n = Z.shape
     N = X.shape[0]
     dt = _dtype_code(X)
@@ -120,9 +144,13 @@ def linear_fwd(Z: torch.Tensor, A: torch.Tensor, b: torch.Tensor, X: torch.Tenso
     if out is None:
         out = torch.empty((N, m), dtype=X.dtype, device=X.device)
     ws = _workspace(OP_FWD, N, m, n, d, X.dtype, X.device, workspace)
-    _lib.check(_lib.load().lcvq_linear_fwd(N, m, n, d, dt, _dev(Z, "Z"), _dev(A, "A"), _dev(b, "b"), _dev(X, "X"),
-                                           _dev(out, "Y"), _opt(packed_out, "packed_out"), _dev(ws, "workspace"),
-                                           ws.numel(), _stream(X.device)), "lcvq_linear_fwd")
+    tail = (_dev(A, "A"), _dev(b, "b"), _dev(X, "X"), _dev(out, "Y"), _opt(packed_out, "packed_out"),
+            _dev(ws, "workspace"), ws.numel(), _stream(X.device))
+    if q_scale == 1.0 and q_shift == 0.0:
+        _lib.check(_lib.load().lcvq_linear_fwd(N, m, n, d, dt, _dev(Z, "Z"), *tail), "lcvq_linear_fwd")
+    else:
+        _lib.check(_lib.load().lcvq_linear_fwd_ex(N, m, n, d, dt, _dev(Z, "Z"), q_scale, q_shift, *tail),
+                   "lcvq_linear_fwd_ex")
     return out
 
 
@@ -150,10 +178,11 @@ def linear_bwd(Z: torch.Tensor, A: torch.Tensor, b: torch.Tensor, X: torch.Tenso
                mask_mode: int = MASK_ROUNDED, accumulate: bool = False, need_dX: bool = True,
                need_dZ: bool = True, need_map: bool = True, dz_dtype: torch.dtype | None = None,
                dX: torch.Tensor | None = None, dZ: torch.Tensor | None = None, dA: torch.Tensor | None = None,
-               db: torch.Tensor | None = None, workspace: torch.Tensor | None = None):
+               db: torch.Tensor | None = None, workspace: torch.Tensor | None = None, q_scale: float = 1.0,
+               q_shift: float = 0.0):
     """Straight-through backward: returns (dX, dZ, dA, db); skipped outputs are None."""
     return _linear_bwd(None, Z, A, b, X, dY, d, mask_mode, accumulate, need_dX, need_dZ, need_map, dz_dtype,
-                       dX, dZ, dA, db, workspace)
+                       dX, dZ, dA, db, workspace, q_scale, q_shift)
 
 
 def linear_bwd_dge(Z: torch.Tensor, A: torch.Tensor, b: torch.Tensor, X: torch.Tensor, dY: torch.Tensor,
@@ -161,17 +190,17 @@ def linear_bwd_dge(Z: torch.Tensor, A: torch.Tensor, b: torch.Tensor, X: torch.T
                    accumulate: bool = False, need_dX: bool = True, need_dZ: bool = True, need_map: bool = True,
                    dz_dtype: torch.dtype | None = None, dX: torch.Tensor | None = None,
                    dZ: torch.Tensor | None = None, dA: torch.Tensor | None = None, db: torch.Tensor | None = None,
-                   workspace: torch.Tensor | None = None):
+                   workspace: torch.Tensor | None = None, q_scale: float = 1.0, q_shift: float = 0.0):
     """Backward with the differentiable gradient estimator (k, slope cap): returns (dX, dZ, dA, db).
 
     The default mask is the latent one, [0 <= Z <= 3], which the chain rule
     gives through clip(f(Z), 0, 3)."""
     return _linear_bwd((float(k), float(cap)), Z, A, b, X, dY, d, mask_mode, accumulate, need_dX, need_dZ,
-                       need_map, dz_dtype, dX, dZ, dA, db, workspace)
+                       need_map, dz_dtype, dX, dZ, dA, db, workspace, q_scale, q_shift)
 
 
 def _linear_bwd(dge, Z, A, b, X, dY, d, mask_mode, accumulate, need_dX, need_dZ, need_map, dz_dtype, dX, dZ, dA,
-                db, workspace):
+                db, workspace, q_scale=1.0, q_shift=0.0):
     m, n = Z.shape
     N = X.shape[0]
     dt = _dtype_code(X)
@@ -190,7 +219,11 @@ def _linear_bwd(dge, Z, A, b, X, dY, d, mask_mode, accumulate, need_dX, need_dZ,
     tail = (1 if accumulate else 0, _opt(dX if need_dX else None, "dX"), _opt(dZ if need_dZ else None, "dZ"),
             _DT[dz_dtype], _opt(dA if need_map else None, "dA"), _opt(db if need_map else None, "db"),
             _dev(ws, "workspace"), ws.numel(), _stream(dev))
-    if dge is None:
+    if q_scale != 1.0 or q_shift != 0.0:
+        est = (EST_STE, 0.0, 0.0) if dge is None else (EST_DGE, *dge)
+        head_ex = head[:6] + (q_scale, q_shift) + head[6:]
+        _lib.check(_lib.load().lcvq_linear_bwd_ex(*head_ex, *est, *tail), "lcvq_linear_bwd_ex")
+    elif dge is None:
         _lib.check(_lib.load().lcvq_linear_bwd(*head, *tail), "lcvq_linear_bwd")
     else:
         _lib.check(_lib.load().lcvq_linear_bwd_dge(*head, *dge, *tail), "lcvq_linear_bwd_dge")

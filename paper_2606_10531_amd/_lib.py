@@ -16,6 +16,7 @@ SRC_LATENT, SRC_CODES_U8, SRC_PACKED2 = 0, 1, 2
 MASK_ROUNDED, MASK_LATENT = 0, 1
 # lcvq_op_t
 OP_FWD, OP_BWD, OP_FWD_PACKED = 0, 1, 2
+EST_STE, EST_DGE = 0, 1
 # lcvq_kernel_t
 KERNELS = ["fwd_prep", "fwd", "bwd_prep", "dx", "dw", "pack", "dequant", "fill", "adam", "packed_prep",
            "packed"]
@@ -30,6 +31,11 @@ SIGNATURES = {
     "lcvq_dequant": (_I32, [_I64, _I64, _I32, _I32, _I32, _P, _P, _P, _P, _I32, _P]),
     "lcvq_workspace_bytes": (_SZ, [_I32, _I64, _I64, _I64, _I32, _I32]),
     "lcvq_linear_fwd": (_I32, [_I64, _I64, _I64, _I32, _I32, _P, _P, _P, _P, _P, _P, _P, _SZ, _P]),
+    "lcvq_linear_fwd_ex": (_I32, [_I64, _I64, _I64, _I32, _I32, _P, ctypes.c_float, ctypes.c_float, _P, _P, _P,
+                                  _P, _P, _P, _SZ, _P]),
+    "lcvq_linear_bwd_ex": (_I32, [_I64, _I64, _I64, _I32, _I32, _P, ctypes.c_float, ctypes.c_float, _P, _P, _P,
+                                  _P, _I32, _I32, ctypes.c_float, ctypes.c_float, _I32, _P, _P, _I32, _P, _P, _P,
+                                  _SZ, _P]),
     "lcvq_linear_fwd_packed": (_I32, [_I64, _I64, _I64, _I32, _P, _P, _P, _P, _P, _I32, _P, _SZ, _P]),
     "lcvq_linear_bwd": (_I32, [_I64, _I64, _I64, _I32, _I32, _P, _P, _P, _P, _P, _I32, _I32,
                                _P, _P, _I32, _P, _P, _P, _SZ, _P]),

@@ -34,6 +34,8 @@ lcvq_status_t hip_fail(hipError_t e, const char *what) {
 }
 
 bool aligned16(const void *p) { return ((uintptr_t)p & 15u) == 0; }
+// quantiser of the code domain: codes = clip(round(Z), 0, 3), gradient factor 1
+constexpr lcvq::Quantizer kCodeDomain{0, 1.0f, 0.0f};
 size_t up256(size_t x) { return (x + 255) & ~(size_t)255; }
 
 // Largest row length of an operand streamed through the 256-row tiles with
@@ -267,7 +269,8 @@ lcvq_status_t lcvq_pack2bit(const void *src, int32_t src_kind, int32_t src_dtype
   if (src == nullptr || packed == nullptr) return fail(LCVQ_EINVAL, "null pointer");
   if (!aligned16(src) || !aligned16(packed)) return fail(LCVQ_EALIGN, "src/packed must be 16-byte aligned");
   Timed tm(LCVQ_K_PACK, (hipStream_t)stream);
-  hipError_t e = tm.done(lcvq::launch_pack2bit(src, src_kind, src_dtype == LCVQ_BF16, m, n, packed, (hipStream_t)stream));
+  hipError_t e = tm.done(lcvq::launch_pack2bit(src, src_kind, src_dtype == LCVQ_BF16, m, n, packed, kCodeDomain,
+                                               (hipStream_t)stream));
   return e == hipSuccess ? ok() : hip_fail(e, "pack2bit launch");
 }
 
@@ -312,9 +315,12 @@ lcvq_status_t lcvq_dequant(int64_t m, int64_t n, int32_t d, int32_t src_kind, in
   return e == hipSuccess ? ok() : hip_fail(e, "dequant launch");
 }
 
-lcvq_status_t lcvq_linear_fwd(int64_t N, int64_t m, int64_t n, int32_t d, int32_t dtype, const void *Z,
-                              const float *A, const float *b, const void *X, void *Y, uint8_t *packed_codes_out,
-                              void *workspace, size_t workspace_bytes, void *stream) {
+}  // extern "C"
+
+// Both forward entry points: `qz` is the quantiser domain (Sec. 3.4).
+static lcvq_status_t linear_fwd(int64_t N, int64_t m, int64_t n, int32_t d, int32_t dtype, const void *Z,
+                                const lcvq::Quantizer &qz, const float *A, const float *b, const void *X, void *Y,
+                                uint8_t *packed_codes_out, void *workspace, size_t workspace_bytes, void *stream) {
   lcvq_status_t s = check_common(N, m, n, d, dtype);
   if (s != LCVQ_OK) return s;
   const bool bf16 = dtype == LCVQ_BF16;
@@ -328,7 +334,13 @@ lcvq_status_t lcvq_linear_fwd(int64_t N, int64_t m, int64_t n, int32_t d, int32_
       hipError_t e = fill_zero(Y, (size_t)N * m * es, st);
       if (e != hipSuccess) return hip_fail(e, "zero fill");
     }
-    if (m > 0 && n > 0 && packed_codes_out != nullptr) return lcvq_pack2bit(Z, LCVQ_SRC_LATENT, dtype, m, n, packed_codes_out, stream);
+    if (m > 0 && n > 0 && packed_codes_out != nullptr) {
+      if (Z == nullptr) return fail(LCVQ_EINVAL, "null Z");
+      if (!aligned16(Z) || !aligned16(packed_codes_out)) return fail(LCVQ_EALIGN, "Z and packed_codes_out must be 16-byte aligned");
+      Timed tm(LCVQ_K_PACK, st);
+      hipError_t e = tm.done(lcvq::launch_pack2bit(Z, LCVQ_SRC_LATENT, bf16, m, n, packed_codes_out, qz, st));
+      if (e != hipSuccess) return hip_fail(e, "pack launch");
+    }
     return ok();
   }
   if (Z == nullptr || A == nullptr || b == nullptr || X == nullptr || Y == nullptr)
@@ -346,8 +358,8 @@ lcvq_status_t lcvq_linear_fwd(int64_t N, int64_t m, int64_t n, int32_t d, int32_
     uint32_t *frag = (uint32_t *)(ws + L.frag);
     {
       Timed tm(LCVQ_K_FWD_PREP, st);
-      e = tm.done(lcvq::launch_fwd_prep_bf16((const uint16_t *)Z, m, n, frag, packed_codes_out, (const uint16_t *)X, N,
-                                             L.Np, L.ldp, d, A, b, (uint16_t *)(ws + L.xp), svec, st));
+      e = tm.done(lcvq::launch_fwd_prep_bf16((const uint16_t *)Z, m, n, qz, frag, packed_codes_out, (const uint16_t *)X,
+                                             N, L.Np, L.ldp, d, A, b, (uint16_t *)(ws + L.xp), svec, st));
     }
     if (e != hipSuccess) return hip_fail(e, "forward prepass launch");
     { Timed tm(LCVQ_K_FWD, st); e = tm.done(lcvq::launch_fwd_bf16(frag, (const uint16_t *)(ws + L.xp), L.ldp, svec, (uint16_t *)Y, N, m, n, st)); }
@@ -355,15 +367,45 @@ lcvq_status_t lcvq_linear_fwd(int64_t N, int64_t m, int64_t n, int32_t d, int32_
   } else {
     { Timed tm(LCVQ_K_FWD_PREP, st); e = tm.done(lcvq::launch_act_transform(X, false, N, N, n, d, A, b, ws + L.xp, n, svec, st)); }
     if (e != hipSuccess) return hip_fail(e, "activation transform launch");
-    { Timed tm(LCVQ_K_FWD, st); e = tm.done(lcvq::launch_fwd_f32((const float *)Z, (const float *)(ws + L.xp), svec, (float *)Y, N, m, n, st)); }
+    {
+      Timed tm(LCVQ_K_FWD, st);
+      e = tm.done(lcvq::launch_fwd_f32((const float *)Z, qz, (const float *)(ws + L.xp), svec, (float *)Y, N, m, n, st));
+    }
     if (e != hipSuccess) return hip_fail(e, "forward product launch");
     if (packed_codes_out != nullptr) {
       Timed tm(LCVQ_K_PACK, st);
-      e = tm.done(lcvq::launch_pack2bit(Z, LCVQ_SRC_LATENT, false, m, n, packed_codes_out, st));
+      e = tm.done(lcvq::launch_pack2bit(Z, LCVQ_SRC_LATENT, false, m, n, packed_codes_out, qz, st));
       if (e != hipSuccess) return hip_fail(e, "pack launch");
     }
   }
   return ok();
+}
+
+// The quantiser of the `_ex` entry points: (1, 0) is the code domain itself.
+static lcvq_status_t make_quantizer(float q_scale, float q_shift, lcvq::Quantizer *qz) {
+  if (!std::isfinite(q_scale) || !std::isfinite(q_shift) || q_scale == 0.0f)
+    return fail(LCVQ_EINVAL, "quantiser scale=%g shift=%g (need finite values, scale != 0)", (double)q_scale,
+                (double)q_shift);
+  *qz = (q_scale == 1.0f && q_shift == 0.0f) ? kCodeDomain : lcvq::Quantizer{1, q_scale, q_shift};
+  return LCVQ_OK;
+}
+
+extern "C" {
+
+lcvq_status_t lcvq_linear_fwd(int64_t N, int64_t m, int64_t n, int32_t d, int32_t dtype, const void *Z,
+                              const float *A, const float *b, const void *X, void *Y, uint8_t *packed_codes_out,
+                              void *workspace, size_t workspace_bytes, void *stream) {
+  return linear_fwd(N, m, n, d, dtype, Z, kCodeDomain, A, b, X, Y, packed_codes_out, workspace, workspace_bytes,
+                    stream);
+}
+
+lcvq_status_t lcvq_linear_fwd_ex(int64_t N, int64_t m, int64_t n, int32_t d, int32_t dtype, const void *Z,
+                                 float q_scale, float q_shift, const float *A, const float *b, const void *X, void *Y,
+                                 uint8_t *packed_codes_out, void *workspace, size_t workspace_bytes, void *stream) {
+  lcvq::Quantizer qz;
+  const lcvq_status_t s = make_quantizer(q_scale, q_shift, &qz);
+  if (s != LCVQ_OK) return s;
+  return linear_fwd(N, m, n, d, dtype, Z, qz, A, b, X, Y, packed_codes_out, workspace, workspace_bytes, stream);
 }
 
 lcvq_status_t lcvq_linear_fwd_packed(int64_t N, int64_t m, int64_t n, int32_t d, const uint8_t *packed,
@@ -413,7 +455,8 @@ lcvq_status_t lcvq_linear_fwd_packed(int64_t N, int64_t m, int64_t n, int32_t d,
 
 // Both backward entry points: `est` selects the estimator of the latent's gradient.
 static lcvq_status_t linear_bwd(int64_t N, int64_t m, int64_t n, int32_t d, int32_t dtype, const void *Z,
-                                const float *A, const float *b, const void *X, const void *dY, int32_t mask_mode,
+                                const lcvq::Quantizer &qz, const float *A, const float *b, const void *X,
+                                const void *dY, int32_t mask_mode,
                                 const lcvq::GradEst &est, int32_t accumulate, void *dX, void *dZ, int32_t dz_dtype,
                                 float *dA, float *db, void *workspace, size_t workspace_bytes, void *stream) {
   lcvq_status_t s = check_common(N, m, n, d, dtype);
@@ -472,7 +515,7 @@ static lcvq_status_t linear_bwd(int64_t N, int64_t m, int64_t n, int32_t d, int3
     {
       // the quantise blocks run when the input-gradient product or the bitmap needs them
       Timed tm(LCVQ_K_BWD_PREP, st);
-      e = tm.done(lcvq::launch_bwd_prep_bf16((const uint16_t *)Z, m, n, run_dx || maskbits ? frag : nullptr,
+      e = tm.done(lcvq::launch_bwd_prep_bf16((const uint16_t *)Z, m, n, qz, run_dx || maskbits ? frag : nullptr,
                                              (const uint16_t *)X, (const uint16_t *)dY, A, d, N,
                                              run_dx ? dyb : nullptr, dZ != nullptr ? xt : nullptr,
                                              dZ != nullptr ? dyt : nullptr, rs, maskbits, mask_mode,
@@ -488,7 +531,7 @@ static lcvq_status_t linear_bwd(int64_t N, int64_t m, int64_t n, int32_t d, int3
     }
     if (dZ != nullptr) {
       Timed tm(LCVQ_K_DW, st);
-      e = tm.done(lcvq::launch_dw_bf16(xt, dyt, maskbits, (const uint16_t *)Z, mask_mode, est, accumulate, dZ,
+      e = tm.done(lcvq::launch_dw_bf16(xt, dyt, maskbits, (const uint16_t *)Z, qz, mask_mode, est, accumulate, dZ,
                                        dz_dtype == LCVQ_BF16, N, m, n, st));
       if (e != hipSuccess) return hip_fail(e, "weight-gradient launch");
     }
@@ -503,7 +546,7 @@ static lcvq_status_t linear_bwd(int64_t N, int64_t m, int64_t n, int32_t d, int3
     if (e != hipSuccess) return hip_fail(e, "row-sum launch");
     zA = zb = nullptr;  // cleared by the row-sum launch
     Timed tm(LCVQ_K_DX, st);
-    e = tm.done(lcvq::launch_dx_f32((const float *)Z, (const float *)dY, rs, A, b, d, (float *)dX, N, m, n, st));
+    e = tm.done(lcvq::launch_dx_f32((const float *)Z, qz, (const float *)dY, rs, A, b, d, (float *)dX, N, m, n, st));
     if (e != hipSuccess) return hip_fail(e, "input-gradient launch");
   }
   if (zA != nullptr) {
@@ -512,7 +555,7 @@ static lcvq_status_t linear_bwd(int64_t N, int64_t m, int64_t n, int32_t d, int3
   }
   if (dZ != nullptr || want_map) {
     Timed tm(LCVQ_K_DW, st);
-    e = tm.done(lcvq::launch_dz_f32((const float *)X, (const float *)dY, (const float *)Z, A, d, mask_mode, est,
+    e = tm.done(lcvq::launch_dz_f32((const float *)X, (const float *)dY, (const float *)Z, qz, A, d, mask_mode, est,
                                     accumulate, (float *)dZ, dA, db, N, m, n, st));
     if (e != hipSuccess) return hip_fail(e, "weight-gradient launch");
   }
@@ -525,18 +568,48 @@ lcvq_status_t lcvq_linear_bwd(int64_t N, int64_t m, int64_t n, int32_t d, int32_
                               const float *A, const float *b, const void *X, const void *dY, int32_t mask_mode,
                               int32_t accumulate, void *dX, void *dZ, int32_t dz_dtype, float *dA, float *db,
                               void *workspace, size_t workspace_bytes, void *stream) {
-  return linear_bwd(N, m, n, d, dtype, Z, A, b, X, dY, mask_mode, lcvq::GradEst{0, 0.0f, 1.0f, 1.0f}, accumulate,
-                    dX, dZ, dz_dtype, dA, db, workspace, workspace_bytes, stream);
+  return linear_bwd(N, m, n, d, dtype, Z, kCodeDomain, A, b, X, dY, mask_mode, lcvq::GradEst{0, 0.0f, 1.0f, 1.0f},
+                    accumulate, dX, dZ, dz_dtype, dA, db, workspace, workspace_bytes, stream);
 }
+
+}  // extern "C"
+
+static lcvq_status_t make_estimator(int32_t estimator, float k, float cap, lcvq::GradEst *est) {
+  if (estimator == LCVQ_EST_STE) {
+    *est = lcvq::GradEst{0, 0.0f, 1.0f, 1.0f};
+    return LCVQ_OK;
+  }
+  if (estimator != LCVQ_EST_DGE) return fail(LCVQ_EINVAL, "estimator=%d", estimator);
+  if (!(k >= 1.0f) || !std::isfinite(k)) return fail(LCVQ_EINVAL, "dge k=%g (need a finite k >= 1)", (double)k);
+  if (!(cap > 0.0f) || !std::isfinite(cap)) return fail(LCVQ_EINVAL, "dge cap=%g (need a finite cap > 0)", (double)cap);
+  *est = lcvq::GradEst{1, (float)(1.0 / (double)k - 1.0), (float)(1.0 / (double)k), cap};
+  return LCVQ_OK;
+}
+
+extern "C" {
 
 lcvq_status_t lcvq_linear_bwd_dge(int64_t N, int64_t m, int64_t n, int32_t d, int32_t dtype, const void *Z,
                                   const float *A, const float *b, const void *X, const void *dY, int32_t mask_mode,
                                   float k, float cap, int32_t accumulate, void *dX, void *dZ, int32_t dz_dtype,
                                   float *dA, float *db, void *workspace, size_t workspace_bytes, void *stream) {
-  if (!(k >= 1.0f) || !std::isfinite(k)) return fail(LCVQ_EINVAL, "dge k=%g (need a finite k >= 1)", (double)k);
-  if (!(cap > 0.0f) || !std::isfinite(cap)) return fail(LCVQ_EINVAL, "dge cap=%g (need a finite cap > 0)", (double)cap);
-  const lcvq::GradEst est{1, (float)(1.0 / (double)k - 1.0), (float)(1.0 / (double)k), cap};
-  return linear_bwd(N, m, n, d, dtype, Z, A, b, X, dY, mask_mode, est, accumulate, dX, dZ, dz_dtype, dA, db,
+  lcvq::GradEst est;
+  const lcvq_status_t s = make_estimator(LCVQ_EST_DGE, k, cap, &est);
+  if (s != LCVQ_OK) return s;
+  return linear_bwd(N, m, n, d, dtype, Z, kCodeDomain, A, b, X, dY, mask_mode, est, accumulate, dX, dZ, dz_dtype,
+                    dA, db, workspace, workspace_bytes, stream);
+}
+
+lcvq_status_t lcvq_linear_bwd_ex(int64_t N, int64_t m, int64_t n, int32_t d, int32_t dtype, const void *Z,
+                                 float q_scale, float q_shift, const float *A, const float *b, const void *X,
+                                 const void *dY, int32_t mask_mode, int32_t estimator, float dge_k, float dge_cap,
+                                 int32_t accumulate, void *dX, void *dZ, int32_t dz_dtype, float *dA, float *db,
+                                 void *workspace, size_t workspace_bytes, void *stream) {
+  lcvq::Quantizer qz;
+  lcvq::GradEst est;
+  lcvq_status_t s = make_quantizer(q_scale, q_shift, &qz);
+  if (s == LCVQ_OK) s = make_estimator(estimator, dge_k, dge_cap, &est);
+  if (s != LCVQ_OK) return s;
+  return linear_bwd(N, m, n, d, dtype, Z, qz, A, b, X, dY, mask_mode, est, accumulate, dX, dZ, dz_dtype, dA, db,
                     workspace, workspace_bytes, stream);
 }
 

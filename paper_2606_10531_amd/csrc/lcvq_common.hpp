@@ -52,6 +52,17 @@ __device__ __forceinline__ bool ste_pass(float z, int mode) {
   return v >= 0.0f && v <= (float)kMaxCode;
 }
 
+// Quantiser domain (Sec. 3.4): the quantiser rounds fp32 fma(w, scale, shift);
+// in the code domain (affine = 0) it rounds w itself, bit for bit.  The latent's
+// gradient gains the factor `scale` (1 in the code domain).
+struct Quantizer {
+  int affine;
+  float scale, shift;
+};
+__device__ __forceinline__ float code_value(float w, const Quantizer &q) {
+  return q.affine ? fmaf(w, q.scale, q.shift) : w;
+}
+
 // Gradient estimator of the latent: straight-through (dge = 0), or the
 // differentiable estimator of eq. dge (Sec. 3.3) with delta = 1, slope
 // s |2x - 1|^e capped at `cap`, where s = 1/k and e = 1/k - 1.

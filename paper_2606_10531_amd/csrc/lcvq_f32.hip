@@ -21,10 +21,11 @@ __device__ __forceinline__ float load_p(const float *P, int64_t i, int64_t k, in
   else return P[i * ld + k];                       // X'[t][c] / dY[t][r]
 }
 template <int kMode>
-__device__ __forceinline__ float load_q(const float *Q, int64_t k, int64_t j, int64_t K, int64_t J, int64_t ld) {
+__device__ __forceinline__ float load_q(const float *Q, int64_t k, int64_t j, int64_t K, int64_t J, int64_t ld,
+                                       const Quantizer &qz) {
   if (k >= K || j >= J) return 0.0f;
-  if constexpr (kMode == 0) return (float)quant_code(Q[j * ld + k]);  // Z[r][c], j = r, k = c
-  else if constexpr (kMode == 1) return (float)quant_code(Q[k * ld + j]);  // Z[r][c], k = r, j = c
+  if constexpr (kMode == 0) return (float)quant_code(code_value(Q[j * ld + k], qz));  // Z[r][c], j = r, k = c
+  else if constexpr (kMode == 1) return (float)quant_code(code_value(Q[k * ld + j], qz));  // Z[r][c], k = r, j = c
   else return Q[k * ld + j];  // X[t][c]
 }
 
@@ -33,7 +34,7 @@ __global__ __launch_bounds__(256) void k_f32(const float *__restrict__ P, int64_
                                              int64_t ldq, int64_t I, int64_t J, int64_t K,
                                              const float *__restrict__ vecI, const float *__restrict__ A,
                                              const float *__restrict__ bvec, const float *__restrict__ Z,
-                                             int mask_mode, GradEst est, int accumulate,
+                                             Quantizer qz, int mask_mode, GradEst est, int accumulate,
                                              float *__restrict__ out, int64_t ldo, float *__restrict__ dA,
                                              float *__restrict__ db) {
   __shared__ float Ps[kFK][kF + 1];
@@ -60,10 +61,10 @@ __global__ __launch_bounds__(256) void k_f32(const float *__restrict__ P, int64_
       }
       if constexpr (kMode == 0) {
         const int kk = e & 15, jj = e >> 4;
-        Qs[kk][jj] = load_q<kMode>(Q, k0 + kk, j0 + jj, K, J, ldq);
+        Qs[kk][jj] = load_q<kMode>(Q, k0 + kk, j0 + jj, K, J, ldq, qz);
       } else {
         const int jj = e & 63, kk = e >> 6;
-        Qs[kk][jj] = load_q<kMode>(Q, k0 + kk, j0 + jj, K, J, ldq);
+        Qs[kk][jj] = load_q<kMode>(Q, k0 + kk, j0 + jj, K, J, ldq, qz);
       }
     }
     __syncthreads();
@@ -127,13 +128,13 @@ __global__ __launch_bounds__(256) void k_f32(const float *__restrict__ P, int64_
         float code[D];
 #pragma unroll
         for (int k = 0; k < D; ++k) {
-          const float z = valid ? Z[r * ldo + cg + k] : 0.0f;
+          const float z = code_value(valid ? Z[r * ldo + cg + k] : 0.0f, qz);
           code[k] = (float)quant_code(z);
           float v = 0.0f;
 #pragma unroll
           for (int j = 0; j < D; ++j) v = fmaf(acc[a][g * D + j], A[j * D + k], v);
           if (valid && out != nullptr) {
-            const float gz = ste_pass(z, mask_mode) ? (est.dge ? v * dge_slope(z, est) : v) : 0.0f;
+            const float gz = ste_pass(z, mask_mode) ? (est.dge ? v * dge_slope(z, est) : v) * qz.scale : 0.0f;
             float *p = out + r * ldo + cg + k;
             *p = accumulate ? *p + gz : gz;
           }
@@ -163,32 +164,32 @@ static inline dim3 grid2(int64_t J, int64_t I) {
   return dim3((unsigned)ceil_div(J, kF), (unsigned)ceil_div(I, kF));
 }
 
-hipError_t launch_fwd_f32(const float *Z, const float *Xp, const float *s, float *Y, int64_t N, int64_t m,
-                          int64_t n, hipStream_t st) {
-  k_f32<0, 8><<<grid2(m, N), 256, 0, st>>>(Xp, n, Z, n, N, m, n, s, nullptr, nullptr, nullptr, 0, GradEst{},
+hipError_t launch_fwd_f32(const float *Z, const Quantizer &qz, const float *Xp, const float *s, float *Y,
+                          int64_t N, int64_t m, int64_t n, hipStream_t st) {
+  k_f32<0, 8><<<grid2(m, N), 256, 0, st>>>(Xp, n, Z, n, N, m, n, s, nullptr, nullptr, nullptr, qz, 0, GradEst{},
                                            0, Y, m, nullptr, nullptr);
   return hipGetLastError();
 }
 
-hipError_t launch_dx_f32(const float *Z, const float *dY, const float *rs, const float *A, const float *b,
-                         int d, float *dX, int64_t N, int64_t m, int64_t n, hipStream_t st) {
+hipError_t launch_dx_f32(const float *Z, const Quantizer &qz, const float *dY, const float *rs, const float *A,
+                         const float *b, int d, float *dX, int64_t N, int64_t m, int64_t n, hipStream_t st) {
   if (d == 8)
-    k_f32<1, 8><<<grid2(n, N), 256, 0, st>>>(dY, m, Z, n, N, n, m, rs, A, b, nullptr, 0, GradEst{}, 0, dX,
+    k_f32<1, 8><<<grid2(n, N), 256, 0, st>>>(dY, m, Z, n, N, n, m, rs, A, b, nullptr, qz, 0, GradEst{}, 0, dX,
                                              n, nullptr, nullptr);
   else
-    k_f32<1, 4><<<grid2(n, N), 256, 0, st>>>(dY, m, Z, n, N, n, m, rs, A, b, nullptr, 0, GradEst{}, 0, dX,
+    k_f32<1, 4><<<grid2(n, N), 256, 0, st>>>(dY, m, Z, n, N, n, m, rs, A, b, nullptr, qz, 0, GradEst{}, 0, dX,
                                              n, nullptr, nullptr);
   return hipGetLastError();
 }
 
-hipError_t launch_dz_f32(const float *X, const float *dY, const float *Z, const float *A, int d,
-                         int mask_mode, const GradEst &est, int accumulate, float *dZ, float *dA, float *db,
+hipError_t launch_dz_f32(const float *X, const float *dY, const float *Z, const Quantizer &qz, const float *A,
+                         int d, int mask_mode, const GradEst &est, int accumulate, float *dZ, float *dA, float *db,
                          int64_t N, int64_t m, int64_t n, hipStream_t st) {
   if (d == 8)
-    k_f32<2, 8><<<grid2(n, m), 256, 0, st>>>(dY, m, X, n, m, n, N, nullptr, A, nullptr, Z, mask_mode, est,
+    k_f32<2, 8><<<grid2(n, m), 256, 0, st>>>(dY, m, X, n, m, n, N, nullptr, A, nullptr, Z, qz, mask_mode, est,
                                              accumulate, dZ, n, dA, db);
   else
-    k_f32<2, 4><<<grid2(n, m), 256, 0, st>>>(dY, m, X, n, m, n, N, nullptr, A, nullptr, Z, mask_mode, est,
+    k_f32<2, 4><<<grid2(n, m), 256, 0, st>>>(dY, m, X, n, m, n, N, nullptr, A, nullptr, Z, qz, mask_mode, est,
                                              accumulate, dZ, n, dA, db);
   return hipGetLastError();
 }

@@ -317,7 +317,8 @@ __global__ __launch_bounds__(256, 1) void k_gemm_codes(
 template <bool kDge>
 __global__ __launch_bounds__(256, 1) void k_gemm_dw(const uint16_t *__restrict__ xt, const uint16_t *__restrict__ dyt,
                                                     int KBt, const uint64_t *__restrict__ maskbits, int64_t ldm8,
-                                                    const uint16_t *__restrict__ Zb, int mask_mode, GradEst est,
+                                                    const uint16_t *__restrict__ Zb, Quantizer qz, int mask_mode,
+                                                    GradEst est,
                                                     int accumulate, void *__restrict__ dZ, int dz_bf16, int m, int n,
                                                     int tiles_m, int tiles_n) {
   constexpr int kStage = 32 * 1024;  // eight 4 KiB B blocks
@@ -471,18 +472,19 @@ __global__ __launch_bounds__(256, 1) void k_gemm_dw(const uint16_t *__restrict__
         const int c = c0 + 64 * wave + 32 * mi + 16 * h + 8 * half;
         const bool cv = c < n;
         const uint32_t e = (uint32_t)(rl * n + c);
+        // (times the quantiser scale: the chain rule through the code-domain value)
         float g[8];
         if constexpr (kDge) {
 #pragma unroll
           for (int q = 0; q < 8; ++q) {
             const uint32_t zw = zv[buf][mi][half][q >> 1];
-            const float z = (q & 1) ? bf16_hi(zw) : bf16_lo(zw);
-            g[q] = ste_pass(z, mask_mode) ? acc[mi][ni][8 * half + q] * dge_slope(z, est) : 0.0f;
+            const float z = code_value((q & 1) ? bf16_hi(zw) : bf16_lo(zw), qz);
+            g[q] = ste_pass(z, mask_mode) ? acc[mi][ni][8 * half + q] * dge_slope(z, est) * qz.scale : 0.0f;
           }
         } else {
           const uint32_t mb = mk[ni][mi] >> (16 * h + 8 * half);
 #pragma unroll
-          for (int q = 0; q < 8; ++q) g[q] = ((mb >> q) & 1u) ? acc[mi][ni][8 * half + q] : 0.0f;
+          for (int q = 0; q < 8; ++q) g[q] = ((mb >> q) & 1u) ? acc[mi][ni][8 * half + q] * qz.scale : 0.0f;
         }
         if (dz_bf16) {
           if (accumulate) {
@@ -544,17 +546,17 @@ hipError_t launch_dx_bf16(const uint32_t *frag, const uint16_t *dyb, const float
 }
 
 hipError_t launch_dw_bf16(const uint16_t *xt, const uint16_t *dyt, const uint64_t *maskbits, const uint16_t *Z,
-                          int mask_mode, const GradEst &est, int accumulate, void *dZ, bool dz_bf16, int64_t N,
-                          int64_t m, int64_t n, hipStream_t st) {
+                          const Quantizer &qz, int mask_mode, const GradEst &est, int accumulate, void *dZ,
+                          bool dz_bf16, int64_t N, int64_t m, int64_t n, hipStream_t st) {
   const int tiles_m = (int)ceil_div(n, kTile), tiles_n = (int)ceil_div(m, kTile);
   const int KBt = (int)(bwd_tokens(N) / 64);  // even
   if (est.dge)
-    k_gemm_dw<true><<<tiles_m * tiles_n, 256, 0, st>>>(xt, dyt, KBt, nullptr, mask_words_per_row(n), Z, mask_mode,
-                                                       est, accumulate, dZ, dz_bf16 ? 1 : 0, (int)m, (int)n, tiles_m,
+    k_gemm_dw<true><<<tiles_m * tiles_n, 256, 0, st>>>(xt, dyt, KBt, nullptr, mask_words_per_row(n), Z, qz,
+                                                       mask_mode, est, accumulate, dZ, dz_bf16 ? 1 : 0, (int)m, (int)n, tiles_m,
                                                        tiles_n);
   else
     k_gemm_dw<false><<<tiles_m * tiles_n, 256, 0, st>>>(xt, dyt, KBt, maskbits, mask_words_per_row(n), nullptr,
-                                                        mask_mode, est, accumulate, dZ, dz_bf16 ? 1 : 0, (int)m,
+                                                        qz, mask_mode, est, accumulate, dZ, dz_bf16 ? 1 : 0, (int)m,
                                                         (int)n, tiles_m, tiles_n);
   return hipGetLastError();
 }

@@ -77,7 +77,7 @@ __device__ __forceinline__ float block_sum256(float v, float *red /* >= 4 floats
 typedef uint8_t CodeTile[64][64 + 8];  // rows of 72 bytes keep 8-byte stores aligned
 template <bool kTrans>
 __device__ __forceinline__ void quant_block(int bq, int by, int gx, const uint16_t *__restrict__ Z, int64_t m,
-                                            int64_t n, uint32_t *__restrict__ frag, int KB,
+                                            int64_t n, const Quantizer &qz, uint32_t *__restrict__ frag, int KB,
                                             uint8_t *__restrict__ packed, CodeTile (&codes)[4],
                                             uint64_t *__restrict__ maskbits = nullptr, int64_t ldm8 = 0,
                                             int mask_mode = 0) {
@@ -101,8 +101,10 @@ __device__ __forceinline__ void quant_block(int bq, int by, int gx, const uint16
       uint32_t lo = 0, hi = 0;
 #pragma unroll
       for (int e = 0; e < 2; ++e) {
-        lo |= (quant_code(bf16_lo(v[q][i][e])) | (quant_code(bf16_hi(v[q][i][e])) << 8)) << (16 * e);
-        hi |= (quant_code(bf16_lo(v[q][i][2 + e])) | (quant_code(bf16_hi(v[q][i][2 + e])) << 8)) << (16 * e);
+        lo |= (quant_code(code_value(bf16_lo(v[q][i][e]), qz)) |
+               (quant_code(code_value(bf16_hi(v[q][i][e]), qz)) << 8)) << (16 * e);
+        hi |= (quant_code(code_value(bf16_lo(v[q][i][2 + e]), qz)) |
+               (quant_code(code_value(bf16_hi(v[q][i][2 + e]), qz)) << 8)) << (16 * e);
       }
       *reinterpret_cast<uint2 *>(&codes[q][rr][cc]) = make_uint2(lo, hi);
       if (kTrans && maskbits != nullptr) {
@@ -113,8 +115,8 @@ __device__ __forceinline__ void quant_block(int bq, int by, int gx, const uint16
 #pragma unroll
         for (int e = 0; e < 4; ++e) {
           const bool in = r < m && c + 2 * e < n;
-          mb |= (in && ste_pass(bf16_lo(v[q][i][e]), mask_mode) ? 1u : 0u) << (2 * e);
-          mb |= (in && ste_pass(bf16_hi(v[q][i][e]), mask_mode) ? 1u : 0u) << (2 * e + 1);
+          mb |= (in && ste_pass(code_value(bf16_lo(v[q][i][e]), qz), mask_mode) ? 1u : 0u) << (2 * e);
+          mb |= (in && ste_pass(code_value(bf16_hi(v[q][i][e]), qz), mask_mode) ? 1u : 0u) << (2 * e + 1);
         }
         mb <<= 8 * ((id >> 0) & 3);
         mb |= (uint32_t)__shfl_xor((int)mb, 1, 64);
@@ -293,7 +295,7 @@ __device__ __forceinline__ void act_block(int64_t tb, int kc, const uint16_t *__
 // (id % gq, id / gq), K = columns), with the 2-bit pack when `packed` is set; blocks [nq, nq + ntb * nkc): the
 // activation transform, block (tb, kc) = ((id - nq) % ntb, (id - nq) / ntb).
 template <int D>
-__global__ __launch_bounds__(256) void k_fwd_prep(const uint16_t *__restrict__ Z, int64_t m, int64_t n,
+__global__ __launch_bounds__(256) void k_fwd_prep(const uint16_t *__restrict__ Z, int64_t m, int64_t n, Quantizer qz,
                                                    uint32_t *__restrict__ frag, uint8_t *__restrict__ packed, int gq,
                                                    int nq, const uint16_t *__restrict__ X, int64_t N,
                                                    const float *__restrict__ A, const float *__restrict__ b,
@@ -303,7 +305,7 @@ __global__ __launch_bounds__(256) void k_fwd_prep(const uint16_t *__restrict__ Z
   __shared__ float red[4][32];
   const int id = blockIdx.x;
   if (id < nq) {
-    quant_block<false>(id % gq, id / gq, KB, Z, m, n, frag, KB, packed, codes);
+    quant_block<false>(id % gq, id / gq, KB, Z, m, n, qz, frag, KB, packed, codes);
   } else {
     const int j = id - nq, ntb = (int)(Np / 32);
     act_block<D>(j % ntb, j / ntb, X, N, n, A, b, Xp, KB, spc, Np, sp, red);
@@ -348,7 +350,7 @@ __global__ __launch_bounds__(256) void k_rowsum(const T *__restrict__ dY, int64_
 // matrix (rows are n/4 bytes, so the flattened layout is the row layout).
 template <typename ST, bool kFromU8>
 __global__ __launch_bounds__(256) void k_pack2bit(const ST *__restrict__ src, int64_t total,
-                                                   uint8_t *__restrict__ packed) {
+                                                   uint8_t *__restrict__ packed, Quantizer qz) {
   const int64_t words = total / 16;
   for (int64_t w = (int64_t)blockIdx.x * 256 + threadIdx.x; w < words; w += (int64_t)gridDim.x * 256) {
     uint32_t bits = 0;
@@ -365,7 +367,7 @@ __global__ __launch_bounds__(256) void k_pack2bit(const ST *__restrict__ src, in
       for (int h = 0; h < 2; ++h) {
         load8(src + w * 16 + 8 * h, v);
 #pragma unroll
-        for (int i = 0; i < 8; ++i) bits |= quant_code(v[i]) << (2 * (8 * h + i));
+        for (int i = 0; i < 8; ++i) bits |= quant_code(code_value(v[i], qz)) << (2 * (8 * h + i));
       }
     }
     *reinterpret_cast<uint32_t *>(packed + w * 4) = bits;
@@ -381,9 +383,9 @@ __global__ __launch_bounds__(256) void k_pack2bit(const ST *__restrict__ src, in
         c = reinterpret_cast<const uint8_t *>(src)[e0 + i];
         c = c > 3u ? 3u : c;
       } else if constexpr (sizeof(ST) == 2) {
-        c = quant_code(bf16_to_f32(reinterpret_cast<const uint16_t *>(src)[e0 + i]));
+        c = quant_code(code_value(bf16_to_f32(reinterpret_cast<const uint16_t *>(src)[e0 + i]), qz));
       } else {
-        c = quant_code(reinterpret_cast<const float *>(src)[e0 + i]);
+        c = quant_code(code_value(reinterpret_cast<const float *>(src)[e0 + i], qz));
       }
       byte |= c << (2 * i);
     }
@@ -575,7 +577,7 @@ __device__ __forceinline__ void dy_part(int bt, int sf0, int sf1, const uint16_t
 // Block 0 clears dA (nza floats) and db (nzb) when the backward overwrites them
 // (the input-gradient kernel, launched after this one, accumulates into them).
 template <int D>
-__global__ __launch_bounds__(256) void k_bwd_prep(const uint16_t *__restrict__ Z, int64_t m, int64_t n,
+__global__ __launch_bounds__(256) void k_bwd_prep(const uint16_t *__restrict__ Z, int64_t m, int64_t n, Quantizer qz,
                                                    uint32_t *__restrict__ frag, int KBq, int gq, int nq,
                                                    const uint16_t *__restrict__ X, const uint16_t *__restrict__ dY,
                                                    const float *__restrict__ A, int64_t N, int KBt, int nfx4,
@@ -605,7 +607,7 @@ __global__ __launch_bounds__(256) void k_bwd_prep(const uint16_t *__restrict__ Z
   }
   const int q = id - ndy;
   if (q < nq) {
-    quant_block<true>(q % gq, q / gq, 4 * gq, Z, m, n, frag, KBq, nullptr, codes, maskbits, ldm8, mask_mode);
+    quant_block<true>(q % gq, q / gq, 4 * gq, Z, m, n, qz, frag, KBq, nullptr, codes, maskbits, ldm8, mask_mode);
     return;
   }
   const int x = q - nq;
@@ -636,7 +638,8 @@ hipError_t launch_act_transform(const void *X, bool bf16, int64_t N, int64_t Np,
   return hipGetLastError();
 }
 
-hipError_t launch_fwd_prep_bf16(const uint16_t *Z, int64_t m, int64_t n, uint32_t *frag, uint8_t *packed,
+hipError_t launch_fwd_prep_bf16(const uint16_t *Z, int64_t m, int64_t n, const Quantizer &qz, uint32_t *frag,
+                                uint8_t *packed,
                                 const uint16_t *X, int64_t N, int64_t Np, int64_t ldp, int d, const float *A,
                                 const float *b, uint16_t *Xp, float *sp, hipStream_t st) {
   const int KB = (int)(ldp / 64);
@@ -644,8 +647,8 @@ hipError_t launch_fwd_prep_bf16(const uint16_t *Z, int64_t m, int64_t n, uint32_
   const int gq = (KB + 3) / 4, nq = gq * (int)(round_up(m, 256) / 64);
   const int ntb = (int)(Np / 32), nkc = act_chunks(ldp), spc = act_steps_per_chunk(ldp);
   const unsigned grid = (unsigned)(nq + ntb * nkc);
-  if (d == 8) k_fwd_prep<8><<<grid, 256, 0, st>>>(Z, m, n, frag, packed, gq, nq, X, N, A, b, Xp, KB, spc, Np, sp);
-  else k_fwd_prep<4><<<grid, 256, 0, st>>>(Z, m, n, frag, packed, gq, nq, X, N, A, b, Xp, KB, spc, Np, sp);
+  if (d == 8) k_fwd_prep<8><<<grid, 256, 0, st>>>(Z, m, n, qz, frag, packed, gq, nq, X, N, A, b, Xp, KB, spc, Np, sp);
+  else k_fwd_prep<4><<<grid, 256, 0, st>>>(Z, m, n, qz, frag, packed, gq, nq, X, N, A, b, Xp, KB, spc, Np, sp);
   return hipGetLastError();
 }
 
@@ -663,12 +666,12 @@ hipError_t launch_rowsum(const void *dY, bool bf16, int64_t N, int64_t Np, int64
 }
 
 hipError_t launch_pack2bit(const void *src, int kind, bool bf16, int64_t m, int64_t n, uint8_t *packed,
-                           hipStream_t st) {
+                           const Quantizer &qz, hipStream_t st) {
   const int64_t total = m * n;
   const int grid = grid_for(total / 16, 256);
-  if (kind == 1) k_pack2bit<uint8_t, true><<<grid, 256, 0, st>>>((const uint8_t *)src, total, packed);
-  else if (bf16) k_pack2bit<uint16_t, false><<<grid, 256, 0, st>>>((const uint16_t *)src, total, packed);
-  else k_pack2bit<float, false><<<grid, 256, 0, st>>>((const float *)src, total, packed);
+  if (kind == 1) k_pack2bit<uint8_t, true><<<grid, 256, 0, st>>>((const uint8_t *)src, total, packed, qz);
+  else if (bf16) k_pack2bit<uint16_t, false><<<grid, 256, 0, st>>>((const uint16_t *)src, total, packed, qz);
+  else k_pack2bit<float, false><<<grid, 256, 0, st>>>((const float *)src, total, packed, qz);
   return hipGetLastError();
 }
 
@@ -703,7 +706,8 @@ hipError_t launch_dequant(const void *src, int kind, bool z_bf16, int64_t m, int
 }  // namespace lcvq
 
 namespace lcvq {
-hipError_t launch_bwd_prep_bf16(const uint16_t *Z, int64_t m, int64_t n, uint32_t *frag, const uint16_t *X,
+hipError_t launch_bwd_prep_bf16(const uint16_t *Z, int64_t m, int64_t n, const Quantizer &qz, uint32_t *frag,
+                                const uint16_t *X,
                                 const uint16_t *dY, const float *A, int d, int64_t N, uint16_t *dyb, uint16_t *xt,
                                 uint16_t *dyt, float *rsp, uint64_t *maskbits, int mask_mode, float *za, int nza,
                                 float *zb, int nzb, hipStream_t st) {
@@ -719,10 +723,10 @@ hipError_t launch_bwd_prep_bf16(const uint16_t *Z, int64_t m, int64_t n, uint32_
   const int nfy = (int)(round_up(m, 256) / 64), spf = rowsum_subtiles_per_part(m), nrp = rowsum_parts(m);
   const unsigned grid = (unsigned)(nq + KBt * (nfx4 + nrp));
   if (d == 8)
-    k_bwd_prep<8><<<grid, 256, 0, st>>>(Z, m, n, frag, KBq, gq, nq, X, dY, A, N, KBt, nfx4, nfy, spf, nrp, dyb, KBq,
+    k_bwd_prep<8><<<grid, 256, 0, st>>>(Z, m, n, qz, frag, KBq, gq, nq, X, dY, A, N, KBt, nfx4, nfy, spf, nrp, dyb, KBq,
                                         xt, dyt, rsp, maskbits, ldm8, mask_mode, za, nza, zb, nzb);
   else
-    k_bwd_prep<4><<<grid, 256, 0, st>>>(Z, m, n, frag, KBq, gq, nq, X, dY, A, N, KBt, nfx4, nfy, spf, nrp, dyb, KBq,
+    k_bwd_prep<4><<<grid, 256, 0, st>>>(Z, m, n, qz, frag, KBq, gq, nq, X, dY, A, N, KBt, nfx4, nfy, spf, nrp, dyb, KBq,
                                         xt, dyt, rsp, maskbits, ldm8, mask_mode, za, nza, zb, nzb);
   return hipGetLastError();
 }

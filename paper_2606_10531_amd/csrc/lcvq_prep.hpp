@@ -20,7 +20,8 @@ inline int act_chunks(int64_t ldp) {
 
 // streaming kernels (lcvq_prep.hip)
 // bf16 forward prepass: codes (+ 2-bit pack) and X' = X A, partial s, in one launch
-hipError_t launch_fwd_prep_bf16(const uint16_t *Z, int64_t m, int64_t n, uint32_t *frag, uint8_t *packed,
+hipError_t launch_fwd_prep_bf16(const uint16_t *Z, int64_t m, int64_t n, const Quantizer &qz, uint32_t *frag,
+                                uint8_t *packed,
                                 const uint16_t *X, int64_t N, int64_t Np, int64_t ldp, int d, const float *A,
                                 const float *b, uint16_t *Xp, float *sp, hipStream_t st);
 // Tokens of the bf16 backward are padded to whole 256-token tiles of the
@@ -51,7 +52,8 @@ inline int64_t mask_words_per_row(int64_t n) { return (n + 63) / 64; }
 // row sums of dY (rsp: rowsum_parts(m) rows of bwd_tokens(N) floats) and the
 // mask bitmap of the straight-through estimator (maskbits, optional; written by
 // the quantise blocks, so only together with frag)
-hipError_t launch_bwd_prep_bf16(const uint16_t *Z, int64_t m, int64_t n, uint32_t *frag, const uint16_t *X,
+hipError_t launch_bwd_prep_bf16(const uint16_t *Z, int64_t m, int64_t n, const Quantizer &qz, uint32_t *frag,
+                                const uint16_t *X,
                                 const uint16_t *dY, const float *A, int d, int64_t N, uint16_t *dyb, uint16_t *xt,
                                 uint16_t *dyt, float *rsp, uint64_t *maskbits, int mask_mode, float *za, int nza,
                                 float *zb, int nzb, hipStream_t st);
@@ -61,7 +63,7 @@ hipError_t launch_act_transform(const void *X, bool bf16, int64_t N, int64_t Np,
 hipError_t launch_rowsum(const void *dY, bool bf16, int64_t N, int64_t Np, int64_t m, float *rs, float *dA,
                          float *db, int d, hipStream_t st);
 hipError_t launch_pack2bit(const void *src, int kind, bool bf16, int64_t m, int64_t n, uint8_t *packed,
-                           hipStream_t st);
+                           const Quantizer &qz, hipStream_t st);
 hipError_t launch_dequant(const void *src, int kind, bool z_bf16, int64_t m, int64_t n, int d,
                           const float *A, const float *b, void *W, bool out_bf16, hipStream_t st);
 
@@ -97,16 +99,16 @@ hipError_t launch_dx_bf16(const uint32_t *frag, const uint16_t *dyb, const float
 // maskbits: the straight-through mask; or, with est.dge set, nullptr and the
 // mask and slope are taken from Z (bf16, m x n) under mask_mode
 hipError_t launch_dw_bf16(const uint16_t *xt, const uint16_t *dyt, const uint64_t *maskbits, const uint16_t *Z,
-                          int mask_mode, const GradEst &est, int accumulate, void *dZ, bool dz_bf16, int64_t N,
-                          int64_t m, int64_t n, hipStream_t st);
+                          const Quantizer &qz, int mask_mode, const GradEst &est, int accumulate, void *dZ,
+                          bool dz_bf16, int64_t N, int64_t m, int64_t n, hipStream_t st);
 
 // fp32 products on the vector ALUs (lcvq_f32.hip)
-hipError_t launch_fwd_f32(const float *Z, const float *Xp, const float *s, float *Y, int64_t N, int64_t m,
-                          int64_t n, hipStream_t st);
-hipError_t launch_dx_f32(const float *Z, const float *dY, const float *rs, const float *A, const float *b,
-                         int d, float *dX, int64_t N, int64_t m, int64_t n, hipStream_t st);
-hipError_t launch_dz_f32(const float *X, const float *dY, const float *Z, const float *A, int d,
-                         int mask_mode, const GradEst &est, int accumulate, float *dZ, float *dA, float *db,
+hipError_t launch_fwd_f32(const float *Z, const Quantizer &qz, const float *Xp, const float *s, float *Y,
+                          int64_t N, int64_t m, int64_t n, hipStream_t st);
+hipError_t launch_dx_f32(const float *Z, const Quantizer &qz, const float *dY, const float *rs, const float *A,
+                         const float *b, int d, float *dX, int64_t N, int64_t m, int64_t n, hipStream_t st);
+hipError_t launch_dz_f32(const float *X, const float *dY, const float *Z, const Quantizer &qz, const float *A,
+                         int d, int mask_mode, const GradEst &est, int accumulate, float *dZ, float *dA, float *db,
                          int64_t N, int64_t m, int64_t n, hipStream_t st);
 
 }  // namespace lcvq

@@ -149,6 +149,28 @@ def test_fwd_packed_validation(lib):
     assert fwd_packed(lib, m=0, Y=None) == L.OK
 
 
+def test_ex_validation(lib):
+    def f(qs=0.5, qb=1.5, **kw):
+        a = dict(N=16, m=64, n=64, d=8, dt=L.BF16)
+        a.update(kw)
+        return lib.lcvq_linear_fwd_ex(a["N"], a["m"], a["n"], a["d"], a["dt"], FAKE, qs, qb, FAKE, FAKE, FAKE, FAKE,
+                                      None, FAKE, 1 << 40, None)
+
+    def g(qs=0.5, qb=1.5, est=L.EST_STE, k=5.0, cap=3.0, mask=1, **kw):
+        return lib.lcvq_linear_bwd_ex(16, 64, 64, kw.get("d", 8), L.BF16, FAKE, qs, qb, FAKE, FAKE, FAKE, FAKE, mask,
+                                      est, k, cap, 0, FAKE, FAKE, L.BF16, FAKE, FAKE, FAKE, 1 << 40, None)
+    for bad in (0.0, float("nan"), float("inf")):
+        assert f(qs=bad) == L.EINVAL and g(qs=bad) == L.EINVAL
+    assert f(qb=float("nan")) == L.EINVAL and g(qb=float("inf")) == L.EINVAL
+    assert "quantiser" in L.last_error()
+    assert g(est=2) == L.EINVAL
+    assert g(est=L.EST_DGE, k=0.5) == L.EINVAL
+    assert g(est=L.EST_DGE, cap=0.0) == L.EINVAL
+    assert f(d=5) == L.EUNSUPPORTED and g(d=3) == L.EUNSUPPORTED
+    assert g(mask=2) == L.EINVAL
+    assert f(N=0) == L.OK                                   # nothing to compute
+
+
 def test_pack_and_dequant_validation(lib):
     p = lib.lcvq_pack2bit
     assert p(FAKE, L.SRC_LATENT, L.BF16, 4, 6, FAKE, None) == L.EINVAL        # n % 4
