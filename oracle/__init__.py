@@ -300,6 +300,55 @@ def linear_forward_packed(packed, A, b, X, d, n):
     return forward(X, decode(unpack2bit(packed, n), A, b, d))
 
 
+# ------------------------------------------------------------ LC encode -----
+
+def inverse_f32(A: np.ndarray) -> np.ndarray:
+    """A^-1 in fp32 by Gauss-Jordan elimination with partial pivoting (largest
+    |pivot|, first on ties), every step one fp32 operation: the pivot row is
+    scaled by the rounded reciprocal of the pivot, and each other row r gets
+    row_r = fma(-f, pivot_row, row_r) with f its entry in the pivot column.  The
+    codes of encode() are decided on fp32 values, so the matrix they use is fixed
+    to this sequence."""
+    M = np.asarray(A, dtype=np.float32).copy()
+    d = M.shape[0]
+    I = np.eye(d, dtype=np.float32)
+    for c in range(d):
+        p = c + int(np.argmax(np.abs(M[c:, c])))
+        if p != c:
+            M[[c, p]] = M[[p, c]]
+            I[[c, p]] = I[[p, c]]
+        r = np.float32(1.0) / M[c, c]
+        M[c] = M[c] * r
+        I[c] = I[c] * r
+        for k in range(d):
+            if k != c:
+                f = M[k, c]
+                M[k] = fma_f32(-f, M[c], M[k]).astype(np.float32)
+                I[k] = fma_f32(-f, I[c], I[k]).astype(np.float32)
+    return I
+
+
+def encode(W: np.ndarray, A: np.ndarray, b: np.ndarray, d: int) -> np.ndarray:
+    """Codes of a dense weight (eq. lc_codebook inverted): per group g of row r,
+    v = A^-1 (w_g - b) and code = clip(round(v), 0, 3).  For A = s G with G
+    orthogonal (eq. init_ab) ||w - A z - b|| = s ||v - z|| is separable over the
+    d coordinates, so this is the nearest codeword of eq. vq_assign.
+
+    Arithmetic in fp32 as the kernel does it: t_j = fp32(w_j - b_j), then
+    v_k = fma chain over j = 0..d-1 of Ainv[k, j] t_j starting from 0."""
+    Wf = np.asarray(W, dtype=np.float32)
+    m, n = Wf.shape
+    Ainv = inverse_f32(A)
+    T = (Wf.reshape(m, n // d, d) - np.asarray(b, dtype=np.float32)).astype(np.float32)
+    V = np.zeros((m, n // d, d), dtype=np.float64)
+    for k in range(d):
+        acc = np.zeros((m, n // d), dtype=np.float64)
+        for j in range(d):
+            acc = fma_f32(np.float32(Ainv[k, j]), T[..., j], acc)
+        V[..., k] = acc
+    return quantize(V.reshape(m, n))
+
+
 # ------------------------------------------------------------ optimiser -----
 
 def adamw_step(theta, grad, m1, m2, step: int, lr: float, beta1: float = 0.9,

@@ -443,6 +443,57 @@ def test_quantiser_scale_in_backward_matches_finite_differences():
     assert np.allclose(out["dZ"], float(scale) * unit["dZ"], rtol=1e-12, atol=0)
 
 
+# ------------------------------------------------------------ LC encode -----
+
+def _orthogonal(d, seed):
+    q, r = np.linalg.qr(np.random.default_rng(seed).standard_normal((d, d)))
+    return q * np.sign(np.diag(r))
+
+
+def test_inverse_f32_exact_cases():
+    P = np.eye(8, dtype=np.float32)[[3, 0, 7, 1, 6, 2, 5, 4]]
+    assert np.array_equal(orc.inverse_f32(P), P.T)              # permutation: exact
+    D = np.diag([2.0, 0.25, 4.0, 8.0]).astype(np.float32)
+    assert np.array_equal(orc.inverse_f32(D), np.diag([0.5, 4.0, 0.25, 0.125]).astype(np.float32))
+    for d in (4, 8):
+        A = (0.02 * (np.eye(d) + 0.1 * np.random.default_rng(d).standard_normal((d, d)))).astype(np.float32)
+        assert np.abs(orc.inverse_f32(A).astype(np.float64) @ A - np.eye(d)).max() < 1e-6
+
+
+@pytest.mark.parametrize("d", [4, 8])
+def test_encode_identity_map_is_the_quantiser(d):
+    W = np.random.default_rng(60 + d).uniform(-2.0, 5.0, (7, 4 * d)).astype(np.float32)
+    assert np.array_equal(orc.encode(W, np.eye(d), np.zeros(d), d), orc.quantize(W))
+
+
+@pytest.mark.parametrize("d", [4, 8])
+def test_encode_returns_the_codes_of_exact_codewords(d):
+    # init map of eq. init_ab: A = s G, b = -s G mu 1; every codeword encodes to itself
+    A, b = orc.init_map(_orthogonal(d, 70 + d))
+    C = np.random.default_rng(71 + d).integers(0, 4, size=(9, 5 * d)).astype(np.uint8)
+    W = orc.decode(C, A, b, d).astype(np.float32)
+    assert np.array_equal(orc.encode(W, A, b, d), C)
+
+
+@pytest.mark.parametrize("d", [4, 8])
+def test_encode_is_the_nearest_codeword_for_an_orthogonal_map(d):
+    # brute force over all 4^d codewords (eq. vq_assign) in fp64
+    A, b = orc.init_map(_orthogonal(d, 80 + d))
+    A, b = A.astype(np.float32), b.astype(np.float32)
+    groups = 400 if d == 4 else 60
+    W = (np.random.default_rng(81 + d).standard_normal((groups, d)) * 1.3).astype(np.float32)
+    Z = np.array(np.meshgrid(*[np.arange(4)] * d, indexing="ij")).reshape(d, -1).T      # all codewords
+    book = Z @ A.astype(np.float64).T + b.astype(np.float64)                            # c = A z + b
+    dist = ((W.astype(np.float64)[:, None, :] - book[None]) ** 2).sum(-1)
+    order = np.argsort(dist, axis=1)
+    best = Z[order[:, 0]]
+    margin = dist[np.arange(groups), order[:, 1]] - dist[np.arange(groups), order[:, 0]]
+    got = orc.encode(W.reshape(1, -1), A, b, d).reshape(groups, d)
+    clear = margin > 1e-4
+    assert clear.sum() > 0.95 * groups
+    assert np.array_equal(got[clear], best[clear])
+
+
 # ------------------------------------------------------------- packing ------
 
 def test_pack_hand_values():
