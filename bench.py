@@ -136,6 +136,10 @@ def hbm_kernels(lc, torch):
              ("dequant_packed_to_bf16", lambda: lc.dequant(packed, A, b, d, n=n, src_kind=lc.SRC_PACKED2,
                                                            out=W), 2.25, "dequant"),
              ("dequant_bf16_latent_to_bf16", lambda: lc.dequant(Z, A, b, d, out=W), 4.0, "dequant"),
+             # LC encode of a dense bf16 weight into packed codes (reads W, writes 2 bits per element)
+             ("encode_bf16_to_packed", lambda: lc._lib.check(lib.lcvq_encode(
+                 m, n, d, W.data_ptr(), lc._lib.BF16, A.data_ptr(), b.data_ptr(), None, packed.data_ptr(),
+                 lc._stream(W.device)), "lcvq_encode"), 2.25, "encode"),
              # per parameter: theta, m1, m2 read + written (24 B), bf16 gradient read, bf16 copy written
              ("adamw_step_fp32_master_bf16_grad",
               lambda: lc.adamw_step(theta, gZ, m1, m2, 1, 1e-4, shadow=shadow), 28.0, "adam")]

@@ -107,6 +107,26 @@ lcvq_status_t lcvq_dequant(int64_t m, int64_t n, int32_t d, int32_t src_kind, in
                            void *W_hat, int32_t out_dtype, void *stream);
 
 /*
+ * lcvq_encode -- codes of a dense weight W under the map A, b: for group g of
+ * row r, v = A^-1 (w_g - b) and code = clip(round(v), 0, 3) (eq. lc_codebook
+ * inverted; round() ties to even).  With A = s G, G orthogonal (the form of
+ * eq. init_ab), these are the nearest codewords A z + b of eq. vq_assign,
+ * because the distance separates over the d coordinates after the rotation; for
+ * other invertible A they are the rounding of A^-1 (w_g - b).  A^-1 is formed in
+ * fp32 by Gauss-Jordan elimination with partial pivoting and v as an fp32 fma
+ * chain, so the codes are a fixed function of the fp32 inputs.  A singular A
+ * gives NaN v, i.e. code 0.
+ *   W          m x n, element type w_dtype (F32 or BF16), 16-byte aligned
+ *   A, b       d x d and d fp32
+ *   codes_out  NULL, or m x n bytes (values 0..3), written
+ *   packed_out NULL, or m * n / 4 bytes in the lcvq_pack2bit layout, written
+ * d in {4, 8} (else LCVQ_EUNSUPPORTED), n % d == 0; at least one output.
+ */
+lcvq_status_t lcvq_encode(int64_t m, int64_t n, int32_t d, const void *W, int32_t w_dtype,
+                          const float *A, const float *b, uint8_t *codes_out, uint8_t *packed_out,
+                          void *stream);
+
+/*
  * lcvq_workspace_bytes -- device workspace needed by lcvq_linear_fwd
  * (op = LCVQ_OP_FWD), lcvq_linear_bwd / lcvq_linear_bwd_dge (op = LCVQ_OP_BWD)
  * or lcvq_linear_fwd_packed (op = LCVQ_OP_FWD_PACKED, dtype LCVQ_BF16; the
@@ -283,7 +303,8 @@ typedef enum {
   LCVQ_K_ADAM = 8,      /* lcvq_adamw_step */
   LCVQ_K_PACKED_PREP = 9,  /* lcvq_linear_fwd_packed: X' and s of up to 16 tokens */
   LCVQ_K_PACKED = 10,      /* lcvq_linear_fwd_packed: Y from the packed codes */
-  LCVQ_K_COUNT = 11
+  LCVQ_K_ENCODE = 11,      /* lcvq_encode */
+  LCVQ_K_COUNT = 12
 } lcvq_kernel_t;
 lcvq_status_t lcvq_timer_enable(uint32_t mask);
 lcvq_status_t lcvq_timer_read(int32_t kernel, double *total_ms, int64_t *launches);

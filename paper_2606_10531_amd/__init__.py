@@ -17,7 +17,7 @@ from ._lib import (BF16, EST_DGE, EST_STE, F32, MASK_LATENT, MASK_ROUNDED, OP_BW
                    SRC_CODES_U8, SRC_LATENT, SRC_PACKED2, LcvqError)
 
 __all__ = ["linear_fwd", "linear_fwd_packed", "linear_bwd", "linear_bwd_dge", "xavier_quantizer", "xavier_init",
-           "pack2bit", "dequant", "adamw_step", "workspace_bytes", "LcvqError", "MASK_ROUNDED", "MASK_LATENT",
+           "pack2bit", "dequant", "encode", "adamw_step", "workspace_bytes", "LcvqError", "MASK_ROUNDED", "MASK_LATENT",
            "SRC_LATENT", "SRC_CODES_U8", "SRC_PACKED2", "EST_STE", "EST_DGE"]
 
 _DT = {torch.float32: F32, torch.bfloat16: BF16}
@@ -89,6 +89,18 @@ def dequant(src: torch.Tensor, A: torch.Tensor, b: torch.Tensor, d: int, n: int 
     _lib.check(_lib.load().lcvq_dequant(m, n, d, src_kind, sdt, _dev(src, "src"), _dev(A, "A"), _dev(b, "b"),
                                         _dev(out, "out"), _DT[out.dtype], _stream(src.device)), "lcvq_dequant")
     return out
+
+
+def encode(W: torch.Tensor, A: torch.Tensor, b: torch.Tensor, d: int, codes: bool = True, packed: bool = False):
+    """LC encode of a dense weight W (m x n, fp32 or bf16): per group the codes
+    clip(round(A^-1 (w_g - b)), 0, 3), the nearest codewords when A is a scaled
+    orthogonal matrix.  Returns (codes m x n uint8 or None, packed m x n/4 uint8 or None)."""
+    m, n = W.shape
+    c = torch.empty((m, n), dtype=torch.uint8, device=W.device) if codes else None
+    p = torch.empty((m, n // 4), dtype=torch.uint8, device=W.device) if packed else None
+    _lib.check(_lib.load().lcvq_encode(m, n, d, _dev(W, "W"), _dtype_code(W), _dev(A, "A"), _dev(b, "b"),
+                                       _opt(c, "codes"), _opt(p, "packed"), _stream(W.device)), "lcvq_encode")
+    return c, p
 
 
 def xavier_quantizer(m: int, n: int, bits: int = 2) -> tuple[float, float]:

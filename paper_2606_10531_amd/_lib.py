@@ -19,7 +19,7 @@ OP_FWD, OP_BWD, OP_FWD_PACKED = 0, 1, 2
 EST_STE, EST_DGE = 0, 1
 # lcvq_kernel_t
 KERNELS = ["fwd_prep", "fwd", "bwd_prep", "dx", "dw", "pack", "dequant", "fill", "adam", "packed_prep",
-           "packed"]
+           "packed", "encode"]
 
 _P = ctypes.c_void_p
 _I64 = ctypes.c_int64
@@ -31,6 +31,7 @@ SIGNATURES = {
     "lcvq_dequant": (_I32, [_I64, _I64, _I32, _I32, _I32, _P, _P, _P, _P, _I32, _P]),
     "lcvq_workspace_bytes": (_SZ, [_I32, _I64, _I64, _I64, _I32, _I32]),
     "lcvq_linear_fwd": (_I32, [_I64, _I64, _I64, _I32, _I32, _P, _P, _P, _P, _P, _P, _P, _SZ, _P]),
+    "lcvq_encode": (_I32, [_I64, _I64, _I32, _P, _I32, _P, _P, _P, _P, _P]),
     "lcvq_linear_fwd_ex": (_I32, [_I64, _I64, _I64, _I32, _I32, _P, ctypes.c_float, ctypes.c_float, _P, _P, _P,
                                   _P, _P, _P, _SZ, _P]),
     "lcvq_linear_bwd_ex": (_I32, [_I64, _I64, _I64, _I32, _I32, _P, ctypes.c_float, ctypes.c_float, _P, _P, _P,

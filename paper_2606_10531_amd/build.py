@@ -10,7 +10,7 @@ PKG = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(PKG)
 CSRC = os.path.join(PKG, "csrc")
 LIB = os.path.join(PKG, "liblcvq.so")
-SOURCES = ["lcvq_api.hip", "lcvq_prep.hip", "lcvq_gemm.hip", "lcvq_f32.hip", "lcvq_adam.hip", "lcvq_packed.hip"]
+SOURCES = ["lcvq_api.hip", "lcvq_prep.hip", "lcvq_gemm.hip", "lcvq_f32.hip", "lcvq_adam.hip", "lcvq_packed.hip", "lcvq_encode.hip"]
 ARCH = "gfx950"
 # Packed fp32 instructions are kept out of every kernel; the host pass warns
 # that it does not know the feature, which is harmless.

@@ -296,6 +296,23 @@ lcvq_status_t lcvq_adamw_step(float *theta, const void *grad, int32_t grad_dtype
   return e == hipSuccess ? ok() : hip_fail(e, "adamw launch");
 }
 
+lcvq_status_t lcvq_encode(int64_t m, int64_t n, int32_t d, const void *W, int32_t w_dtype, const float *A,
+                          const float *b, uint8_t *codes_out, uint8_t *packed_out, void *stream) {
+  if (m < 0 || n < 0) return fail(LCVQ_EINVAL, "negative size");
+  if (d != 4 && d != 8) return fail(LCVQ_EUNSUPPORTED, "d=%d (4 or 8)", d);
+  if (n % d != 0) return fail(LCVQ_EINVAL, "n=%lld is not a multiple of d=%d", (long long)n, d);
+  if (w_dtype != LCVQ_F32 && w_dtype != LCVQ_BF16) return fail(LCVQ_EINVAL, "w_dtype=%d", w_dtype);
+  if (codes_out == nullptr && packed_out == nullptr) return fail(LCVQ_EINVAL, "no output requested");
+  if (m == 0 || n == 0) return ok();
+  if (W == nullptr || A == nullptr || b == nullptr) return fail(LCVQ_EINVAL, "null required pointer (W, A, b)");
+  if (!aligned16(W) || (codes_out && !aligned16(codes_out)) || (packed_out && !aligned16(packed_out)))
+    return fail(LCVQ_EALIGN, "W, codes_out and packed_out must be 16-byte aligned");
+  Timed tm(LCVQ_K_ENCODE, (hipStream_t)stream);
+  hipError_t e = tm.done(lcvq::launch_encode(W, w_dtype == LCVQ_BF16, m, n, d, A, b, codes_out, packed_out,
+                                             (hipStream_t)stream));
+  return e == hipSuccess ? ok() : hip_fail(e, "encode launch");
+}
+
 lcvq_status_t lcvq_dequant(int64_t m, int64_t n, int32_t d, int32_t src_kind, int32_t src_dtype,
                            const void *src, const float *A, const float *b, void *W_hat, int32_t out_dtype,
                            void *stream) {

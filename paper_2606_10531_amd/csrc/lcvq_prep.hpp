@@ -85,6 +85,10 @@ hipError_t launch_packed_prep(const uint16_t *X, int Nc, int64_t m, int64_t n, i
 hipError_t launch_packed_gemv(const uint8_t *packed, int64_t m, int64_t n, const uint16_t *xq, const float *sp,
                               int Nc, float *part, int *counters, void *Y, bool y_bf16, hipStream_t st);
 
+// LC encode (lcvq_encode.hip): codes (m x n bytes) and / or packed codes of a dense weight
+hipError_t launch_encode(const void *W, bool w_bf16, int64_t m, int64_t n, int d, const float *A, const float *b,
+                         uint8_t *codes, uint8_t *packed, hipStream_t st);
+
 // optimiser (lcvq_adam.hip); shadow_kind 0 none, 1 fp32, 2 bf16
 hipError_t launch_adamw(float *theta, const void *grad, bool grad_bf16, float *m1, float *m2, void *shadow,
                         int shadow_kind, int64_t numel, float lr, float beta1, float beta2, float eps,

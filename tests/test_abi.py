@@ -171,6 +171,21 @@ def test_ex_validation(lib):
     assert f(N=0) == L.OK                                   # nothing to compute
 
 
+def test_encode_validation(lib):
+    def e(m=64, n=64, d=8, W=FAKE, wdt=L.BF16, codes=FAKE, packed=None):
+        return lib.lcvq_encode(m, n, d, W, wdt, FAKE, FAKE, codes, packed, None)
+    assert e(d=5) == L.EUNSUPPORTED
+    assert e(n=60) == L.EINVAL                              # n % d
+    assert e(m=-1) == L.EINVAL
+    assert e(wdt=7) == L.EINVAL
+    assert e(codes=None, packed=None) == L.EINVAL           # nothing to write
+    assert "output" in L.last_error()
+    assert e(W=None) == L.EINVAL
+    assert e(W=MIS) == L.EALIGN
+    assert e(codes=None, packed=MIS) == L.EALIGN
+    assert e(m=0) == L.OK and e(n=0) == L.OK                # empty: no launch
+
+
 def test_pack_and_dequant_validation(lib):
     p = lib.lcvq_pack2bit
     assert p(FAKE, L.SRC_LATENT, L.BF16, 4, 6, FAKE, None) == L.EINVAL        # n % 4
