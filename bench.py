@@ -27,6 +27,7 @@ PEAK_MFMA_BF16 = 2500.0      # TFLOP/s, MI355X dense bf16 matrix cores (publishe
 PEAK_HBM = 8000.0            # GB/s, MI355X HBM3E (published)
 DEFAULT_WORKLOAD = "lcvq_4096x4096_n4096_bf16"
 MATRIX_KERNELS = ("fwd", "dx", "dw")
+OTHER_WORKLOADS = ("lcvq_mlp7b_n8192_bf16", "lcvq_mlp70b_n4096_bf16", "lcvq_block7b_n16384_bf16")
 
 
 def kernel_source_digest() -> str:
@@ -56,19 +57,31 @@ def measured_traffic(kernel: str, workload: str):
 class Layer:
     """Device buffers and the fwd+bwd step of one LC-VQ weight matrix."""
 
-    def __init__(self, lc, torch, N, m, n, d, k):
+    def __init__(self, lc, torch, N, m, n, d, k, on_device=False):
+        """Inputs from the host generators of the workload recipe, or (on_device)
+        drawn on the GPU with the same distributions from a seeded torch
+        generator: the larger workloads are only timed here, and drawing
+        gigabytes on the host would take longer than timing them."""
         import numpy as np
 
         import synth
-        inp = synth.layer_inputs(N, m, n, d, "bf16", k=k)
-        self.inp = inp
         self.lc, self.N, self.m, self.n, self.d = lc, N, m, n, d
+        A, b = synth.draw_map(d, k)
+        self.A, self.b = torch.from_numpy(A).cuda(), torch.from_numpy(b).cuda()
+        if on_device:
+            g = torch.Generator(device="cuda").manual_seed(3000 + k)
+            self.inp = None
+            self.Z = torch.empty((m, n), device="cuda").uniform_(-0.5, 3.5, generator=g).to(torch.bfloat16)
+            self.X = torch.randn((N, n), device="cuda", generator=g).to(torch.bfloat16)
+            self.dY = torch.randn((N, m), device="cuda", generator=g).to(torch.bfloat16)
+        else:
+            inp = synth.layer_inputs(N, m, n, d, "bf16", k=k)
+            self.inp = inp
 
-        def dev(bits):
-            return torch.from_numpy(np.ascontiguousarray(bits).view(np.int16)).view(torch.bfloat16).cuda()
+            def dev(bits):
+                return torch.from_numpy(np.ascontiguousarray(bits).view(np.int16)).view(torch.bfloat16).cuda()
 
-        self.Z, self.X, self.dY = dev(inp["Z"]), dev(inp["X"]), dev(inp["dY"])
-        self.A, self.b = torch.from_numpy(inp["A"]).cuda(), torch.from_numpy(inp["b"]).cuda()
+            self.Z, self.X, self.dY = dev(inp["Z"]), dev(inp["X"]), dev(inp["dY"])
         bf = torch.bfloat16
         self.Y = torch.empty((N, m), dtype=bf, device="cuda")
         self.packed = torch.empty((m, n // 4), dtype=torch.uint8, device="cuda")
@@ -191,6 +204,56 @@ def variant_step(lc, torch, layers, steps, which, label):
     flops = sum(L.flops() for L in layers)
     return {"variant": label, "ms_per_step": round(ms, 4), "TFLOP/s": round(flops / (ms * 1e-3) / 1e12, 2),
             "dw_us": round(1e3 * dw_ms / max(cnt, 1), 2)}
+
+
+def workload_steps(lc, torch, names, steps):
+    """The fwd + bwd step on the other Llama-shaped workloads (every matrix of
+    the workload in turn on one stream), timed like the main step.  The 7B
+    decoder block also runs the AdamW update of each matrix's latent (fp32
+    master, bf16 copy used by the next forward) and of its map A and offset b,
+    inside the timed step, as one training step would."""
+    import synth
+    out = {}
+    for name in names:
+        wl = synth.WORKLOADS[name]
+        layers = [Layer(lc, torch, wl["N"], m, n, wl["d"], k, on_device=True) for k, (m, n) in enumerate(wl["mats"])]
+        adam = name.startswith("lcvq_block7b")
+        states = []
+        if adam:
+            for L in layers:
+                th = {"Z": L.Z.float(), "A": L.A, "b": L.b}   # A and b are updated in place
+                states.append({key: (t, torch.zeros_like(t), torch.zeros_like(t)) for key, t in th.items()})
+        count = [0]
+
+        def step():
+            for L in layers:
+                L.step()
+            if adam:
+                count[0] += 1
+                for L, st in zip(layers, states):
+                    for key, grad, shadow in (("Z", L.dZ, L.Z), ("A", L.dA, None), ("b", L.db, None)):
+                        th, m1, m2 = st[key]
+                        lc.adamw_step(th, grad.reshape(-1), m1.reshape(-1), m2.reshape(-1), count[0], 1e-4,
+                                      shadow=None if shadow is None else shadow.reshape(-1))
+
+        for _ in range(3):
+            step()
+        start, stop = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        torch.cuda.synchronize()
+        start.record()
+        for _ in range(steps):
+            step()
+        stop.record()
+        torch.cuda.synchronize()
+        ms = start.elapsed_time(stop) / steps
+        flops = sum(L.flops() for L in layers)
+        out[name] = {"N": wl["N"], "matrices": [list(x) for x in wl["mats"]], "ms_per_step": round(ms, 3),
+                     "TFLOP/s": round(flops / (ms * 1e-3) / 1e12, 2),
+                     "frac_of_peak": round(flops / (ms * 1e-3) / 1e12 / PEAK_MFMA_BF16, 4),
+                     "step": "fwd (+2-bit pack) + straight-through bwd" + (" + AdamW of Z, A, b" if adam else "")}
+        del layers, states
+        torch.cuda.empty_cache()
+    return out
 
 
 def packed_decode(lc, torch, token_counts=(1, 4, 16)):
@@ -321,6 +384,7 @@ def main():
     ap.add_argument("--workload", default=DEFAULT_WORKLOAD)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-hbm", action="store_true")
+    ap.add_argument("--no-workloads", action="store_true", help="skip timing the larger Llama-shaped workloads")
     ap.add_argument("--cpu-seconds", type=float, default=10.0)
     ap.add_argument("--copy-probe", type=int, default=0, metavar="BYTES",
                     help="only run a plain device-to-device copy of BYTES (counter calibration) and exit")
@@ -421,6 +485,9 @@ def main():
                                    "differentiable gradient estimator, k=5, slope cap 3, latent mask")
     res["xavier_step"] = variant_step(lc, torch, layers, args.steps, "step_xavier",
                                       "latent in the Xavier domain: codes of W_p / s' + t, gradient / s'")
+    if not args.no_workloads:
+        res["workloads"] = workload_steps(lc, torch, [w for w in OTHER_WORKLOADS if w != args.workload],
+                                          max(3, args.steps // 10))
     L0 = layers[0]
     res["library_gemm_same_shape"] = library_gemm(torch, L0.N, L0.m, L0.n)
     if not args.no_hbm:
