@@ -151,6 +151,11 @@ __global__ __launch_bounds__(256) void k_packed_gemv(const uint8_t *__restrict__
       xf[buf][i] = __builtin_amdgcn_raw_buffer_load_b128(
           rX, xlive ? (uint32_t)(((j * 8 + i) * 64 + lane) * 16) : kOffNone, 0, 0);
   };
+  // bf16 1.0 in both halves, held in a vector register: with the mask from a
+  // scalar register each operand dword is then one v_and_or_b32 (a literal
+  // would not fit that instruction and costs a separate and + or)
+  uint32_t one;
+  asm volatile("v_mov_b32 %0, 0x3f803f80" : "=v"(one));
   auto compute = [&](int buf) {
 #pragma unroll
     for (int kk = 0; kk < 4; ++kk) {
@@ -158,7 +163,6 @@ __global__ __launch_bounds__(256) void k_packed_gemv(const uint8_t *__restrict__
 #pragma unroll
       for (int rb = 0; rb < 4; ++rb) {
         const uint32_t w0 = cw[buf][rb][kk], w6 = w0 >> 6, w12 = w0 >> 12;
-        constexpr uint32_t one = 0x3F803F80u;  // bf16 1.0 in both halves
         u32x4 e, o;
         e[0] = (w0 & 0x00030003u) | one;
         e[1] = (w0 & 0x000C000Cu) | one;
