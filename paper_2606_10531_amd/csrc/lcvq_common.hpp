@@ -8,7 +8,6 @@ namespace lcvq {
 
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
-typedef float floatx16 __attribute__((ext_vector_type(16)));
 typedef float floatx4 __attribute__((ext_vector_type(4)));
 typedef short shortx4 __attribute__((ext_vector_type(4)));
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
@@ -81,45 +80,43 @@ __device__ __forceinline__ float dge_slope(float z, const GradEst &g) {
   return fminf(f, g.cap);
 }
 
-// ---- codes in the matrix-core operand layout -----------------------------
-// Row permutation of a 32-row MFMA block.  In a 32x32 accumulator, lane L
-// holds rows 8 (i / 4) + 4 (L / 32) + (i % 4), i = 0..15.  Feeding weight-side
-// index perm32(m) into MFMA row m makes register i of lane L hold weight-side
-// index 16 (L / 32) + i, so every group of d = 4 or 8 consecutive columns is
-// lane-local and the lane's 16 results are contiguous in memory.
-__host__ __device__ __forceinline__ int perm32(int m) { return (m & 3) + 4 * (m >> 3) + 16 * ((m >> 2) & 1); }
+// ---- operand layouts of v_mfma_f32_16x16x32_bf16 -------------------------
+// The instruction reads, in lane L, eight K values of A row L % 16 and eight K
+// values of B column L % 16 (K group L / 16 of the 32), and leaves rows
+// 4 (L / 16) + e, e = 0..3, of output column L % 16 in the lane.  A 32-row slab
+// of the weight side is two 16-row MFMA blocks; MFMA row m = 16 rb + i of the
+// slab carries weight-side row slab_row(m) = 8 (i / 4) + 4 rb + (i % 4), so that
+// lane L ends with weight-side rows 8 (L / 16) .. + 7 of the slab (block 0:
+// the first four, block 1: the last four) for one column: whole groups of
+// d = 4 or 8, contiguous in memory.
+__host__ __device__ __forceinline__ int slab_row(int m) { return 8 * ((m & 15) >> 2) + 4 * (m >> 4) + (m & 3); }
 
-// A 32 x 64 (M x K) slab of codes occupies 1 KiB: lane L owns 16 bytes holding
-// the codes of weight-side index perm32(L % 32) of the slab and K = 16 kk +
-// 8 (L / 32) + i (dword kk, nibble i at bits 4i..4i+3).  That is exactly the
-// A operand of v_mfma_f32_32x32x16_bf16 for four K-substeps of 16.
+// A 32 x 64 (M x K) slab of codes occupies 1 KiB: lane L owns 16 bytes, dword
+// 2 rb + kk2 holding the codes of weight-side row slab_row(16 rb + L % 16) of
+// the slab and K = 32 kk2 + 8 (L / 16) + i (nibble i at bits 4i..4i+3): the A
+// operands of the slab's two row blocks for the step's two 32-wide K sub-steps.
 // Slabs are stored M-slab-major: slab (mb, kb) at byte ((mb * KB) + kb) * 1024.
-__device__ __forceinline__ uint32_t frag_dword_index(int mb, int kb, int KB, int lane, int kk) {
-  return ((uint32_t)(mb * KB + kb) * 64u + (uint32_t)lane) * 4u + (uint32_t)kk;
+__device__ __forceinline__ uint32_t frag_dword_index(int mb, int kb, int KB, int lane, int dw) {
+  return ((uint32_t)(mb * KB + kb) * 64u + (uint32_t)lane) * 4u + (uint32_t)dw;
 }
 
-// Activations in the B-operand layout of v_mfma_f32_32x32x16_bf16: a block of
-// 32 tokens x 64 K (4 KiB) holds, for K substep kk, 1 KiB in which lane L owns
-// the 16 bytes of token 32 tb + L % 32, K = 64 kb + 16 kk + 8 (L / 32) + 0..7.
-// Blocks are token-block-major: element index of (t, k) with KB K steps is
-// (((t / 32) * KB + k / 64) * 4 + (k % 64) / 16) * 512 + ((t % 32) + 32 ((k % 16) / 8)) * 8 + k % 8.
+// Activations in the B-operand layout: a block of 32 tokens x 64 K (4 KiB)
+// holds four 1 KiB fragments, fragment 2 th + kk2 for tokens 32 tb + 16 th +
+// 0..15 and K 64 kb + 32 kk2 + 0..31, in which lane L owns the 16 bytes of token
+// 32 tb + 16 th + L % 16, K = 64 kb + 32 kk2 + 8 (L / 16) + 0..7.  Blocks are
+// token-block-major; the element index of (t, k) with KB K steps is returned.
 __host__ __device__ __forceinline__ int64_t bfrag_index(int64_t t, int64_t k, int64_t KB) {
-  return (((t >> 5) * KB + (k >> 6)) * 4 + ((k & 63) >> 4)) * 512 + ((t & 31) + 32 * ((k & 15) >> 3)) * 8 + (k & 7);
+  return (((t >> 5) * KB + (k >> 6)) * 4 + 2 * ((t >> 4) & 1) + ((k >> 5) & 1)) * 512 +
+         ((t & 15) + 16 * ((k >> 3) & 3)) * 8 + (k & 7);
 }
-
-// Inverse of perm32.
-__host__ __device__ __forceinline__ int perm32_inv(int m) { return (m & 3) + 4 * (m >> 4) + 8 * ((m >> 2) & 3); }
 
 // Token-K operand fragments of the weight-gradient product (features f on the
-// MFMA M or N axis, tokens t on K): block (f / 32, t / 64) holds 4 KiB; for
-// K substep kk (16 tokens) 1 KiB in which lane L owns the 16 bytes of feature
-// 32 (f / 32) + sel(L % 32), tokens 64 kb + 16 kk + 8 (L / 32) + 0..7, with
-// sel = perm32 on the M side (in-features) and the identity on the N side.
-// KBt = number of 64-token steps.  Returns the element index of (f, t).
-__host__ __device__ __forceinline__ int64_t tfrag_index(int64_t f, int64_t t, int64_t KBt, bool mside) {
-  const int l = mside ? perm32_inv((int)(f & 31)) : (int)(f & 31);
-  return (((f >> 5) * KBt + (t >> 6)) * 4 + ((t & 63) >> 4)) * 512 + (l + 32 * ((t & 15) >> 3)) * 8 + (t & 7);
-}
+// MFMA M or N axis, tokens t on K): block (f / 32, t / 64) holds four 1 KiB
+// fragments, fragment 2 fh + kk2 for features 16 fh .. + 15 of the block (in
+// MFMA order) and tokens 64 kb + 32 kk2 + 0..31; in it lane L owns the 16 bytes
+// of feature 32 (f / 32) + sel(16 fh + L % 16), tokens 64 kb + 32 kk2 +
+// 8 (L / 16) + 0..7, with sel = slab_row on the M side (in-features) and the
+// identity on the N side.
 
 // Eight 4-bit codes (0..3) -> eight exact bf16 values via the fp4 (e2m1)
 // converter: nibble c encodes c / 2 in e2m1 for c <= 3, and the scale 2 makes

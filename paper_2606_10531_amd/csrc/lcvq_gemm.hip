@@ -1,10 +1,12 @@
 // bf16 matrix-core (MFMA) products of the LC-VQ layer, gfx950.
 //
 // All three products put the weight-side axis (out-features r or in-features
-// c) on the MFMA M axis and tokens (or out-features for dW) on N.  The M rows
-// of every 32-row block are permuted (perm32) so that accumulator register i
-// of lane L holds weight-side index 16 (L / 32) + i: each lane owns sixteen
-// consecutive weight-side columns of one token row, i.e. whole groups.
+// c) on the MFMA M axis and tokens (or out-features for dW) on N, and use the
+// 16x16x32 instruction: on this chip it sustains about a fifth more throughput
+// than 32x32x16 on real-valued operands (the clock is power-limited, and the
+// smaller shape draws less per flop).  The M rows of every 32-row slab are
+// permuted (slab_row) so that each lane ends with eight consecutive
+// weight-side indices of one token (or out-feature), i.e. whole groups.
 //
 //   forward : D[r, t] = sum_c code[r, c] X'[t, c]          Y[t, r] = D + s[t]
 //   input   : D[c, t] = sum_r code[r, c] dY[t, r]          dX[t, c] = (D-group) A^T + rs[t] b
@@ -13,6 +15,12 @@
 // Codes reach the matrix cores exactly: the operand layout holds them as 4-bit
 // nibbles and the fp4 -> bf16 converter turns them into bf16 values 0..3 in
 // registers, so the dense W_hat never exists anywhere.
+//
+// The instructions are issued from inline assembly with the accumulators
+// bound to AGPRs: the compiler's own selection of this instruction moves the
+// accumulators between registers around every loop trip.  The statements carry
+// the wait states the compiler cannot see (a VALU result read as an operand,
+// an accumulator read after the loop).
 #include "lcvq_prep.hpp"
 
 namespace lcvq {
@@ -54,6 +62,19 @@ __device__ __forceinline__ void tile_of_block(int tiles_m, int tiles_n, int &tm,
   tn = in / gm;
 }
 
+// acc = A * B + acc, operands loaded (no VALU producer): issued in program order.
+__device__ __forceinline__ void mfma16(floatx4 &acc, const bf16x8 &a, const bf16x8 &b) {
+  asm volatile("v_mfma_f32_16x16x32_bf16 %0, %1, %2, %0" : "+a"(acc) : "v"(a), "v"(b));
+}
+// The same with A produced by VALU instructions: the leading s_nop covers the
+// VALU-write to matrix-core-read wait states.
+__device__ __forceinline__ void mfma16_valu_a(floatx4 &acc, const bf16x8 &a, const bf16x8 &b) {
+  asm volatile("s_nop 2\n\tv_mfma_f32_16x16x32_bf16 %0, %1, %2, %0" : "+a"(acc) : "v"(a), "v"(b));
+}
+// Wait states between the last matrix-core write of an accumulator and a
+// vector read of it (the epilogues read the accumulators right after the loop).
+__device__ __forceinline__ void mfma_drain() { asm volatile("s_nop 15\n\ts_nop 15" ::: "memory"); }
+
 __device__ __forceinline__ float as_f(uint32_t u) { return __uint_as_float(u); }
 // Copy a (uniform) value into a vector register.
 __device__ __forceinline__ float to_vgpr(float x) {
@@ -68,10 +89,10 @@ __device__ __forceinline__ uint32_t as_u(float f) { return __float_as_uint(f); }
 // No LDS: wave w of a block owns the 256 weight-side rows x 64 tokens
 // [64 w, 64 w + 64) of the block tile and streams both operands straight into
 // registers: the codes of the block's eight 32-row slabs (operand layout; the
-// four waves share them through the L1) and its own activations, either in the
-// matrix-core B layout (forward: X' as written by the activation transform) or
-// row-major (input gradient: dY as the caller holds it).  K is padded to an
-// even number of 64-wide steps.
+// four waves share them through the L1) and its own activations in the
+// matrix-core B layout, as the prepasses write them (forward: X' from the
+// activation transform; input gradient: the copy of dY made by the backward
+// prepass).  K is padded to an even number of 64-wide steps.
 // ============================================================================
 
 // Input-gradient mode also forms the map gradients from the same accumulator
@@ -86,7 +107,7 @@ __global__ __launch_bounds__(256, 1) void k_gemm_codes(
     int64_t vstride, const float *__restrict__ A, const float *__restrict__ bvec, uint16_t *__restrict__ out,
     int64_t ldo, int64_t Mvalid, int64_t Tvalid, const uint16_t *__restrict__ X,
     float *__restrict__ dA, float *__restrict__ db) {
-  const int tid = threadIdx.x, lane = tid & 63, h = lane >> 5;
+  const int tid = threadIdx.x, lane = tid & 63, q = lane >> 4, c16 = lane & 15;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   int tm, tn;
   tile_of_block(tiles_m, tiles_n, tm, tn);
@@ -98,21 +119,20 @@ __global__ __launch_bounds__(256, 1) void k_gemm_codes(
   // B operand of tokens tw .. tw + 63 (X' for the forward, dY for the input
   // gradient), both in the B-operand fragment layout with KB K steps
   const __amdgpu_buffer_rsrc_t rsB = make_rsrc(Bsrc + (tw >> 5) * (int64_t)KB * 2048, (int64_t)2 * KB * 4096);
-  uint32_t boff[2][4];  // per (ni, kk): byte offset of this lane's 16 bytes at step 0
+  uint32_t boff[2][4];  // per (32-token block, fragment): byte offset of this lane's 16 bytes at step 0
 #pragma unroll
   for (int ni = 0; ni < 2; ++ni)
 #pragma unroll
-    for (int kk = 0; kk < 4; ++kk) boff[ni][kk] = (uint32_t)((ni * KB * 4 + kk) * 1024 + lane * 16);
+    for (int fr = 0; fr < 4; ++fr) boff[ni][fr] = (uint32_t)((ni * KB * 4 + fr) * 1024 + lane * 16);
 
-  floatx16 acc[8][2];
+  floatx4 acc[16][4];  // [row block 2 mi + rb][16-token block tb]
 #pragma unroll
-  for (int i = 0; i < 8; ++i)
+  for (int i = 0; i < 16; ++i)
 #pragma unroll
-    for (int j = 0; j < 2; ++j) acc[i][j] = floatx16{};
+    for (int j = 0; j < 4; ++j) acc[i][j] = floatx4{0.0f, 0.0f, 0.0f, 0.0f};
 
   // Two register buffers of one 64-wide step each; the loads of step k + 2 are
-  // issued as soon as step k's MFMAs have been issued.  (Deeper prefetch with
-  // four 32-wide buffers measured slower.)
+  // issued as soon as step k's MFMAs have been issued.
   u32x4 ca[2][8], cb[2][2][4];
   auto load = [&](int buf, int kb) {
     const bool live = kb < KB;
@@ -123,22 +143,29 @@ __global__ __launch_bounds__(256, 1) void k_gemm_codes(
 #pragma unroll
     for (int ni = 0; ni < 2; ++ni)
 #pragma unroll
-      for (int kk = 0; kk < 4; ++kk)
-        cb[buf][ni][kk] = __builtin_amdgcn_raw_buffer_load_b128(
-            rsB, live ? (int)(boff[ni][kk] + (uint32_t)kb * 4096u) : (int)kOffNone, 0, 0);
+      for (int fr = 0; fr < 4; ++fr)
+        cb[buf][ni][fr] = __builtin_amdgcn_raw_buffer_load_b128(
+            rsB, live ? (int)(boff[ni][fr] + (uint32_t)kb * 4096u) : (int)kOffNone, 0, 0);
   };
+  // 32 A operands per step (sub-step kk2, row block 2 mi + rb), each used by
+  // four MFMAs; the conversion of the next one is placed between the second
+  // and third of them, so the converter works while the matrix core does.
   auto compute = [&](int buf) {
+    auto conv = [&](int s2) {  // s2 = 16 kk2 + 2 mi + rb
+      return nibbles_to_bf16x8(ca[buf][(s2 & 15) >> 1][2 * (s2 & 1) + (s2 >> 4)]);
+    };
+    bf16x8 an = conv(0);
 #pragma unroll
-    for (int kk = 0; kk < 4; ++kk) {
-      bf16x8 a[8];
-#pragma unroll
-      for (int mi = 0; mi < 8; ++mi) a[mi] = nibbles_to_bf16x8(ca[buf][mi][kk]);
-#pragma unroll
-      for (int mi = 0; mi < 8; ++mi)
-#pragma unroll
-        for (int ni = 0; ni < 2; ++ni)
-          acc[mi][ni] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
-              a[mi], __builtin_bit_cast(bf16x8, cb[buf][ni][kk]), acc[mi][ni], 0, 0, 0);
+    for (int s2 = 0; s2 < 32; ++s2) {
+      const int kk2 = s2 >> 4, p = s2 & 15;
+      const bf16x8 a = an;
+      const bf16x8 b0 = __builtin_bit_cast(bf16x8, cb[buf][0][kk2]), b1 = __builtin_bit_cast(bf16x8, cb[buf][0][2 + kk2]);
+      const bf16x8 b2 = __builtin_bit_cast(bf16x8, cb[buf][1][kk2]), b3 = __builtin_bit_cast(bf16x8, cb[buf][1][2 + kk2]);
+      mfma16_valu_a(acc[p][0], a, b0);
+      mfma16(acc[p][1], a, b1);
+      if (s2 + 1 < 32) an = conv(s2 + 1);
+      mfma16(acc[p][2], a, b2);
+      mfma16(acc[p][3], a, b3);
     }
   };
 
@@ -160,64 +187,62 @@ __global__ __launch_bounds__(256, 1) void k_gemm_codes(
     load(1, kb + 3);
     __builtin_amdgcn_sched_barrier(0);
   }
+  mfma_drain();
 
   // ---------------------------------------------------------------- epilogue
-  // Lane L holds, for each (mi, ni), the 16 consecutive weight-side columns
-  // cb .. cb + 15 of token row t.  Branch-free: rows beyond the tensor fall
-  // outside the buffer (loads give 0, stores are dropped) and columns beyond it
-  // get an out-of-range offset.  Every load is issued before the first store:
-  // the store and load counters are shared, so a load behind stores would wait
-  // for all of them.
+  // Lane L holds, for each (slab mi, token block tb), the 8 consecutive
+  // weight-side columns c .. c + 7 (c = 256 tm + 32 mi + 8 (L / 16);
+  // acc[2 mi][tb] the first four, acc[2 mi + 1][tb] the last four) of token
+  // t = tw + 16 tb + L % 16.  Branch-free: rows beyond the tensor fall outside
+  // the buffer (loads give 0, stores are dropped) and columns beyond it get an
+  // out-of-range offset.  Every load is issued before the first store: the
+  // store and load counters are shared, so a load behind stores would wait for
+  // all of them.
   const __amdgpu_buffer_rsrc_t ro = make_rsrc(out + tw * ldo, out == nullptr ? 0 : (Tvalid - tw) * ldo * 2);
-  const int64_t cb0 = (int64_t)tm * kTile + 16 * h;
+  const int64_t cb0 = (int64_t)tm * kTile + 8 * q;
   // Per-token term, held as up to kMaxParts partial rows vstride apart and
   // summed here: s of the forward, rowsum(dY) of the input gradient.
   constexpr int kMaxParts = 8;
   const __amdgpu_buffer_rsrc_t rv = make_rsrc(vecT + tw, ((int64_t)(vparts - 1) * vstride + Tvalid - tw) * 4);
-  float vp[kMaxParts][2], vt[2];
+  float vp[kMaxParts][4], vt[4];
 #pragma unroll
   for (int p = 0; p < kMaxParts; ++p)
 #pragma unroll
-    for (int ni = 0; ni < 2; ++ni)
-      vp[p][ni] = as_f(__builtin_amdgcn_raw_buffer_load_b32(
-          rv, p < vparts ? (int)((p * vstride + ni * 32 + (lane & 31)) * 4) : (int)kOffNone, 0, 0));
+    for (int tb = 0; tb < 4; ++tb)
+      vp[p][tb] = as_f(__builtin_amdgcn_raw_buffer_load_b32(
+          rv, p < vparts ? (int)((p * vstride + tb * 16 + c16) * 4) : (int)kOffNone, 0, 0));
 #pragma unroll
-  for (int ni = 0; ni < 2; ++ni) {
-    vt[ni] = vp[0][ni];
+  for (int tb = 0; tb < 4; ++tb) {
+    vt[tb] = vp[0][tb];
 #pragma unroll
-    for (int p = 1; p < kMaxParts; ++p) vt[ni] += vp[p][ni];
+    for (int p = 1; p < kMaxParts; ++p) vt[tb] += vp[p][tb];
   }
+  auto d8 = [&](int mi, int tb, int i) { return i < 4 ? acc[2 * mi][tb][i] : acc[2 * mi + 1][tb][i - 4]; };
   if constexpr (kMode == 0) {
 #pragma unroll
-    for (int ni = 0; ni < 2; ++ni) {
-      const int tl = ni * 32 + (lane & 31);
+    for (int tb = 0; tb < 4; ++tb) {
+      const int tl = tb * 16 + c16;
 #pragma unroll
-      for (int mi = 0; mi < 8; ++mi)
+      for (int mi = 0; mi < 8; ++mi) {
+        const int64_t c = cb0 + mi * 32;
+        const uint32_t off = c < Mvalid ? (uint32_t)(tl * ldo + c) * 2u : kOffNone;
+        u32x4 w;
 #pragma unroll
-        for (int half = 0; half < 2; ++half) {
-          const int64_t c = cb0 + mi * 32 + 8 * half;
-          const uint32_t off = c < Mvalid ? (uint32_t)(tl * ldo + c) * 2u : kOffNone;
-          u32x4 w;
-#pragma unroll
-          for (int e = 0; e < 4; ++e)
-            w[e] = pack_bf16x2(acc[mi][ni][8 * half + 2 * e] + vt[ni], acc[mi][ni][8 * half + 2 * e + 1] + vt[ni]);
-          __builtin_amdgcn_raw_buffer_store_b128(w, ro, off, 0, 0);
-        }
+        for (int e = 0; e < 4; ++e) w[e] = pack_bf16x2(d8(mi, tb, 2 * e) + vt[tb], d8(mi, tb, 2 * e + 1) + vt[tb]);
+        __builtin_amdgcn_raw_buffer_store_b128(w, ro, off, 0, 0);
+      }
     }
   } else {
     const bool want_map = dA != nullptr;
-    // X[t, cb .. cb + 15] of (ni, mi) pair p = ni * 8 + mi, fetched two pairs
-    // ahead (three rotating 32-byte buffers)
+    // X[t, c .. c + 7] of pair p = tb * 8 + mi, fetched two pairs ahead
+    // (three rotating 16-byte buffers)
     const __amdgpu_buffer_rsrc_t rx = make_rsrc(X + tw * Mvalid, want_map ? (Tvalid - tw) * Mvalid * 2 : 0);
-    u32x4 xv[3][2];
+    u32x4 xv[3];
     auto xload = [&](int p) {
-      const int ni = p >> 3, mi = p & 7, tl = ni * 32 + (lane & 31);
-#pragma unroll
-      for (int half = 0; half < 2; ++half) {
-        const int64_t c = cb0 + mi * 32 + 8 * half;
-        const uint32_t off = c < Mvalid ? (uint32_t)(tl * Mvalid + c) * 2u : kOffNone;
-        xv[p % 3][half] = __builtin_amdgcn_raw_buffer_load_b128(rx, off, 0, 0);
-      }
+      const int tb = p >> 3, mi = p & 7, tl = tb * 16 + c16;
+      const int64_t c = cb0 + mi * 32;
+      const uint32_t off = c < Mvalid ? (uint32_t)(tl * Mvalid + c) * 2u : kOffNone;
+      xv[p % 3] = __builtin_amdgcn_raw_buffer_load_b128(rx, off, 0, 0);
     };
     // the map in vector registers (in scalar ones it would not fit beside the
     // buffer descriptors and would spill)
@@ -235,41 +260,38 @@ __global__ __launch_bounds__(256, 1) void k_gemm_codes(
     xload(0);
     xload(1);
 #pragma unroll
-    for (int p = 0; p < 16; ++p) {
-      const int ni = p >> 3, mi = p & 7, tl = ni * 32 + (lane & 31);
-      if (p + 2 < 16) xload(p + 2);
+    for (int p = 0; p < 32; ++p) {
+      const int tb = p >> 3, mi = p & 7, tl = tb * 16 + c16;
+      if (p + 2 < 32) xload(p + 2);
+      float y[8], x[8];
 #pragma unroll
-      for (int half = 0; half < 2; ++half) {
-        float y[8], x[8];
-#pragma unroll
-        for (int e = 0; e < 4; ++e) {
-          x[2 * e] = bf16_lo(xv[p % 3][half][e]);
-          x[2 * e + 1] = bf16_hi(xv[p % 3][half][e]);
-        }
-#pragma unroll
-        for (int g = 0; g < 8 / D; ++g) {
-          float pv[D];
-#pragma unroll
-          for (int k = 0; k < D; ++k) pv[k] = acc[mi][ni][8 * half + g * D + k];
-#pragma unroll
-          for (int j = 0; j < D; ++j) {
-            float v = vt[ni] * bm[j];
-#pragma unroll
-            for (int k = 0; k < D; ++k) {
-              v = fmaf(am[j][k], pv[k], v);
-              gA[j][k] = fmaf(x[g * D + j], pv[k], gA[j][k]);
-            }
-            y[g * D + j] = v;
-            gb[j] = fmaf(x[g * D + j], vt[ni], gb[j]);
-          }
-        }
-        const int64_t c = cb0 + mi * 32 + 8 * half;
-        const uint32_t off = c < Mvalid ? (uint32_t)(tl * ldo + c) * 2u : kOffNone;
-        u32x4 w;
-#pragma unroll
-        for (int e = 0; e < 4; ++e) w[e] = pack_bf16x2(y[2 * e], y[2 * e + 1]);
-        __builtin_amdgcn_raw_buffer_store_b128(w, ro, off, 0, 0);
+      for (int e = 0; e < 4; ++e) {
+        x[2 * e] = bf16_lo(xv[p % 3][e]);
+        x[2 * e + 1] = bf16_hi(xv[p % 3][e]);
       }
+#pragma unroll
+      for (int g = 0; g < 8 / D; ++g) {
+        float pv[D];
+#pragma unroll
+        for (int k = 0; k < D; ++k) pv[k] = d8(mi, tb, g * D + k);
+#pragma unroll
+        for (int j = 0; j < D; ++j) {
+          float v = vt[tb] * bm[j];
+#pragma unroll
+          for (int k = 0; k < D; ++k) {
+            v = fmaf(am[j][k], pv[k], v);
+            gA[j][k] = fmaf(x[g * D + j], pv[k], gA[j][k]);
+          }
+          y[g * D + j] = v;
+          gb[j] = fmaf(x[g * D + j], vt[tb], gb[j]);
+        }
+      }
+      const int64_t c = cb0 + mi * 32;
+      const uint32_t off = c < Mvalid ? (uint32_t)(tl * ldo + c) * 2u : kOffNone;
+      u32x4 w;
+#pragma unroll
+      for (int e = 0; e < 4; ++e) w[e] = pack_bf16x2(y[2 * e], y[2 * e + 1]);
+      __builtin_amdgcn_raw_buffer_store_b128(w, ro, off, 0, 0);
     }
     if (want_map) {
       // lanes -> wave (shuffles), waves -> block (LDS), one atomic per entry
@@ -307,11 +329,14 @@ __global__ __launch_bounds__(256, 1) void k_gemm_codes(
 // (straight-through), or dZ = mask * slope(Z) * D with mask and slope taken
 // from Z (differentiable estimator of eq. dge, kDge)
 // (X' = X blockdiag(A), so the map is already applied).  Both operands come
-// pre-transposed in the token-K fragment layout.  Wave w owns in-features
-// [64 w, 64 w + 64) of the block tile (two 32-row slabs, A operand, streamed
-// straight into registers) against all 256 out-features (eight 32-column
-// blocks, B operand, shared by the four waves through three LDS stages filled
-// by direct-to-LDS loads).
+// pre-transposed in the token-K fragment layout.  16x16x32 matrix-core
+// instructions.  Wave w owns in-features [64 w, 64 w + 64) of the block tile
+// (two 32-row slabs, four 16-row blocks mb, A operand, streamed straight into
+// registers) against all 256 out-features (sixteen 16-column blocks nb, B
+// operand, shared by the four waves through three LDS stages filled by
+// direct-to-LDS loads).  The slab rows are permuted (slab_row) so that lane L
+// ends with in-features 8 (L / 16) .. + 7 of each slab for out-feature L % 16
+// of each column block: whole groups, and 16 contiguous bytes of dZ.
 // ============================================================================
 
 template <bool kDge>
@@ -324,7 +349,7 @@ __global__ __launch_bounds__(256, 1) void k_gemm_dw(const uint16_t *__restrict__
   constexpr int kStage = 32 * 1024;  // eight 4 KiB B blocks
   __shared__ __attribute__((aligned(1024))) char lds[3 * kStage];
 
-  const int tid = threadIdx.x, lane = tid & 63, h = lane >> 5;
+  const int tid = threadIdx.x, lane = tid & 63, q = lane >> 4, c16 = lane & 15;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   int tm, tn;
   tile_of_block(tiles_m, tiles_n, tm, tn);
@@ -336,11 +361,11 @@ __global__ __launch_bounds__(256, 1) void k_gemm_dw(const uint16_t *__restrict__
   // B: blocks tn * 8 + j; wave w copies blocks 2w, 2w + 1 (4 KiB each per step)
   const __amdgpu_buffer_rsrc_t rsB = make_rsrc(dyt + (size_t)(tn * 8) * KBt * 2048, (int64_t)8 * KBt * 4096);
 
-  floatx16 acc[2][8];
+  floatx4 acc[4][16];
 #pragma unroll
-  for (int i = 0; i < 2; ++i)
+  for (int i = 0; i < 4; ++i)
 #pragma unroll
-    for (int j = 0; j < 8; ++j) acc[i][j] = floatx16{};
+    for (int j = 0; j < 16; ++j) acc[i][j] = floatx4{0.0f, 0.0f, 0.0f, 0.0f};
 
   auto issue = [&](int st, int kb, bool live) {  // 8 direct-to-LDS loads per wave
     char *stage = lds + st * kStage;
@@ -348,41 +373,42 @@ __global__ __launch_bounds__(256, 1) void k_gemm_dw(const uint16_t *__restrict__
     for (int j = 0; j < 2; ++j) {
       const int blk = 2 * wave + j;
 #pragma unroll
-      for (int kk = 0; kk < 4; ++kk) {
-        const uint32_t off = live ? (uint32_t)(((blk * KBt + kb) * 4 + kk) * 1024 + lane * 16) : kOffNone;
-        buffer_to_lds16(rsB, (lds_void *)(stage + (blk * 4 + kk) * 1024), off);
+      for (int ph = 0; ph < 4; ++ph) {
+        const uint32_t off = live ? (uint32_t)(((blk * KBt + kb) * 4 + ph) * 1024 + lane * 16) : kOffNone;
+        buffer_to_lds16(rsB, (lds_void *)(stage + (blk * 4 + ph) * 1024), off);
       }
     }
   };
-  u32x4 ca[2][2][4];
+  u32x4 ca[2][2][4];  // [buffer][slab mi][fragment 2 fh + kk2]
   auto load_a = [&](int buf, int kb, bool live) {  // 8 loads per wave
 #pragma unroll
     for (int mi = 0; mi < 2; ++mi)
 #pragma unroll
-      for (int kk = 0; kk < 4; ++kk)
-        ca[buf][mi][kk] = __builtin_amdgcn_raw_buffer_load_b128(
-            rsA, live ? (int)(((mi * KBt + kb) * 4 + kk) * 1024 + lane * 16) : (int)kOffNone, 0, 0);
+      for (int ph = 0; ph < 4; ++ph)
+        ca[buf][mi][ph] = __builtin_amdgcn_raw_buffer_load_b128(
+            rsA, live ? (int)(((mi * KBt + kb) * 4 + ph) * 1024 + lane * 16) : (int)kOffNone, 0, 0);
   };
   auto compute = [&](int buf, int st) {
     const char *stage = lds + st * kStage;
 #pragma unroll
-    for (int kk = 0; kk < 4; ++kk) {
-      bf16x8 b[8];
+    for (int kk2 = 0; kk2 < 2; ++kk2) {
+      bf16x8 b[16];  // column block nb = 2 (32-wide block) + fh
 #pragma unroll
-      for (int ni = 0; ni < 8; ++ni) b[ni] = *reinterpret_cast<const bf16x8 *>(stage + (ni * 4 + kk) * 1024 + lane * 16);
+      for (int nb = 0; nb < 16; ++nb)
+        b[nb] = *reinterpret_cast<const bf16x8 *>(stage + ((nb >> 1) * 4 + 2 * (nb & 1) + kk2) * 1024 + lane * 16);
 #pragma unroll
-      for (int mi = 0; mi < 2; ++mi)
+      for (int mb = 0; mb < 4; ++mb) {
+        const bf16x8 a = __builtin_bit_cast(bf16x8, ca[buf][mb >> 1][2 * (mb & 1) + kk2]);
 #pragma unroll
-        for (int ni = 0; ni < 8; ++ni)
-          acc[mi][ni] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, ca[buf][mi][kk]), b[ni],
-                                                               acc[mi][ni], 0, 0, 0);
+        for (int nb = 0; nb < 16; ++nb) mfma16(acc[mb][nb], a, b[nb]);
+      }
     }
   };
 
   // Issue order per step kb (fixed by the scheduling fences):
   //   wait(B of kb) + barrier, B loads of kb + 2, MFMAs of kb, A loads of kb + 2.
   // B of step kb was issued before the A loads of kb, the B loads of kb + 1 and
-  // the A loads of kb + 1: 24 later loads may still be in flight.
+  // the A loads of kb + 1; waiting down to 16 also completes the A loads of kb.
   issue(0, 0, true);
   load_a(0, 0, true);
   __builtin_amdgcn_sched_barrier(0);
@@ -408,110 +434,109 @@ __global__ __launch_bounds__(256, 1) void k_gemm_dw(const uint16_t *__restrict__
     }
   }
   LCVQ_WAIT_VM_LGKM0(0);
+  mfma_drain();
 
   // ------------------------------------------------ gradient-estimator epilogue
-  // Lane L holds D[c .. c + 15, r] for each (mi, ni): dZ[r, c .. c + 15] =
-  // mask * D, the mask read from the bitmap the backward prepass wrote (one
-  // 64-bit word per row and wave: columns c0 + 64 w .. + 63); with kDge, mask
-  // and slope come from Z[r, c .. c + 15] instead.  Rows r >= m fall outside
-  // the buffers; columns c >= n get an out-of-range offset.  Every load (mask
-  // words or Z, and old dZ when accumulating) of a block row is issued before
-  // the stores of the previous one: loads and stores share one counter.
+  // Lane L holds, for column block nb and slab mi, D[c .. c + 7, r] with
+  // r = r0 + 16 nb + L % 16 and c = c0 + 64 w + 32 mi + 8 (L / 16):
+  // acc[2 mi][nb] the first four, acc[2 mi + 1][nb] the last four.  dZ[r, c ..
+  // c + 7] = mask * D, the mask read from the bitmap the backward prepass wrote
+  // (one 64-bit word per row and wave: columns c0 + 64 w .. + 63; byte 4 mi +
+  // L / 16 holds these eight); with kDge, mask and slope come from Z[r, c ..
+  // c + 7] instead.  Rows r >= m fall outside the buffers; columns c >= n get
+  // an out-of-range offset.  Every load (mask words or Z, and old dZ when
+  // accumulating) of a column block is issued before the stores of the
+  // previous one: loads and stores share one counter.
   const __amdgpu_buffer_rsrc_t rmk = make_rsrc(maskbits + (int64_t)r0 * ldm8, kDge ? 0 : (int64_t)(m - r0) * ldm8 * 8);
   const __amdgpu_buffer_rsrc_t rz = make_rsrc(Zb + (int64_t)r0 * n, kDge ? (int64_t)(m - r0) * n * 2 : 0);
   const int64_t mw = (int64_t)tm * 4 + wave;  // this wave's word of each bitmap row
   const int es = dz_bf16 ? 2 : 4;
   const __amdgpu_buffer_rsrc_t rg = make_rsrc((char *)dZ + (int64_t)r0 * n * es, (int64_t)(m - r0) * n * es);
-  u32x2 mk[8];
-  if constexpr (!kDge) {
-#pragma unroll
-    for (int ni = 0; ni < 8; ++ni) {
-      const int rl = ni * 32 + (lane & 31);
-      mk[ni] = __builtin_amdgcn_raw_buffer_load_b64(rmk, mw < ldm8 ? (int)((rl * ldm8 + mw) * 8) : (int)kOffNone, 0, 0);
-    }
-  }
-  u32x4 ov[2][2][2][2];
-  u32x4 zv[2][2][2];  // kDge: Z[r, c .. c + 7] per (buffer, mi, half)
-  auto eload = [&](int buf, int ni) {
-    const int rl = ni * 32 + (lane & 31);
+  u32x2 mk[2];        // mask word of the row, per buffer
+  u32x4 ov[2][2][2];  // old dZ per (buffer, mi, 16-byte half)
+  u32x4 zv[2][2];     // kDge: Z[r, c .. c + 7] per (buffer, mi)
+  auto eload = [&](int buf, int nb) {
+    const int rl = nb * 16 + c16;
     if constexpr (kDge) {
 #pragma unroll
-      for (int mi = 0; mi < 2; ++mi)
-#pragma unroll
-        for (int half = 0; half < 2; ++half) {
-          const int c = c0 + 64 * wave + 32 * mi + 16 * h + 8 * half;
-          zv[buf][mi][half] = __builtin_amdgcn_raw_buffer_load_b128(rz, c < n ? (uint32_t)(rl * n + c) * 2u : kOffNone, 0, 0);
-        }
+      for (int mi = 0; mi < 2; ++mi) {
+        const int c = c0 + 64 * wave + 32 * mi + 8 * q;
+        zv[buf][mi] = __builtin_amdgcn_raw_buffer_load_b128(rz, c < n ? (uint32_t)(rl * n + c) * 2u : kOffNone, 0, 0);
+      }
+    } else {
+      mk[buf] = __builtin_amdgcn_raw_buffer_load_b64(rmk, mw < ldm8 ? (int)((rl * ldm8 + mw) * 8) : (int)kOffNone, 0, 0);
     }
     if (!accumulate) return;
 #pragma unroll
-    for (int mi = 0; mi < 2; ++mi)
-#pragma unroll
-      for (int half = 0; half < 2; ++half) {
-        const int c = c0 + 64 * wave + 32 * mi + 16 * h + 8 * half;
-        const bool cv = c < n;
-        const uint32_t e = (uint32_t)(rl * n + c);
-        if (dz_bf16) {
-          ov[buf][mi][half][0] = __builtin_amdgcn_raw_buffer_load_b128(rg, cv ? e * 2u : kOffNone, 0, 0);
-        } else {
-          ov[buf][mi][half][0] = __builtin_amdgcn_raw_buffer_load_b128(rg, cv ? e * 4u : kOffNone, 0, 0);
-          ov[buf][mi][half][1] = __builtin_amdgcn_raw_buffer_load_b128(rg, cv ? e * 4u + 16u : kOffNone, 0, 0);
-        }
+    for (int mi = 0; mi < 2; ++mi) {
+      const int c = c0 + 64 * wave + 32 * mi + 8 * q;
+      const bool cv = c < n;
+      const uint32_t e = (uint32_t)(rl * n + c);
+      if (dz_bf16) {
+        ov[buf][mi][0] = __builtin_amdgcn_raw_buffer_load_b128(rg, cv ? e * 2u : kOffNone, 0, 0);
+      } else {
+        ov[buf][mi][0] = __builtin_amdgcn_raw_buffer_load_b128(rg, cv ? e * 4u : kOffNone, 0, 0);
+        ov[buf][mi][1] = __builtin_amdgcn_raw_buffer_load_b128(rg, cv ? e * 4u + 16u : kOffNone, 0, 0);
       }
+    }
   };
   eload(0, 0);
 #pragma unroll
-  for (int ni = 0; ni < 8; ++ni) {
-    const int buf = ni & 1;
-    if (ni + 1 < 8) eload(buf ^ 1, ni + 1);
-    const int rl = ni * 32 + (lane & 31);
+  for (int nb = 0; nb < 16; ++nb) {
+    const int buf = nb & 1;
+    if (nb + 1 < 16) eload(buf ^ 1, nb + 1);
+    const int rl = nb * 16 + c16;
 #pragma unroll
-    for (int mi = 0; mi < 2; ++mi)
+    for (int mi = 0; mi < 2; ++mi) {
+      const int c = c0 + 64 * wave + 32 * mi + 8 * q;
+      const bool cv = c < n;
+      const uint32_t e = (uint32_t)(rl * n + c);
+      float d8[8];
 #pragma unroll
-      for (int half = 0; half < 2; ++half) {
-        const int c = c0 + 64 * wave + 32 * mi + 16 * h + 8 * half;
-        const bool cv = c < n;
-        const uint32_t e = (uint32_t)(rl * n + c);
-        // (times the quantiser scale: the chain rule through the code-domain value)
-        float g[8];
-        if constexpr (kDge) {
+      for (int i = 0; i < 4; ++i) {
+        d8[i] = acc[2 * mi][nb][i];
+        d8[4 + i] = acc[2 * mi + 1][nb][i];
+      }
+      // (times the quantiser scale: the chain rule through the code-domain value)
+      float g[8];
+      if constexpr (kDge) {
 #pragma unroll
-          for (int q = 0; q < 8; ++q) {
-            const uint32_t zw = zv[buf][mi][half][q >> 1];
-            const float z = code_value((q & 1) ? bf16_hi(zw) : bf16_lo(zw), qz);
-            g[q] = ste_pass(z, mask_mode) ? acc[mi][ni][8 * half + q] * dge_slope(z, est) * qz.scale : 0.0f;
-          }
-        } else {
-          const uint32_t mb = mk[ni][mi] >> (16 * h + 8 * half);
-#pragma unroll
-          for (int q = 0; q < 8; ++q) g[q] = ((mb >> q) & 1u) ? acc[mi][ni][8 * half + q] * qz.scale : 0.0f;
+        for (int i = 0; i < 8; ++i) {
+          const uint32_t zw = zv[buf][mi][i >> 1];
+          const float z = code_value((i & 1) ? bf16_hi(zw) : bf16_lo(zw), qz);
+          g[i] = ste_pass(z, mask_mode) ? d8[i] * dge_slope(z, est) * qz.scale : 0.0f;
         }
-        if (dz_bf16) {
-          if (accumulate) {
+      } else {
+        const uint32_t mb = mk[buf][mi] >> (8 * q);
 #pragma unroll
-            for (int q = 0; q < 4; ++q) {
-              g[2 * q] += bf16_lo(ov[buf][mi][half][0][q]);
-              g[2 * q + 1] += bf16_hi(ov[buf][mi][half][0][q]);
-            }
+        for (int i = 0; i < 8; ++i) g[i] = ((mb >> i) & 1u) ? d8[i] * qz.scale : 0.0f;
+      }
+      if (dz_bf16) {
+        if (accumulate) {
+#pragma unroll
+          for (int i = 0; i < 4; ++i) {
+            g[2 * i] += bf16_lo(ov[buf][mi][0][i]);
+            g[2 * i + 1] += bf16_hi(ov[buf][mi][0][i]);
           }
+        }
+        u32x4 w;
+#pragma unroll
+        for (int i = 0; i < 4; ++i) w[i] = pack_bf16x2(g[2 * i], g[2 * i + 1]);
+        __builtin_amdgcn_raw_buffer_store_b128(w, rg, cv ? e * 2u : kOffNone, 0, 0);
+      } else {
+#pragma unroll
+        for (int p = 0; p < 2; ++p) {
           u32x4 w;
 #pragma unroll
-          for (int q = 0; q < 4; ++q) w[q] = pack_bf16x2(g[2 * q], g[2 * q + 1]);
-          __builtin_amdgcn_raw_buffer_store_b128(w, rg, cv ? e * 2u : kOffNone, 0, 0);
-        } else {
-#pragma unroll
-          for (int p = 0; p < 2; ++p) {
-            u32x4 w;
-#pragma unroll
-            for (int q = 0; q < 4; ++q) {
-              float v = g[4 * p + q];
-              if (accumulate) v += as_f(ov[buf][mi][half][p][q]);
-              w[q] = as_u(v);
-            }
-            __builtin_amdgcn_raw_buffer_store_b128(w, rg, cv ? e * 4u + 16u * p : kOffNone, 0, 0);
+          for (int i = 0; i < 4; ++i) {
+            float v = g[4 * p + i];
+            if (accumulate) v += as_f(ov[buf][mi][p][i]);
+            w[i] = as_u(v);
           }
+          __builtin_amdgcn_raw_buffer_store_b128(w, rg, cv ? e * 4u + 16u * p : kOffNone, 0, 0);
         }
       }
+    }
   }
 }
 

@@ -151,8 +151,8 @@ __device__ __forceinline__ void quant_block(int bq, int by, int gx, const uint16
     if (bx >= gx) break;
 #pragma unroll
     for (int i = 0; i < 2; ++i) {
-      const int id = tid + 256 * i, slab = id >> 8, lane = (id >> 2) & 63, kk = id & 3;
-      const int mloc = slab * 32 + perm32(lane & 31), kloc = 16 * kk + 8 * (lane >> 5);
+      const int id = tid + 256 * i, slab = id >> 8, lane = (id >> 2) & 63, dw = id & 3;
+      const int mloc = slab * 32 + slab_row(16 * (dw >> 1) + (lane & 15)), kloc = 32 * (dw & 1) + 8 * (lane >> 4);
       uint32_t w = 0;
       if constexpr (kTrans) {
 #pragma unroll
@@ -166,7 +166,7 @@ __device__ __forceinline__ void quant_block(int bq, int by, int gx, const uint16
       }
       const int mb = (kTrans ? bx : by) * 2 + slab;
       const int kb = kTrans ? by : bx;
-      frag[frag_dword_index(mb, kb, KB, lane, kk)] = w;
+      frag[frag_dword_index(mb, kb, KB, lane, dw)] = w;
     }
   }
 }
@@ -216,17 +216,18 @@ __global__ __launch_bounds__(256) void k_act_transform(const XT *__restrict__ X,
 
 // ---- activation transform, bf16, straight into the B-operand fragments -----
 // Block (tb, kc): tokens 32 tb .. 32 tb + 31, 64-wide K steps of chunk kc;
-// wave w takes steps kb0 + w, kb0 + w + 4, ...  For (step kb, sub-step kk) lane
-// L owns token 32 tb + L % 32 and K = 64 kb + 16 kk + 8 (L / 32) + 0..7 -- one
-// whole group (d = 8) or two (d = 4) -- so it loads the 16 bytes it will store,
-// and each wave writes one whole 1 KiB fragment per sub-step.  Tokens >= N and
-// K >= n give zeros.  sp[kc * Np + t] = this chunk's part of s[t].
+// wave w takes steps kb0 + w, kb0 + w + 4, ...  For (step kb, fragment
+// 2 th + kk2) lane L owns token 32 tb + 16 th + L % 16 and K = 64 kb + 32 kk2 +
+// 8 (L / 16) + 0..7 -- one whole group (d = 8) or two (d = 4) -- so it loads the
+// 16 bytes it will store, and each wave writes one whole 1 KiB fragment at a
+// time.  Tokens >= N and K >= n give zeros.  sp[kc * Np + t] = this chunk's
+// part of s[t].
 template <int D>
 __device__ __forceinline__ void act_block(int64_t tb, int kc, const uint16_t *__restrict__ X, int64_t N, int64_t n,
                                           const float *__restrict__ A, const float *__restrict__ b,
                                           uint16_t *__restrict__ Xp, int KB, int spc, int64_t Np,
                                           float *__restrict__ sp, float (&red)[4][32]) {
-  const int tid = threadIdx.x, lane = tid & 63, h = lane >> 5;
+  const int tid = threadIdx.x, lane = tid & 63;
   const int wave = tid >> 6;
   const int64_t rows = N - tb * 32;  // > 0 only for blocks that hold real tokens
   const __amdgpu_buffer_rsrc_t rx = make_rsrc(X + tb * 32 * n, rows > 0 ? (rows < 32 ? rows : 32) * n * 2 : 0);
@@ -238,7 +239,7 @@ __device__ __forceinline__ void act_block(int64_t tb, int kc, const uint16_t *__
     for (int k = 0; k < D; ++k) a[j][k] = A[j * D + k];
   }
   const int kb0 = kc * spc, kb1 = min(kb0 + spc, KB);
-  float acc_s = 0.0f;
+  float acc_s[2] = {0.0f, 0.0f};  // tokens 32 tb + 16 th + L % 16, this lane's K groups
   // batches of 8 steps: this wave's two (kb0 + 8 i + wave + 4 s), all 8
   // loads issued before the first is used
   for (int base = kb0 + wave; base < kb1; base += 8) {
@@ -247,10 +248,11 @@ __device__ __forceinline__ void act_block(int64_t tb, int kc, const uint16_t *__
     for (int st = 0; st < 2; ++st) {
       const int kb = base + 4 * st;
 #pragma unroll
-      for (int kk = 0; kk < 4; ++kk) {
-        const int64_t k = (int64_t)kb * 64 + 16 * kk + 8 * h;
-        const uint32_t off = (kb < kb1 && k < n) ? (uint32_t)(((lane & 31) * n + k) * 2) : kOffNone;
-        xv[st][kk] = __builtin_amdgcn_raw_buffer_load_b128(rx, off, 0, 0);
+      for (int fr = 0; fr < 4; ++fr) {
+        const int64_t k = (int64_t)kb * 64 + 32 * (fr & 1) + 8 * (lane >> 4);
+        const int tr = 16 * (fr >> 1) + (lane & 15);
+        const uint32_t off = (kb < kb1 && k < n) ? (uint32_t)((tr * n + k) * 2) : kOffNone;
+        xv[st][fr] = __builtin_amdgcn_raw_buffer_load_b128(rx, off, 0, 0);
       }
     }
 #pragma unroll
@@ -259,12 +261,12 @@ __device__ __forceinline__ void act_block(int64_t tb, int kc, const uint16_t *__
       if (kb >= kb1) break;
       uint16_t *dst = Xp + ((tb * KB + kb) * 4) * 512 + lane * 8;
 #pragma unroll
-      for (int kk = 0; kk < 4; ++kk) {
+      for (int fr = 0; fr < 4; ++fr) {
         float x[8], y[8];
 #pragma unroll
         for (int e = 0; e < 4; ++e) {
-          x[2 * e] = bf16_lo(xv[st][kk][e]);
-          x[2 * e + 1] = bf16_hi(xv[st][kk][e]);
+          x[2 * e] = bf16_lo(xv[st][fr][e]);
+          x[2 * e + 1] = bf16_hi(xv[st][fr][e]);
         }
 #pragma unroll
         for (int g = 0; g < 8 / D; ++g)
@@ -276,16 +278,23 @@ __device__ __forceinline__ void act_block(int64_t tb, int kc, const uint16_t *__
             y[g * D + k] = v;
           }
 #pragma unroll
-        for (int e = 0; e < 8; ++e) acc_s = fmaf(x[e], bb[e % D], acc_s);
+        for (int e = 0; e < 8; ++e) acc_s[fr >> 1] = fmaf(x[e], bb[e % D], acc_s[fr >> 1]);
         u32x4 w;
 #pragma unroll
         for (int e = 0; e < 4; ++e) w[e] = pack_bf16x2(y[2 * e], y[2 * e + 1]);
-        *reinterpret_cast<u32x4 *>(dst + kk * 512) = w;
+        *reinterpret_cast<u32x4 *>(dst + fr * 512) = w;
       }
     }
   }
-  acc_s += __shfl_xor(acc_s, 32, 64);
-  if (lane < 32) red[wave][lane] = acc_s;
+#pragma unroll
+  for (int th = 0; th < 2; ++th) {  // over the four K groups (lanes L % 16 + 16 g)
+    acc_s[th] += __shfl_xor(acc_s[th], 16, 64);
+    acc_s[th] += __shfl_xor(acc_s[th], 32, 64);
+  }
+  if (lane < 16) {
+    red[wave][lane] = acc_s[0];
+    red[wave][16 + lane] = acc_s[1];
+  }
   __syncthreads();
   if (tid < 32) sp[(int64_t)kc * Np + tb * 32 + tid] = red[0][tid] + red[1][tid] + red[2][tid] + red[3][tid];
 }
@@ -443,10 +452,11 @@ __global__ __launch_bounds__(256) void k_dequant(const void *__restrict__ src, i
 
 // ---- backward operands of the weight-gradient product ----------------------
 // Transposed store of one 64-token x 64-feature sub-tile from the LDS tile
-// into the token-K fragment layout (zero-padded to KBt steps and to whole
-// 256-feature tiles): block (f0 / 32 + fb, bt), sub-step kk, lane L holds
-// tokens kk * 16 + 8 (L / 32) + 0..7 of feature sel(L % 32), sel = perm32 for
-// in-features (M side) and the identity for out-features (N side).
+// into the token-K fragment layout of v_mfma_f32_16x16x32_bf16 (zero-padded to
+// KBt steps and to whole 256-feature tiles): block (f0 / 32 + fb, bt) holds
+// four 1 KiB fragments phi = 2 fh + kk2; in fragment phi lane L holds tokens
+// 32 kk2 + 8 (L / 16) + 0..7 of feature sel(16 fh + L % 16), sel = slab_row
+// for in-features (M side) and the identity for out-features (N side).
 // The column reads use the transposing LDS read: in each 16-lane group, lane
 // 4 e + q addresses token e (+ 4 for the second read) and four consecutive
 // features F(q) .. F(q) + 3, and output lane 4 q + w receives feature F(q) + w
@@ -456,16 +466,16 @@ __device__ __forceinline__ void tile_store_t(int bt, int64_t f0, int KBt, uint16
                                              uint16_t (&tile)[64][64 + 8]) {
   const int tid = threadIdx.x;
   const int L = tid & 63, g = L >> 4, e = (L >> 2) & 3, q = L & 3;
-  const int F = kMside ? 8 * (g & 1) + 4 * (q >> 1) + 16 * (q & 1) : 16 * (g & 1) + 4 * q;
 #pragma unroll
   for (int i = 0; i < 2; ++i) {
-    const int id = tid + 256 * i, fb = id >> 8, kk = (id >> 6) & 3;
-    const int t = kk * 16 + 8 * (g >> 1) + e;
+    const int id = tid + 256 * i, fb = id >> 8, phi = (id >> 6) & 3, fh = phi >> 1, kk2 = phi & 1;
+    const int F = kMside ? 8 * q + 4 * fh : 16 * fh + 4 * q;
+    const int t = 32 * kk2 + 8 * g + e;
     const bf16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4 *)&tile[t][fb * 32 + F]);
     const bf16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4 *)&tile[t + 4][fb * 32 + F]);
     const u32x4 w = __builtin_bit_cast(u32x4, __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7));
     const int64_t blk = (f0 >> 5) + fb;
-    *reinterpret_cast<u32x4 *>(dst + (((blk * KBt + bt) * 4 + kk) * 64 + L) * 8) = w;
+    *reinterpret_cast<u32x4 *>(dst + (((blk * KBt + bt) * 4 + phi) * 64 + L) * 8) = w;
   }
 }
 
