@@ -7,7 +7,7 @@ weight matrix, on seeded synthetic inputs already resident in HBM.  The
 reported value is the work of the three products, 6 N m n flop, divided by the
 step time.  Prints one JSON line.
 
-  python bench.py [--steps K] [--warmup W] [--workload NAME] [--no-cpu-baseline]
+  python bench.py [--steps K] [--warmup W] [--workload NAME] [--no-cpu-baseline] [--workloads]
 """
 from __future__ import annotations
 
@@ -384,7 +384,8 @@ def main():
     ap.add_argument("--workload", default=DEFAULT_WORKLOAD)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-hbm", action="store_true")
-    ap.add_argument("--no-workloads", action="store_true", help="skip timing the larger Llama-shaped workloads")
+    ap.add_argument("--workloads", action="store_true",
+                    help="also time the larger Llama-shaped workloads (7B MLP, 70B MLP, 7B block with AdamW)")
     ap.add_argument("--cpu-seconds", type=float, default=10.0)
     ap.add_argument("--copy-probe", type=int, default=0, metavar="BYTES",
                     help="only run a plain device-to-device copy of BYTES (counter calibration) and exit")
@@ -485,7 +486,7 @@ def main():
                                    "differentiable gradient estimator, k=5, slope cap 3, latent mask")
     res["xavier_step"] = variant_step(lc, torch, layers, args.steps, "step_xavier",
                                       "latent in the Xavier domain: codes of W_p / s' + t, gradient / s'")
-    if not args.no_workloads:
+    if args.workloads:
         res["workloads"] = workload_steps(lc, torch, [w for w in OTHER_WORKLOADS if w != args.workload],
                                           max(3, args.steps // 10))
     L0 = layers[0]
