@@ -18,9 +18,12 @@
 //
 // The instructions are issued from inline assembly with the accumulators
 // bound to AGPRs: the compiler's own selection of this instruction moves the
-// accumulators between registers around every loop trip.  The statements carry
-// the wait states the compiler cannot see (a VALU result read as an operand,
-// an accumulator read after the loop).
+// accumulators between registers around every loop trip.  The compiler cannot
+// see hazards inside such statements, so the code provides the wait states
+// itself: after the zeroing of the accumulators (acc_fence), before an MFMA
+// that reads a just-converted codes operand (mfma16_valu_a), and after the
+// loop (mfma_drain).  All other operands come from loads, which the compiler's
+// waits cover.
 #include "lcvq_prep.hpp"
 
 namespace lcvq {
@@ -71,8 +74,28 @@ __device__ __forceinline__ void mfma16(floatx4 &acc, const bf16x8 &a, const bf16
 __device__ __forceinline__ void mfma16_valu_a(floatx4 &acc, const bf16x8 &a, const bf16x8 &b) {
   asm volatile("s_nop 2\n\tv_mfma_f32_16x16x32_bf16 %0, %1, %2, %0" : "+a"(acc) : "v"(a), "v"(b));
 }
-// Wait states between the last matrix-core write of an accumulator and a
-// vector read of it (the epilogues read the accumulators right after the loop).
+// Wait states between the zeroing of the accumulators (vector writes) and the
+// first matrix-core read of them, R x C accumulators.  Each statement passes
+// four accumulators through itself, so every zeroing write precedes the whole
+// chain and every MFMA follows it: at least R C / 4 statements and a final
+// s_nop 4 lie between a write and a read.
+template <int R, int C>
+__device__ __forceinline__ void acc_fence(floatx4 (&acc)[R][C]) {
+  static_assert(C % 4 == 0, "four accumulators per statement");
+#pragma unroll
+  for (int i = 0; i < R; ++i)
+#pragma unroll
+    for (int j = 0; j < C; j += 4) {
+      if (i + 1 < R || j + 4 < C)
+        asm volatile("s_nop 0" : "+a"(acc[i][j]), "+a"(acc[i][j + 1]), "+a"(acc[i][j + 2]), "+a"(acc[i][j + 3]));
+      else
+        asm volatile("s_nop 4" : "+a"(acc[i][j]), "+a"(acc[i][j + 1]), "+a"(acc[i][j + 2]), "+a"(acc[i][j + 3]));
+    }
+}
+// Wait states between the last matrix-core write of an accumulator and the
+// epilogue's vector reads of it.  The statement is a scheduling boundary with
+// a memory clobber; the reads are copies the compiler places at their uses,
+// which all lie in the epilogue after it.
 __device__ __forceinline__ void mfma_drain() { asm volatile("s_nop 15\n\ts_nop 15" ::: "memory"); }
 
 __device__ __forceinline__ float as_f(uint32_t u) { return __uint_as_float(u); }
@@ -130,6 +153,7 @@ __global__ __launch_bounds__(256, 1) void k_gemm_codes(
   for (int i = 0; i < 16; ++i)
 #pragma unroll
     for (int j = 0; j < 4; ++j) acc[i][j] = floatx4{0.0f, 0.0f, 0.0f, 0.0f};
+  acc_fence(acc);
 
   // Two register buffers of one 64-wide step each; the loads of step k + 2 are
   // issued as soon as step k's MFMAs have been issued.
@@ -366,6 +390,7 @@ __global__ __launch_bounds__(256, 1) void k_gemm_dw(const uint16_t *__restrict__
   for (int i = 0; i < 4; ++i)
 #pragma unroll
     for (int j = 0; j < 16; ++j) acc[i][j] = floatx4{0.0f, 0.0f, 0.0f, 0.0f};
+  acc_fence(acc);
 
   auto issue = [&](int st, int kb, bool live) {  // 8 direct-to-LDS loads per wave
     char *stage = lds + st * kStage;
