@@ -120,11 +120,18 @@ __global__ __launch_bounds__(256) void k_packed_prep(const uint16_t *__restrict_
 // holds, for step j and sub-step i = 2 kk + (E: 0, O: 1), eight of the codes of
 // dword kk of its 16 bytes (columns 256 j + 64 q + 16 kk .. + 15, in the order
 // above) and the matching eight X'' values, fragment (j, i) of the prepass.
+//
+// kXL (few tokens): the X'' rows of the Nc tokens for the block's steps are
+// copied once into LDS (dynamic, 512 Nc bytes per step plus a zero chunk) and
+// each step reads its fragments from there, instead of every wave loading
+// eight mostly idle 1 KiB fragments per step from the L2.
+template <bool kXL>
 __global__ __launch_bounds__(256) void k_packed_gemv(const uint8_t *__restrict__ packed, int64_t m, int64_t n, int KT,
                                                      int KS, int spb, const uint16_t *__restrict__ xq, int64_t nP,
                                                      const float *__restrict__ sp, int nchunks, int Nc,
                                                      float *__restrict__ part, int *__restrict__ counters,
                                                      void *__restrict__ Y, int y_bf16) {
+  extern __shared__ u32x4 xl[];
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int q = lane >> 4, tl = lane & 15;
   const int rt = (int)blockIdx.x / KS, ks = (int)blockIdx.x % KS;
@@ -139,6 +146,17 @@ __global__ __launch_bounds__(256) void k_packed_gemv(const uint8_t *__restrict__
 #pragma unroll
   for (int rb = 0; rb < 4; ++rb) acc[rb] = floatx4{0.0f, 0.0f, 0.0f, 0.0f};
   u32x4 cw[2][4], xf[2][8];
+  const int nch = (j1 - j0) * 32 * Nc;  // kXL: 16-byte chunks in LDS; chunk nch is zero
+  if constexpr (kXL) {
+    // chunk c = ((jj * 8 + i) * 4 + q) * Nc + t  <-  fragment (j0 + jj, i), lane 16 q + t
+    for (int c = tid; c < nch; c += 256) {
+      const int t = c % Nc, fq = c / Nc;
+      xl[c] = __builtin_amdgcn_raw_buffer_load_b128(
+          rX, (uint32_t)(((j0 * 8 + (fq >> 2)) * 64 + (fq & 3) * 16 + t) * 16), 0, 0);
+    }
+    if (tid == 0) xl[nch] = u32x4{0u, 0u, 0u, 0u};
+    __syncthreads();
+  }
   auto load = [&](int buf, int j) {
     const bool live = j < j1;
     const bool xlive = live && tl < Nc;  // X' rows of absent tokens are zero: not loaded
@@ -146,10 +164,17 @@ __global__ __launch_bounds__(256) void k_packed_gemv(const uint8_t *__restrict__
     for (int rb = 0; rb < 4; ++rb)
       cw[buf][rb] = __builtin_amdgcn_raw_buffer_load_b128(
           rP, live ? (uint32_t)((16 * rb + tl) * ldb + 64 * j + 16 * q) : kOffNone, 0, 0);
+    if constexpr (kXL) {
+      const int base = xlive ? ((j - j0) * 32 + q) * Nc + tl : nch;
+      const int stride = xlive ? 4 * Nc : 0;
 #pragma unroll
-    for (int i = 0; i < 8; ++i)
-      xf[buf][i] = __builtin_amdgcn_raw_buffer_load_b128(
-          rX, xlive ? (uint32_t)(((j * 8 + i) * 64 + lane) * 16) : kOffNone, 0, 0);
+      for (int i = 0; i < 8; ++i) xf[buf][i] = xl[base + i * stride];
+    } else {
+#pragma unroll
+      for (int i = 0; i < 8; ++i)
+        xf[buf][i] = __builtin_amdgcn_raw_buffer_load_b128(
+            rX, xlive ? (uint32_t)(((j * 8 + i) * 64 + lane) * 16) : kOffNone, 0, 0);
+    }
   };
   // bf16 1.0 in both halves, held in a vector register: with the mask from a
   // scalar register each operand dword is then one v_and_or_b32 (a literal
@@ -290,8 +315,16 @@ hipError_t launch_packed_prep(const uint16_t *X, int Nc, int64_t m, int64_t n, i
 hipError_t launch_packed_gemv(const uint8_t *packed, int64_t m, int64_t n, const uint16_t *xq, const float *sp,
                               int Nc, float *part, int *counters, void *Y, bool y_bf16, hipStream_t st) {
   const PackedPlan p = packed_plan(m, n);
-  k_packed_gemv<<<p.row_tiles * p.KS, 256, 0, st>>>(packed, m, n, p.KT, p.KS, p.spb, xq, p.nP, sp, p.nchunks, Nc,
-                                                    part, counters, Y, y_bf16 ? 1 : 0);
+  // X'' of the block's steps in LDS when it fits in 48 KiB (few tokens) and
+  // the block has enough steps to repay the copy and its barrier (on short K
+  // ranges the product is latency-bound and the copy only adds to it)
+  const size_t xl_bytes = ((size_t)p.spb * 32 * Nc + 1) * 16;
+  if (xl_bytes <= 48 * 1024 && p.spb >= 24)
+    k_packed_gemv<true><<<p.row_tiles * p.KS, 256, xl_bytes, st>>>(packed, m, n, p.KT, p.KS, p.spb, xq, p.nP, sp,
+                                                                   p.nchunks, Nc, part, counters, Y, y_bf16 ? 1 : 0);
+  else
+    k_packed_gemv<false><<<p.row_tiles * p.KS, 256, 0, st>>>(packed, m, n, p.KT, p.KS, p.spb, xq, p.nP, sp,
+                                                             p.nchunks, Nc, part, counters, Y, y_bf16 ? 1 : 0);
   return hipGetLastError();
 }
 

@@ -122,3 +122,31 @@ def test_packed_forward_full_size_sampled(lc, N, m, n):
     rows = np.unique(np.concatenate([np.arange(32), r.integers(0, m, 96), [m - 1]]))
     ref = orc.linear_forward_packed(P[rows], A.astype(np.float64), b.astype(np.float64), orc.widen(X, "bf16"), d, n)
     assert rel_fro(to_host(Y)[:, rows], ref) <= TOL
+
+
+@pytest.mark.parametrize("N,m,n", [(3, 12344, 6144), (1, 12352, 6144)])
+def test_packed_forward_few_tokens_long_rows(lc, N, m, n):
+    """Few tokens with at least 24 product steps per block: the X'' rows are
+    staged in LDS once per block; ragged last row tile (m % 64 != 0)."""
+    d = 8
+    inp, P = _inputs(N, m, n, d, seed=m + N)
+    got = _run(lc, inp, P, d, "f32")[0]
+    assert rel_fro(got, _ref(inp, P, d, n)) <= TOL
+
+
+@pytest.mark.parametrize("N", [2, 3])
+def test_packed_forward_full_size_two_three_tokens(lc, N):
+    """28672 x 8192 at 2 tokens (X'' staged in LDS) and 3 tokens (streamed),
+    sampled rows."""
+    import torch
+    m, n, d = 28672, 8192, 8
+    r = synth.rng(m + n + N)
+    P = r.integers(0, 256, size=(m, n // 4), dtype=np.uint8)
+    X = synth.draw_activations(N, n, 7 + N, "bf16")
+    A, b = synth.draw_map(d, 1)
+    Y = lc.linear_fwd_packed(torch.from_numpy(P).cuda(), torch.from_numpy(A).cuda(), torch.from_numpy(b).cuda(),
+                             to_dev(X, "bf16"), d)
+    torch.cuda.synchronize()
+    rows = np.unique(np.concatenate([np.arange(32), r.integers(0, m, 96), [m - 1]]))
+    ref = orc.linear_forward_packed(P[rows], A.astype(np.float64), b.astype(np.float64), orc.widen(X, "bf16"), d, n)
+    assert rel_fro(to_host(Y)[:, rows], ref) <= TOL
