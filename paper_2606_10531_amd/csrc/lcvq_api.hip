@@ -455,6 +455,13 @@ lcvq_status_t lcvq_linear_fwd_packed(int64_t N, int64_t m, int64_t n, int32_t d,
   int *counters = (int *)(ws + L.counters);
   for (int64_t t0 = 0; t0 < N; t0 += 16) {
     const int Nc = (int)std::min<int64_t>(16, N - t0);
+    if (lcvq::packed_fused(m, n, Nc)) {  // the product block computes its own X'' and s
+      Timed tm(LCVQ_K_PACKED, st);
+      e = tm.done(lcvq::launch_packed_fused(packed, m, n, (const uint16_t *)X + t0 * n, Nc, d, A, b,
+                                            (char *)Y + t0 * m * ys, y_dtype == LCVQ_BF16, st));
+      if (e != hipSuccess) return hip_fail(e, "packed product launch");
+      continue;
+    }
     {
       Timed tm(LCVQ_K_PACKED_PREP, st);
       e = tm.done(lcvq::launch_packed_prep((const uint16_t *)X + t0 * n, Nc, m, n, d, A, b, xq, sp, counters, st));

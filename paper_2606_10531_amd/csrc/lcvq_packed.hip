@@ -42,18 +42,48 @@ constexpr int kPkStep = 256;    // K columns per product step (64 bytes of codes
 // c >= n are written as zeros up to nP (a multiple of 256).  Thread tid takes
 // the 16 columns c0 = 4096 chunk + 16 tid .., i.e. step j = c0 / 256, lane
 // group q = (c0 / 64) % 4 and dword kk = (c0 / 16) % 4 of the product.
+// One 16-column group of one token: X'[g D + k] = sum_j X[g D + j] A[j, k] is
+// rounded to bf16 and scaled exactly by 2^(7 - p) for the mantissa position p
+// its code takes in the product (the two operand dwords ev / od, in element
+// order); s gains sum_j X[g D + j] b[j] and loses sum X'', the offset of the
+// 1.0 bits of the decoded codes.
 template <int D>
-__global__ __launch_bounds__(256) void k_packed_prep(const uint16_t *__restrict__ X, int Nc, int64_t n, int64_t nP,
-                                                     const float *__restrict__ A, const float *__restrict__ b,
-                                                     uint16_t *__restrict__ xq, float *__restrict__ sp,
-                                                     int *__restrict__ counters, int ncounters) {
-  const int tid = threadIdx.x, t = blockIdx.y;
-  const int64_t c0 = (int64_t)blockIdx.x * kPkChunk + 16 * tid;
-  if (blockIdx.x == 0 && blockIdx.y == 0)
-    for (int i = tid; i < ncounters; i += 256) counters[i] = 0;
-  float x[16];
-  if (t < Nc && c0 < n) {  // n is a multiple of 64: the 16 columns are whole
-    const uint4 *src = reinterpret_cast<const uint4 *>(X + (int64_t)t * n + c0);
+__device__ __forceinline__ void xpp_group(const float (&x)[16], const float *__restrict__ A,
+                                          const float *__restrict__ b, float &s, u32x4 &ev, u32x4 &od) {
+  float xp[16];
+#pragma unroll
+  for (int g = 0; g < 16 / D; ++g)
+#pragma unroll
+    for (int k = 0; k < D; ++k) {
+      float v = 0.0f;
+#pragma unroll
+      for (int j = 0; j < D; ++j) v = fmaf(x[g * D + j], A[j * D + k], v);
+      xp[g * D + k] = v;
+      s = fmaf(x[g * D + k], b[k], s);
+    }
+  constexpr int kCode[16] = {0, 8, 1, 9, 2, 10, 3, 11, 4, 12, 5, 13, 6, 14, 7, 15};
+  constexpr float kScale[16] = {128.f, 128.f, 32.f, 32.f, 8.f, 8.f, 128.f, 128.f,
+                                32.f, 32.f, 8.f, 8.f, 128.f, 128.f, 32.f, 32.f};
+  uint32_t h[16];
+#pragma unroll
+  for (int e = 0; e < 16; ++e) {
+    h[e] = f32_to_bf16(xp[kCode[e]]);                           // X' rounded to bf16 ..
+    const float sc = __uint_as_float(h[e] << 16) * kScale[e];   // .. then scaled exactly
+    h[e] = __float_as_uint(sc) >> 16;
+    s -= sc;
+  }
+#pragma unroll
+  for (int e = 0; e < 4; ++e) {
+    ev[e] = h[2 * e] | h[2 * e + 1] << 16;
+    od[e] = h[8 + 2 * e] | h[8 + 2 * e + 1] << 16;
+  }
+}
+
+// Loads the 16 columns c0 .. c0 + 15 of one token row (zeros when c0 >= n;
+// n is a multiple of 64, so a group is whole or absent).
+__device__ __forceinline__ void load_x16(const uint16_t *__restrict__ row, int64_t c0, int64_t n, float (&x)[16]) {
+  if (c0 < n) {
+    const uint4 *src = reinterpret_cast<const uint4 *>(row + c0);
     const uint4 u0 = src[0], u1 = src[1];
     const uint32_t w[8] = {u0.x, u0.y, u0.z, u0.w, u1.x, u1.y, u1.z, u1.w};
 #pragma unroll
@@ -65,37 +95,26 @@ __global__ __launch_bounds__(256) void k_packed_prep(const uint16_t *__restrict_
 #pragma unroll
     for (int e = 0; e < 16; ++e) x[e] = 0.0f;
   }
-  // X'[g D + k] = sum_j X[g D + j] A[j, k];  s += sum_j X[g D + j] b[j]
-  float xp[16], s = 0.0f;
-#pragma unroll
-  for (int g = 0; g < 16 / D; ++g)
-#pragma unroll
-    for (int k = 0; k < D; ++k) {
-      float v = 0.0f;
-#pragma unroll
-      for (int j = 0; j < D; ++j) v = fmaf(x[g * D + j], A[j * D + k], v);
-      xp[g * D + k] = v;
-      s = fmaf(x[g * D + k], b[k], s);
-    }
+}
+
+template <int D>
+__global__ __launch_bounds__(256) void k_packed_prep(const uint16_t *__restrict__ X, int Nc, int64_t n, int64_t nP,
+                                                     const float *__restrict__ A, const float *__restrict__ b,
+                                                     uint16_t *__restrict__ xq, float *__restrict__ sp,
+                                                     int *__restrict__ counters, int ncounters) {
+  const int tid = threadIdx.x, t = blockIdx.y;
+  const int64_t c0 = (int64_t)blockIdx.x * kPkChunk + 16 * tid;
+  if (blockIdx.x == 0 && blockIdx.y == 0)
+    for (int i = tid; i < ncounters; i += 256) counters[i] = 0;
+  float x[16];
+  load_x16(X + (int64_t)t * n, t < Nc ? c0 : n, n, x);  // absent tokens: zeros
+  float s = 0.0f;
   if (c0 < nP) {
-    // X'' of the two operands (codes, scale 2^(7 - p)) in element order; the
-    // offset sum_c X''[c] is taken off s
-    constexpr int kCode[16] = {0, 8, 1, 9, 2, 10, 3, 11, 4, 12, 5, 13, 6, 14, 7, 15};
-    constexpr float kScale[16] = {128.f, 128.f, 32.f, 32.f, 8.f, 8.f, 128.f, 128.f,
-                                  32.f, 32.f, 8.f, 8.f, 128.f, 128.f, 32.f, 32.f};
-    uint32_t h[16];
-#pragma unroll
-    for (int e = 0; e < 16; ++e) {
-      h[e] = f32_to_bf16(xp[kCode[e]]);                           // X' rounded to bf16 ..
-      const float sc = __uint_as_float(h[e] << 16) * kScale[e];   // .. then scaled exactly
-      h[e] = __float_as_uint(sc) >> 16;
-      s -= sc;
-    }
-    const uint4 ev = make_uint4(h[0] | h[1] << 16, h[2] | h[3] << 16, h[4] | h[5] << 16, h[6] | h[7] << 16);
-    const uint4 od = make_uint4(h[8] | h[9] << 16, h[10] | h[11] << 16, h[12] | h[13] << 16, h[14] | h[15] << 16);
+    u32x4 ev, od;
+    xpp_group<D>(x, A, b, s, ev, od);
     const int64_t j = c0 / kPkStep;
     const int qq = (int)((c0 / 64) % 4), kk = (int)((c0 / 16) % 4);
-    uint4 *dst = reinterpret_cast<uint4 *>(xq);
+    u32x4 *dst = reinterpret_cast<u32x4 *>(xq);
     dst[(j * 8 + 2 * kk) * 64 + qq * 16 + t] = ev;
     dst[(j * 8 + 2 * kk + 1) * 64 + qq * 16 + t] = od;
   }
@@ -121,17 +140,21 @@ __global__ __launch_bounds__(256) void k_packed_prep(const uint16_t *__restrict_
 // dword kk of its 16 bytes (columns 256 j + 64 q + 16 kk .. + 15, in the order
 // above) and the matching eight X'' values, fragment (j, i) of the prepass.
 //
-// kXL (few tokens): the X'' rows of the Nc tokens for the block's steps are
-// copied once into LDS (dynamic, 512 Nc bytes per step plus a zero chunk) and
-// each step reads its fragments from there, instead of every wave loading
-// eight mostly idle 1 KiB fragments per step from the L2.
-template <bool kXL>
+// kXL (few tokens): the X'' rows of the Nc tokens for the block's steps sit
+// in LDS (dynamic, 512 Nc bytes per step plus a zero chunk) and each step reads
+// its fragments from there, instead of every wave loading eight mostly idle
+// 1 KiB fragments per step from the L2.  kXL = 1 copies them from the prepass
+// output; kXL = 2 (one block per row tile, KS = 1) computes them from X in the
+// block, with the partial sums of s, so that no prepass launch is needed.
+template <int kXL, int D>
 __global__ __launch_bounds__(256) void k_packed_gemv(const uint8_t *__restrict__ packed, int64_t m, int64_t n, int KT,
                                                      int KS, int spb, const uint16_t *__restrict__ xq, int64_t nP,
                                                      const float *__restrict__ sp, int nchunks, int Nc,
                                                      float *__restrict__ part, int *__restrict__ counters,
-                                                     void *__restrict__ Y, int y_bf16) {
+                                                     void *__restrict__ Y, int y_bf16, const uint16_t *__restrict__ X,
+                                                     const float *__restrict__ A, const float *__restrict__ b) {
   extern __shared__ u32x4 xl[];
+  __shared__ float s_red[4][16];  // kXL = 2: offsets s per wave and token
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int q = lane >> 4, tl = lane & 15;
   const int rt = (int)blockIdx.x / KS, ks = (int)blockIdx.x % KS;
@@ -147,12 +170,36 @@ __global__ __launch_bounds__(256) void k_packed_gemv(const uint8_t *__restrict__
   for (int rb = 0; rb < 4; ++rb) acc[rb] = floatx4{0.0f, 0.0f, 0.0f, 0.0f};
   u32x4 cw[2][4], xf[2][8];
   const int nch = (j1 - j0) * 32 * Nc;  // kXL: 16-byte chunks in LDS; chunk nch is zero
-  if constexpr (kXL) {
-    // chunk c = ((jj * 8 + i) * 4 + q) * Nc + t  <-  fragment (j0 + jj, i), lane 16 q + t
+  // chunk c = ((jj * 8 + i) * 4 + q) * Nc + t holds fragment (j0 + jj, i), lane 16 q + t
+  if constexpr (kXL == 1) {
     for (int c = tid; c < nch; c += 256) {
       const int t = c % Nc, fq = c / Nc;
       xl[c] = __builtin_amdgcn_raw_buffer_load_b128(
           rX, (uint32_t)(((j0 * 8 + (fq >> 2)) * 64 + (fq & 3) * 16 + t) * 16), 0, 0);
+    }
+    if (tid == 0) xl[nch] = u32x4{0u, 0u, 0u, 0u};
+    __syncthreads();
+  } else if constexpr (kXL == 2) {
+    // token by token, thread tid takes the 16-column groups g16 = tid + 256 i
+    // of the block's steps (step j0 + g16 / 16, lane group (g16 / 4) % 4,
+    // dword g16 % 4); the offsets s are summed in a fixed order (per thread,
+    // across the wave, then across the four waves in the epilogue), so the
+    // result does not depend on scheduling
+    const int ng = (j1 - j0) * 16;
+    for (int t = 0; t < Nc; ++t) {
+      float s = 0.0f;
+      for (int g16 = tid; g16 < ng; g16 += 256) {
+        float x[16];
+        load_x16(X + (int64_t)t * n, (int64_t)j0 * kPkStep + 16 * g16, n, x);
+        u32x4 ev, od;
+        xpp_group<D>(x, A, b, s, ev, od);
+        const int jj = g16 >> 4, qq = (g16 >> 2) & 3, kk = g16 & 3;
+        xl[((jj * 8 + 2 * kk) * 4 + qq) * Nc + t] = ev;
+        xl[((jj * 8 + 2 * kk + 1) * 4 + qq) * Nc + t] = od;
+      }
+#pragma unroll
+      for (int o = 32; o > 0; o >>= 1) s += __shfl_xor(s, o);
+      if (lane == 0) s_red[wave][t] = s;
     }
     if (tid == 0) xl[nch] = u32x4{0u, 0u, 0u, 0u};
     __syncthreads();
@@ -164,7 +211,7 @@ __global__ __launch_bounds__(256) void k_packed_gemv(const uint8_t *__restrict__
     for (int rb = 0; rb < 4; ++rb)
       cw[buf][rb] = __builtin_amdgcn_raw_buffer_load_b128(
           rP, live ? (uint32_t)((16 * rb + tl) * ldb + 64 * j + 16 * q) : kOffNone, 0, 0);
-    if constexpr (kXL) {
+    if constexpr (kXL > 0) {
       const int base = xlive ? ((j - j0) * 32 + q) * Nc + tl : nch;
       const int stride = xlive ? 4 * Nc : 0;
 #pragma unroll
@@ -270,7 +317,9 @@ __global__ __launch_bounds__(256) void k_packed_gemv(const uint8_t *__restrict__
   }
   if (tl >= Nc || row >= m) return;
   float s = 0.0f;
-  for (int c = 0; c < nchunks; ++c) s += sp[c * 16 + tl];
+  if constexpr (kXL == 2) s = (s_red[0][tl] + s_red[1][tl]) + (s_red[2][tl] + s_red[3][tl]);
+  else
+    for (int c = 0; c < nchunks; ++c) s += sp[c * 16 + tl];
   const int64_t o = (int64_t)tl * m + row;
   if (y_bf16) {
     uint2 w;
@@ -312,19 +361,46 @@ hipError_t launch_packed_prep(const uint16_t *X, int Nc, int64_t m, int64_t n, i
   return hipGetLastError();
 }
 
+// X'' of a block's steps in LDS when it fits in 48 KiB (few tokens) and the
+// block has enough steps to repay the copy and its barrier (on short K ranges
+// the product is latency-bound and the copy only adds to it).
+static bool packed_xl(const PackedPlan &p, int Nc) {
+  return ((size_t)p.spb * 32 * Nc + 1) * 16 <= 48 * 1024 && p.spb >= 24;
+}
+
+bool packed_fused(int64_t m, int64_t n, int Nc) {
+  const PackedPlan p = packed_plan(m, n);
+  return p.KS == 1 && p.KT > 0 && packed_xl(p, Nc);
+}
+
 hipError_t launch_packed_gemv(const uint8_t *packed, int64_t m, int64_t n, const uint16_t *xq, const float *sp,
                               int Nc, float *part, int *counters, void *Y, bool y_bf16, hipStream_t st) {
   const PackedPlan p = packed_plan(m, n);
-  // X'' of the block's steps in LDS when it fits in 48 KiB (few tokens) and
-  // the block has enough steps to repay the copy and its barrier (on short K
-  // ranges the product is latency-bound and the copy only adds to it)
   const size_t xl_bytes = ((size_t)p.spb * 32 * Nc + 1) * 16;
-  if (xl_bytes <= 48 * 1024 && p.spb >= 24)
-    k_packed_gemv<true><<<p.row_tiles * p.KS, 256, xl_bytes, st>>>(packed, m, n, p.KT, p.KS, p.spb, xq, p.nP, sp,
-                                                                   p.nchunks, Nc, part, counters, Y, y_bf16 ? 1 : 0);
+  if (packed_xl(p, Nc))
+    k_packed_gemv<1, 8><<<p.row_tiles * p.KS, 256, xl_bytes, st>>>(
+        packed, m, n, p.KT, p.KS, p.spb, xq, p.nP, sp, p.nchunks, Nc, part, counters, Y, y_bf16 ? 1 : 0, nullptr,
+        nullptr, nullptr);
   else
-    k_packed_gemv<false><<<p.row_tiles * p.KS, 256, 0, st>>>(packed, m, n, p.KT, p.KS, p.spb, xq, p.nP, sp,
-                                                             p.nchunks, Nc, part, counters, Y, y_bf16 ? 1 : 0);
+    k_packed_gemv<0, 8><<<p.row_tiles * p.KS, 256, 0, st>>>(packed, m, n, p.KT, p.KS, p.spb, xq, p.nP, sp,
+                                                            p.nchunks, Nc, part, counters, Y, y_bf16 ? 1 : 0,
+                                                            nullptr, nullptr, nullptr);
+  return hipGetLastError();
+}
+
+hipError_t launch_packed_fused(const uint8_t *packed, int64_t m, int64_t n, const uint16_t *X, int Nc, int d,
+                               const float *A, const float *b, void *Y, bool y_bf16, hipStream_t st) {
+  const PackedPlan p = packed_plan(m, n);
+  if (!(p.KS == 1 && p.KT > 0 && packed_xl(p, Nc))) return hipErrorInvalidValue;
+  const size_t xl_bytes = ((size_t)p.spb * 32 * Nc + 1) * 16;
+  if (d == 8)
+    k_packed_gemv<2, 8><<<p.row_tiles, 256, xl_bytes, st>>>(packed, m, n, p.KT, 1, p.spb, nullptr, p.nP, nullptr,
+                                                            p.nchunks, Nc, nullptr, nullptr, Y, y_bf16 ? 1 : 0, X,
+                                                            A, b);
+  else
+    k_packed_gemv<2, 4><<<p.row_tiles, 256, xl_bytes, st>>>(packed, m, n, p.KT, 1, p.spb, nullptr, p.nP, nullptr,
+                                                            p.nchunks, Nc, nullptr, nullptr, Y, y_bf16 ? 1 : 0, X,
+                                                            A, b);
   return hipGetLastError();
 }
 

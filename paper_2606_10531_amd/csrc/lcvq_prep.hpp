@@ -84,6 +84,12 @@ hipError_t launch_packed_prep(const uint16_t *X, int Nc, int64_t m, int64_t n, i
 // Y (Nc x m, bf16 or fp32) = codes X'^T + s; part holds row_tiles * KS * 16 * 64 fp32 split-K partials
 hipError_t launch_packed_gemv(const uint8_t *packed, int64_t m, int64_t n, const uint16_t *xq, const float *sp,
                               int Nc, float *part, int *counters, void *Y, bool y_bf16, hipStream_t st);
+// Whether the product for Nc tokens runs as one launch that also does the
+// prepass (one block per row tile, few tokens, long rows); then
+// launch_packed_fused replaces launch_packed_prep + launch_packed_gemv.
+bool packed_fused(int64_t m, int64_t n, int Nc);
+hipError_t launch_packed_fused(const uint8_t *packed, int64_t m, int64_t n, const uint16_t *X, int Nc, int d,
+                               const float *A, const float *b, void *Y, bool y_bf16, hipStream_t st);
 
 // LC encode (lcvq_encode.hip): codes (m x n bytes) and / or packed codes of a dense weight
 hipError_t launch_encode(const void *W, bool w_bf16, int64_t m, int64_t n, int d, const float *A, const float *b,
