@@ -300,11 +300,13 @@ def packed_decode(lc, torch, token_counts=(1, 4, 16)):
         pus, qus = 1e3 * pm / max(pc, 1), 1e3 * qm / max(qc, 1)
         nbytes = sum(m * n / 4 + 2 * N * (n + m) for m, n in mats) / len(mats)
         gbps = nbytes / (pus * 1e-6) / 1e9
-        out[f"N{N}"] = {"product_us": round(pus, 2), "prepass_us": round(qus, 2), "call_us": round(call_us, 2),
+        out[f"N{N}"] = {"product_us": round(pus, 2), "prepass_us": round(qus, 2),
+                        "prepass_launches_per_call": round(qc / max(pc, 1), 2), "call_us": round(call_us, 2),
                         "GB/s": round(gbps, 1), "frac_hbm": round(gbps / PEAK_HBM, 3),
                         "bytes_per_call": int(nbytes)}
     out["shapes"] = [[28672, 8192], [8192, 28672]]
-    out["note"] = "GB/s and frac_hbm over the product kernel's average duration; call_us includes the prepass"
+    out["note"] = ("GB/s and frac_hbm over the product kernel's average duration; call_us includes the prepass, "
+                   "which is launched only where the product blocks do not compute X'' themselves")
     del P
     return out
 
