@@ -47,7 +47,7 @@ struct FwdLayout {
   int64_t Np, ldp;
 };
 struct BwdLayout {
-  size_t rs, frag, dyb, xt, dyt, mask, total;
+  size_t rs, frag, xt, dyt, mask, total;
 };
 
 FwdLayout fwd_layout(int64_t N, int64_t m, int64_t n, bool bf16) {
@@ -78,21 +78,21 @@ BwdLayout bwd_layout(int64_t N, int64_t m, int64_t n, bool bf16) {
   BwdLayout L{};
   L.rs = 0;
   if (bf16) {
-    // partial row sums of dY; codes and dY in the input-gradient operand
-    // layouts (K = out-features padded to 128); X' and dY in the token-K
-    // fragment layout (features padded to 256); tokens padded to 256 throughout
+    // partial row sums of dY; codes in the input-gradient operand layout
+    // (K = out-features padded to 128; that product reads dY in place); X' and
+    // dY in the token-K fragment layout (features padded to 256); tokens padded
+    // to 256 throughout
     const size_t Nt = (size_t)lcvq::bwd_tokens(N);
     const size_t rs = up256((size_t)lcvq::rowsum_parts(m) * Nt * 4);
     const size_t frag = (size_t)(lcvq::round_up(n, 256) / 32) * (lcvq::round_up(m, 128) / 64) * 1024;
     L.frag = rs;
-    L.dyb = L.frag + up256(frag);
-    L.xt = L.dyb + up256(Nt * (size_t)lcvq::round_up(m, 128) * 2);
+    L.xt = L.frag + up256(frag);
     L.dyt = L.xt + up256((size_t)lcvq::round_up(n, 256) * Nt * 2);
     // straight-through mask of Z, one bit per element (rows of whole 64-bit words)
     L.mask = L.dyt + up256((size_t)lcvq::round_up(m, 256) * Nt * 2);
     L.total = L.mask + up256((size_t)m * lcvq::mask_words_per_row(n) * 8);
   } else {
-    L.frag = L.dyb = L.xt = L.dyt = L.mask = L.total = up256((size_t)N * 4);
+    L.frag = L.xt = L.dyt = L.mask = L.total = up256((size_t)N * 4);
   }
   return L;
 }
@@ -526,14 +526,14 @@ static lcvq_status_t linear_bwd(int64_t N, int64_t m, int64_t n, int32_t d, int3
   const bool clear_map = want_map && !accumulate;
 
   if (bf16) {
-    // 1. one prepass launch: codes and dY in the input-gradient operand layouts
-    //    (when dX or dA/db are wanted), X' = X blockdiag(A) and dY in the
+    // 1. one prepass launch: codes in the input-gradient operand layout (when
+    //    dX or dA/db are wanted), X' = X blockdiag(A) and dY in the
     //    weight-gradient fragments (when dZ is wanted), and the partial row sums
     //    of dY; its first block clears dA/db when overwriting them
     // 2. dX = (dY codes) A-map + rowsum(dY) b (+ dA, db)    3. dZ = mask * dY^T X'
     const bool run_dx = dX != nullptr || want_map;
     uint32_t *frag = (uint32_t *)(ws + L.frag);
-    uint16_t *dyb = (uint16_t *)(ws + L.dyb), *xt = (uint16_t *)(ws + L.xt), *dyt = (uint16_t *)(ws + L.dyt);
+    uint16_t *xt = (uint16_t *)(ws + L.xt), *dyt = (uint16_t *)(ws + L.dyt);
     // the straight-through mask as a bitmap (the differentiable estimator reads Z itself)
     uint64_t *maskbits = dZ != nullptr && !est.dge ? (uint64_t *)(ws + L.mask) : nullptr;
     {
@@ -541,7 +541,7 @@ static lcvq_status_t linear_bwd(int64_t N, int64_t m, int64_t n, int32_t d, int3
       Timed tm(LCVQ_K_BWD_PREP, st);
       e = tm.done(lcvq::launch_bwd_prep_bf16((const uint16_t *)Z, m, n, qz, run_dx || maskbits ? frag : nullptr,
                                              (const uint16_t *)X, (const uint16_t *)dY, A, d, N,
-                                             run_dx ? dyb : nullptr, dZ != nullptr ? xt : nullptr,
+                                             dZ != nullptr ? xt : nullptr,
                                              dZ != nullptr ? dyt : nullptr, rs, maskbits, mask_mode,
                                              clear_map ? dA : nullptr, clear_map ? d * d : 0,
                                              clear_map ? db : nullptr, clear_map ? d : 0, st));
@@ -549,7 +549,7 @@ static lcvq_status_t linear_bwd(int64_t N, int64_t m, int64_t n, int32_t d, int3
     }
     if (run_dx) {
       Timed tm(LCVQ_K_DX, st);
-      e = tm.done(lcvq::launch_dx_bf16(frag, dyb, rs, A, b, d, (uint16_t *)dX, (const uint16_t *)X, dA, db, N, m,
+      e = tm.done(lcvq::launch_dx_bf16(frag, (const uint16_t *)dY, rs, A, b, d, (uint16_t *)dX, (const uint16_t *)X, dA, db, N, m,
                                        n, st));
       if (e != hipSuccess) return hip_fail(e, "input-gradient launch");
     }

@@ -104,11 +104,7 @@ __device__ __forceinline__ uint32_t frag_dword_index(int mb, int kb, int KB, int
 // holds four 1 KiB fragments, fragment 2 th + kk2 for tokens 32 tb + 16 th +
 // 0..15 and K 64 kb + 32 kk2 + 0..31, in which lane L owns the 16 bytes of token
 // 32 tb + 16 th + L % 16, K = 64 kb + 32 kk2 + 8 (L / 16) + 0..7.  Blocks are
-// token-block-major; the element index of (t, k) with KB K steps is returned.
-__host__ __device__ __forceinline__ int64_t bfrag_index(int64_t t, int64_t k, int64_t KB) {
-  return (((t >> 5) * KB + (k >> 6)) * 4 + 2 * ((t >> 4) & 1) + ((k >> 5) & 1)) * 512 +
-         ((t & 15) + 16 * ((k >> 3) & 3)) * 8 + (k & 7);
-}
+// token-block-major.
 
 // Token-K operand fragments of the weight-gradient product (features f on the
 // MFMA M or N axis, tokens t on K): block (f / 32, t / 64) holds four 1 KiB

@@ -112,10 +112,13 @@ __device__ __forceinline__ uint32_t as_u(float f) { return __float_as_uint(f); }
 // No LDS: wave w of a block owns the 256 weight-side rows x 64 tokens
 // [64 w, 64 w + 64) of the block tile and streams both operands straight into
 // registers: the codes of the block's eight 32-row slabs (operand layout; the
-// four waves share them through the L1) and its own activations in the
-// matrix-core B layout, as the prepasses write them (forward: X' from the
-// activation transform; input gradient: the copy of dY made by the backward
-// prepass).  K is padded to an even number of 64-wide steps.
+// four waves share them through the L1) and its own activations: for the
+// forward X' in the matrix-core B layout, as the activation transform writes
+// it; for the input gradient dY itself, row-major, read in place (a lane's B
+// operand, eight consecutive out-features of one token, is 16 contiguous bytes
+// of dY, and the 16 token rows a load touches are each read in whole 128-byte
+// lines by its two K halves).  K is padded to an even number of 64-wide steps;
+// out-features >= ldB read as zero.
 // ============================================================================
 
 // Input-gradient mode also forms the map gradients from the same accumulator
@@ -123,9 +126,9 @@ __device__ __forceinline__ uint32_t as_u(float f) { return __float_as_uint(f); }
 // db[j] = sum_{t,g} X[t, g*D + j] rs[t] (the chain rule through X' = X blockdiag(A)
 // and s = X b~), reduced lanes -> wave -> block and added with one atomic per
 // block per entry.  X is N x Mvalid row-major; dA == nullptr skips this.
-template <int kMode, int D>  // kMode 0: forward (B = X' fragments), 1: input gradient (B = dY fragments)
+template <int kMode, int D>  // kMode 0: forward (B = X' fragments), 1: input gradient (B = dY, row length ldB)
 __global__ __launch_bounds__(256, 1) void k_gemm_codes(
-    const uint32_t *__restrict__ frag, int KB, const uint16_t *__restrict__ Bsrc,
+    const uint32_t *__restrict__ frag, int KB, const uint16_t *__restrict__ Bsrc, int64_t ldB,
     int tiles_m, int tiles_n, const float *__restrict__ vecT, int vparts,
     int64_t vstride, const float *__restrict__ A, const float *__restrict__ bvec, uint16_t *__restrict__ out,
     int64_t ldo, int64_t Mvalid, int64_t Tvalid, const uint16_t *__restrict__ X,
@@ -139,14 +142,24 @@ __global__ __launch_bounds__(256, 1) void k_gemm_codes(
 
   // codes: slabs tm * 8 + mi, 1 KiB per (slab, step), lane owns 16 bytes
   const __amdgpu_buffer_rsrc_t rsA = make_rsrc(frag + (size_t)(tm * 8) * KB * 256, (int64_t)8 * KB * 1024);
-  // B operand of tokens tw .. tw + 63 (X' for the forward, dY for the input
-  // gradient), both in the B-operand fragment layout with KB K steps
-  const __amdgpu_buffer_rsrc_t rsB = make_rsrc(Bsrc + (tw >> 5) * (int64_t)KB * 2048, (int64_t)2 * KB * 4096);
+  // B operand of tokens tw .. tw + 63: X' in the B-operand fragment layout
+  // with KB K steps (forward), or rows tw .. tw + 63 of dY (input gradient;
+  // rows past Tvalid lie beyond the buffer and read as zero).  Fragment
+  // 2 th + kk2 of 32-token block ni holds tokens 32 ni + 16 th + L % 16 and
+  // K = 32 kk2 + 8 (L / 16) + 0..7 of each step.
+  const __amdgpu_buffer_rsrc_t rsB =
+      kMode == 0 ? make_rsrc(Bsrc + (tw >> 5) * (int64_t)KB * 2048, (int64_t)2 * KB * 4096)
+                 : make_rsrc(Bsrc + tw * ldB, (Tvalid - tw < 64 ? Tvalid - tw : 64) * ldB * 2);
   uint32_t boff[2][4];  // per (32-token block, fragment): byte offset of this lane's 16 bytes at step 0
 #pragma unroll
   for (int ni = 0; ni < 2; ++ni)
 #pragma unroll
-    for (int fr = 0; fr < 4; ++fr) boff[ni][fr] = (uint32_t)((ni * KB * 4 + fr) * 1024 + lane * 16);
+    for (int fr = 0; fr < 4; ++fr)
+      boff[ni][fr] = kMode == 0 ? (uint32_t)((ni * KB * 4 + fr) * 1024 + lane * 16)
+                                : (uint32_t)(((ni * 32 + (fr >> 1) * 16 + c16) * ldB + (fr & 1) * 32 + 8 * q) * 2);
+  // bytes per K step; input gradient: the last out-feature chunk a lane may read
+  const uint32_t bstep = kMode == 0 ? 4096u : 128u;
+  const int kB_last = kMode == 0 ? KB * 64 : (int)ldB - 8;
 
   floatx4 acc[16][4];  // [row block 2 mi + rb][16-token block tb]
 #pragma unroll
@@ -167,9 +180,12 @@ __global__ __launch_bounds__(256, 1) void k_gemm_codes(
 #pragma unroll
     for (int ni = 0; ni < 2; ++ni)
 #pragma unroll
-      for (int fr = 0; fr < 4; ++fr)
+      for (int fr = 0; fr < 4; ++fr) {
+        // input gradient: K chunks at or past ldB (the last, padded steps) are not read
+        const bool kin = kMode == 0 || kb * 64 + (fr & 1) * 32 + 8 * q <= kB_last;
         cb[buf][ni][fr] = __builtin_amdgcn_raw_buffer_load_b128(
-            rsB, live ? (int)(boff[ni][fr] + (uint32_t)kb * 4096u) : (int)kOffNone, 0, 0);
+            rsB, live && kin ? (int)(boff[ni][fr] + (uint32_t)kb * bstep) : (int)kOffNone, 0, 0);
+      }
   };
   // 32 A operands per step (sub-step kk2, row block 2 mi + rb), each used by
   // four MFMAs; the conversion of the next one is placed between the second
@@ -573,12 +589,12 @@ hipError_t launch_fwd_bf16(const uint32_t *frag, const uint16_t *Xp, int64_t ldp
   const int tiles_m = (int)ceil_div(m, kTile), tiles_n = (int)ceil_div(N, kTile);
   const int KB = (int)(ldp / kKStep);  // even: ldp is a multiple of 128
   const int64_t Np = (int64_t)tiles_n * kTile;
-  k_gemm_codes<0, 8><<<tiles_m * tiles_n, 256, 0, st>>>(frag, KB, Xp, tiles_m, tiles_n, s,
+  k_gemm_codes<0, 8><<<tiles_m * tiles_n, 256, 0, st>>>(frag, KB, Xp, 0, tiles_m, tiles_n, s,
                                                         act_chunks(ldp), Np, nullptr, nullptr, Y, m, m, N, nullptr, nullptr, nullptr);
   return hipGetLastError();
 }
 
-hipError_t launch_dx_bf16(const uint32_t *frag, const uint16_t *dyb, const float *rsp, const float *A, const float *b,
+hipError_t launch_dx_bf16(const uint32_t *frag, const uint16_t *dY, const float *rsp, const float *A, const float *b,
                           int d, uint16_t *dX, const uint16_t *X, float *dA, float *db, int64_t N, int64_t m, int64_t n,
                           hipStream_t st) {
   const int parts = rowsum_parts(m);
@@ -587,10 +603,10 @@ hipError_t launch_dx_bf16(const uint32_t *frag, const uint16_t *dyb, const float
   const int KB = (int)(round_up(m, 128) / kKStep);  // even, matches the operand layout
   // dX == nullptr: the product still runs for dA/db; its stores are dropped.
   if (d == 8)
-    k_gemm_codes<1, 8><<<tiles_m * tiles_n, 256, 0, st>>>(frag, KB, dyb, tiles_m, tiles_n, rsp,
+    k_gemm_codes<1, 8><<<tiles_m * tiles_n, 256, 0, st>>>(frag, KB, dY, m, tiles_m, tiles_n, rsp,
                                                           parts, Nt, A, b, dX, n, n, N, X, dA, db);
   else
-    k_gemm_codes<1, 4><<<tiles_m * tiles_n, 256, 0, st>>>(frag, KB, dyb, tiles_m, tiles_n, rsp,
+    k_gemm_codes<1, 4><<<tiles_m * tiles_n, 256, 0, st>>>(frag, KB, dY, m, tiles_m, tiles_n, rsp,
                                                           parts, Nt, A, b, dX, n, n, N, X, dA, db);
   return hipGetLastError();
 }

@@ -538,13 +538,12 @@ __device__ __forceinline__ void x_block(int bt, int fx4, const uint16_t *__restr
 }
 
 // dY part (bt, p): sub-tiles [sf0, sf1) of 64 out-features for tokens
-// 64 bt .. 64 bt + 63, written transposed into dyt (when set), copied into the
-// B-operand layout of the input-gradient product with KBm 64-wide K steps (dyb,
-// when set; features < 64 KBm) and summed per row into rsum[0..1] (rows tid / 8 and tid / 8 + 32, totals in threads with
+// 64 bt .. 64 bt + 63, written transposed into dyt (when set) and summed per
+// row into rsum[0..1] (rows tid / 8 and tid / 8 + 32, totals in threads with
 // tid % 8 == 0).  Sub-tiles are loaded four at a time.
 __device__ __forceinline__ void dy_part(int bt, int sf0, int sf1, const uint16_t *__restrict__ dY, int64_t m,
-                                        int64_t N, int KBt, uint16_t *__restrict__ dyt, uint16_t *__restrict__ dyb,
-                                        int KBm, uint16_t (&tile)[64][64 + 8], float (&rsum)[2]) {
+                                        int64_t N, int KBt, uint16_t *__restrict__ dyt,
+                                        uint16_t (&tile)[64][64 + 8], float (&rsum)[2]) {
   const int tid = threadIdx.x;
   for (int base = sf0; base < sf1; base += 4) {
     u32x4 v[4][2];
@@ -564,10 +563,6 @@ __device__ __forceinline__ void dy_part(int bt, int sf0, int sf1, const uint16_t
         sum += __shfl_xor(sum, 4, 64);
         rsum[i] += sum;
         if (dyt != nullptr) *reinterpret_cast<u32x4 *>(&tile[id >> 3][(id & 7) * 8]) = v[q][i];
-        // the same 8 values are one lane's chunk of the input-gradient B operand
-        const int64_t f = (int64_t)(base + q) * 64 + (id & 7) * 8;
-        if (dyb != nullptr && f < (int64_t)KBm * 64)
-          *reinterpret_cast<u32x4 *>(dyb + bfrag_index((int64_t)bt * 64 + (id >> 3), f, KBm)) = v[q][i];
       }
       if (dyt == nullptr) continue;
       __syncthreads();
@@ -591,7 +586,7 @@ __global__ __launch_bounds__(256) void k_bwd_prep(const uint16_t *__restrict__ Z
                                                    uint32_t *__restrict__ frag, int KBq, int gq, int nq,
                                                    const uint16_t *__restrict__ X, const uint16_t *__restrict__ dY,
                                                    const float *__restrict__ A, int64_t N, int KBt, int nfx4,
-                                                   int nfy, int spf, int nrp, uint16_t *__restrict__ dyb, int KBm,
+                                                   int nfy, int spf, int nrp,
                                                    uint16_t *__restrict__ xt, uint16_t *__restrict__ dyt,
                                                    float *__restrict__ rsp, uint64_t *__restrict__ maskbits,
                                                    int64_t ldm8, int mask_mode,
@@ -607,7 +602,7 @@ __global__ __launch_bounds__(256) void k_bwd_prep(const uint16_t *__restrict__ Z
   float rsum[2] = {0.0f, 0.0f};
   if (id < ndy) {
     const int bt = id % KBt, p = id / KBt;
-    dy_part(bt, p * spf, min((p + 1) * spf, nfy), dY, m, N, KBt, dyt, dyb, KBm, tile, rsum);
+    dy_part(bt, p * spf, min((p + 1) * spf, nfy), dY, m, N, KBt, dyt, tile, rsum);
     if ((tid & 7) == 0) {
       const int64_t Nt = (int64_t)KBt * 64, t = (int64_t)bt * 64 + (tid >> 3);
       rsp[(int64_t)p * Nt + t] = rsum[0];
@@ -718,7 +713,7 @@ hipError_t launch_dequant(const void *src, int kind, bool z_bf16, int64_t m, int
 namespace lcvq {
 hipError_t launch_bwd_prep_bf16(const uint16_t *Z, int64_t m, int64_t n, const Quantizer &qz, uint32_t *frag,
                                 const uint16_t *X,
-                                const uint16_t *dY, const float *A, int d, int64_t N, uint16_t *dyb, uint16_t *xt,
+                                const uint16_t *dY, const float *A, int d, int64_t N, uint16_t *xt,
                                 uint16_t *dyt, float *rsp, uint64_t *maskbits, int mask_mode, float *za, int nza,
                                 float *zb, int nzb, hipStream_t st) {
   const int64_t ldm8 = mask_words_per_row(n);
@@ -727,16 +722,16 @@ hipError_t launch_bwd_prep_bf16(const uint16_t *Z, int64_t m, int64_t n, const Q
   const int gq = (int)(round_up(n, 256) / 256), KBq = (int)(round_up(m, 128) / 64);
   const int nq = frag != nullptr ? gq * KBq : 0;
   // X' blocks (only when xt is wanted) and dY parts (always: they give the row
-  // sums; their copies are written only where dyt / dyb are set)
+  // sums; the transposed copy is written only where dyt is set)
   const int KBt = (int)(bwd_tokens(N) / 64);
   const int nfx4 = xt != nullptr ? (int)(round_up(n, 256) / 256) : 0;
   const int nfy = (int)(round_up(m, 256) / 64), spf = rowsum_subtiles_per_part(m), nrp = rowsum_parts(m);
   const unsigned grid = (unsigned)(nq + KBt * (nfx4 + nrp));
   if (d == 8)
-    k_bwd_prep<8><<<grid, 256, 0, st>>>(Z, m, n, qz, frag, KBq, gq, nq, X, dY, A, N, KBt, nfx4, nfy, spf, nrp, dyb, KBq,
+    k_bwd_prep<8><<<grid, 256, 0, st>>>(Z, m, n, qz, frag, KBq, gq, nq, X, dY, A, N, KBt, nfx4, nfy, spf, nrp,
                                         xt, dyt, rsp, maskbits, ldm8, mask_mode, za, nza, zb, nzb);
   else
-    k_bwd_prep<4><<<grid, 256, 0, st>>>(Z, m, n, qz, frag, KBq, gq, nq, X, dY, A, N, KBt, nfx4, nfy, spf, nrp, dyb, KBq,
+    k_bwd_prep<4><<<grid, 256, 0, st>>>(Z, m, n, qz, frag, KBq, gq, nq, X, dY, A, N, KBt, nfx4, nfy, spf, nrp,
                                         xt, dyt, rsp, maskbits, ldm8, mask_mode, za, nza, zb, nzb);
   return hipGetLastError();
 }

@@ -47,14 +47,13 @@ inline int rowsum_parts(int64_t m) {
 inline int64_t mask_words_per_row(int64_t n) { return (n + 63) / 64; }
 
 // bf16 backward prepass in one launch: codes of the input-gradient product
-// (frag, optional), dY in that product's B-operand layout (dyb, optional), the
-// weight-gradient operands (xt, dyt; skipped when xt is nullptr), the partial
+// (frag, optional; that product reads dY in place), the weight-gradient operands (xt, dyt; skipped when xt is nullptr), the partial
 // row sums of dY (rsp: rowsum_parts(m) rows of bwd_tokens(N) floats) and the
 // mask bitmap of the straight-through estimator (maskbits, optional; written by
 // the quantise blocks, so only together with frag)
 hipError_t launch_bwd_prep_bf16(const uint16_t *Z, int64_t m, int64_t n, const Quantizer &qz, uint32_t *frag,
                                 const uint16_t *X,
-                                const uint16_t *dY, const float *A, int d, int64_t N, uint16_t *dyb, uint16_t *xt,
+                                const uint16_t *dY, const float *A, int d, int64_t N, uint16_t *xt,
                                 uint16_t *dyt, float *rsp, uint64_t *maskbits, int mask_mode, float *za, int nza,
                                 float *zb, int nzb, hipStream_t st);
 hipError_t launch_act_transform(const void *X, bool bf16, int64_t N, int64_t Np, int64_t n, int d,
@@ -103,7 +102,7 @@ hipError_t launch_adamw(float *theta, const void *grad, bool grad_bf16, float *m
 // bf16 matrix-core products (lcvq_gemm.hip)
 hipError_t launch_fwd_bf16(const uint32_t *frag, const uint16_t *Xp, int64_t ldp, const float *s,
                            uint16_t *Y, int64_t N, int64_t m, int64_t n, hipStream_t st);
-hipError_t launch_dx_bf16(const uint32_t *frag, const uint16_t *dyb, const float *rsp, const float *A, const float *b,
+hipError_t launch_dx_bf16(const uint32_t *frag, const uint16_t *dY, const float *rsp, const float *A, const float *b,
                           int d, uint16_t *dX, const uint16_t *X, float *dA, float *db, int64_t N, int64_t m, int64_t n,
                           hipStream_t st);
 // maskbits: the straight-through mask; or, with est.dge set, nullptr and the
