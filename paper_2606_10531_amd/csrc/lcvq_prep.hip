@@ -71,14 +71,16 @@ __device__ __forceinline__ float block_sum256(float v, float *red /* >= 4 floats
 // (rows r), tile columns 4 bq .. 4 bq + 3 (columns c; those at or past gx are
 // skipped).  kTrans = false: the operand's M axis is r and its K axis c
 // (forward product); kTrans = true: M is c and K is r (input-gradient
-// product).  Elements beyond Z hold code 0.  All loads of the four tiles are
+// product).  Elements beyond Z are quantised from 0 (their products meet zero
+// operands or are not stored).  All loads of the four tiles are
 // issued before the first is used.  With `packed`, the forward also writes the
-// 2-bit codes.
+// 2-bit codes.  The forward stores each thread's eight codes as one operand
+// dword; the transposed layout goes through the LDS tiles `codes`.
 typedef uint8_t CodeTile[64][64 + 8];  // rows of 72 bytes keep 8-byte stores aligned
 template <bool kTrans>
 __device__ __forceinline__ void quant_block(int bq, int by, int gx, const uint16_t *__restrict__ Z, int64_t m,
                                             int64_t n, const Quantizer &qz, uint32_t *__restrict__ frag, int KB,
-                                            uint8_t *__restrict__ packed, CodeTile (&codes)[4],
+                                            uint8_t *__restrict__ packed, CodeTile *codes,
                                             uint64_t *__restrict__ maskbits = nullptr, int64_t ldm8 = 0,
                                             int mask_mode = 0) {
   const int tid = threadIdx.x;
@@ -106,7 +108,20 @@ __device__ __forceinline__ void quant_block(int bq, int by, int gx, const uint16
         hi |= (quant_code(code_value(bf16_lo(v[q][i][2 + e]), qz)) |
                (quant_code(code_value(bf16_hi(v[q][i][2 + e]), qz)) << 8)) << (16 * e);
       }
-      *reinterpret_cast<uint2 *>(&codes[q][rr][cc]) = make_uint2(lo, hi);
+      if constexpr (kTrans) {
+        *reinterpret_cast<uint2 *>(&codes[q][rr][cc]) = make_uint2(lo, hi);
+      } else if (4 * bq + q < gx) {
+        // K = columns: the eight codes are one operand dword, nibble i = column
+        // cc + i, stored straight from here.  Row rr of the tile is slab rr / 32,
+        // MFMA row m with slab_row(m) = rr % 32, i.e. lane 16 ((cc / 8) % 4) + m % 16
+        // and dword 2 (m / 16) + cc / 32.
+        const int s = rr & 31, mrow = 16 * ((s >> 2) & 1) + 4 * (s >> 3) + (s & 3);
+        const uint32_t w = (lo & 0xfu) | ((lo >> 4) & 0xf0u) | ((lo >> 8) & 0xf00u) | ((lo >> 12) & 0xf000u) |
+                           ((hi & 0xfu) << 16) | ((hi << 12) & 0xf00000u) | ((hi << 8) & 0xf000000u) |
+                           ((hi << 4) & 0xf0000000u);
+        frag[frag_dword_index(by * 2 + (rr >> 5), 4 * bq + q, KB, 16 * ((cc >> 3) & 3) + (mrow & 15),
+                              2 * (mrow >> 4) + (cc >> 5))] = w;
+      }
       if (kTrans && maskbits != nullptr) {
         // straight-through mask of these 8 latents -> byte (cc / 8) of the
         // row's 64-bit word; threads cc / 8 = 0 and 4 store the two halves
@@ -144,6 +159,7 @@ __device__ __forceinline__ void quant_block(int bq, int by, int gx, const uint16
         }
       }
     }
+  if constexpr (!kTrans) return;  // the operand dwords are stored above
   __syncthreads();
 #pragma unroll
   for (int q = 0; q < 4; ++q) {
@@ -153,20 +169,11 @@ __device__ __forceinline__ void quant_block(int bq, int by, int gx, const uint16
     for (int i = 0; i < 2; ++i) {
       const int id = tid + 256 * i, slab = id >> 8, lane = (id >> 2) & 63, dw = id & 3;
       const int mloc = slab * 32 + slab_row(16 * (dw >> 1) + (lane & 15)), kloc = 32 * (dw & 1) + 8 * (lane >> 4);
+      // K = rows: the eight codes of a dword are a column of the tile
       uint32_t w = 0;
-      if constexpr (kTrans) {
 #pragma unroll
-        for (int j = 0; j < 8; ++j) w |= (uint32_t)codes[q][kloc + j][mloc] << (4 * j);
-      } else {
-        // eight consecutive codes (bytes, each <= 3) -> eight nibbles
-        const uint2 c8 = *reinterpret_cast<const uint2 *>(&codes[q][mloc][kloc]);
-        w = (c8.x & 0xfu) | ((c8.x >> 4) & 0xf0u) | ((c8.x >> 8) & 0xf00u) | ((c8.x >> 12) & 0xf000u) |
-            ((c8.y & 0xfu) << 16) | ((c8.y << 12) & 0xf00000u) | ((c8.y << 8) & 0xf000000u) |
-            ((c8.y << 4) & 0xf0000000u);
-      }
-      const int mb = (kTrans ? bx : by) * 2 + slab;
-      const int kb = kTrans ? by : bx;
-      frag[frag_dword_index(mb, kb, KB, lane, dw)] = w;
+      for (int j = 0; j < 8; ++j) w |= (uint32_t)codes[q][kloc + j][mloc] << (4 * j);
+      frag[frag_dword_index(bx * 2 + slab, by, KB, lane, dw)] = w;
     }
   }
 }
@@ -310,11 +317,10 @@ __global__ __launch_bounds__(256) void k_fwd_prep(const uint16_t *__restrict__ Z
                                                    const float *__restrict__ A, const float *__restrict__ b,
                                                    uint16_t *__restrict__ Xp, int KB, int spc, int64_t Np,
                                                    float *__restrict__ sp) {
-  __shared__ CodeTile codes[4];
   __shared__ float red[4][32];
   const int id = blockIdx.x;
   if (id < nq) {
-    quant_block<false>(id % gq, id / gq, KB, Z, m, n, qz, frag, KB, packed, codes);
+    quant_block<false>(id % gq, id / gq, KB, Z, m, n, qz, frag, KB, packed, nullptr);
   } else {
     const int j = id - nq, ntb = (int)(Np / 32);
     act_block<D>(j % ntb, j / ntb, X, N, n, A, b, Xp, KB, spc, Np, sp, red);
