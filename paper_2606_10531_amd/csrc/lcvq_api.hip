@@ -530,7 +530,9 @@ static lcvq_status_t linear_bwd(int64_t N, int64_t m, int64_t n, int32_t d, int3
     //    dX or dA/db are wanted), X' = X blockdiag(A) and dY in the
     //    weight-gradient fragments (when dZ is wanted), and the partial row sums
     //    of dY; its first block clears dA/db when overwriting them
-    // 2. dX = (dY codes) A-map + rowsum(dY) b (+ dA, db)    3. dZ = mask * dY^T X'
+    // 2. dZ = mask * dY^T X'    3. dX = (dY codes) A-map + rowsum(dY) b (+ dA, db)
+    //    (the two products are independent; in this order the step measured
+    //    slightly shorter)
     const bool run_dx = dX != nullptr || want_map;
     uint32_t *frag = (uint32_t *)(ws + L.frag);
     uint16_t *xt = (uint16_t *)(ws + L.xt), *dyt = (uint16_t *)(ws + L.dyt);
@@ -547,17 +549,17 @@ static lcvq_status_t linear_bwd(int64_t N, int64_t m, int64_t n, int32_t d, int3
                                              clear_map ? db : nullptr, clear_map ? d : 0, st));
       if (e != hipSuccess) return hip_fail(e, "backward prepass launch");
     }
-    if (run_dx) {
-      Timed tm(LCVQ_K_DX, st);
-      e = tm.done(lcvq::launch_dx_bf16(frag, (const uint16_t *)dY, rs, A, b, d, (uint16_t *)dX, (const uint16_t *)X, dA, db, N, m,
-                                       n, st));
-      if (e != hipSuccess) return hip_fail(e, "input-gradient launch");
-    }
     if (dZ != nullptr) {
       Timed tm(LCVQ_K_DW, st);
       e = tm.done(lcvq::launch_dw_bf16(xt, dyt, maskbits, (const uint16_t *)Z, qz, mask_mode, est, accumulate, dZ,
                                        dz_dtype == LCVQ_BF16, N, m, n, st));
       if (e != hipSuccess) return hip_fail(e, "weight-gradient launch");
+    }
+    if (run_dx) {
+      Timed tm(LCVQ_K_DX, st);
+      e = tm.done(lcvq::launch_dx_bf16(frag, (const uint16_t *)dY, rs, A, b, d, (uint16_t *)dX, (const uint16_t *)X, dA, db, N, m,
+                                       n, st));
+      if (e != hipSuccess) return hip_fail(e, "input-gradient launch");
     }
     return ok();
   }
