@@ -9,8 +9,9 @@
 // weight-side indices of one token (or out-feature), i.e. whole groups.
 //
 //   forward : D[r, t] = sum_c code[r, c] X'[t, c]          Y[t, r] = D + s[t]
-//   input   : D[c, t] = sum_r code[r, c] dY[t, r]          dX[t, c] = (D-group) A^T + rs[t] b
-//   weight  : D[c, r] = sum_t X[t, c] dY[t, r]  (= dW[r,c]) dZ = mask * (dW-group) A, dA, db
+//   input   : D[c, t] = sum_r code[r, c] dY[t, r]          dX[t, c] = (D-group) A^T + rs[t] b,
+//                                                           dA, db from D and X
+//   weight  : D[c, r] = sum_t X'[t, c] dY[t, r]             dZ[r, c] = mask * D  (D = dW blockdiag(A))
 //
 // Codes reach the matrix cores exactly: the operand layout holds them as 4-bit
 // nibbles and the fp4 -> bf16 converter turns them into bf16 values 0..3 in
