@@ -311,6 +311,52 @@ def packed_decode(lc, torch, token_counts=(1, 4, 16)):
     return out
 
 
+def step_distribution(torch, step, K):
+    """Per-step times of K more steps, each between its own pair of events
+    (reported beside the K-step mean, which comes from a run without them)."""
+    evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(K)]
+    torch.cuda.synchronize()
+    for s, e in evs:
+        s.record()
+        step()
+        e.record()
+    torch.cuda.synchronize()
+    t = sorted(s.elapsed_time(e) for s, e in evs)
+    return {"median_ms": round(t[len(t) // 2], 4), "min_ms": round(t[0], 4), "max_ms": round(t[-1], 4), "steps": K}
+
+
+def sample_sclk(torch, step, seconds=20.0):
+    """The shader clock reported by rocm-smi while steps keep the GPU busy
+    (sampled once, from a helper thread; None where the tool is unavailable)."""
+    import re
+    import shutil
+    import subprocess
+    import threading
+    import time
+    tool = shutil.which("rocm-smi") or ("/opt/rocm/bin/rocm-smi" if os.path.exists("/opt/rocm/bin/rocm-smi") else None)
+    if tool is None:
+        return None
+    out = {}
+
+    def probe():
+        time.sleep(0.2)
+        try:
+            out["text"] = subprocess.run([tool, "--showclocks"], capture_output=True, text=True, timeout=15).stdout
+        except Exception as ex:  # noqa: BLE001 -- reported, not raised
+            out["error"] = str(ex)
+
+    th = threading.Thread(target=probe)
+    th.start()
+    t0 = time.time()
+    while th.is_alive() and time.time() - t0 < seconds:
+        for _ in range(20):
+            step()
+        torch.cuda.synchronize()
+    th.join()
+    m = re.search(r"sclk[^\n]*?\((\d+)\s*mhz\)", out.get("text", ""), re.IGNORECASE)
+    return {"sclk_mhz": int(m.group(1)) if m else None, "source": "rocm-smi --showclocks during steps"}
+
+
 def library_gemm(torch, N, m, n):
     """Context: one plain bf16 product of the same shape (Y = X W^T, N(0,1) data)
     through torch.matmul, i.e. the vendor GEMM library, with no quantisation."""
@@ -465,6 +511,9 @@ def main():
     lib.lcvq_timer_enable(0)
     dom_us = 1e3 * dom_ms / max(dom_cnt, 1)
 
+    dist = step_distribution(torch, step, args.steps)
+    sclk = sample_sclk(torch, step)
+
     flops = sum(L.flops() for L in layers)
     value = flops / (ms_step * 1e-3) / 1e12
     per_launch_flop = 2.0 * sum(L.N * L.m * L.n for L in layers) / len(layers)
@@ -483,6 +532,8 @@ def main():
                      "traffic": traffic, "avg_launch_us": round(dom_us, 2), "launches": dom_cnt,
                      "flop_per_launch": per_launch_flop, "ms_per_step_with_kernel_events": round(ms_step_ev, 4)},
         "kernels_us_per_step": breakdown,
+        "step_distribution": dist,
+        "gpu_clock": sclk,
     }
     res["dge_step"] = variant_step(lc, torch, layers, args.steps, "step_dge",
                                    "differentiable gradient estimator, k=5, slope cap 3, latent mask")
