@@ -325,25 +325,29 @@ def step_distribution(torch, step, K):
     return {"median_ms": round(t[len(t) // 2], 4), "min_ms": round(t[0], 4), "max_ms": round(t[-1], 4), "steps": K}
 
 
-def sample_sclk(torch, step, seconds=20.0):
-    """The shader clock reported by rocm-smi while steps keep the GPU busy
-    (sampled once, from a helper thread; None where the tool is unavailable)."""
+def sample_sclk(torch, step, seconds=2.0):
+    """The shader clock level the driver marks as current in sysfs
+    (pp_dpm_sclk), read while steps keep the GPU busy; None where no such file
+    is readable.  A plain file read: no helper program is started."""
+    import glob
     import re
-    import shutil
-    import subprocess
     import threading
     import time
-    tool = shutil.which("rocm-smi") or ("/opt/rocm/bin/rocm-smi" if os.path.exists("/opt/rocm/bin/rocm-smi") else None)
-    if tool is None:
+    files = sorted(glob.glob("/sys/class/drm/card*/device/pp_dpm_sclk"))
+    if not files:
         return None
-    out = {}
+    readings = []
 
     def probe():
         time.sleep(0.2)
-        try:
-            out["text"] = subprocess.run([tool, "--showclocks"], capture_output=True, text=True, timeout=15).stdout
-        except Exception as ex:  # noqa: BLE001 -- reported, not raised
-            out["error"] = str(ex)
+        for f in files:
+            try:
+                txt = open(f).read()
+            except OSError:
+                continue
+            m = re.search(r"(\d+)\s*mhz\s*\*", txt, re.IGNORECASE)
+            if m:
+                readings.append(int(m.group(1)))
 
     th = threading.Thread(target=probe)
     th.start()
@@ -353,8 +357,7 @@ def sample_sclk(torch, step, seconds=20.0):
             step()
         torch.cuda.synchronize()
     th.join()
-    m = re.search(r"sclk[^\n]*?\((\d+)\s*mhz\)", out.get("text", ""), re.IGNORECASE)
-    return {"sclk_mhz": int(m.group(1)) if m else None, "source": "rocm-smi --showclocks during steps"}
+    return {"sclk_mhz": max(readings) if readings else None, "source": "sysfs pp_dpm_sclk (current level) during steps"}
 
 
 def library_gemm(torch, N, m, n):
