@@ -401,7 +401,7 @@ def cpu_baseline(layer, max_seconds: float):
         ref = orc.linear_backward(v["Z"], A64, b64, v["X"], v["dY"], d)
         reps += 1
         el = time.perf_counter() - t0
-        if el >= max_seconds or reps >= 5:
+        if el >= max_seconds or reps >= 200:
             break
     per = el / reps
 
