@@ -125,11 +125,12 @@ def test_packed_forward_full_size_sampled(lc, N, m, n):
 
 
 @pytest.mark.parametrize("d", [8, 4])
-@pytest.mark.parametrize("N,m,n", [(3, 12344, 6144), (1, 12352, 6144), (2, 12344, 6208)])
+@pytest.mark.parametrize("N,m,n", [(3, 12344, 6144), (1, 12352, 6144), (2, 12344, 6208), (17, 12352, 6144)])
 def test_packed_forward_few_tokens_long_rows(lc, N, m, n, d):
     """Few tokens with at least 24 product steps per block and one block per
     row tile: each block computes the X'' rows of its steps into LDS itself
-    (no prepass); ragged last row tile (m % 64 != 0), K not a multiple of 256.
+    (no prepass); ragged last row tile (m % 64 != 0), K not a multiple of 256;
+    17 tokens: a 16-token pass with the prepass, then a 1-token pass without.
     Two calls give the same bits (the offsets are summed in a fixed order)."""
     inp, P = _inputs(N, m, n, d, seed=m + N + d)
     got = _run(lc, inp, P, d, "f32", calls=2)
