@@ -15,6 +15,11 @@
 //             on N.  The packed codes (0.25 byte per weight) are the only
 //             large stream; they are read once per pass, 16 bytes per lane.
 //
+// For few tokens and long rows the X' rows of a block's steps are held in LDS;
+// where one block covers a whole row tile (no K split) it also computes them
+// (and its share of s) from X itself, so that pass is a single launch with no
+// prepass.
+//
 // Decoding without conversions: a 32-bit word w holds 16 codes, code i at bits
 // 2i, 2i + 1.  A bf16 whose exponent field reads 1.0 and whose mantissa holds a
 // code c at bits p, p + 1 has the value 1 + c 2^(p - 7); the low and high halves
