@@ -19,8 +19,12 @@
  *
  * Conventions shared by every call
  *  - All tensors are dense, row-major, caller-owned DEVICE pointers; the
- *    library allocates no device memory and keeps no mutable global state
- *    apart from the optional kernel timer below.
+ *    library allocates no device memory.  Its only mutable global state is
+ *    the kernel timer below (instrumentation, off unless enabled): every
+ *    layer call is otherwise a pure function of its arguments.
+ *  - A layer call takes at most 2^22 - 256 = 4194048 tokens (N); more returns
+ *    LCVQ_EUNSUPPORTED (split the tokens over several calls, accumulating the
+ *    weight gradients).
  *  - `stream` is a hipStream_t passed as void* (NULL = the null stream).
  *    Every call only enqueues work on it and returns; device-side results are
  *    visible after the caller synchronises that stream.
@@ -107,15 +111,46 @@ lcvq_status_t lcvq_dequant(int64_t m, int64_t n, int32_t d, int32_t src_kind, in
                            void *W_hat, int32_t out_dtype, void *stream);
 
 /*
+ * lcvq_xavier_quantizer -- the quantiser domain of the Xavier
+ * reparameterisation (Sec. 3.4, eq. xavier_preprocess) for an m x n matrix of
+ * 2-bit codes: a = sqrt(6 / (m + n)), s' = 2a / 3, t = 3/2, and
+ *   *q_scale = 1 / s',  *q_shift = t
+ * (computed in double, each rounded to fp32 once), the values to pass to the
+ * _ex layer calls so that codes = clip(round(W_p / s' + t), 0, 3).  Host-side
+ * only: writes the two floats through host pointers, launches nothing.
+ * m, n > 0 and non-NULL outputs (else LCVQ_EINVAL).
+ */
+lcvq_status_t lcvq_xavier_quantizer(int64_t m, int64_t n, float *q_scale, float *q_shift);
+
+/*
+ * lcvq_xavier_init -- initial proxy weights of the Xavier reparameterisation
+ * (Sec. 3.4, eq. xavier_preprocess): W_p = s' (W_z - t) for codes W_z, with s'
+ * and t as in lcvq_xavier_quantizer, evaluated per element in fp32 as
+ * fma(s', code, -s' t) (s' and -s' t rounded to fp32 once): the result of
+ * lcvq_dequant with A = s' I and b = -s' t, bit for bit.
+ *   codes     m x n bytes (src_kind LCVQ_SRC_CODES_U8; values above 3 are taken
+ *             as 3) or m * n / 4 packed bytes (LCVQ_SRC_PACKED2)
+ *   W_p       m x n of element type out_dtype (F32 or BF16), written
+ * Requires m, n > 0, n % 4 == 0, both pointers 16-byte aligned.  Round trip:
+ * the _ex calls with lcvq_xavier_quantizer's values give these codes back.
+ */
+lcvq_status_t lcvq_xavier_init(int64_t m, int64_t n, int32_t src_kind, const void *codes, void *W_p,
+                               int32_t out_dtype, void *stream);
+
+/*
  * lcvq_encode -- codes of a dense weight W under the map A, b: for group g of
  * row r, v = A^-1 (w_g - b) and code = clip(round(v), 0, 3) (eq. lc_codebook
  * inverted; round() ties to even).  With A = s G, G orthogonal (the form of
  * eq. init_ab), these are the nearest codewords A z + b of eq. vq_assign,
  * because the distance separates over the d coordinates after the rotation; for
- * other invertible A they are the rounding of A^-1 (w_g - b).  A^-1 is formed in
- * fp32 by Gauss-Jordan elimination with partial pivoting and v as an fp32 fma
- * chain, so the codes are a fixed function of the fp32 inputs.  A singular A
- * gives NaN v, i.e. code 0.
+ * other invertible A they are the rounding of A^-1 (w_g - b).  The kernel
+ * evaluates v in fp32 (A^-1 by Gauss-Jordan elimination with partial
+ * pivoting, then a d-term fma chain), so its codes equal those of the exact v
+ * except where the exact v lies within that evaluation's rounding error of a
+ * decision boundary (0.5, 1.5, 2.5).  Non-finite weights follow the written
+ * sum sum_j Ainv[k, j] (w_j - b_j) in IEEE arithmetic (NaN gives code 0).  A
+ * map with a zero pivot (singular) gives NaN v, i.e. code 0; the codes of a
+ * nearly singular map carry no meaning.
  *   W          m x n, element type w_dtype (F32 or BF16), 16-byte aligned
  *   A, b       d x d and d fp32
  *   codes_out  NULL, or m x n bytes (values 0..3), written
@@ -162,8 +197,8 @@ lcvq_status_t lcvq_linear_fwd(int64_t N, int64_t m, int64_t n, int32_t d, int32_
  *   codes = clip(round(Z * q_scale + q_shift), 0, 3).
  * This is the Xavier reparameterisation of Sec. 3.4 (eq. xavier_preprocess):
  * with proxy weights W_p = s' (W_z - t), s' = 2a / 3, t = 3/2,
- * a = sqrt(6 / (m + n)), pass Z = W_p, q_scale = 1 / s', q_shift = t.  Such
- * W_p are made from codes by lcvq_dequant with A = s' I and b = -s' t.
+ * a = sqrt(6 / (m + n)), pass Z = W_p, q_scale = 1 / s', q_shift = t (as
+ * lcvq_xavier_quantizer gives them).  lcvq_xavier_init makes such W_p from codes.
  * q_scale = 1, q_shift = 0 is lcvq_linear_fwd exactly.  q_scale must be finite
  * and nonzero, q_shift finite (else LCVQ_EINVAL).  packed_codes_out receives
  * these codes.  All else as lcvq_linear_fwd.
@@ -281,6 +316,8 @@ lcvq_status_t lcvq_adamw_step(float *theta, const void *grad, int32_t grad_dtype
 
 /*
  * Instrumentation: device time of individual kernels, measured with HIP events.
+ * This timer is the library's one piece of global mutable state (a process-wide
+ * record list guarded by a mutex); it is off until enabled and changes no result.
  * lcvq_timer_enable(mask) makes every later launch of a kernel whose bit
  * (1 << lcvq_kernel_t) is set in `mask`, by any thread, record a start event
  * immediately before and a stop event immediately after it on the launch's

@@ -302,51 +302,33 @@ def linear_forward_packed(packed, A, b, X, d, n):
 
 # ------------------------------------------------------------ LC encode -----
 
-def inverse_f32(A: np.ndarray) -> np.ndarray:
-    """A^-1 in fp32 by Gauss-Jordan elimination with partial pivoting (largest
-    |pivot|, first on ties), every step one fp32 operation: the pivot row is
-    scaled by the rounded reciprocal of the pivot, and each other row r gets
-    row_r = fma(-f, pivot_row, row_r) with f its entry in the pivot column.  The
-    codes of encode() are decided on fp32 values, so the matrix they use is fixed
-    to this sequence."""
-    M = np.asarray(A, dtype=np.float32).copy()
-    d = M.shape[0]
-    I = np.eye(d, dtype=np.float32)
-    for c in range(d):
-        p = c + int(np.argmax(np.abs(M[c:, c])))
-        if p != c:
-            M[[c, p]] = M[[p, c]]
-            I[[c, p]] = I[[p, c]]
-        r = np.float32(1.0) / M[c, c]
-        M[c] = M[c] * r
-        I[c] = I[c] * r
+def encode_values(W: np.ndarray, A: np.ndarray, b: np.ndarray, d: int) -> np.ndarray:
+    """Continuous code vector of every group of a dense weight: the codeword
+    relation w_g = A z + b of eq. lc_codebook (Sec. 2.2) solved for z, i.e.
+        v[r, g*d + k] = sum_j Ainv[k, j] * (W[r, g*d + j] - b[j]),   Ainv = A^-1,
+    in fp64 (A^-1 by LAPACK; the sum written out, so a non-finite weight gives
+    the IEEE result of the written formula).  Raises for a singular A."""
+    W = np.asarray(W, dtype=np.float64)
+    m, n = W.shape
+    assert n % d == 0
+    Ainv = np.linalg.inv(np.asarray(A, dtype=np.float64))
+    T = W.reshape(m, n // d, d) - np.asarray(b, dtype=np.float64)
+    V = np.zeros_like(T)
+    with np.errstate(invalid="ignore"):
         for k in range(d):
-            if k != c:
-                f = M[k, c]
-                M[k] = fma_f32(-f, M[c], M[k]).astype(np.float32)
-                I[k] = fma_f32(-f, I[c], I[k]).astype(np.float32)
-    return I
+            for j in range(d):
+                V[..., k] += Ainv[k, j] * T[..., j]
+    return V.reshape(m, n)
 
 
 def encode(W: np.ndarray, A: np.ndarray, b: np.ndarray, d: int) -> np.ndarray:
-    """Codes of a dense weight (eq. lc_codebook inverted): per group g of row r,
-    v = A^-1 (w_g - b) and code = clip(round(v), 0, 3).  For A = s G with G
-    orthogonal (eq. init_ab) ||w - A z - b|| = s ||v - z|| is separable over the
-    d coordinates, so this is the nearest codeword of eq. vq_assign.
-
-    Arithmetic in fp32 as the kernel does it: t_j = fp32(w_j - b_j), then
-    v_k = fma chain over j = 0..d-1 of Ainv[k, j] t_j starting from 0."""
-    Wf = np.asarray(W, dtype=np.float32)
-    m, n = Wf.shape
-    Ainv = inverse_f32(A)
-    T = (Wf.reshape(m, n // d, d) - np.asarray(b, dtype=np.float32)).astype(np.float32)
-    V = np.zeros((m, n // d, d), dtype=np.float64)
-    for k in range(d):
-        acc = np.zeros((m, n // d), dtype=np.float64)
-        for j in range(d):
-            acc = fma_f32(np.float32(Ainv[k, j]), T[..., j], acc)
-        V[..., k] = acc
-    return quantize(V.reshape(m, n))
+    """Codes of a dense weight under the map A, b: per group, clip(round(v), 0, 3)
+    with v = A^-1 (w_g - b) (encode_values).  For A = s G with G orthogonal (the
+    form of eq. init_ab) the squared distance ||w_g - A z - b||^2 = s^2 ||v - z||^2
+    separates over the d coordinates, so these are the nearest codewords of
+    eq. vq_assign; for other maps they are the rounding of A^-1 (w_g - b).
+    Returns uint8 codes."""
+    return quantize(encode_values(W, A, b, d))
 
 
 # ------------------------------------------------------------ optimiser -----

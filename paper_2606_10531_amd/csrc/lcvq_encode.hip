@@ -5,12 +5,12 @@
 // coordinates, so these are the nearest codewords of eq. vq_assign; for other
 // maps they are the rounding of A^-1 (w_g - b).
 //
-// The codes are decided on fp32 values computed in a fixed order:
-//   A^-1: Gauss-Jordan with partial pivoting (largest |pivot|, first on ties);
-//         the pivot row times the correctly rounded reciprocal of the pivot,
-//         then row_k = fma(-f, pivot_row, row_k) for every other row k;
-//   v_k:  t_j = w_j - b_j, then v_k = fma(Ainv[k, j], t_j, v_k) for j = 0..d-1
-//         starting from 0.
+// v is evaluated in fp32: A^-1 by Gauss-Jordan elimination with partial
+// pivoting (largest |pivot|), the pivot row times the reciprocal of the pivot,
+// then row_k = fma(-f, pivot_row, row_k) for every other row k; then
+// t_j = w_j - b_j and v_k = sum_j Ainv[k, j] t_j as an fma chain.  The codes
+// therefore equal those of the exact v except within that evaluation's
+// rounding error of a decision boundary.
 // Each block inverts A once (one thread, in LDS); HBM-bound otherwise: the
 // weight is read once (2 or 4 bytes per element), the codes written once
 // (1 byte and / or 2 bits per element).
