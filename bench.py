@@ -7,7 +7,12 @@ weight matrix, on seeded synthetic inputs already resident in HBM.  The
 reported value is the work of the three products, 6 N m n flop, divided by the
 step time.  Prints one JSON line.
 
-  python bench.py [--steps K] [--warmup W] [--workload NAME] [--no-cpu-baseline] [--workloads]
+  python bench.py [--steps K] [--warmup W] [--workload NAME] [--no-cpu-baseline] [--no-workloads]
+
+By default it also times the larger Llama-shaped workloads (7B MLP, 70B MLP
+with the 2-bit pack, a 7B decoder block with AdamW of Z, A and b) for
+--workload-steps steps each, the streaming kernels, the packed-codes forward
+and the fp64 oracle on the host cores.
 """
 from __future__ import annotations
 
@@ -421,7 +426,16 @@ def cpu_baseline(layer, max_seconds: float):
                           "dZ": rel(host(layer.dZ), ref["dZ"]), "dA": rel(host(layer.dA), ref["dA"]),
                           "db": rel(host(layer.db), ref["db"])},
               "tolerance": 2e-2}
-    return {"value": round(layer.flops() / per / 1e12, 5), "unit": "TFLOP/s", "cores": cores, "kind": "oracle",
+    model = None
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.lower().startswith("model name"):
+                model = line.split(":", 1)[1].strip()
+                break
+    except OSError:
+        pass
+    return {"value": round(layer.flops() / per / 1e12, 5), "unit": "TFLOP/s", "cores": cores,
+            "nproc": len(os.sched_getaffinity(0)), "cpu_model": model, "kind": "oracle",
             "sample": f"full {layer.m}x{layer.n} layer, {layer.N} tokens, fwd+bwd in fp64 (numpy/OpenBLAS), "
                       f"{reps} repetition(s), {per:.2f} s each",
             "parity": parity}
@@ -435,8 +449,9 @@ def main():
     ap.add_argument("--workload", default=DEFAULT_WORKLOAD)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-hbm", action="store_true")
-    ap.add_argument("--workloads", action="store_true",
-                    help="also time the larger Llama-shaped workloads (7B MLP, 70B MLP, 7B block with AdamW)")
+    ap.add_argument("--no-workloads", action="store_true",
+                    help="skip the larger Llama-shaped workloads (7B MLP, 70B MLP + pack, 7B block with AdamW)")
+    ap.add_argument("--workload-steps", type=int, default=10)
     ap.add_argument("--cpu-seconds", type=float, default=10.0)
     ap.add_argument("--copy-probe", type=int, default=0, metavar="BYTES",
                     help="only run a plain device-to-device copy of BYTES (counter calibration) and exit")
@@ -474,21 +489,6 @@ def main():
         step()
     torch.cuda.synchronize()
 
-    # per-kernel breakdown (untimed passes, one kernel's events at a time) to
-    # pick the dominant kernel
-    breakdown = {}
-    for kid, name in enumerate(lc._lib.KERNELS):
-        lib.lcvq_timer_enable(1 << kid)
-        for _ in range(3):
-            step()
-        torch.cuda.synchronize()
-        ms, cnt = timer_read(lib, kid)
-        if cnt:
-            breakdown[name] = round(1e3 * ms / 3, 2)      # us per step
-    lib.lcvq_timer_enable(0)
-    dominant = max(MATRIX_KERNELS, key=lambda k: breakdown.get(k, 0.0))
-    dom_id = lc._lib.KERNELS.index(dominant)
-
     # timed region: K steps between two events, nothing else recorded
     start, stop = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     torch.cuda.synchronize()
@@ -499,10 +499,12 @@ def main():
     torch.cuda.synchronize()
     ms_step = start.elapsed_time(stop) / args.steps
 
-    # the same K steps again with every launch of the dominant kernel bracketed
-    # by HIP events on its stream (the extra event records lengthen the step, so
-    # the step time above comes from the run without them)
-    lib.lcvq_timer_enable(1 << dom_id)
+    # the same K steps again with every kernel launch bracketed by HIP events on
+    # its stream (the library's timer): the per-kernel breakdown and the dominant
+    # kernel's average launch time come from this one run, so the breakdown sums
+    # to no more than this run's step time (the extra event records lengthen the
+    # step a little, which is why `value` comes from the run above)
+    lib.lcvq_timer_enable((1 << len(lc._lib.KERNELS)) - 1)
     torch.cuda.synchronize()
     start.record()
     for _ in range(args.steps):
@@ -510,9 +512,16 @@ def main():
     stop.record()
     torch.cuda.synchronize()
     ms_step_ev = start.elapsed_time(stop) / args.steps
-    dom_ms, dom_cnt = timer_read(lib, dom_id)
+    breakdown, launch_us, launches = {}, {}, {}
+    for kid, name in enumerate(lc._lib.KERNELS):
+        ms, cnt = timer_read(lib, kid)
+        if cnt:
+            breakdown[name] = round(1e3 * ms / args.steps, 2)       # us per step
+            launch_us[name] = 1e3 * ms / cnt
+            launches[name] = cnt
     lib.lcvq_timer_enable(0)
-    dom_us = 1e3 * dom_ms / max(dom_cnt, 1)
+    dominant = max(MATRIX_KERNELS, key=lambda k: breakdown.get(k, 0.0))
+    dom_us, dom_cnt = launch_us[dominant], launches[dominant]
 
     dist = step_distribution(torch, step, args.steps)
     sclk = sample_sclk(torch, step)
@@ -535,6 +544,8 @@ def main():
                      "traffic": traffic, "avg_launch_us": round(dom_us, 2), "launches": dom_cnt,
                      "flop_per_launch": per_launch_flop, "ms_per_step_with_kernel_events": round(ms_step_ev, 4)},
         "kernels_us_per_step": breakdown,
+        "kernels_us_per_step_note": ("every launch bracketed by HIP events over the same K steps, run again after "
+                                     "the timed region; sums to at most ms_per_step_with_kernel_events"),
         "step_distribution": dist,
         "gpu_clock": sclk,
     }
@@ -542,9 +553,9 @@ def main():
                                    "differentiable gradient estimator, k=5, slope cap 3, latent mask")
     res["xavier_step"] = variant_step(lc, torch, layers, args.steps, "step_xavier",
                                       "latent in the Xavier domain: codes of W_p / s' + t, gradient / s'")
-    if args.workloads:
+    if not args.no_workloads:
         res["workloads"] = workload_steps(lc, torch, [w for w in OTHER_WORKLOADS if w != args.workload],
-                                          max(3, args.steps // 10))
+                                          args.workload_steps)
     L0 = layers[0]
     res["library_gemm_same_shape"] = library_gemm(torch, L0.N, L0.m, L0.n)
     if not args.no_hbm:

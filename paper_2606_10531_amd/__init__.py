@@ -8,7 +8,6 @@ library's HIP kernels; there is no CPU or PyTorch fallback.
 from __future__ import annotations
 
 import ctypes
-import math
 
 import torch
 
@@ -27,6 +26,34 @@ def _dtype_code(t: torch.Tensor) -> int:
     if t.dtype not in _DT:
         raise TypeError(f"unsupported dtype {t.dtype} (float32 or bfloat16)")
     return _DT[t.dtype]
+
+
+def _check(t, name: str, shape=None, dtype=None) -> None:
+    """Shape and dtype of one argument, checked before anything reaches the library
+    (a mis-shaped buffer would be read or written out of bounds by the kernels, and
+    a wrong dtype silently reinterpreted)."""
+    if not isinstance(t, torch.Tensor):
+        raise TypeError(f"{name} must be a tensor, got {type(t).__name__}")
+    if shape is not None and tuple(t.shape) != tuple(shape):
+        raise ValueError(f"{name} has shape {tuple(t.shape)}, expected {tuple(shape)}")
+    if dtype is not None:
+        ok = t.dtype in dtype if isinstance(dtype, tuple) else t.dtype == dtype
+        if not ok:
+            raise TypeError(f"{name} has dtype {t.dtype}, expected {dtype}")
+
+
+def _check_map(A, b, d: int) -> None:
+    if d not in (4, 8):
+        raise ValueError(f"group size d={d} (4 or 8)")
+    _check(A, "A", (d, d), torch.float32)
+    _check(b, "b", (d,), torch.float32)
+
+
+def _check_2d(t, name: str) -> tuple:
+    _check(t, name)
+    if t.dim() != 2:
+        raise ValueError(f"{name} must be 2-D, got shape {tuple(t.shape)}")
+    return tuple(t.shape)
 
 
 def _dev(t: torch.Tensor, name: str) -> int:
@@ -55,19 +82,25 @@ def _workspace(op, N, m, n, d, dtype, device, workspace):
     need = workspace_bytes(op, N, m, n, d, dtype)
     if workspace is None:
         workspace = torch.empty(max(need, 256), dtype=torch.uint8, device=device)
-    elif workspace.numel() * workspace.element_size() < need:
-        raise ValueError(f"workspace has {workspace.numel() * workspace.element_size()} bytes, need {need}")
+    elif workspace.dtype != torch.uint8 or workspace.dim() != 1:
+        raise TypeError(f"workspace must be a 1-D uint8 tensor (got {workspace.dtype}, {workspace.dim()}-D)")
+    elif workspace.numel() < need:
+        raise ValueError(f"workspace has {workspace.numel()} bytes, need {need}")
     return workspace
 
 
 def pack2bit(src: torch.Tensor, out: torch.Tensor | None = None) -> torch.Tensor:
     """Packed 2-bit codes (m x n/4 uint8) of a latent tensor (fp32/bf16) or of uint8 codes."""
-    m, n = src.shape
+    m, n = _check_2d(src, "src")
     if src.dtype == torch.uint8:
         kind, sdt = SRC_CODES_U8, F32
     else:
         kind, sdt = SRC_LATENT, _dtype_code(src)
-    if out is None:
+    if n % 4 != 0:
+        raise ValueError(f"n={n} is not a multiple of 4")
+    if out is not None:
+        _check(out, "out", (m, n // 4), torch.uint8)
+    else:
         out = torch.empty((m, n // 4), dtype=torch.uint8, device=src.device)
     _lib.check(_lib.load().lcvq_pack2bit(_dev(src, "src"), kind, sdt, m, n, _dev(out, "out"),
                                          _stream(src.device)), "lcvq_pack2bit")
@@ -78,13 +111,25 @@ def dequant(src: torch.Tensor, A: torch.Tensor, b: torch.Tensor, d: int, n: int 
             src_kind: int | None = None, out_dtype: torch.dtype = torch.bfloat16,
             out: torch.Tensor | None = None) -> torch.Tensor:
     """Dense W_hat (m x n) from latents, uint8 codes or packed 2-bit codes (pass n for packed)."""
+    _check_2d(src, "src")
     if src_kind is None:
         src_kind = SRC_CODES_U8 if src.dtype == torch.uint8 else SRC_LATENT
     m = src.shape[0]
     if n is None:
         n = src.shape[1] * (4 if src_kind == SRC_PACKED2 else 1)
+    if src_kind == SRC_PACKED2:
+        _check(src, "src", (m, n // 4), torch.uint8)
+        if n % 4 != 0:
+            raise ValueError(f"n={n} is not a multiple of 4")
+    elif src_kind == SRC_CODES_U8:
+        _check(src, "src", (m, n), torch.uint8)
+    else:
+        _check(src, "src", (m, n), (torch.float32, torch.bfloat16))
+    _check_map(A, b, d)
     sdt = _dtype_code(src) if src_kind == SRC_LATENT else F32
-    if out is None:
+    if out is not None:
+        _check(out, "out", (m, n), (torch.float32, torch.bfloat16))
+    else:
         out = torch.empty((m, n), dtype=out_dtype, device=src.device)
     _lib.check(_lib.load().lcvq_dequant(m, n, d, src_kind, sdt, _dev(src, "src"), _dev(A, "A"), _dev(b, "b"),
                                         _dev(out, "out"), _DT[out.dtype], _stream(src.device)), "lcvq_dequant")
@@ -95,7 +140,9 @@ def encode(W: torch.Tensor, A: torch.Tensor, b: torch.Tensor, d: int, codes: boo
     """LC encode of a dense weight W (m x n, fp32 or bf16): per group the codes
     clip(round(A^-1 (w_g - b)), 0, 3), the nearest codewords when A is a scaled
     orthogonal matrix.  Returns (codes m x n uint8 or None, packed m x n/4 uint8 or None)."""
-    m, n = W.shape
+    m, n = _check_2d(W, "W")
+    _check(W, "W", dtype=(torch.float32, torch.bfloat16))
+    _check_map(A, b, d)
     c = torch.empty((m, n), dtype=torch.uint8, device=W.device) if codes else None
     p = torch.empty((m, n // 4), dtype=torch.uint8, device=W.device) if packed else None
     _lib.check(_lib.load().lcvq_encode(m, n, d, _dev(W, "W"), _dtype_code(W), _dev(A, "A"), _dev(b, "b"),
@@ -103,23 +150,29 @@ def encode(W: torch.Tensor, A: torch.Tensor, b: torch.Tensor, d: int, codes: boo
     return c, p
 
 
-def xavier_quantizer(m: int, n: int, bits: int = 2) -> tuple[float, float]:
-    """(q_scale, q_shift) = (1 / s', t) of the Xavier reparameterisation (eq. xavier_preprocess,
-    Sec. 3.4): s' = 2a / (2^b - 1), t = (2^b - 1) / 2, a = sqrt(6 / (m + n)); q_scale rounded to fp32."""
-    a = math.sqrt(6.0 / (m + n))
-    sp, t = 2.0 * a / (2 ** bits - 1), (2 ** bits - 1) / 2.0
-    return float(torch.tensor(1.0 / sp, dtype=torch.float32)), t
+def xavier_quantizer(m: int, n: int) -> tuple[float, float]:
+    """(q_scale, q_shift) = (1 / s', t) of the Xavier reparameterisation (Sec. 3.4,
+    eq. xavier_preprocess) for 2-bit codes, from lcvq_xavier_quantizer."""
+    qs, qb = ctypes.c_float(), ctypes.c_float()
+    _lib.check(_lib.load().lcvq_xavier_quantizer(m, n, ctypes.byref(qs), ctypes.byref(qb)),
+               "lcvq_xavier_quantizer")
+    return qs.value, qb.value
 
 
-def xavier_init(codes: torch.Tensor, m: int, n: int, d: int, src_kind: int | None = None,
-                out_dtype: torch.dtype = torch.float32, bits: int = 2) -> torch.Tensor:
-    """Initial proxy weights W_p = s' (W_z - t) (eq. xavier_preprocess) from uint8 or packed codes:
-    lcvq_dequant with A = s' I and b = -s' t."""
-    a = math.sqrt(6.0 / (m + n))
-    sp, t = 2.0 * a / (2 ** bits - 1), (2 ** bits - 1) / 2.0
-    A = torch.eye(d, dtype=torch.float32, device=codes.device) * sp
-    b = torch.full((d,), -sp * t, dtype=torch.float32, device=codes.device)
-    return dequant(codes, A, b, d, n=n, src_kind=src_kind, out_dtype=out_dtype)
+def xavier_init(codes: torch.Tensor, m: int, n: int, src_kind: int | None = None,
+                out_dtype: torch.dtype = torch.float32, out: torch.Tensor | None = None) -> torch.Tensor:
+    """Initial proxy weights W_p = s' (W_z - t) (Sec. 3.4, eq. xavier_preprocess) of
+    uint8 (m x n) or packed (m x n/4) codes, from lcvq_xavier_init."""
+    if src_kind is None:
+        src_kind = SRC_CODES_U8 if tuple(codes.shape) == (m, n) else SRC_PACKED2
+    _check(codes, "codes", (m, n) if src_kind == SRC_CODES_U8 else (m, n // 4), torch.uint8)
+    if out is not None:
+        _check(out, "out", (m, n), (torch.float32, torch.bfloat16))
+    else:
+        out = torch.empty((m, n), dtype=out_dtype, device=codes.device)
+    _lib.check(_lib.load().lcvq_xavier_init(m, n, src_kind, _dev(codes, "codes"), _dev(out, "out"), _DT[out.dtype],
+                                            _stream(codes.device)), "lcvq_xavier_init")
+    return out
 
 
 def adamw_step(theta: torch.Tensor, grad: torch.Tensor, m1: torch.Tensor, m2: torch.Tensor, step: int,
@@ -128,8 +181,10 @@ def adamw_step(theta: torch.Tensor, grad: torch.Tensor, m1: torch.Tensor, m2: to
     """One in-place AdamW update of fp32 `theta`, `m1`, `m2` from `grad` (fp32 or bf16);
     `shadow` (fp32 or bf16, optional) receives the updated theta."""
     for t, nm in ((theta, "theta"), (m1, "m1"), (m2, "m2")):
-        if t.dtype != torch.float32:
-            raise TypeError(f"{nm} must be float32")
+        _check(t, nm, dtype=torch.float32)
+    _check(grad, "grad", dtype=(torch.float32, torch.bfloat16))
+    if shadow is not None:
+        _check(shadow, "shadow", dtype=(torch.float32, torch.bfloat16))
     numel = theta.numel()
     for t, nm in ((grad, "grad"), (m1, "m1"), (m2, "m2")) + (((shadow, "shadow"),) if shadow is not None else ()):
         if t.numel() != numel:
@@ -148,12 +203,18 @@ def linear_fwd(Z: torch.Tensor, A: torch.Tensor, b: torch.Tensor, X: torch.Tenso
 
     q_scale, q_shift: the quantiser rounds Z * q_scale + q_shift (see xavier_quantizer);
     the default is the code domain."""
-    m, n = Z.shape
-    N = X.shape[0]
-    dt = _dtype_code(X)
-    if Z.dtype != X.dtype:
-        raise TypeError("Z and X must share a dtype")
-    if out is None:
+    m, n = _check_2d(Z, "Z")
+    dt = _dtype_code(Z)
+    N = _check_2d(X, "X")[0]
+    _check(X, "X", (N, n), Z.dtype)
+    _check_map(A, b, d)
+    if packed_out is not None:
+        if n % 4 != 0:
+            raise ValueError(f"packed codes need n % 4 == 0 (n={n})")
+        _check(packed_out, "packed_out", (m, n // 4), torch.uint8)
+    if out is not None:
+        _check(out, "out", (N, m), Z.dtype)
+    else:
         out = torch.empty((N, m), dtype=X.dtype, device=X.device)
     ws = _workspace(OP_FWD, N, m, n, d, X.dtype, X.device, workspace)
     tail = (_dev(A, "A"), _dev(b, "b"), _dev(X, "X"), _dev(out, "Y"), _opt(packed_out, "packed_out"),
@@ -170,13 +231,15 @@ def linear_fwd_packed(packed: torch.Tensor, A: torch.Tensor, b: torch.Tensor, X:
                       out_dtype: torch.dtype = torch.bfloat16, workspace: torch.Tensor | None = None,
                       out: torch.Tensor | None = None) -> torch.Tensor:
     """Y = X W_hat^T (N x m, bf16 or fp32) from packed 2-bit codes (m x n/4 uint8) and bf16 X (N x n)."""
-    m, n = packed.shape[0], packed.shape[1] * 4
-    N = X.shape[0]
-    if packed.dtype != torch.uint8:
-        raise TypeError("packed codes must be uint8")
-    if X.dtype != torch.bfloat16:
-        raise TypeError("X must be bfloat16")
-    if out is None:
+    m, n4 = _check_2d(packed, "packed")
+    n = 4 * n4
+    _check(packed, "packed", dtype=torch.uint8)
+    N = _check_2d(X, "X")[0]
+    _check(X, "X", (N, n), torch.bfloat16)
+    _check_map(A, b, d)
+    if out is not None:
+        _check(out, "out", (N, m), (torch.float32, torch.bfloat16))
+    else:
         out = torch.empty((N, m), dtype=out_dtype, device=X.device)
     ws = _workspace(OP_FWD_PACKED, N, m, n, d, torch.bfloat16, X.device, workspace)
     _lib.check(_lib.load().lcvq_linear_fwd_packed(N, m, n, d, _dev(packed, "packed"), _dev(A, "A"), _dev(b, "b"),
@@ -213,12 +276,26 @@ def linear_bwd_dge(Z: torch.Tensor, A: torch.Tensor, b: torch.Tensor, X: torch.T
 
 def _linear_bwd(dge, Z, A, b, X, dY, d, mask_mode, accumulate, need_dX, need_dZ, need_map, dz_dtype, dX, dZ, dA,
                 db, workspace, q_scale=1.0, q_shift=0.0):
-    m, n = Z.shape
-    N = X.shape[0]
-    dt = _dtype_code(X)
+    m, n = _check_2d(Z, "Z")
+    dt = _dtype_code(Z)
+    N = _check_2d(X, "X")[0]
+    _check(X, "X", (N, n), Z.dtype)
+    _check(dY, "dY", (N, m), Z.dtype)
+    _check_map(A, b, d)
     dev = X.device
     if dz_dtype is None:
         dz_dtype = dZ.dtype if dZ is not None else Z.dtype
+    if dz_dtype not in (torch.float32, Z.dtype):
+        raise TypeError(f"dZ dtype {dz_dtype}: float32 or the latent's dtype {Z.dtype}")
+    if dX is not None:
+        _check(dX, "dX", (N, n), Z.dtype)
+    if dZ is not None:
+        _check(dZ, "dZ", (m, n), dz_dtype)
+    if (dA is None) != (db is None):
+        raise ValueError("dA and db are given together or not at all")
+    if dA is not None:
+        _check(dA, "dA", (d, d), torch.float32)
+        _check(db, "db", (d,), torch.float32)
     if need_dX and dX is None:
         dX = torch.empty((N, n), dtype=X.dtype, device=dev)
     if need_dZ and dZ is None:

@@ -44,6 +44,8 @@ SIGNATURES = {
                                    ctypes.c_float, _I32, _P, _P, _I32, _P, _P, _P, _SZ, _P]),
     "lcvq_adamw_step": (_I32, [_P, _P, _I32, _P, _P, _P, _I32, _I64, ctypes.c_float, ctypes.c_float,
                                 ctypes.c_float, ctypes.c_float, ctypes.c_float, _I32, _P]),
+    "lcvq_xavier_quantizer": (_I32, [_I64, _I64, ctypes.POINTER(ctypes.c_float), ctypes.POINTER(ctypes.c_float)]),
+    "lcvq_xavier_init": (_I32, [_I64, _I64, _I32, _P, _P, _I32, _P]),
     "lcvq_timer_enable": (_I32, [ctypes.c_uint32]),
     "lcvq_timer_read": (_I32, [_I32, ctypes.POINTER(ctypes.c_double), ctypes.POINTER(ctypes.c_int64)]),
     "lcvq_status_string": (ctypes.c_char_p, [_I32]),

@@ -41,6 +41,10 @@ size_t up256(size_t x) { return (x + 255) & ~(size_t)255; }
 // Largest row length of an operand streamed through the 256-row tiles with
 // 32-bit buffer offsets (256 rows * ld * 4 bytes must stay below 2^31).
 constexpr int64_t kMaxLd = (int64_t)1 << 21;
+// Most tokens of one layer call: the weight-gradient operands of eight 32-row
+// slabs take 8 * (tokens / 64) * 4 KiB, which must stay below the 2^31 bytes a
+// buffer resource addresses (tokens padded to 256, at most 2^22 - 256).
+constexpr int64_t kMaxTokens = ((int64_t)1 << 22) - 256;
 
 struct FwdLayout {
   size_t xp, s, frag, total;
@@ -176,6 +180,7 @@ lcvq_status_t check_common(int64_t N, int64_t m, int64_t n, int32_t d, int32_t d
   if (d != 4 && d != 8) return fail(LCVQ_EUNSUPPORTED, "group size d=%d (supported: 4, 8)", d);
   if (n % d != 0) return fail(LCVQ_EINVAL, "n=%lld is not a multiple of d=%d", (long long)n, d);
   if (dtype != LCVQ_F32 && dtype != LCVQ_BF16) return fail(LCVQ_EINVAL, "dtype=%d", dtype);
+  if (N > kMaxTokens) return fail(LCVQ_EUNSUPPORTED, "N=%lld tokens (at most %lld per call)", (long long)N, (long long)kMaxTokens);
   if (dtype == LCVQ_BF16) {
     if (m % 8 != 0 || n % 8 != 0)
       return fail(LCVQ_EUNSUPPORTED, "bf16 path needs m and n multiples of 8 (m=%lld n=%lld)", (long long)m, (long long)n);
@@ -330,6 +335,41 @@ lcvq_status_t lcvq_dequant(int64_t m, int64_t n, int32_t d, int32_t src_kind, in
   hipError_t e = tm.done(lcvq::launch_dequant(src, src_kind, src_dtype == LCVQ_BF16, m, n, d, A, b, W_hat,
                                               out_dtype == LCVQ_BF16, (hipStream_t)stream));
   return e == hipSuccess ? ok() : hip_fail(e, "dequant launch");
+}
+
+// eq. xavier_preprocess (Sec. 3.4) for b = 2 bits: a = sqrt(6 / (m + n)),
+// s' = 2a / (2^b - 1), t = (2^b - 1) / 2; evaluated in double, rounded to fp32 once.
+static bool xavier_scale(int64_t m, int64_t n, double *sp, double *t) {
+  if (m <= 0 || n <= 0) return false;
+  const double a = std::sqrt(6.0 / ((double)m + (double)n));
+  *sp = 2.0 * a / (double)lcvq::kMaxCode;
+  *t = (double)lcvq::kMaxCode / 2.0;
+  return true;
+}
+
+lcvq_status_t lcvq_xavier_quantizer(int64_t m, int64_t n, float *q_scale, float *q_shift) {
+  double sp, t;
+  if (!xavier_scale(m, n, &sp, &t)) return fail(LCVQ_EINVAL, "m=%lld n=%lld (need m, n > 0)", (long long)m, (long long)n);
+  if (q_scale == nullptr || q_shift == nullptr) return fail(LCVQ_EINVAL, "null output pointer");
+  *q_scale = (float)(1.0 / sp);
+  *q_shift = (float)t;
+  return ok();
+}
+
+lcvq_status_t lcvq_xavier_init(int64_t m, int64_t n, int32_t src_kind, const void *codes, void *W_p,
+                               int32_t out_dtype, void *stream) {
+  double sp, t;
+  if (!xavier_scale(m, n, &sp, &t)) return fail(LCVQ_EINVAL, "m=%lld n=%lld (need m, n > 0)", (long long)m, (long long)n);
+  if (src_kind != LCVQ_SRC_CODES_U8 && src_kind != LCVQ_SRC_PACKED2)
+    return fail(LCVQ_EINVAL, "src_kind=%d (CODES_U8 or PACKED2)", src_kind);
+  if (n % 4 != 0) return fail(LCVQ_EINVAL, "n=%lld is not a multiple of 4", (long long)n);
+  if (out_dtype != LCVQ_F32 && out_dtype != LCVQ_BF16) return fail(LCVQ_EINVAL, "out_dtype=%d", out_dtype);
+  if (codes == nullptr || W_p == nullptr) return fail(LCVQ_EINVAL, "null pointer");
+  if (!aligned16(codes) || !aligned16(W_p)) return fail(LCVQ_EALIGN, "codes/W_p must be 16-byte aligned");
+  Timed tm(LCVQ_K_DEQUANT, (hipStream_t)stream);
+  hipError_t e = tm.done(lcvq::launch_decode_scalar(codes, src_kind, m * n, (float)sp, (float)(-sp * t), W_p,
+                                                    out_dtype == LCVQ_BF16, (hipStream_t)stream));
+  return e == hipSuccess ? ok() : hip_fail(e, "xavier init launch");
 }
 
 }  // extern "C"

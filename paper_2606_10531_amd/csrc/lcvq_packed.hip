@@ -296,19 +296,23 @@ __global__ __launch_bounds__(256) void k_packed_gemv(const uint8_t *__restrict__
   const int64_t row = r0 + 16 * rb + 4 * q;  // m is a multiple of 8: the four rows are all in or all out
   if (KS > 1) {
     // The blocks of a row tile may run on different XCDs (separate L2s).  The
-    // partials are written and read with device-scope atomics (coherent across
-    // the XCDs without writing back or invalidating whole caches, which a
-    // device-scope fence would do in every block); the counter is bumped once
-    // this block's stores have completed (vmcnt 0, then the barrier).
+    // partials are written and read with device-scope atomics, so each one is
+    // performed at device scope.  Ordering: the block's partial stores precede
+    // the barrier, the barrier precedes thread 0's arrival increment, which is a
+    // device-scope release; the block that arrives last acquires at device
+    // scope (fence by thread 0, then the barrier) before any of its threads
+    // reads the partials.  Only that block pays for the acquire.
     float *pp = part + (((int64_t)rt * KS + ks) * 16 + tl) * kPkRows + 16 * rb + 4 * q;
     if (tl < Nc) {
 #pragma unroll
       for (int e = 0; e < 4; ++e) __hip_atomic_store(pp + e, v[e], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     }
-    __builtin_amdgcn_s_waitcnt(0);
+    __builtin_amdgcn_s_waitcnt(0);  // this wave's partial stores have completed
     __syncthreads();
-    if (tid == 0)
-      last = __hip_atomic_fetch_add(counters + rt, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) == KS - 1;
+    if (tid == 0) {
+      last = __hip_atomic_fetch_add(counters + rt, 1, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_AGENT) == KS - 1;
+      if (last) __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
+    }
     __syncthreads();
     if (!last) return;
     if (tl < Nc) {

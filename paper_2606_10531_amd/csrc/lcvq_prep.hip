@@ -408,11 +408,11 @@ __global__ __launch_bounds__(256) void k_pack2bit(const ST *__restrict__ src, in
   }
 }
 
-// ---- stand-alone dense decode (def. forward) -------------------------------
-// Thread -> one group of D codes -> D outputs W_hat[r, g*D + j].  Groups never
+// ---- stand-alone dense decode (def. forward) from latents -------------------
+// Thread -> one group of D latents -> D outputs W_hat[r, g*D + j].  Groups never
 // straddle rows (n % D == 0), so the flattened group index is enough.
-template <int D, int kSrc, typename ZT, typename OT>
-__global__ __launch_bounds__(256) void k_dequant(const void *__restrict__ src, int64_t groups,
+template <int D, typename ZT, typename OT>
+__global__ __launch_bounds__(256) void k_dequant(const ZT *__restrict__ src, int64_t groups,
                                                   const float *__restrict__ A,
                                                   const float *__restrict__ b, OT *__restrict__ W) {
   float a[D][D], bb[D];
@@ -423,28 +423,10 @@ __global__ __launch_bounds__(256) void k_dequant(const void *__restrict__ src, i
     for (int k = 0; k < D; ++k) a[j][k] = A[j * D + k];
   }
   for (int64_t q = (int64_t)blockIdx.x * 256 + threadIdx.x; q < groups; q += (int64_t)gridDim.x * 256) {
-    float c[D];
-    if constexpr (kSrc == 0) {  // latent
-      float z[D];
-      loadD<D>(reinterpret_cast<const ZT *>(src) + q * D, z);
+    float z[D], c[D], y[D];
+    loadD<D>(src + q * D, z);
 #pragma unroll
-      for (int k = 0; k < D; ++k) c[k] = (float)quant_code(z[k]);
-    } else if constexpr (kSrc == 1) {  // one byte per code
-      const uint8_t *p = reinterpret_cast<const uint8_t *>(src) + q * D;
-      uint32_t w0 = *reinterpret_cast<const uint32_t *>(p);
-      uint32_t w1 = D == 8 ? *reinterpret_cast<const uint32_t *>(p + 4) : 0u;
-#pragma unroll
-      for (int k = 0; k < D; ++k) {
-        uint32_t v = ((k < 4 ? w0 : w1) >> (8 * (k & 3))) & 0xffu;
-        c[k] = (float)(v > 3u ? 3u : v);
-      }
-    } else {  // packed 2-bit
-      const uint8_t *p = reinterpret_cast<const uint8_t *>(src) + q * (D / 4);
-      uint32_t w = D == 8 ? (uint32_t)*reinterpret_cast<const uint16_t *>(p) : (uint32_t)*p;
-#pragma unroll
-      for (int k = 0; k < D; ++k) c[k] = (float)((w >> (2 * k)) & 3u);
-    }
-    float y[D];
+    for (int k = 0; k < D; ++k) c[k] = (float)quant_code(z[k]);
 #pragma unroll
     for (int j = 0; j < D; ++j) {
       float v = bb[j];
@@ -453,6 +435,94 @@ __global__ __launch_bounds__(256) void k_dequant(const void *__restrict__ src, i
       y[j] = v;
     }
     storeD<D>(W + q * D, y);
+  }
+}
+
+// ---- dense decode from byte or packed codes, 16 source bytes per lane --------
+// A thread decodes one 16-byte chunk of the source per trip: 16 codes of one
+// byte each (kSrc 1; values above 3 are taken as 3) or 64 packed 2-bit codes
+// (kSrc 2, lcvq_pack2bit layout), i.e. whole groups (16 and 64 are multiples of
+// D), and stores their W_hat values, contiguous in the flattened m x n matrix
+// (groups never straddle rows).  Two chunks are loaded before either is
+// decoded, so a wave keeps 2 KiB of loads in flight.  The map is A, b (device),
+// or with kScalar the diagonal map W = fma(scale, code, shift), which is the
+// fp32 result of A = scale I, b = shift bit for bit (the other terms add
+// 0 * code).  Codes past the last whole chunk (fewer than one chunk's worth)
+// are decoded one group per thread by block 0.
+template <int D, int kSrc, typename OT, bool kScalar>
+__global__ __launch_bounds__(256) void k_decode_codes(const uint8_t *__restrict__ src, int64_t chunks,
+                                                       int64_t groups, const float *__restrict__ A,
+                                                       const float *__restrict__ b, float scale, float shift,
+                                                       OT *__restrict__ W) {
+  constexpr int kCodes = kSrc == 2 ? 64 : 16;  // codes per 16-byte chunk
+  float a[D][D], bb[D];
+  if constexpr (!kScalar) {
+#pragma unroll
+    for (int j = 0; j < D; ++j) {
+      bb[j] = b[j];
+#pragma unroll
+      for (int k = 0; k < D; ++k) a[j][k] = A[j * D + k];
+    }
+  }
+  auto map_group = [&](const float (&c)[D], OT *dst) {
+    float y[D];
+#pragma unroll
+    for (int j = 0; j < D; ++j) {
+      if constexpr (kScalar) {
+        y[j] = fmaf(scale, c[j], shift);
+      } else {
+        float v = bb[j];
+#pragma unroll
+        for (int k = 0; k < D; ++k) v = fmaf(a[j][k], c[k], v);
+        y[j] = v;
+      }
+    }
+    storeD<D>(dst, y);
+  };
+  auto decode = [&](const u32x4 &v, int64_t ch) {
+#pragma unroll
+    for (int g = 0; g < kCodes / D; ++g) {
+      float c[D];
+#pragma unroll
+      for (int k = 0; k < D; ++k) {
+        const int i = g * D + k;
+        uint32_t code;
+        if constexpr (kSrc == 2) {
+          code = (v[i >> 4] >> (2 * (i & 15))) & 3u;
+        } else {
+          code = (v[i >> 2] >> (8 * (i & 3))) & 0xffu;
+          code = code > 3u ? 3u : code;
+        }
+        c[k] = (float)code;
+      }
+      map_group(c, W + ch * kCodes + g * D);
+    }
+  };
+  const u32x4 *s16 = reinterpret_cast<const u32x4 *>(src);
+  const int64_t stride = (int64_t)gridDim.x * 256;
+  int64_t ch = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  for (; ch + stride < chunks; ch += 2 * stride) {
+    const u32x4 v0 = s16[ch], v1 = s16[ch + stride];
+    decode(v0, ch);
+    decode(v1, ch + stride);
+  }
+  if (ch < chunks) decode(s16[ch], ch);
+  const int64_t g = chunks * (kCodes / D) + threadIdx.x;
+  if (blockIdx.x == 0 && g < groups) {
+    float c[D];
+#pragma unroll
+    for (int k = 0; k < D; ++k) {
+      const int64_t e = g * D + k;
+      uint32_t code;
+      if constexpr (kSrc == 2) {
+        code = (src[e >> 2] >> (2 * (e & 3))) & 3u;
+      } else {
+        code = src[e];
+        code = code > 3u ? 3u : code;
+      }
+      c[k] = (float)code;
+    }
+    map_group(c, W + g * D);
   }
 }
 
@@ -686,30 +756,53 @@ hipError_t launch_pack2bit(const void *src, int kind, bool bf16, int64_t m, int6
   return hipGetLastError();
 }
 
+template <int D, typename OT, bool kScalar>
+static void decode_codes_dispatch(int kind, const void *src, int64_t total, const float *A, const float *b,
+                                  float scale, float shift, void *W, hipStream_t st) {
+  const int64_t per = kind == 2 ? 64 : 16;  // codes per 16-byte chunk
+  const int64_t chunks = total / per, groups = total / D;
+  const int grid = grid_for(chunks, 512);   // two chunks per thread
+  if (kind == 2)
+    k_decode_codes<D, 2, OT, kScalar><<<grid, 256, 0, st>>>((const uint8_t *)src, chunks, groups, A, b, scale, shift,
+                                                            (OT *)W);
+  else
+    k_decode_codes<D, 1, OT, kScalar><<<grid, 256, 0, st>>>((const uint8_t *)src, chunks, groups, A, b, scale, shift,
+                                                            (OT *)W);
+}
+
 template <int D, typename OT>
-static void dequant_dispatch(int kind, bool zbf16, const void *src, int64_t groups, const float *A,
-                             const float *b, void *W, int grid, hipStream_t st) {
-  OT *w = (OT *)W;
-  if (kind == 0) {
-    if (zbf16) k_dequant<D, 0, uint16_t, OT><<<grid, 256, 0, st>>>(src, groups, A, b, w);
-    else k_dequant<D, 0, float, OT><<<grid, 256, 0, st>>>(src, groups, A, b, w);
-  } else if (kind == 1) {
-    k_dequant<D, 1, uint8_t, OT><<<grid, 256, 0, st>>>(src, groups, A, b, w);
-  } else {
-    k_dequant<D, 2, uint8_t, OT><<<grid, 256, 0, st>>>(src, groups, A, b, w);
+static void dequant_dispatch(int kind, bool zbf16, const void *src, int64_t m, int64_t n, const float *A,
+                             const float *b, void *W, hipStream_t st) {
+  if (kind != 0) {
+    decode_codes_dispatch<D, OT, false>(kind, src, m * n, A, b, 1.0f, 0.0f, W, st);
+    return;
   }
+  const int64_t groups = m * n / D;
+  const int grid = grid_for(groups, 256);
+  if (zbf16) k_dequant<D, uint16_t, OT><<<grid, 256, 0, st>>>((const uint16_t *)src, groups, A, b, (OT *)W);
+  else k_dequant<D, float, OT><<<grid, 256, 0, st>>>((const float *)src, groups, A, b, (OT *)W);
 }
 
 hipError_t launch_dequant(const void *src, int kind, bool z_bf16, int64_t m, int64_t n, int d,
                           const float *A, const float *b, void *W, bool out_bf16, hipStream_t st) {
-  const int64_t groups = m * n / d;
-  const int grid = grid_for(groups, 256);
   if (d == 8) {
-    if (out_bf16) dequant_dispatch<8, uint16_t>(kind, z_bf16, src, groups, A, b, W, grid, st);
-    else dequant_dispatch<8, float>(kind, z_bf16, src, groups, A, b, W, grid, st);
+    if (out_bf16) dequant_dispatch<8, uint16_t>(kind, z_bf16, src, m, n, A, b, W, st);
+    else dequant_dispatch<8, float>(kind, z_bf16, src, m, n, A, b, W, st);
   } else {
-    if (out_bf16) dequant_dispatch<4, uint16_t>(kind, z_bf16, src, groups, A, b, W, grid, st);
-    else dequant_dispatch<4, float>(kind, z_bf16, src, groups, A, b, W, grid, st);
+    if (out_bf16) dequant_dispatch<4, uint16_t>(kind, z_bf16, src, m, n, A, b, W, st);
+    else dequant_dispatch<4, float>(kind, z_bf16, src, m, n, A, b, W, st);
+  }
+  return hipGetLastError();
+}
+
+hipError_t launch_decode_scalar(const void *src, int kind, int64_t total, float scale, float shift, void *W,
+                                bool out_bf16, hipStream_t st) {
+  if (total % 8 == 0) {
+    if (out_bf16) decode_codes_dispatch<8, uint16_t, true>(kind, src, total, nullptr, nullptr, scale, shift, W, st);
+    else decode_codes_dispatch<8, float, true>(kind, src, total, nullptr, nullptr, scale, shift, W, st);
+  } else {
+    if (out_bf16) decode_codes_dispatch<4, uint16_t, true>(kind, src, total, nullptr, nullptr, scale, shift, W, st);
+    else decode_codes_dispatch<4, float, true>(kind, src, total, nullptr, nullptr, scale, shift, W, st);
   }
   return hipGetLastError();
 }

@@ -65,6 +65,10 @@ hipError_t launch_pack2bit(const void *src, int kind, bool bf16, int64_t m, int6
                            const Quantizer &qz, hipStream_t st);
 hipError_t launch_dequant(const void *src, int kind, bool z_bf16, int64_t m, int64_t n, int d,
                           const float *A, const float *b, void *W, bool out_bf16, hipStream_t st);
+// W[i] = fma(scale, code[i], shift) over `total` codes (kind 1: bytes, 2: packed
+// 2-bit; total % 4 == 0): the decode of the diagonal map scale I, shift
+hipError_t launch_decode_scalar(const void *src, int kind, int64_t total, float scale, float shift, void *W,
+                                bool out_bf16, hipStream_t st);
 
 // layer output from packed 2-bit codes, 16 tokens per pass (lcvq_packed.hip)
 struct PackedPlan {

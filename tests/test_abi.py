@@ -227,3 +227,89 @@ def test_binding_refuses_cpu_tensors():
     Z = torch.zeros(8, 8)
     with pytest.raises(ValueError, match="GPU"):
         lc.pack2bit(Z)
+
+
+def test_token_bound(lib):
+    # at most 2^22 - 256 tokens per layer call (the weight-gradient operands'
+    # 32-bit buffer range); beyond it nothing is enqueued
+    big = (1 << 22) - 255
+    assert fwd(lib, N=big) == L.EUNSUPPORTED and "tokens" in L.last_error()
+    assert bwd(lib, N=big) == L.EUNSUPPORTED
+    assert fwd(lib, N=big, dt=L.F32) == L.EUNSUPPORTED
+    assert fwd(lib, N=big - 1, wsb=16) == L.EWORKSPACE       # the largest N passes the bound
+
+
+def test_xavier_quantizer_is_host_arithmetic(lib):
+    """eq. xavier_preprocess: (1 / s', t) with s' = 2 sqrt(6 / (m + n)) / 3, t = 3 / 2,
+    each rounded to fp32 (host-only call, no GPU needed)."""
+    import numpy as np
+    import oracle as orc
+    qs, qb = ctypes.c_float(), ctypes.c_float()
+    for m, n in ((4096, 4096), (28672, 8192), (1, 1)):
+        assert lib.lcvq_xavier_quantizer(m, n, ctypes.byref(qs), ctypes.byref(qb)) == L.OK
+        sp, t = orc.xavier_params(m, n)
+        assert qs.value == float(np.float32(1.0 / sp)) and qb.value == 1.5 == t
+    assert lib.lcvq_xavier_quantizer(0, 5, ctypes.byref(qs), ctypes.byref(qb)) == L.EINVAL
+    assert lib.lcvq_xavier_quantizer(5, 5, None, ctypes.byref(qb)) == L.EINVAL
+
+
+def test_xavier_init_validation(lib):
+    def x(m=64, n=64, kind=L.SRC_CODES_U8, codes=FAKE, W=FAKE, odt=L.F32):
+        return lib.lcvq_xavier_init(m, n, kind, codes, W, odt, None)
+    assert x(m=0) == L.EINVAL
+    assert x(kind=L.SRC_LATENT) == L.EINVAL
+    assert x(n=62) == L.EINVAL                               # n % 4
+    assert x(odt=7) == L.EINVAL
+    assert x(codes=None) == L.EINVAL
+    assert x(W=MIS) == L.EALIGN
+    assert x(kind=L.SRC_PACKED2, codes=MIS) == L.EALIGN
+
+
+def test_binding_checks_shapes_and_dtypes_before_any_call():
+    """The torch binding validates every tensor against (N, m, n, d) and the
+    activation dtype before it touches the device or the C ABI (checked here with
+    CPU tensors: a well-formed call fails only at the device check)."""
+    torch = pytest.importorskip("torch")
+    import paper_2606_10531_amd as lc
+    bf, f32 = torch.bfloat16, torch.float32
+    N, m, n, d = 4, 16, 32, 8
+    Z, X, dY = torch.zeros(m, n, dtype=bf), torch.zeros(N, n, dtype=bf), torch.zeros(N, m, dtype=bf)
+    A, b = torch.zeros(d, d), torch.zeros(d)
+    with pytest.raises(ValueError, match="GPU"):               # well formed: reaches the device check
+        lc.linear_fwd(Z, A, b, X, d)
+    with pytest.raises(ValueError, match="GPU"):
+        lc.linear_bwd(Z, A, b, X, dY, d)
+    bad_fwd = [dict(X=torch.zeros(N, n + 8, dtype=bf)), dict(X=torch.zeros(N, n, dtype=f32)),
+               dict(A=torch.zeros(d, d + 1)), dict(A=torch.zeros(d, d, dtype=bf)), dict(b=torch.zeros(d + 1)),
+               dict(out=torch.zeros(N, m + 8, dtype=bf)), dict(out=torch.zeros(N, m, dtype=f32)),
+               dict(packed_out=torch.zeros(m, n // 4 + 1, dtype=torch.uint8)),
+               dict(packed_out=torch.zeros(m, n // 4, dtype=torch.int8)),
+               dict(workspace=torch.zeros(1 << 20, dtype=torch.int32))]
+    for kw in bad_fwd:
+        args = dict(Z=Z, A=A, b=b, X=X, d=d)
+        args.update(kw)
+        with pytest.raises((TypeError, ValueError)) as ei:
+            lc.linear_fwd(**args)
+        assert "GPU" not in str(ei.value), kw
+    bad_bwd = [dict(dY=torch.zeros(N, m + 8, dtype=bf)), dict(dY=torch.zeros(N, m, dtype=f32)),
+               dict(dX=torch.zeros(N, n, dtype=f32)), dict(dZ=torch.zeros(m, n + 8, dtype=bf)),
+               dict(dZ=torch.zeros(m, n, dtype=torch.float16)), dict(dA=torch.zeros(d, d), db=None),
+               dict(dA=torch.zeros(d, d), db=torch.zeros(d + 1)), dict(dA=torch.zeros(d, d, dtype=bf),
+                                                                      db=torch.zeros(d))]
+    for kw in bad_bwd:
+        args = dict(Z=Z, A=A, b=b, X=X, dY=dY, d=d)
+        args.update(kw)
+        with pytest.raises((TypeError, ValueError)) as ei:
+            lc.linear_bwd(**args)
+        assert "GPU" not in str(ei.value), kw
+    P = torch.zeros(m, n // 4, dtype=torch.uint8)
+    with pytest.raises(TypeError):
+        lc.linear_fwd_packed(P, A, b, torch.zeros(N, n, dtype=f32), d)
+    with pytest.raises(ValueError, match="shape"):
+        lc.linear_fwd_packed(P, A, b, torch.zeros(N, n + 4, dtype=bf), d)
+    with pytest.raises(ValueError, match="shape"):
+        lc.dequant(P, A, b, d, n=n + 4, src_kind=lc.SRC_PACKED2)
+    with pytest.raises(ValueError, match="shape"):
+        lc.xavier_init(P, m, n + 4, src_kind=lc.SRC_PACKED2)
+    with pytest.raises(ValueError, match="shape"):
+        lc.pack2bit(Z, out=torch.zeros(m, n, dtype=torch.uint8))

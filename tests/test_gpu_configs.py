@@ -16,7 +16,7 @@ import pytest
 
 import oracle as orc
 import synth
-from helpers import rel_fro, to_dev, to_host
+from helpers import assert_close, rel_fro, to_dev, to_host
 
 pytestmark = pytest.mark.gpu
 
@@ -63,14 +63,14 @@ def _check_matrix(lc, N, m, n, d, k, pack):
     if pack:
         assert np.array_equal(P2h, want)
     W = orc.decode(codes, A64, b64, d)
-    assert rel_fro(Yh, orc.forward(v["X"][tok], W)) <= TOL
-    assert rel_fro(dXh, orc.grad_input(v["dY"][tok], W)) <= TOL
+    assert_close(Yh, orc.forward(v["X"][tok], W), TOL, 'Y')
+    assert_close(dXh, orc.grad_input(v["dY"][tok], W), TOL, 'dX')
     del W
     mask = orc.ste_mask(v["Z"][rows])
-    assert rel_fro(dZh, orc.grad_latent(orc.grad_weight(v["dY"][:, rows], v["X"]), A64, d, mask)) <= TOL
+    assert_close(dZh, orc.grad_latent(orc.grad_weight(v["dY"][:, rows], v["X"]), A64, d, mask), TOL, 'dZ')
     dA_ref, db_ref = orc.grad_map(orc.grad_weight(v["dY"], v["X"]), codes, d)
-    assert rel_fro(dAh, dA_ref) <= TOL
-    assert rel_fro(dbh, db_ref) <= TOL
+    assert_close(dAh, dA_ref, TOL, 'dA')
+    assert_close(dbh, db_ref, TOL, 'db')
 
 
 def _cases():

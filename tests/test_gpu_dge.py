@@ -8,7 +8,7 @@ import pytest
 
 import oracle as orc
 import synth
-from helpers import rel_fro, to_dev, to_host
+from helpers import assert_close, rel_fro, to_dev, to_host
 
 pytestmark = pytest.mark.gpu
 
@@ -65,7 +65,7 @@ SHAPES = [(300, 320, 512), (513, 520, 1096), (77, 24, 64), (1, 8, 8)]
 def test_dge_bf16(lc, N, m, n, d, mask_mode):
     got, ref, mask, _ = _run(lc, N, m, n, d, "bf16", mask_mode, 5.0, 3.0, seed=N + m + n + d + mask_mode)
     for key in ("dX", "dZ", "dA", "db"):
-        assert rel_fro(got[key], ref[key]) <= TOL["bf16"], (key, rel_fro(got[key], ref[key]))
+        assert_close(got[key], ref[key], TOL["bf16"], key)
     assert np.all(np.isfinite(got["dZ"]))
     assert np.all(got["dZ"][~mask] == 0.0)
 
@@ -75,7 +75,7 @@ def test_dge_bf16(lc, N, m, n, d, mask_mode):
 def test_dge_fp32(lc, N, m, n, d, mask_mode):
     got, ref, mask, _ = _run(lc, N, m, n, d, "f32", mask_mode, 5.0, 3.0, seed=11 + d + mask_mode)
     for key in ("dX", "dZ", "dA", "db"):
-        assert rel_fro(got[key], ref[key]) <= TOL["f32"], (key, rel_fro(got[key], ref[key]))
+        assert_close(got[key], ref[key], TOL["f32"], key)
     assert np.all(got["dZ"][~mask] == 0.0)
 
 
@@ -85,7 +85,7 @@ def test_dge_other_sharpness_and_caps(lc, dtype, k, cap):
     import torch
     got, ref, mask, _ = _run(lc, 96, 64, 256, 8, dtype, 1, k, cap, seed=int(10 * k + cap),
                              dz_dtype=torch.float32)
-    assert rel_fro(got["dZ"], ref["dZ"]) <= TOL[dtype]
+    assert_close(got["dZ"], ref["dZ"], TOL[dtype], 'dZ')
     assert np.all(got["dZ"][~mask] == 0.0)
 
 
@@ -142,7 +142,7 @@ def test_dge_accumulate(lc, dtype):
     got, ref, _, _ = _run(lc, 96, 64, 128, 8, dtype, 1, 5.0, 3.0, seed=21, dz_dtype=torch.float32,
                           accumulate_twice=True)
     for key in ("dZ", "dA", "db"):
-        assert rel_fro(got[key], 2 * ref[key]) <= TOL[dtype], key
+        assert_close(got[key], 2 * ref[key], TOL[dtype], key)
 
 
 def test_dge_4096_sampled(lc):
@@ -161,9 +161,9 @@ def test_dge_4096_sampled(lc):
     dW_rows = orc.grad_weight(v["dY"][:, rows], v["X"])
     mask = orc.ste_mask(v["Z"][rows], orc.MASK_LATENT)
     want = np.where(mask, orc.grad_codes(dW_rows, A64, d) * orc.dge_slope(v["Z"][rows], 5.0, 3.0), 0.0)
-    assert rel_fro(to_host(dZ[rows]), want) <= TOL["bf16"]
+    assert_close(to_host(dZ[rows]), want, TOL["bf16"], 'dZ')
     assert np.all(to_host(dZ[rows])[~mask] == 0.0)
     codes = orc.quantize(v["Z"])
     dA_ref, db_ref = orc.grad_map(orc.grad_weight(v["dY"], v["X"]), codes, d)
-    assert rel_fro(to_host(dA), dA_ref) <= TOL["bf16"]
-    assert rel_fro(to_host(db), db_ref) <= TOL["bf16"]
+    assert_close(to_host(dA), dA_ref, TOL["bf16"], 'dA')
+    assert_close(to_host(db), db_ref, TOL["bf16"], 'db')

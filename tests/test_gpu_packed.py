@@ -8,7 +8,7 @@ import pytest
 
 import oracle as orc
 import synth
-from helpers import rel_fro, to_dev, to_host
+from helpers import assert_close, rel_fro, to_dev, to_host
 
 pytestmark = pytest.mark.gpu
 
@@ -59,7 +59,7 @@ def test_packed_forward(lc, N, m, n, d, y_dtype):
     got = _run(lc, inp, P, d, y_dtype, calls=2)
     ref = _ref(inp, P, d, n)
     for Y in got:   # a second call (counters reset by its prepass) gives the same result
-        assert rel_fro(Y, ref) <= TOL, rel_fro(Y, ref)
+        assert_close(Y, ref, TOL, 'Y')
     assert np.array_equal(got[0], got[1])
 
 
@@ -86,7 +86,7 @@ def test_packed_forward_extreme_codes(lc):
     for byte in (0xFF, 0x00, 0x1B):
         P = np.full((m, n // 4), byte, np.uint8)
         got = _run(lc, inp, P, d, "f32")[0]
-        assert rel_fro(got, _ref(inp, P, d, n)) <= TOL
+        assert_close(got, _ref(inp, P, d, n), TOL, 'Y')
 
 
 def test_packed_forward_degenerate(lc):
@@ -121,7 +121,7 @@ def test_packed_forward_full_size_sampled(lc, N, m, n):
     torch.cuda.synchronize()
     rows = np.unique(np.concatenate([np.arange(32), r.integers(0, m, 96), [m - 1]]))
     ref = orc.linear_forward_packed(P[rows], A.astype(np.float64), b.astype(np.float64), orc.widen(X, "bf16"), d, n)
-    assert rel_fro(to_host(Y)[:, rows], ref) <= TOL
+    assert_close(to_host(Y)[:, rows], ref, TOL, 'Y')
 
 
 @pytest.mark.parametrize("d", [8, 4])
@@ -134,7 +134,7 @@ def test_packed_forward_few_tokens_long_rows(lc, N, m, n, d):
     Two calls give the same bits (the offsets are summed in a fixed order)."""
     inp, P = _inputs(N, m, n, d, seed=m + N + d)
     got = _run(lc, inp, P, d, "f32", calls=2)
-    assert rel_fro(got[0], _ref(inp, P, d, n)) <= TOL
+    assert_close(got[0], _ref(inp, P, d, n), TOL, 'Y')
     assert np.array_equal(got[0], got[1])
 
 
@@ -153,4 +153,4 @@ def test_packed_forward_full_size_two_three_tokens(lc, N):
     torch.cuda.synchronize()
     rows = np.unique(np.concatenate([np.arange(32), r.integers(0, m, 96), [m - 1]]))
     ref = orc.linear_forward_packed(P[rows], A.astype(np.float64), b.astype(np.float64), orc.widen(X, "bf16"), d, n)
-    assert rel_fro(to_host(Y)[:, rows], ref) <= TOL
+    assert_close(to_host(Y)[:, rows], ref, TOL, 'Y')

@@ -9,7 +9,7 @@ import pytest
 
 import oracle as orc
 import synth
-from helpers import rel_fro, to_dev, to_host, unpack2bit
+from helpers import assert_close, to_dev, to_host, unpack2bit
 
 pytestmark = pytest.mark.gpu
 
@@ -86,29 +86,42 @@ def test_xavier_layer(lc, N, m, n, d, dtype, mask_mode, dge):
     got, ref, packed, mask = _run(lc, N, m, n, d, dtype, mask_mode, dge, seed=N + m + d)
     assert np.array_equal(packed, orc.pack2bit(ref["codes"]))
     for key in ("Y", "dX", "dZ", "dA", "db"):
-        assert rel_fro(got[key], ref[key]) <= TOL[dtype], (key, rel_fro(got[key], ref[key]))
+        assert_close(got[key], ref[key], TOL[dtype], key)
     assert np.all(got["dZ"][~mask] == 0.0)
     assert mask.any() and (~mask).any()
 
 
+def test_xavier_quantizer_values(lc):
+    """lcvq_xavier_quantizer against eq. xavier_preprocess: (1 / s', t) rounded to fp32."""
+    for m, n in ((4096, 4096), (11008, 4096), (3, 5)):
+        sp, t = orc.xavier_params(m, n)
+        qs, qb = lc.xavier_quantizer(m, n)
+        assert qs == float(np.float32(1.0 / sp)) and qb == float(np.float32(t))
+
+
+@pytest.mark.parametrize("src", ["u8", "packed"])
 @pytest.mark.parametrize("dtype", ["bf16", "f32"])
-def test_xavier_init_round_trip(lc, dtype):
-    """codes -> W_p = s'(W_z - t) (lcvq_dequant) -> forward with the Xavier quantiser
-    returns the same codes."""
+def test_xavier_init_round_trip(lc, dtype, src):
+    """codes -> W_p = s'(W_z - t) (lcvq_xavier_init) -> forward with the Xavier quantiser
+    returns the same codes; W_p equals lcvq_dequant with A = s' I, b = -s' t bit for bit."""
     import torch
-    m, n, d = 200, 256, 8
+    m, n, d = 200, 264, 8
     codes = synth.rng(5).integers(0, 4, size=(m, n), dtype=np.uint8)
     tdt = torch.bfloat16 if dtype == "bf16" else torch.float32
-    W = lc.xavier_init(torch.from_numpy(codes).cuda(), m, n, d, out_dtype=tdt)
+    csrc = torch.from_numpy(codes if src == "u8" else orc.pack2bit(codes)).cuda()
+    W = lc.xavier_init(csrc, m, n, out_dtype=tdt)
     qs, qb = lc.xavier_quantizer(m, n)
     packed = torch.empty((m, n // 4), dtype=torch.uint8, device="cuda")
     X = torch.zeros((4, n), dtype=tdt, device="cuda")
     lc.linear_fwd(W, torch.eye(d, device="cuda"), torch.zeros(d, device="cuda"), X, d, packed_out=packed,
                   q_scale=qs, q_shift=qb)
+    sp, t = orc.xavier_params(m, n)
+    Wd = lc.dequant(csrc, torch.eye(d, device="cuda") * sp, torch.full((d,), -sp * t, device="cuda"), d, n=n,
+                    src_kind=lc.SRC_CODES_U8 if src == "u8" else lc.SRC_PACKED2, out_dtype=tdt)
     torch.cuda.synchronize()
     assert np.array_equal(packed.cpu().numpy(), orc.pack2bit(codes))
-    sp, t = orc.xavier_params(m, n)
-    assert rel_fro(to_host(W), sp * (codes.astype(np.float64) - t)) <= (4e-3 if dtype == "bf16" else 1e-7)
+    assert torch.equal(W, Wd)
+    assert_close(to_host(W), sp * (codes.astype(np.float64) - t), 4e-3 if dtype == "bf16" else 1e-7, "W_p")
 
 
 @pytest.mark.parametrize("dtype", ["bf16", "f32"])
