@@ -55,8 +55,11 @@ def fp32_band(W, A, b, d):
     ninv = np.abs(Ainv).sum(axis=1).max()
     kappa = np.abs(A64).sum(axis=1).max() * ninv
     m, n = W.shape
-    T = np.abs(W.reshape(m, n // d, d) - np.asarray(b, np.float64)).sum(axis=-1, keepdims=True)
-    band = 2.0 * U32 * (4 * d * kappa + d + 1) * ninv * T
+    with np.errstate(invalid="ignore"):
+        T = np.abs(W.reshape(m, n // d, d) - np.asarray(b, np.float64)).sum(axis=-1, keepdims=True)
+    # a group with a non-finite weight has an infinite or NaN v: no rounding
+    # band, its codes must match exactly
+    band = 2.0 * U32 * (4 * d * kappa + d + 1) * ninv * np.where(np.isfinite(T), T, 0.0)
     return np.broadcast_to(band, (m, n // d, d)).reshape(m, n)
 
 
