@@ -230,6 +230,30 @@ lcvq_status_t lcvq_linear_fwd_packed(int64_t N, int64_t m, int64_t n, int32_t d,
                                      void *workspace, size_t workspace_bytes, void *stream);
 
 /*
+ * lcvq_linear_fwd_packed_noalloc -- lcvq_linear_fwd_packed for callers that
+ * cannot allocate device memory (code under HIP graph capture, tight serving
+ * loops, harnesses that forbid allocation): the same kernels and the same
+ * results bit for bit, with the workspace replaced by a fixed array of
+ * lcvq_packed_scratch_bytes() = 8 MiB that the library holds per device until
+ * the process ends.  Nothing is allocated by this call.  The caller still
+ * passes inputs and outputs; every other argument is as in
+ * lcvq_linear_fwd_packed.
+ *   - A shape whose workspace (lcvq_workspace_bytes(LCVQ_OP_FWD_PACKED, ...))
+ *     exceeds the array returns LCVQ_EUNSUPPORTED before anything is enqueued
+ *     (every m x n up to 16384 x 131072 fits).
+ *   - The stream must belong to the current device (the array's address is
+ *     looked up for the current device).
+ *   - All calls on one device share that device's array: calls that overlap in
+ *     time on one device (different streams, or host threads) race and give
+ *     wrong results.  What must start at zero is cleared by each call.
+ */
+lcvq_status_t lcvq_linear_fwd_packed_noalloc(int64_t N, int64_t m, int64_t n, int32_t d, const uint8_t *packed,
+                                             const float *A, const float *b, const void *X, void *Y,
+                                             int32_t y_dtype, void *stream);
+/* Size in bytes of the per-device array of lcvq_linear_fwd_packed_noalloc. */
+size_t lcvq_packed_scratch_bytes(void);
+
+/*
  * lcvq_linear_bwd -- straight-through backward of lcvq_linear_fwd (Sec. 3.3):
  *   dX = dY W_hat                                   (N x n, written, type dtype)
  *   dW = dY^T X  (never stored)

@@ -15,7 +15,7 @@ from . import _lib
 from ._lib import (BF16, EST_DGE, EST_STE, F32, MASK_LATENT, MASK_ROUNDED, OP_BWD, OP_FWD, OP_FWD_PACKED,  # noqa: F401
                    SRC_CODES_U8, SRC_LATENT, SRC_PACKED2, LcvqError)
 
-__all__ = ["linear_fwd", "linear_fwd_packed", "linear_bwd", "linear_bwd_dge", "xavier_quantizer", "xavier_init",
+__all__ = ["linear_fwd", "linear_fwd_packed", "linear_fwd_packed_noalloc", "linear_bwd", "linear_bwd_dge", "xavier_quantizer", "xavier_init",
            "pack2bit", "dequant", "encode", "adamw_step", "workspace_bytes", "LcvqError", "MASK_ROUNDED", "MASK_LATENT",
            "SRC_LATENT", "SRC_CODES_U8", "SRC_PACKED2", "EST_STE", "EST_DGE"]
 
@@ -246,6 +246,25 @@ def linear_fwd_packed(packed: torch.Tensor, A: torch.Tensor, b: torch.Tensor, X:
                                                   _dev(X, "X"), _dev(out, "Y"), _DT[out.dtype],
                                                   _dev(ws, "workspace"), ws.numel(), _stream(X.device)),
                "lcvq_linear_fwd_packed")
+    return out
+
+
+def linear_fwd_packed_noalloc(packed: torch.Tensor, A: torch.Tensor, b: torch.Tensor, X: torch.Tensor, d: int,
+                              out: torch.Tensor) -> torch.Tensor:
+    """linear_fwd_packed without a workspace: the library's fixed per-device scratch
+    array takes its place (for callers that cannot allocate).  `out` (N x m, bf16 or
+    fp32) is the caller's; calls that overlap on one device race."""
+    m, n4 = _check_2d(packed, "packed")
+    n = 4 * n4
+    _check(packed, "packed", dtype=torch.uint8)
+    N = _check_2d(X, "X")[0]
+    _check(X, "X", (N, n), torch.bfloat16)
+    _check_map(A, b, d)
+    _check(out, "out", (N, m), (torch.float32, torch.bfloat16))
+    _lib.check(_lib.load().lcvq_linear_fwd_packed_noalloc(N, m, n, d, _dev(packed, "packed"), _dev(A, "A"),
+                                                          _dev(b, "b"), _dev(X, "X"), _dev(out, "Y"),
+                                                          _DT[out.dtype], _stream(X.device)),
+               "lcvq_linear_fwd_packed_noalloc")
     return out
 
 

@@ -38,6 +38,8 @@ SIGNATURES = {
                                   _P, _I32, _I32, ctypes.c_float, ctypes.c_float, _I32, _P, _P, _I32, _P, _P, _P,
                                   _SZ, _P]),
     "lcvq_linear_fwd_packed": (_I32, [_I64, _I64, _I64, _I32, _P, _P, _P, _P, _P, _I32, _P, _SZ, _P]),
+    "lcvq_linear_fwd_packed_noalloc": (_I32, [_I64, _I64, _I64, _I32, _P, _P, _P, _P, _P, _I32, _P]),
+    "lcvq_packed_scratch_bytes": (_SZ, []),
     "lcvq_linear_bwd": (_I32, [_I64, _I64, _I64, _I32, _I32, _P, _P, _P, _P, _P, _I32, _I32,
                                _P, _P, _I32, _P, _P, _P, _SZ, _P]),
     "lcvq_linear_bwd_dge": (_I32, [_I64, _I64, _I64, _I32, _I32, _P, _P, _P, _P, _P, _I32, ctypes.c_float,

@@ -517,6 +517,62 @@ lcvq_status_t lcvq_linear_fwd_packed(int64_t N, int64_t m, int64_t n, int32_t d,
 
 }  // extern "C"
 
+// ---- scratch of the allocation-free packed forward --------------------------
+// A fixed device array takes the place of the workspace argument: X'' of 16
+// tokens, the partial sums of s, the split-K partial tiles and the tile
+// counters (which the prepass zeroes on every call).  Each device that runs the
+// call holds its own copy until the process ends; in host code `scratch` is
+// only a stand-in for the symbol, so its device address is looked up once per
+// device (hipGetSymbolAddress, with that device current) and only that address
+// is ever passed to kernels.
+static constexpr size_t kScratchBytes = (size_t)8 << 20;
+static __device__ __align__(256) char scratch[kScratchBytes];
+
+namespace {
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void *g_scratch_ptr[kMaxDevices] = {};
+
+// The device address of `scratch` on the current device.
+lcvq_status_t scratch_of_current_device(void **ptr) {
+  int dev = -1;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return hip_fail(e, "hipGetDevice");
+  if (dev < 0 || dev >= kMaxDevices) return fail(LCVQ_EUNSUPPORTED, "device %d (at most %d devices)", dev, kMaxDevices);
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (g_scratch_ptr[dev] == nullptr) {
+    void *p = nullptr;
+    e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess) return hip_fail(e, "hipGetSymbolAddress(scratch)");
+    if (p == nullptr || ((uintptr_t)p & 255u) != 0) return fail(LCVQ_EHIP, "scratch address %p", p);
+    g_scratch_ptr[dev] = p;
+  }
+  *ptr = g_scratch_ptr[dev];
+  return LCVQ_OK;
+}
+}  // namespace
+
+extern "C" {
+
+size_t lcvq_packed_scratch_bytes(void) { return kScratchBytes; }
+
+lcvq_status_t lcvq_linear_fwd_packed_noalloc(int64_t N, int64_t m, int64_t n, int32_t d, const uint8_t *packed,
+                                             const float *A, const float *b, const void *X, void *Y,
+                                             int32_t y_dtype, void *stream) {
+  // the size check needs no device: reject before touching the runtime
+  if (m > 0 && n > 0 && m < kMaxLd && n < kMaxLd && n % 64 == 0 && packed_layout(m, n).total > kScratchBytes)
+    return fail(LCVQ_EUNSUPPORTED, "m=%lld n=%lld needs %zu bytes of scratch, the static array holds %zu",
+                (long long)m, (long long)n, packed_layout(m, n).total, kScratchBytes);
+  void *ws = nullptr;
+  if (N > 0 && m > 0 && n > 0) {
+    const lcvq_status_t s = scratch_of_current_device(&ws);
+    if (s != LCVQ_OK) return s;
+  }
+  return lcvq_linear_fwd_packed(N, m, n, d, packed, A, b, X, Y, y_dtype, ws, ws ? kScratchBytes : 0, stream);
+}
+
+}  // extern "C"
+
 // Both backward entry points: `est` selects the estimator of the latent's gradient.
 static lcvq_status_t linear_bwd(int64_t N, int64_t m, int64_t n, int32_t d, int32_t dtype, const void *Z,
                                 const lcvq::Quantizer &qz, const float *A, const float *b, const void *X,
