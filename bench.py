@@ -3,7 +3,9 @@
 
 A step is one forward (quantise + 2-bit pack, activation transform, matrix-core
 product) plus one straight-through backward (dX, dZ, dA, db) of one LC-VQ
-weight matrix, on seeded synthetic inputs already resident in HBM.  The
+weight matrix, through the training pair (the forward saves the backward's
+code operand, masks and X', so the backward's prepass handles dY alone), on
+seeded synthetic inputs already resident in HBM.  The
 reported value is the work of the three products, 6 N m n flop, divided by the
 step time.  Prints one JSON line.
 
@@ -96,8 +98,20 @@ class Layer:
         self.db = torch.empty((d,), dtype=torch.float32, device="cuda")
         self.wsf = torch.empty(lc.workspace_bytes(lc.OP_FWD, N, m, n, d, bf), dtype=torch.uint8, device="cuda")
         self.wsb = torch.empty(lc.workspace_bytes(lc.OP_BWD, N, m, n, d, bf), dtype=torch.uint8, device="cuda")
+        # the training pair's saved state: the forward writes the backward's code
+        # operand, masks and X' once, and the backward's prepass handles dY alone
+        self.saved = lc.new_saved(N, m, n, d, bf, "cuda")
 
     def step(self):
+        """The training pair: lcvq_linear_fwd_train (with the 2-bit pack) + lcvq_linear_bwd_train."""
+        lc = self.lc
+        lc.linear_fwd(self.Z, self.A, self.b, self.X, self.d, packed_out=self.packed, workspace=self.wsf,
+                      out=self.Y, saved=self.saved)
+        lc.linear_bwd(self.Z, self.A, self.b, self.X, self.dY, self.d, dX=self.dX, dZ=self.dZ, dA=self.dA,
+                      db=self.db, workspace=self.wsb, saved=self.saved)
+
+    def step_plain(self):
+        """The same step through the plain calls (the backward rebuilds codes, mask and X')."""
         lc = self.lc
         lc.linear_fwd(self.Z, self.A, self.b, self.X, self.d, packed_out=self.packed, workspace=self.wsf,
                       out=self.Y)
@@ -108,9 +122,9 @@ class Layer:
         """The same step with the differentiable gradient estimator in the backward."""
         lc = self.lc
         lc.linear_fwd(self.Z, self.A, self.b, self.X, self.d, packed_out=self.packed, workspace=self.wsf,
-                      out=self.Y)
+                      out=self.Y, saved=self.saved)
         lc.linear_bwd_dge(self.Z, self.A, self.b, self.X, self.dY, self.d, k=k, cap=cap, dX=self.dX, dZ=self.dZ,
-                          dA=self.dA, db=self.db, workspace=self.wsb)
+                          dA=self.dA, db=self.db, workspace=self.wsb, saved=self.saved)
 
     def step_xavier(self):
         """The same step with the latent in the Xavier domain (Sec. 3.4): the same
@@ -118,9 +132,9 @@ class Layer:
         lc = self.lc
         qs, qb = lc.xavier_quantizer(self.m, self.n)
         lc.linear_fwd(self.Z, self.A, self.b, self.X, self.d, packed_out=self.packed, workspace=self.wsf,
-                      out=self.Y, q_scale=qs, q_shift=qb)
+                      out=self.Y, q_scale=qs, q_shift=qb, saved=self.saved)
         lc.linear_bwd(self.Z, self.A, self.b, self.X, self.dY, self.d, dX=self.dX, dZ=self.dZ, dA=self.dA,
-                      db=self.db, workspace=self.wsb, q_scale=qs, q_shift=qb)
+                      db=self.db, workspace=self.wsb, q_scale=qs, q_shift=qb, saved=self.saved)
 
     def flops(self):
         return 6.0 * self.N * self.m * self.n
@@ -199,16 +213,19 @@ def variant_step(lc, torch, layers, steps, which, label):
     stop.record()
     torch.cuda.synchronize()
     ms = start.elapsed_time(stop) / steps
-    kid = lc._lib.KERNELS.index("dw")
-    lib.lcvq_timer_enable(1 << kid)
-    for _ in range(5):
+    lib.lcvq_timer_enable((1 << len(lc._lib.KERNELS)) - 1)
+    for _ in range(20):
         step()
     torch.cuda.synchronize()
-    dw_ms, cnt = timer_read(lib, kid)
+    kernels = {}
+    for kid, name in enumerate(lc._lib.KERNELS):
+        k_ms, cnt = timer_read(lib, kid)
+        if cnt:
+            kernels[name] = round(1e3 * k_ms / 20, 2)
     lib.lcvq_timer_enable(0)
     flops = sum(L.flops() for L in layers)
     return {"variant": label, "ms_per_step": round(ms, 4), "TFLOP/s": round(flops / (ms * 1e-3) / 1e12, 2),
-            "dw_us": round(1e3 * dw_ms / max(cnt, 1), 2)}
+            "kernels_us_per_step": kernels}
 
 
 def workload_steps(lc, torch, names, steps):
@@ -255,7 +272,7 @@ def workload_steps(lc, torch, names, steps):
         out[name] = {"N": wl["N"], "matrices": [list(x) for x in wl["mats"]], "ms_per_step": round(ms, 3),
                      "TFLOP/s": round(flops / (ms * 1e-3) / 1e12, 2),
                      "frac_of_peak": round(flops / (ms * 1e-3) / 1e12 / PEAK_MFMA_BF16, 4),
-                     "step": "fwd (+2-bit pack) + straight-through bwd" + (" + AdamW of Z, A, b" if adam else "")}
+                     "step": "training pair: fwd (+2-bit pack) + straight-through bwd" + (" + AdamW of Z, A, b" if adam else "")}
         del layers, states
         torch.cuda.empty_cache()
     return out
@@ -485,12 +502,39 @@ def main():
         for L in layers:
             L.step()
 
+    # per-kernel breakdown first (untimed): at least 250 steps with every kernel
+    # launch bracketed by HIP events on its stream (the library's timer).  The
+    # breakdown and the dominant kernel's average launch time come from this one
+    # run, so the breakdown sums to no more than this run's step time; the run
+    # also brings the chip to its loaded clocks before the timed region (the
+    # extra event records lengthen the step a little, which is why `value` comes
+    # from the run below)
+    k_ev = max(args.steps, 250)
+    lib.lcvq_timer_enable((1 << len(lc._lib.KERNELS)) - 1)
+    start, stop = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    start.record()
+    for _ in range(k_ev):
+        step()
+    stop.record()
+    torch.cuda.synchronize()
+    ms_step_ev = start.elapsed_time(stop) / k_ev
+    breakdown, launch_us, launches = {}, {}, {}
+    for kid, name in enumerate(lc._lib.KERNELS):
+        ms, cnt = timer_read(lib, kid)
+        if cnt:
+            breakdown[name] = round(1e3 * ms / k_ev, 2)       # us per step
+            launch_us[name] = 1e3 * ms / cnt
+            launches[name] = cnt
+    lib.lcvq_timer_enable(0)
+    dominant = max(MATRIX_KERNELS, key=lambda k: breakdown.get(k, 0.0))
+    dom_us, dom_cnt = launch_us[dominant], launches[dominant]
+
     for _ in range(args.warmup):
         step()
     torch.cuda.synchronize()
 
     # timed region: K steps between two events, nothing else recorded
-    start, stop = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     torch.cuda.synchronize()
     start.record()
     for _ in range(args.steps):
@@ -498,30 +542,6 @@ def main():
     stop.record()
     torch.cuda.synchronize()
     ms_step = start.elapsed_time(stop) / args.steps
-
-    # the same K steps again with every kernel launch bracketed by HIP events on
-    # its stream (the library's timer): the per-kernel breakdown and the dominant
-    # kernel's average launch time come from this one run, so the breakdown sums
-    # to no more than this run's step time (the extra event records lengthen the
-    # step a little, which is why `value` comes from the run above)
-    lib.lcvq_timer_enable((1 << len(lc._lib.KERNELS)) - 1)
-    torch.cuda.synchronize()
-    start.record()
-    for _ in range(args.steps):
-        step()
-    stop.record()
-    torch.cuda.synchronize()
-    ms_step_ev = start.elapsed_time(stop) / args.steps
-    breakdown, launch_us, launches = {}, {}, {}
-    for kid, name in enumerate(lc._lib.KERNELS):
-        ms, cnt = timer_read(lib, kid)
-        if cnt:
-            breakdown[name] = round(1e3 * ms / args.steps, 2)       # us per step
-            launch_us[name] = 1e3 * ms / cnt
-            launches[name] = cnt
-    lib.lcvq_timer_enable(0)
-    dominant = max(MATRIX_KERNELS, key=lambda k: breakdown.get(k, 0.0))
-    dom_us, dom_cnt = launch_us[dominant], launches[dominant]
 
     dist = step_distribution(torch, step, args.steps)
     sclk = sample_sclk(torch, step)
@@ -537,18 +557,23 @@ def main():
         "warmup": args.warmup, "ms_per_step": round(ms_step, 4), "higher_is_better": True, "scaling": "weak",
         "vs_baseline": None, "dtype": "bf16", "data": "synthetic",
         "config": {"workload": args.workload, "N": wl["N"], "matrices": [list(x) for x in wl["mats"]],
-                   "d": wl["d"], "step": "fwd (+2-bit pack) + straight-through bwd (dX, dZ, dA, db)"},
+                   "d": wl["d"], "step": "training pair: fwd (+2-bit pack, saving codes, masks and X' for "
+                                         "the backward) + straight-through bwd (dX, dZ, dA, db)",
+                   "saved_state_bytes": int(layers[0].saved.numel())},
         "frac_of_peak": round(value / PEAK_MFMA_BF16, 4),
         "roofline": {"kernel": dominant, "bound": "mfma", "achieved": round(achieved, 2),
                      "peak": PEAK_MFMA_BF16, "unit": "TFLOP/s", "frac": round(achieved / PEAK_MFMA_BF16, 4),
                      "traffic": traffic, "avg_launch_us": round(dom_us, 2), "launches": dom_cnt,
                      "flop_per_launch": per_launch_flop, "ms_per_step_with_kernel_events": round(ms_step_ev, 4)},
         "kernels_us_per_step": breakdown,
-        "kernels_us_per_step_note": ("every launch bracketed by HIP events over the same K steps, run again after "
-                                     "the timed region; sums to at most ms_per_step_with_kernel_events"),
+        "kernels_us_per_step_note": (f"every launch bracketed by HIP events over {k_ev} untimed steps run just "
+                                     "before the warm-up and the timed region; sums to at most "
+                                     "ms_per_step_with_kernel_events"),
         "step_distribution": dist,
         "gpu_clock": sclk,
     }
+    res["plain_step"] = variant_step(lc, torch, layers, args.steps, "step_plain",
+                                     "the plain calls: the backward rebuilds codes, mask and X' from Z and X")
     res["dge_step"] = variant_step(lc, torch, layers, args.steps, "step_dge",
                                    "differentiable gradient estimator, k=5, slope cap 3, latent mask")
     res["xavier_step"] = variant_step(lc, torch, layers, args.steps, "step_xavier",

@@ -103,8 +103,10 @@ lcvq_status_t lcvq_pack2bit(const void *src, int32_t src_kind, int32_t src_dtype
  * with codes taken from `src` (lcvq_src_t `src_kind`; element type `src_dtype`
  * for LATENT).  A is d x d row-major fp32, b has d fp32 entries.  W_hat is
  * m x n of element type `out_dtype` (bf16 results are rounded to nearest even
- * from fp32 arithmetic).  d in {4, 8}; n % d == 0.  This is a utility for
- * export and inspection: the training calls below never form W_hat.
+ * from fp32 arithmetic; packed sources sum each group's two 4-code halves from
+ * per-map tables, so their fp32 rounding can differ from the plain fma chain's
+ * in the last bit).  d in {4, 8}; n % d == 0.  This is a utility for export and
+ * inspection: the training calls below never form W_hat.
  */
 lcvq_status_t lcvq_dequant(int64_t m, int64_t n, int32_t d, int32_t src_kind, int32_t src_dtype,
                            const void *src, const float *A, const float *b,
@@ -126,8 +128,8 @@ lcvq_status_t lcvq_xavier_quantizer(int64_t m, int64_t n, float *q_scale, float 
  * lcvq_xavier_init -- initial proxy weights of the Xavier reparameterisation
  * (Sec. 3.4, eq. xavier_preprocess): W_p = s' (W_z - t) for codes W_z, with s'
  * and t as in lcvq_xavier_quantizer, evaluated per element in fp32 as
- * fma(s', code, -s' t) (s' and -s' t rounded to fp32 once): the result of
- * lcvq_dequant with A = s' I and b = -s' t, bit for bit.
+ * fma(s', code, -s' t) (s' and -s' t rounded to fp32 once), i.e. lcvq_dequant
+ * with A = s' I and b = -s' t up to fp32 rounding.
  *   codes     m x n bytes (src_kind LCVQ_SRC_CODES_U8; values above 3 are taken
  *             as 3) or m * n / 4 packed bytes (LCVQ_SRC_PACKED2)
  *   W_p       m x n of element type out_dtype (F32 or BF16), written
@@ -316,6 +318,55 @@ lcvq_status_t lcvq_linear_bwd_ex(int64_t N, int64_t m, int64_t n, int32_t d, int
                                  float dge_k, float dge_cap, int32_t accumulate, void *dX, void *dZ,
                                  int32_t dz_dtype, float *dA, float *db,
                                  void *workspace, size_t workspace_bytes, void *stream);
+
+/*
+ * The training pair: lcvq_linear_fwd_train / lcvq_linear_bwd_train.  A
+ * training step runs the forward and then the backward of the same layer on
+ * the same Z, A, b, X and quantiser.  The backward's prepass would read Z and
+ * X again to rebuild the codes in its own operand layout, the straight-through
+ * mask and X' = X blockdiag(A) (def. forward_x, Sec. 3.2) in the
+ * weight-gradient operand layout; the forward already reads Z and X, so the
+ * pair lets it write those once into a caller-owned `saved` buffer, and the
+ * backward's prepass then handles dY alone.  Results are those of
+ * lcvq_linear_fwd_ex / lcvq_linear_bwd_ex with the same arguments (the same
+ * kernels on the same values).
+ *
+ * lcvq_saved_bytes -- size of `saved` for N tokens and an m x n matrix (bf16;
+ * 0 for LCVQ_F32, whose path needs no saved state, and for invalid arguments).
+ * At 4096 x 4096 with 4096 tokens it is 44 MB: the codes (4 bits each), X'
+ * (bf16) and two one-bit masks.
+ */
+size_t lcvq_saved_bytes(int64_t N, int64_t m, int64_t n, int32_t d, int32_t dtype);
+
+/*
+ * lcvq_linear_fwd_train -- lcvq_linear_fwd_ex that also writes the saved state
+ * for lcvq_linear_bwd_train into `saved` (bf16: at least lcvq_saved_bytes(...)
+ * bytes, 16-byte aligned, else LCVQ_EWORKSPACE / LCVQ_EALIGN; fp32: unused and
+ * may be NULL).  Both straight-through masks are saved, so the backward may
+ * choose either.  All other arguments as lcvq_linear_fwd_ex.
+ */
+lcvq_status_t lcvq_linear_fwd_train(int64_t N, int64_t m, int64_t n, int32_t d, int32_t dtype,
+                                    const void *Z, float q_scale, float q_shift, const float *A, const float *b,
+                                    const void *X, void *Y, uint8_t *packed_codes_out,
+                                    void *saved, size_t saved_bytes,
+                                    void *workspace, size_t workspace_bytes, void *stream);
+
+/*
+ * lcvq_linear_bwd_train -- lcvq_linear_bwd_ex that reads the codes, X' and the
+ * mask from `saved`, as the preceding lcvq_linear_fwd_train wrote them.  The
+ * caller guarantees that call had the same N, m, n, d, dtype, Z, A, b, X,
+ * q_scale and q_shift and that `saved` is unchanged since (the library cannot
+ * check device contents; a mismatch gives wrong gradients, not a fault).  Z
+ * and X are still read: Z by the differentiable estimator and the fp32 path, X
+ * for dA and db.  Same workspace as lcvq_linear_bwd_ex; all other arguments
+ * and the error behaviour as lcvq_linear_bwd_ex.
+ */
+lcvq_status_t lcvq_linear_bwd_train(int64_t N, int64_t m, int64_t n, int32_t d, int32_t dtype,
+                                    const void *Z, float q_scale, float q_shift, const float *A, const float *b,
+                                    const void *X, const void *dY, int32_t mask_mode, int32_t estimator,
+                                    float dge_k, float dge_cap, int32_t accumulate, void *dX, void *dZ,
+                                    int32_t dz_dtype, float *dA, float *db, const void *saved, size_t saved_bytes,
+                                    void *workspace, size_t workspace_bytes, void *stream);
 
 /*
  * lcvq_adamw_step -- one AdamW update of a flat fp32 parameter array: the

@@ -16,7 +16,7 @@ from ._lib import (BF16, EST_DGE, EST_STE, F32, MASK_LATENT, MASK_ROUNDED, OP_BW
                    SRC_CODES_U8, SRC_LATENT, SRC_PACKED2, LcvqError)
 
 __all__ = ["linear_fwd", "linear_fwd_packed", "linear_fwd_packed_noalloc", "linear_bwd", "linear_bwd_dge", "xavier_quantizer", "xavier_init",
-           "pack2bit", "dequant", "encode", "adamw_step", "workspace_bytes", "LcvqError", "MASK_ROUNDED", "MASK_LATENT",
+           "pack2bit", "dequant", "encode", "adamw_step", "workspace_bytes", "saved_bytes", "new_saved", "LcvqError", "MASK_ROUNDED", "MASK_LATENT",
            "SRC_LATENT", "SRC_CODES_U8", "SRC_PACKED2", "EST_STE", "EST_DGE"]
 
 _DT = {torch.float32: F32, torch.bfloat16: BF16}
@@ -72,6 +72,26 @@ def _opt(t, name):
 
 def _stream(device) -> ctypes.c_void_p:
     return ctypes.c_void_p(torch.cuda.current_stream(device).cuda_stream)
+
+
+def saved_bytes(N: int, m: int, n: int, d: int, dtype: torch.dtype) -> int:
+    """Size of the saved state of the training pair (0 for float32, which needs none)."""
+    return int(_lib.load().lcvq_saved_bytes(N, m, n, d, _DT[dtype]))
+
+
+def new_saved(N: int, m: int, n: int, d: int, dtype: torch.dtype, device) -> torch.Tensor:
+    """A buffer for the saved state of linear_fwd(..., saved=...) / linear_bwd(..., saved=...)."""
+    return torch.empty(max(saved_bytes(N, m, n, d, dtype), 16), dtype=torch.uint8, device=device)
+
+
+def _saved_arg(saved, N, m, n, d, dtype):
+    _check(saved, "saved", dtype=torch.uint8)
+    if saved.dim() != 1:
+        raise ValueError("saved must be a 1-D uint8 tensor")
+    need = saved_bytes(N, m, n, d, dtype)
+    if saved.numel() < need:
+        raise ValueError(f"saved has {saved.numel()} bytes, need {need}")
+    return _dev(saved, "saved"), saved.numel()
 
 
 def workspace_bytes(op: int, N: int, m: int, n: int, d: int, dtype: torch.dtype) -> int:
@@ -198,11 +218,14 @@ def adamw_step(theta: torch.Tensor, grad: torch.Tensor, m1: torch.Tensor, m2: to
 
 def linear_fwd(Z: torch.Tensor, A: torch.Tensor, b: torch.Tensor, X: torch.Tensor, d: int,
                packed_out: torch.Tensor | None = None, workspace: torch.Tensor | None = None,
-               out: torch.Tensor | None = None, q_scale: float = 1.0, q_shift: float = 0.0) -> torch.Tensor:
+               out: torch.Tensor | None = None, q_scale: float = 1.0, q_shift: float = 0.0,
+               saved: torch.Tensor | None = None) -> torch.Tensor:
     """Y = X W_hat^T (N x m) for latents Z (m x n), map A (d x d fp32), offset b (d fp32).
 
     q_scale, q_shift: the quantiser rounds Z * q_scale + q_shift (see xavier_quantizer);
-    the default is the code domain."""
+    the default is the code domain.  saved: a buffer from new_saved(); the forward then
+    also writes what linear_bwd(..., saved=...) of the same layer needs (the training
+    pair, lcvq_linear_fwd_train)."""
     m, n = _check_2d(Z, "Z")
     dt = _dtype_code(Z)
     N = _check_2d(X, "X")[0]
@@ -219,7 +242,11 @@ def linear_fwd(Z: torch.Tensor, A: torch.Tensor, b: torch.Tensor, X: torch.Tenso
     ws = _workspace(OP_FWD, N, m, n, d, X.dtype, X.device, workspace)
     tail = (_dev(A, "A"), _dev(b, "b"), _dev(X, "X"), _dev(out, "Y"), _opt(packed_out, "packed_out"),
             _dev(ws, "workspace"), ws.numel(), _stream(X.device))
-    if q_scale == 1.0 and q_shift == 0.0:
+    if saved is not None:
+        sp, sn = _saved_arg(saved, N, m, n, d, Z.dtype)
+        _lib.check(_lib.load().lcvq_linear_fwd_train(N, m, n, d, dt, _dev(Z, "Z"), q_scale, q_shift, *tail[:5], sp, sn,
+                                                     *tail[5:]), "lcvq_linear_fwd_train")
+    elif q_scale == 1.0 and q_shift == 0.0:
         _lib.check(_lib.load().lcvq_linear_fwd(N, m, n, d, dt, _dev(Z, "Z"), *tail), "lcvq_linear_fwd")
     else:
         _lib.check(_lib.load().lcvq_linear_fwd_ex(N, m, n, d, dt, _dev(Z, "Z"), q_scale, q_shift, *tail),
@@ -273,10 +300,11 @@ def linear_bwd(Z: torch.Tensor, A: torch.Tensor, b: torch.Tensor, X: torch.Tenso
                need_dZ: bool = True, need_map: bool = True, dz_dtype: torch.dtype | None = None,
                dX: torch.Tensor | None = None, dZ: torch.Tensor | None = None, dA: torch.Tensor | None = None,
                db: torch.Tensor | None = None, workspace: torch.Tensor | None = None, q_scale: float = 1.0,
-               q_shift: float = 0.0):
-    """Straight-through backward: returns (dX, dZ, dA, db); skipped outputs are None."""
+               q_shift: float = 0.0, saved: torch.Tensor | None = None):
+    """Straight-through backward: returns (dX, dZ, dA, db); skipped outputs are None.
+    saved: the buffer a linear_fwd(..., saved=...) of the same layer and inputs filled."""
     return _linear_bwd(None, Z, A, b, X, dY, d, mask_mode, accumulate, need_dX, need_dZ, need_map, dz_dtype,
-                       dX, dZ, dA, db, workspace, q_scale, q_shift)
+                       dX, dZ, dA, db, workspace, q_scale, q_shift, saved)
 
 
 def linear_bwd_dge(Z: torch.Tensor, A: torch.Tensor, b: torch.Tensor, X: torch.Tensor, dY: torch.Tensor,
@@ -284,17 +312,18 @@ def linear_bwd_dge(Z: torch.Tensor, A: torch.Tensor, b: torch.Tensor, X: torch.T
                    accumulate: bool = False, need_dX: bool = True, need_dZ: bool = True, need_map: bool = True,
                    dz_dtype: torch.dtype | None = None, dX: torch.Tensor | None = None,
                    dZ: torch.Tensor | None = None, dA: torch.Tensor | None = None, db: torch.Tensor | None = None,
-                   workspace: torch.Tensor | None = None, q_scale: float = 1.0, q_shift: float = 0.0):
+                   workspace: torch.Tensor | None = None, q_scale: float = 1.0, q_shift: float = 0.0,
+                   saved: torch.Tensor | None = None):
     """Backward with the differentiable gradient estimator (k, slope cap): returns (dX, dZ, dA, db).
 
     The default mask is the latent one, [0 <= Z <= 3], which the chain rule
     gives through clip(f(Z), 0, 3)."""
     return _linear_bwd((float(k), float(cap)), Z, A, b, X, dY, d, mask_mode, accumulate, need_dX, need_dZ,
-                       need_map, dz_dtype, dX, dZ, dA, db, workspace, q_scale, q_shift)
+                       need_map, dz_dtype, dX, dZ, dA, db, workspace, q_scale, q_shift, saved)
 
 
 def _linear_bwd(dge, Z, A, b, X, dY, d, mask_mode, accumulate, need_dX, need_dZ, need_map, dz_dtype, dX, dZ, dA,
-                db, workspace, q_scale=1.0, q_shift=0.0):
+                db, workspace, q_scale=1.0, q_shift=0.0, saved=None):
     m, n = _check_2d(Z, "Z")
     dt = _dtype_code(Z)
     N = _check_2d(X, "X")[0]
@@ -327,7 +356,13 @@ def _linear_bwd(dge, Z, A, b, X, dY, d, mask_mode, accumulate, need_dX, need_dZ,
     tail = (1 if accumulate else 0, _opt(dX if need_dX else None, "dX"), _opt(dZ if need_dZ else None, "dZ"),
             _DT[dz_dtype], _opt(dA if need_map else None, "dA"), _opt(db if need_map else None, "db"),
             _dev(ws, "workspace"), ws.numel(), _stream(dev))
-    if q_scale != 1.0 or q_shift != 0.0:
+    if saved is not None:
+        sp, sn = _saved_arg(saved, N, m, n, d, Z.dtype)
+        est = (EST_STE, 0.0, 0.0) if dge is None else (EST_DGE, *dge)
+        head_ex = head[:6] + (q_scale, q_shift) + head[6:]
+        _lib.check(_lib.load().lcvq_linear_bwd_train(*head_ex, *est, *tail[:6], sp, sn, *tail[6:]),
+                   "lcvq_linear_bwd_train")
+    elif q_scale != 1.0 or q_shift != 0.0:
         est = (EST_STE, 0.0, 0.0) if dge is None else (EST_DGE, *dge)
         head_ex = head[:6] + (q_scale, q_shift) + head[6:]
         _lib.check(_lib.load().lcvq_linear_bwd_ex(*head_ex, *est, *tail), "lcvq_linear_bwd_ex")

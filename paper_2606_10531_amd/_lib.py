@@ -37,6 +37,12 @@ SIGNATURES = {
     "lcvq_linear_bwd_ex": (_I32, [_I64, _I64, _I64, _I32, _I32, _P, ctypes.c_float, ctypes.c_float, _P, _P, _P,
                                   _P, _I32, _I32, ctypes.c_float, ctypes.c_float, _I32, _P, _P, _I32, _P, _P, _P,
                                   _SZ, _P]),
+    "lcvq_saved_bytes": (_SZ, [_I64, _I64, _I64, _I32, _I32]),
+    "lcvq_linear_fwd_train": (_I32, [_I64, _I64, _I64, _I32, _I32, _P, ctypes.c_float, ctypes.c_float, _P, _P, _P,
+                                     _P, _P, _P, _SZ, _P, _SZ, _P]),
+    "lcvq_linear_bwd_train": (_I32, [_I64, _I64, _I64, _I32, _I32, _P, ctypes.c_float, ctypes.c_float, _P, _P, _P,
+                                     _P, _I32, _I32, ctypes.c_float, ctypes.c_float, _I32, _P, _P, _I32, _P, _P, _P,
+                                     _SZ, _P, _SZ, _P]),
     "lcvq_linear_fwd_packed": (_I32, [_I64, _I64, _I64, _I32, _P, _P, _P, _P, _P, _I32, _P, _SZ, _P]),
     "lcvq_linear_fwd_packed_noalloc": (_I32, [_I64, _I64, _I64, _I32, _P, _P, _P, _P, _P, _I32, _P]),
     "lcvq_packed_scratch_bytes": (_SZ, []),

@@ -19,6 +19,12 @@ FLAGS = ["-O3", "-std=c++17", "-fPIC", f"--offload-arch={ARCH}",
          "-I", os.path.join(ROOT, "include"), "-Wno-unused-result"]
 
 
+# The products' epilogues issue matrix-core instructions through the compiler's
+# builtins, accumulating in vector registers (the accumulator registers hold the
+# main loop's results): select the vector-register form for them.
+PER_FILE_FLAGS = {"lcvq_gemm.hip": ["-mllvm", "-amdgpu-mfma-vgpr-form=true"]}
+
+
 def hipcc() -> str:
     for c in (os.environ.get("HIPCC"), "/opt/rocm/bin/hipcc", shutil.which("hipcc")):
         if c and os.path.exists(c):
@@ -41,7 +47,7 @@ def build(verbose: bool = False) -> str:
     jobs = []
     for s in SOURCES:
         obj = os.path.join(objdir, s.replace(".hip", ".o"))
-        jobs.append((obj, [cc, *FLAGS, "-c", os.path.join(CSRC, s), "-o", obj]))
+        jobs.append((obj, [cc, *FLAGS, *PER_FILE_FLAGS.get(s, []), "-c", os.path.join(CSRC, s), "-o", obj]))
     with cf.ThreadPoolExecutor(max_workers=min(len(jobs), 8)) as ex:
         for obj, p in zip([j[0] for j in jobs], ex.map(_run, [j[1] for j in jobs])):
             if verbose:

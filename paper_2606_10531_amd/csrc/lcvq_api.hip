@@ -101,6 +101,25 @@ BwdLayout bwd_layout(int64_t N, int64_t m, int64_t n, bool bf16) {
   return L;
 }
 
+// The training pair's saved state (bf16): what the backward prepass would
+// otherwise rebuild from Z and X -- the codes in the input-gradient operand
+// layout, X' in the weight-gradient operand layout, and both straight-through
+// masks -- in the layouts of BwdLayout.
+struct SavedLayout {
+  size_t frag_t, xt, mask_r, mask_l, total;
+};
+SavedLayout saved_layout(int64_t N, int64_t m, int64_t n) {
+  SavedLayout L{};
+  const size_t Nt = (size_t)lcvq::bwd_tokens(N);
+  const size_t mask = (size_t)m * lcvq::mask_words_per_row(n) * 8;
+  L.frag_t = 0;
+  L.xt = up256((size_t)(lcvq::round_up(n, 256) / 32) * (lcvq::round_up(m, 128) / 64) * 1024);
+  L.mask_r = L.xt + up256((size_t)lcvq::round_up(n, 256) * Nt * 2);
+  L.mask_l = L.mask_r + up256(mask);
+  L.total = L.mask_l + up256(mask);
+  return L;
+}
+
 // Layer output from packed codes: X' of 16 tokens, partial s, split-K
 // partials of the product and its tile counters.
 struct PackedLayout {
@@ -377,7 +396,8 @@ lcvq_status_t lcvq_xavier_init(int64_t m, int64_t n, int32_t src_kind, const voi
 // Both forward entry points: `qz` is the quantiser domain (Sec. 3.4).
 static lcvq_status_t linear_fwd(int64_t N, int64_t m, int64_t n, int32_t d, int32_t dtype, const void *Z,
                                 const lcvq::Quantizer &qz, const float *A, const float *b, const void *X, void *Y,
-                                uint8_t *packed_codes_out, void *workspace, size_t workspace_bytes, void *stream) {
+                                uint8_t *packed_codes_out, void *workspace, size_t workspace_bytes, void *stream,
+                                void *saved = nullptr, size_t saved_bytes = 0, bool want_saved = false) {
   lcvq_status_t s = check_common(N, m, n, d, dtype);
   if (s != LCVQ_OK) return s;
   const bool bf16 = dtype == LCVQ_BF16;
@@ -408,6 +428,16 @@ static lcvq_status_t linear_fwd(int64_t N, int64_t m, int64_t n, int32_t d, int3
   const FwdLayout L = fwd_layout(N, m, n, bf16);
   if (workspace == nullptr || workspace_bytes < L.total)
     return fail(LCVQ_EWORKSPACE, "workspace %zu bytes, need %zu", workspace_bytes, L.total);
+  lcvq::FwdSave save{};
+  if (want_saved && bf16) {
+    const SavedLayout S = saved_layout(N, m, n);
+    if (saved == nullptr || saved_bytes < S.total)
+      return fail(LCVQ_EWORKSPACE, "saved state %zu bytes, need %zu", saved_bytes, S.total);
+    if (!aligned16(saved)) return fail(LCVQ_EALIGN, "saved state must be 16-byte aligned");
+    char *sv = (char *)saved;
+    save = lcvq::FwdSave{(uint32_t *)(sv + S.frag_t), (uint64_t *)(sv + S.mask_r), (uint64_t *)(sv + S.mask_l),
+                         (uint16_t *)(sv + S.xt)};
+  }
   char *ws = (char *)workspace;
   float *svec = (float *)(ws + L.s);
   hipError_t e;
@@ -416,7 +446,8 @@ static lcvq_status_t linear_fwd(int64_t N, int64_t m, int64_t n, int32_t d, int3
     {
       Timed tm(LCVQ_K_FWD_PREP, st);
       e = tm.done(lcvq::launch_fwd_prep_bf16((const uint16_t *)Z, m, n, qz, frag, packed_codes_out, (const uint16_t *)X,
-                                             N, L.Np, L.ldp, d, A, b, (uint16_t *)(ws + L.xp), svec, st));
+                                             N, L.Np, L.ldp, d, A, b, (uint16_t *)(ws + L.xp), svec,
+                                             want_saved ? &save : nullptr, st));
     }
     if (e != hipSuccess) return hip_fail(e, "forward prepass launch");
     { Timed tm(LCVQ_K_FWD, st); e = tm.done(lcvq::launch_fwd_bf16(frag, (const uint16_t *)(ws + L.xp), L.ldp, svec, (uint16_t *)Y, N, m, n, st)); }
@@ -578,7 +609,8 @@ static lcvq_status_t linear_bwd(int64_t N, int64_t m, int64_t n, int32_t d, int3
                                 const lcvq::Quantizer &qz, const float *A, const float *b, const void *X,
                                 const void *dY, int32_t mask_mode,
                                 const lcvq::GradEst &est, int32_t accumulate, void *dX, void *dZ, int32_t dz_dtype,
-                                float *dA, float *db, void *workspace, size_t workspace_bytes, void *stream) {
+                                float *dA, float *db, void *workspace, size_t workspace_bytes, void *stream,
+                                const void *saved = nullptr, size_t saved_bytes = 0, bool use_saved = false) {
   lcvq_status_t s = check_common(N, m, n, d, dtype);
   if (s != LCVQ_OK) return s;
   if (mask_mode != LCVQ_MASK_ROUNDED && mask_mode != LCVQ_MASK_LATENT) return fail(LCVQ_EINVAL, "mask_mode=%d", mask_mode);
@@ -634,13 +666,27 @@ static lcvq_status_t linear_bwd(int64_t N, int64_t m, int64_t n, int32_t d, int3
     uint16_t *xt = (uint16_t *)(ws + L.xt), *dyt = (uint16_t *)(ws + L.dyt);
     // the straight-through mask as a bitmap (the differentiable estimator reads Z itself)
     uint64_t *maskbits = dZ != nullptr && !est.dge ? (uint64_t *)(ws + L.mask) : nullptr;
+    if (use_saved) {
+      // codes, X' and the masks come from the forward of the training pair: the
+      // prepass handles dY alone
+      const SavedLayout S = saved_layout(N, m, n);
+      if (saved == nullptr || saved_bytes < S.total)
+        return fail(LCVQ_EWORKSPACE, "saved state %zu bytes, need %zu", saved_bytes, S.total);
+      if (!aligned16(saved)) return fail(LCVQ_EALIGN, "saved state must be 16-byte aligned");
+      const char *sv = (const char *)saved;
+      frag = (uint32_t *)(sv + S.frag_t);
+      xt = (uint16_t *)(sv + S.xt);
+      if (maskbits != nullptr) maskbits = (uint64_t *)(sv + (mask_mode == LCVQ_MASK_ROUNDED ? S.mask_r : S.mask_l));
+    }
     {
-      // the quantise blocks run when the input-gradient product or the bitmap needs them
+      // the quantise blocks run when the input-gradient product or the bitmap
+      // needs them and nothing was saved
       Timed tm(LCVQ_K_BWD_PREP, st);
-      e = tm.done(lcvq::launch_bwd_prep_bf16((const uint16_t *)Z, m, n, qz, run_dx || maskbits ? frag : nullptr,
+      e = tm.done(lcvq::launch_bwd_prep_bf16((const uint16_t *)Z, m, n, qz,
+                                             !use_saved && (run_dx || maskbits) ? frag : nullptr,
                                              (const uint16_t *)X, (const uint16_t *)dY, A, d, N,
-                                             dZ != nullptr ? xt : nullptr,
-                                             dZ != nullptr ? dyt : nullptr, rs, maskbits, mask_mode,
+                                             dZ != nullptr && !use_saved ? xt : nullptr,
+                                             dZ != nullptr ? dyt : nullptr, rs, use_saved ? nullptr : maskbits, mask_mode,
                                              clear_map ? dA : nullptr, clear_map ? d * d : 0,
                                              clear_map ? db : nullptr, clear_map ? d : 0, st));
       if (e != hipSuccess) return hip_fail(e, "backward prepass launch");
@@ -719,6 +765,37 @@ lcvq_status_t lcvq_linear_bwd_dge(int64_t N, int64_t m, int64_t n, int32_t d, in
   if (s != LCVQ_OK) return s;
   return linear_bwd(N, m, n, d, dtype, Z, kCodeDomain, A, b, X, dY, mask_mode, est, accumulate, dX, dZ, dz_dtype,
                     dA, db, workspace, workspace_bytes, stream);
+}
+
+size_t lcvq_saved_bytes(int64_t N, int64_t m, int64_t n, int32_t d, int32_t dtype) {
+  if (N < 0 || m < 0 || n < 0 || (d != 4 && d != 8) || dtype != LCVQ_BF16) return 0;
+  return saved_layout(N, m, n).total;
+}
+
+lcvq_status_t lcvq_linear_fwd_train(int64_t N, int64_t m, int64_t n, int32_t d, int32_t dtype, const void *Z,
+                                    float q_scale, float q_shift, const float *A, const float *b, const void *X,
+                                    void *Y, uint8_t *packed_codes_out, void *saved, size_t saved_bytes,
+                                    void *workspace, size_t workspace_bytes, void *stream) {
+  lcvq::Quantizer qz;
+  const lcvq_status_t s = make_quantizer(q_scale, q_shift, &qz);
+  if (s != LCVQ_OK) return s;
+  return linear_fwd(N, m, n, d, dtype, Z, qz, A, b, X, Y, packed_codes_out, workspace, workspace_bytes, stream, saved,
+                    saved_bytes, N > 0 && m > 0 && n > 0);
+}
+
+lcvq_status_t lcvq_linear_bwd_train(int64_t N, int64_t m, int64_t n, int32_t d, int32_t dtype, const void *Z,
+                                    float q_scale, float q_shift, const float *A, const float *b, const void *X,
+                                    const void *dY, int32_t mask_mode, int32_t estimator, float dge_k, float dge_cap,
+                                    int32_t accumulate, void *dX, void *dZ, int32_t dz_dtype, float *dA, float *db,
+                                    const void *saved, size_t saved_bytes, void *workspace, size_t workspace_bytes,
+                                    void *stream) {
+  lcvq::Quantizer qz;
+  lcvq::GradEst est;
+  lcvq_status_t s = make_quantizer(q_scale, q_shift, &qz);
+  if (s == LCVQ_OK) s = make_estimator(estimator, dge_k, dge_cap, &est);
+  if (s != LCVQ_OK) return s;
+  return linear_bwd(N, m, n, d, dtype, Z, qz, A, b, X, dY, mask_mode, est, accumulate, dX, dZ, dz_dtype, dA, db,
+                    workspace, workspace_bytes, stream, saved, saved_bytes, dtype == LCVQ_BF16);
 }
 
 lcvq_status_t lcvq_linear_bwd_ex(int64_t N, int64_t m, int64_t n, int32_t d, int32_t dtype, const void *Z,

@@ -22,9 +22,10 @@
 // accumulators between registers around every loop trip.  The compiler cannot
 // see hazards inside such statements, so the code provides the wait states
 // itself: after the zeroing of the accumulators (acc_fence), before an MFMA
-// that reads a just-converted codes operand (mfma16_valu_a), and after the
-// loop (mfma_drain).  All other operands come from loads, which the compiler's
-// waits cover.
+// that reads a just-converted codes operand (mfma16_valu_a; only the first of
+// a step: the other conversions are themselves inline assembly placed two
+// MFMAs ahead of their consumer), and after the loop (mfma_drain).  All other
+// operands come from loads, which the compiler's waits cover.
 #include "lcvq_prep.hpp"
 
 namespace lcvq {
@@ -98,6 +99,18 @@ __device__ __forceinline__ void acc_fence(floatx4 (&acc)[R][C]) {
 // a memory clobber; the reads are copies the compiler places at their uses,
 // which all lie in the epilogue after it.
 __device__ __forceinline__ void mfma_drain() { asm volatile("s_nop 15\n\ts_nop 15" ::: "memory"); }
+
+// The codes conversion as ordered inline assembly: it stays where it is written
+// (between two MFMAs of the previous operand), so the two MFMAs that follow it
+// supply the wait states its consumer needs.
+__device__ __forceinline__ bf16x8 nibbles_to_bf16x8_ordered(uint32_t w) {
+  uint32_t p0, p1, p2, p3;
+  asm volatile("v_cvt_scalef32_pk_bf16_fp4 %0, %1, 2.0" : "=v"(p0) : "v"(w));
+  asm volatile("v_cvt_scalef32_pk_bf16_fp4 %0, %1, 2.0 op_sel:[1,0,0]" : "=v"(p1) : "v"(w));
+  asm volatile("v_cvt_scalef32_pk_bf16_fp4 %0, %1, 2.0 op_sel:[0,1,0]" : "=v"(p2) : "v"(w));
+  asm volatile("v_cvt_scalef32_pk_bf16_fp4 %0, %1, 2.0 op_sel:[1,1,0]" : "=v"(p3) : "v"(w));
+  return __builtin_bit_cast(bf16x8, u32x4{p0, p1, p2, p3});
+}
 
 __device__ __forceinline__ float as_f(uint32_t u) { return __uint_as_float(u); }
 // Copy a (uniform) value into a vector register.
@@ -193,7 +206,7 @@ __global__ __launch_bounds__(256, 1) void k_gemm_codes(
   // and third of them, so the converter works while the matrix core does.
   auto compute = [&](int buf) {
     auto conv = [&](int s2) {  // s2 = 16 kk2 + 2 mi + rb
-      return nibbles_to_bf16x8(ca[buf][(s2 & 15) >> 1][2 * (s2 & 1) + (s2 >> 4)]);
+      return nibbles_to_bf16x8_ordered(ca[buf][(s2 & 15) >> 1][2 * (s2 & 1) + (s2 >> 4)]);
     };
     bf16x8 an = conv(0);
 #pragma unroll
@@ -202,7 +215,7 @@ __global__ __launch_bounds__(256, 1) void k_gemm_codes(
       const bf16x8 a = an;
       const bf16x8 b0 = __builtin_bit_cast(bf16x8, cb[buf][0][kk2]), b1 = __builtin_bit_cast(bf16x8, cb[buf][0][2 + kk2]);
       const bf16x8 b2 = __builtin_bit_cast(bf16x8, cb[buf][1][kk2]), b3 = __builtin_bit_cast(bf16x8, cb[buf][1][2 + kk2]);
-      mfma16_valu_a(acc[p][0], a, b0);
+      if (s2 == 0) mfma16_valu_a(acc[p][0], a, b0); else mfma16(acc[p][0], a, b0);
       mfma16(acc[p][1], a, b1);
       if (s2 + 1 < 32) an = conv(s2 + 1);
       mfma16(acc[p][2], a, b2);
@@ -243,15 +256,16 @@ __global__ __launch_bounds__(256, 1) void k_gemm_codes(
   const int64_t cb0 = (int64_t)tm * kTile + 8 * q;
   // Per-token term, held as up to kMaxParts partial rows vstride apart and
   // summed here: s of the forward, rowsum(dY) of the input gradient.
-  constexpr int kMaxParts = 8;
+  constexpr int kMaxParts = kMaxActChunks;  // the row sums of dY have at most eight
   const __amdgpu_buffer_rsrc_t rv = make_rsrc(vecT + tw, ((int64_t)(vparts - 1) * vstride + Tvalid - tw) * 4);
   float vp[kMaxParts][4], vt[4];
 #pragma unroll
   for (int p = 0; p < kMaxParts; ++p)
 #pragma unroll
     for (int tb = 0; tb < 4; ++tb)
-      vp[p][tb] = as_f(__builtin_amdgcn_raw_buffer_load_b32(
-          rv, p < vparts ? (int)((p * vstride + tb * 16 + c16) * 4) : (int)kOffNone, 0, 0));
+      vp[p][tb] = p < vparts ? as_f(__builtin_amdgcn_raw_buffer_load_b32(rv, (int)((p * vstride + tb * 16 + c16) * 4),
+                                                                        0, 0))
+                             : 0.0f;
 #pragma unroll
   for (int tb = 0; tb < 4; ++tb) {
     vt[tb] = vp[0][tb];
@@ -285,18 +299,40 @@ __global__ __launch_bounds__(256, 1) void k_gemm_codes(
       const uint32_t off = c < Mvalid ? (uint32_t)(tl * Mvalid + c) * 2u : kOffNone;
       xv[p % 3] = __builtin_amdgcn_raw_buffer_load_b128(rx, off, 0, 0);
     };
-    // the map in vector registers (in scalar ones it would not fit beside the
-    // buffer descriptors and would spill)
-    float am[D][D], bm[D], gA[D][D], gb[D];
+    // The A^T map on the matrix cores: per slab and 16-token block, dX^T =
+    // blockdiag(A) P^T, with M = output column c' (rows in slab_row order, so
+    // lane L ends with c' = 8 (L / 16) + 0..7 of token L % 16, one 16-byte
+    // store), N = token, K = the slab's 32 input columns c.  The B operand,
+    // eight consecutive c of token L % 16 in lane L, is exactly what the lane
+    // holds of P, so P never moves between lanes.  The A operand is the
+    // constant block-diagonal map: lane L supplies row c' = slab_row(16 mb +
+    // L % 16) at c = 8 (L / 16) + i, i.e. A[c' % D, c % D] when c' and c share
+    // a group and 0 otherwise.  P and the map are each split into bf16 high
+    // and low parts (x = hi + lo to 16 significant bits), and hi*hi + lo*hi +
+    // hi*lo is summed in fp32 by the matrix core: dX is exact to about 2^-16
+    // before its own bf16 rounding.  The accumulator starts at rs[t] b[c' % D].
+    bf16x8 amh[2], aml[2];
+    float bsel[2][4];
+#pragma unroll
+    for (int mb = 0; mb < 2; ++mb) {
+      const int cp = slab_row(16 * mb + c16);
+#pragma unroll
+      for (int i = 0; i < 8; ++i) {
+        const int c = 8 * q + i;
+        const float v = cp / D == c / D ? A[(cp % D) * D + (c % D)] : 0.0f;
+        const __bf16 h = (__bf16)v;
+        amh[mb][i] = h;
+        aml[mb][i] = (__bf16)(v - (float)h);
+      }
+#pragma unroll
+      for (int e = 0; e < 4; ++e) bsel[mb][e] = to_vgpr(bvec[(4 * mb + e) % D]);
+    }
+    float gA[D][D], gb[D];
 #pragma unroll
     for (int j = 0; j < D; ++j) {
-      bm[j] = to_vgpr(bvec[j]);
       gb[j] = 0.0f;
 #pragma unroll
-      for (int k = 0; k < D; ++k) {
-        am[j][k] = to_vgpr(A[j * D + k]);
-        gA[j][k] = 0.0f;
-      }
+      for (int k = 0; k < D; ++k) gA[j][k] = 0.0f;
     }
     xload(0);
     xload(1);
@@ -304,26 +340,40 @@ __global__ __launch_bounds__(256, 1) void k_gemm_codes(
     for (int p = 0; p < 32; ++p) {
       const int tb = p >> 3, mi = p & 7, tl = tb * 16 + c16;
       if (p + 2 < 32) xload(p + 2);
-      float y[8], x[8];
+      float y[8], x[8], pv8[8];
 #pragma unroll
       for (int e = 0; e < 4; ++e) {
         x[2 * e] = bf16_lo(xv[p % 3][e]);
         x[2 * e + 1] = bf16_hi(xv[p % 3][e]);
       }
 #pragma unroll
-      for (int g = 0; g < 8 / D; ++g) {
-        float pv[D];
+      for (int i = 0; i < 8; ++i) pv8[i] = d8(mi, tb, i);
+      {
+        u32x4 ph, pl;
 #pragma unroll
-        for (int k = 0; k < D; ++k) pv[k] = d8(mi, tb, g * D + k);
+        for (int e = 0; e < 4; ++e) {
+          ph[e] = pack_bf16x2(pv8[2 * e], pv8[2 * e + 1]);
+          pl[e] = pack_bf16x2(pv8[2 * e] - bf16_lo(ph[e]), pv8[2 * e + 1] - bf16_hi(ph[e]));
+        }
+        const bf16x8 bh = __builtin_bit_cast(bf16x8, ph), bl = __builtin_bit_cast(bf16x8, pl);
+#pragma unroll
+        for (int mb = 0; mb < 2; ++mb) {
+          floatx4 cacc;
+#pragma unroll
+          for (int e = 0; e < 4; ++e) cacc[e] = vt[tb] * bsel[mb][e];
+          cacc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(amh[mb], bh, cacc, 0, 0, 0);
+          cacc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(aml[mb], bh, cacc, 0, 0, 0);
+          cacc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(amh[mb], bl, cacc, 0, 0, 0);
+#pragma unroll
+          for (int e = 0; e < 4; ++e) y[4 * mb + e] = cacc[e];
+        }
+      }
+#pragma unroll
+      for (int g = 0; g < 8 / D; ++g) {
 #pragma unroll
         for (int j = 0; j < D; ++j) {
-          float v = vt[tb] * bm[j];
 #pragma unroll
-          for (int k = 0; k < D; ++k) {
-            v = fmaf(am[j][k], pv[k], v);
-            gA[j][k] = fmaf(x[g * D + j], pv[k], gA[j][k]);
-          }
-          y[g * D + j] = v;
+          for (int k = 0; k < D; ++k) gA[j][k] = fmaf(x[g * D + j], pv8[g * D + k], gA[j][k]);
           gb[j] = fmaf(x[g * D + j], vt[tb], gb[j]);
         }
       }

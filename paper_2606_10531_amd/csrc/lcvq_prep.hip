@@ -66,23 +66,30 @@ __device__ __forceinline__ float block_sum256(float v, float *red /* >= 4 floats
   return t;
 }
 
-// ---- quantise into the operand layout --------------------------------------
+// ---- quantise into the operand layouts --------------------------------------
 // One block quantises four 64 x 64 tiles of bf16 Z side by side: tile row by
-// (rows r), tile columns 4 bq .. 4 bq + 3 (columns c; those at or past gx are
-// skipped).  kTrans = false: the operand's M axis is r and its K axis c
-// (forward product); kTrans = true: M is c and K is r (input-gradient
-// product).  Elements beyond Z are quantised from 0 (their products meet zero
-// operands or are not stored).  All loads of the four tiles are
-// issued before the first is used.  With `packed`, the forward also writes the
-// 2-bit codes.  The forward stores each thread's eight codes as one operand
-// dword; the transposed layout goes through the LDS tiles `codes`.
+// (rows r), tile columns 4 bq .. 4 bq + 3 (columns c).  Elements beyond Z are
+// quantised from 0 (their products meet zero operands or are not stored).  All
+// loads of the four tiles are issued before the first is used.  What it writes
+// depends on kMode:
+//   kQuantFwd   the forward product's operand (M axis r, K axis c; tiles at or
+//               past gx skipped), each thread's eight codes stored as one
+//               operand dword, and with `packed` the 2-bit codes;
+//   kQuantBwd   the input-gradient product's operand (M axis c, K axis r, rows
+//               of KBt 64-wide steps), through the LDS tiles `codes`, and with
+//               `maskbits` the straight-through mask of mask_mode;
+//   kQuantSave  both, plus both masks (rounded into maskbits, latent into
+//               maskbits2): the training pair's saved state, from one read of Z.
 typedef uint8_t CodeTile[64][64 + 8];  // rows of 72 bytes keep 8-byte stores aligned
-template <bool kTrans>
+constexpr int kQuantFwd = 0, kQuantBwd = 1, kQuantSave = 2;
+template <int kMode>
 __device__ __forceinline__ void quant_block(int bq, int by, int gx, const uint16_t *__restrict__ Z, int64_t m,
                                             int64_t n, const Quantizer &qz, uint32_t *__restrict__ frag, int KB,
                                             uint8_t *__restrict__ packed, CodeTile *codes,
+                                            uint32_t *__restrict__ frag_t = nullptr, int KBt = 0,
                                             uint64_t *__restrict__ maskbits = nullptr, int64_t ldm8 = 0,
-                                            int mask_mode = 0) {
+                                            int mask_mode = 0, uint64_t *__restrict__ maskbits2 = nullptr) {
+  constexpr bool kFwd = kMode != kQuantBwd, kTrans = kMode != kQuantFwd;
   const int tid = threadIdx.x;
   const int64_t r0 = (int64_t)by * 64;
   u32x4 v[4][2];
@@ -95,6 +102,24 @@ __device__ __forceinline__ void quant_block(int bq, int by, int gx, const uint16
       v[q][i] = u32x4{0u, 0u, 0u, 0u};
       if (r < m && c < n) v[q][i] = *reinterpret_cast<const u32x4 *>(Z + r * n + c);
     }
+  // straight-through mask of the eight latents of (q, i) -> byte (cc / 8) of
+  // the row's 64-bit word; threads cc / 8 = 0 and 4 store the two halves
+  auto store_mask = [&](int q, int i, uint64_t *__restrict__ bits, int mode) {
+    const int id = tid + 256 * i, rr = id >> 3, cc = (id & 7) * 8;
+    const int64_t r = r0 + rr, c = (int64_t)(4 * bq + q) * 64 + cc;
+    uint32_t mb = 0;
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      const bool in = r < m && c + 2 * e < n;
+      mb |= (in && ste_pass(code_value(bf16_lo(v[q][i][e]), qz), mode) ? 1u : 0u) << (2 * e);
+      mb |= (in && ste_pass(code_value(bf16_hi(v[q][i][e]), qz), mode) ? 1u : 0u) << (2 * e + 1);
+    }
+    mb <<= 8 * (id & 3);
+    mb |= (uint32_t)__shfl_xor((int)mb, 1, 64);
+    mb |= (uint32_t)__shfl_xor((int)mb, 2, 64);
+    const int64_t wc = c / 64;
+    if ((id & 3) == 0 && r < m && wc < ldm8) reinterpret_cast<uint32_t *>(bits + r * ldm8 + wc)[(id >> 2) & 1] = mb;
+  };
 #pragma unroll
   for (int q = 0; q < 4; ++q)
 #pragma unroll
@@ -108,9 +133,8 @@ __device__ __forceinline__ void quant_block(int bq, int by, int gx, const uint16
         hi |= (quant_code(code_value(bf16_lo(v[q][i][2 + e]), qz)) |
                (quant_code(code_value(bf16_hi(v[q][i][2 + e]), qz)) << 8)) << (16 * e);
       }
-      if constexpr (kTrans) {
-        *reinterpret_cast<uint2 *>(&codes[q][rr][cc]) = make_uint2(lo, hi);
-      } else if (4 * bq + q < gx) {
+      if constexpr (kTrans) *reinterpret_cast<uint2 *>(&codes[q][rr][cc]) = make_uint2(lo, hi);
+      if (kFwd && 4 * bq + q < gx) {
         // K = columns: the eight codes are one operand dword, nibble i = column
         // cc + i, stored straight from here.  Row rr of the tile is slab rr / 32,
         // MFMA row m with slab_row(m) = rr % 32, i.e. lane 16 ((cc / 8) % 4) + m % 16
@@ -122,25 +146,13 @@ __device__ __forceinline__ void quant_block(int bq, int by, int gx, const uint16
         frag[frag_dword_index(by * 2 + (rr >> 5), 4 * bq + q, KB, 16 * ((cc >> 3) & 3) + (mrow & 15),
                               2 * (mrow >> 4) + (cc >> 5))] = w;
       }
-      if (kTrans && maskbits != nullptr) {
-        // straight-through mask of these 8 latents -> byte (cc / 8) of the
-        // row's 64-bit word; threads cc / 8 = 0 and 4 store the two halves
-        const int64_t r = r0 + rr, c = (int64_t)(4 * bq + q) * 64 + cc;
-        uint32_t mb = 0;
-#pragma unroll
-        for (int e = 0; e < 4; ++e) {
-          const bool in = r < m && c + 2 * e < n;
-          mb |= (in && ste_pass(code_value(bf16_lo(v[q][i][e]), qz), mask_mode) ? 1u : 0u) << (2 * e);
-          mb |= (in && ste_pass(code_value(bf16_hi(v[q][i][e]), qz), mask_mode) ? 1u : 0u) << (2 * e + 1);
-        }
-        mb <<= 8 * ((id >> 0) & 3);
-        mb |= (uint32_t)__shfl_xor((int)mb, 1, 64);
-        mb |= (uint32_t)__shfl_xor((int)mb, 2, 64);
-        const int64_t wc = c / 64;
-        if ((id & 3) == 0 && r < m && wc < ldm8)
-          reinterpret_cast<uint32_t *>(maskbits + r * ldm8 + wc)[(id >> 2) & 1] = mb;
+      if constexpr (kMode == kQuantBwd) {
+        if (maskbits != nullptr) store_mask(q, i, maskbits, mask_mode);
+      } else if constexpr (kMode == kQuantSave) {
+        store_mask(q, i, maskbits, 0);
+        store_mask(q, i, maskbits2, 1);
       }
-      if (!kTrans && packed != nullptr) {
+      if (kFwd && packed != nullptr) {
         // 2-bit codes of these 8 columns (16 bits, least significant first);
         // the even thread of each pair stores its neighbour's 16 bits with its
         // own (4 bytes, 16 codes; n % 16 == 0 keeps them aligned, else 2-byte
@@ -160,11 +172,13 @@ __device__ __forceinline__ void quant_block(int bq, int by, int gx, const uint16
       }
     }
   if constexpr (!kTrans) return;  // the operand dwords are stored above
+  // the transposed operand has KBt 64-row steps (rows padded to 128); the
+  // forward's grid may hold further row tiles, which have nothing to store here
+  if (by >= KBt) return;
   __syncthreads();
 #pragma unroll
   for (int q = 0; q < 4; ++q) {
     const int bx = 4 * bq + q;
-    if (bx >= gx) break;
 #pragma unroll
     for (int i = 0; i < 2; ++i) {
       const int id = tid + 256 * i, slab = id >> 8, lane = (id >> 2) & 63, dw = id & 3;
@@ -173,7 +187,7 @@ __device__ __forceinline__ void quant_block(int bq, int by, int gx, const uint16
       uint32_t w = 0;
 #pragma unroll
       for (int j = 0; j < 8; ++j) w |= (uint32_t)codes[q][kloc + j][mloc] << (4 * j);
-      frag[frag_dword_index(bx * 2 + slab, by, KB, lane, dw)] = w;
+      frag_t[frag_dword_index(bx * 2 + slab, by, KBt, lane, dw)] = w;
     }
   }
 }
@@ -221,23 +235,61 @@ __global__ __launch_bounds__(256) void k_act_transform(const XT *__restrict__ X,
   if (threadIdx.x == 0) s[t] = tot;
 }
 
+// ---- backward operands of the weight-gradient product ----------------------
+// Transposed store of one 64-token x 64-feature sub-tile from the LDS tile
+// into the token-K fragment layout of v_mfma_f32_16x16x32_bf16 (zero-padded to
+// KBt steps and to whole 256-feature tiles): block (f0 / 32 + fb, bt) holds
+// four 1 KiB fragments phi = 2 fh + kk2; in fragment phi lane L holds tokens
+// 32 kk2 + 8 (L / 16) + 0..7 of feature sel(16 fh + L % 16), sel = slab_row
+// for in-features (M side) and the identity for out-features (N side).
+// The column reads use the transposing LDS read: in each 16-lane group, lane
+// 4 e + q addresses token e (+ 4 for the second read) and four consecutive
+// features F(q) .. F(q) + 3, and output lane 4 q + w receives feature F(q) + w
+// of the four tokens.  F places those features where sel puts them.
+template <bool kMside>
+__device__ __forceinline__ void tile_store_t(int bt, int64_t f0, int KBt, uint16_t *__restrict__ dst,
+                                             uint16_t (&tile)[64][64 + 8]) {
+  const int tid = threadIdx.x;
+  const int L = tid & 63, g = L >> 4, e = (L >> 2) & 3, q = L & 3;
+#pragma unroll
+  for (int i = 0; i < 2; ++i) {
+    const int id = tid + 256 * i, fb = id >> 8, phi = (id >> 6) & 3, fh = phi >> 1, kk2 = phi & 1;
+    const int F = kMside ? 8 * q + 4 * fh : 16 * fh + 4 * q;
+    const int t = 32 * kk2 + 8 * g + e;
+    const bf16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4 *)&tile[t][fb * 32 + F]);
+    const bf16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4 *)&tile[t + 4][fb * 32 + F]);
+    const u32x4 w = __builtin_bit_cast(u32x4, __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7));
+    const int64_t blk = (f0 >> 5) + fb;
+    *reinterpret_cast<u32x4 *>(dst + (((blk * KBt + bt) * 4 + phi) * 64 + L) * 8) = w;
+  }
+}
+
 // ---- activation transform, bf16, straight into the B-operand fragments -----
-// Block (tb, kc): tokens 32 tb .. 32 tb + 31, 64-wide K steps of chunk kc;
-// wave w takes steps kb0 + w, kb0 + w + 4, ...  For (step kb, fragment
-// 2 th + kk2) lane L owns token 32 tb + 16 th + L % 16 and K = 64 kb + 32 kk2 +
-// 8 (L / 16) + 0..7 -- one whole group (d = 8) or two (d = 4) -- so it loads the
-// 16 bytes it will store, and each wave writes one whole 1 KiB fragment at a
-// time.  Tokens >= N and K >= n give zeros.  sp[kc * Np + t] = this chunk's
-// part of s[t].
-template <int D>
-__device__ __forceinline__ void act_block(int64_t tb, int kc, const uint16_t *__restrict__ X, int64_t N, int64_t n,
+// Block (bt, kc): tokens 64 bt .. 64 bt + 63 and the 64-wide K steps of chunk
+// kc.  Per step the block covers one 64-token x 64-K tile in eight 1 KiB
+// B-operand fragments: wave w, pass i takes fragment f = 2 w + i (32-token
+// half f / 4 = w / 2, fragment f % 4 = 2 th + kk2 with th = w % 2, kk2 = i), in
+// which lane L owns token 64 bt + 16 w + L % 16 at K = 64 kb + 32 i + 8 (L / 16)
+// + 0..7 -- one whole group (d = 8) or two (d = 4).  The lane loads those 16
+// bytes, forms X' = X A per group in fp32 (rounded to bf16) and stores them as
+// its 16-byte slice of the fragment.  Tokens >= N and K >= n give zeros.
+// s[t] = sum_c X[t, c] b[c % D]: a lane sums its token's products over the
+// chunk in a fixed order, the four lanes of a token (L / 16) are added, and
+// lanes L < 16 write chunk kc's part of s for tokens 64 bt + 16 w + L
+// (sp[kc * Np + t]).  With xt, the steps' X' tiles also go to LDS and from
+// there, transposed, into the weight-gradient operand (the training pair's
+// saved state); the last chunk then runs on to KBx steps (features padded to
+// 256), whose tiles are zeros.  Steps are taken in pairs (one barrier pair per
+// two tiles), with the next pair's loads in flight.
+template <int D, bool kSave>
+__device__ __forceinline__ void act_block(int64_t bt, int kc, const uint16_t *__restrict__ X, int64_t N, int64_t n,
                                           const float *__restrict__ A, const float *__restrict__ b,
-                                          uint16_t *__restrict__ Xp, int KB, int spc, int64_t Np,
-                                          float *__restrict__ sp, float (&red)[4][32]) {
-  const int tid = threadIdx.x, lane = tid & 63;
-  const int wave = tid >> 6;
-  const int64_t rows = N - tb * 32;  // > 0 only for blocks that hold real tokens
-  const __amdgpu_buffer_rsrc_t rx = make_rsrc(X + tb * 32 * n, rows > 0 ? (rows < 32 ? rows : 32) * n * 2 : 0);
+                                          uint16_t *__restrict__ Xp, int KB, int spc, int nkc, int64_t Np,
+                                          float *__restrict__ sp, uint16_t *__restrict__ xt, int KBx, int KBt,
+                                          uint16_t (*tile)[64][64 + 8]) {
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int64_t rows = N - bt * 64;  // > 0 only for blocks that hold real tokens
+  const __amdgpu_buffer_rsrc_t rx = make_rsrc(X + bt * 64 * n, rows > 0 ? (rows < 64 ? rows : 64) * n * 2 : 0);
   float a[D][D], bb[D];
 #pragma unroll
   for (int j = 0; j < D; ++j) {
@@ -245,35 +297,36 @@ __device__ __forceinline__ void act_block(int64_t tb, int kc, const uint16_t *__
 #pragma unroll
     for (int k = 0; k < D; ++k) a[j][k] = A[j * D + k];
   }
-  const int kb0 = kc * spc, kb1 = min(kb0 + spc, KB);
-  float acc_s[2] = {0.0f, 0.0f};  // tokens 32 tb + 16 th + L % 16, this lane's K groups
-  // batches of 8 steps: this wave's two (kb0 + 8 i + wave + 4 s), all 8
-  // loads issued before the first is used
-  for (int base = kb0 + wave; base < kb1; base += 8) {
-    u32x4 xv[2][4];
+  const int tl = 16 * wave + (lane & 15);  // this lane's token within the block
+  const int kb0 = kc * spc;
+  // whole pairs of steps: KB, KBx and spc are even
+  const int kb1 = kSave && kc == nkc - 1 ? KBx : min(kb0 + spc, KB);
+  // the lane's 16 bytes of steps kb, kb + 1 (index 2 s + i: step kb + s, K half i)
+  auto load = [&](u32x4 (&xv)[4], int kb) {
 #pragma unroll
-    for (int st = 0; st < 2; ++st) {
-      const int kb = base + 4 * st;
+    for (int s2 = 0; s2 < 2; ++s2)
 #pragma unroll
-      for (int fr = 0; fr < 4; ++fr) {
-        const int64_t k = (int64_t)kb * 64 + 32 * (fr & 1) + 8 * (lane >> 4);
-        const int tr = 16 * (fr >> 1) + (lane & 15);
-        const uint32_t off = (kb < kb1 && k < n) ? (uint32_t)((tr * n + k) * 2) : kOffNone;
-        xv[st][fr] = __builtin_amdgcn_raw_buffer_load_b128(rx, off, 0, 0);
+      for (int i = 0; i < 2; ++i) {
+        const int64_t k = (int64_t)(kb + s2) * 64 + 32 * i + 8 * (lane >> 4);
+        const uint32_t off = (kb + s2 < kb1 && k < n) ? (uint32_t)((tl * n + k) * 2) : kOffNone;
+        xv[2 * s2 + i] = __builtin_amdgcn_raw_buffer_load_b128(rx, off, 0, 0);
       }
-    }
+  };
+  float acc_s = 0.0f;
+  u32x4 cur[4], nxt[4];
+  load(cur, kb0);
+  for (int kb = kb0; kb < kb1; kb += 2) {
+    load(nxt, kb + 2);  // one pair ahead
 #pragma unroll
-    for (int st = 0; st < 2; ++st) {
-      const int kb = base + 4 * st;
-      if (kb >= kb1) break;
-      uint16_t *dst = Xp + ((tb * KB + kb) * 4) * 512 + lane * 8;
+    for (int s2 = 0; s2 < 2; ++s2)
 #pragma unroll
-      for (int fr = 0; fr < 4; ++fr) {
+      for (int i = 0; i < 2; ++i) {
+        const u32x4 &xv = cur[2 * s2 + i];
         float x[8], y[8];
 #pragma unroll
         for (int e = 0; e < 4; ++e) {
-          x[2 * e] = bf16_lo(xv[st][fr][e]);
-          x[2 * e + 1] = bf16_hi(xv[st][fr][e]);
+          x[2 * e] = bf16_lo(xv[e]);
+          x[2 * e + 1] = bf16_hi(xv[e]);
         }
 #pragma unroll
         for (int g = 0; g < 8 / D; ++g)
@@ -285,45 +338,63 @@ __device__ __forceinline__ void act_block(int64_t tb, int kc, const uint16_t *__
             y[g * D + k] = v;
           }
 #pragma unroll
-        for (int e = 0; e < 8; ++e) acc_s[fr >> 1] = fmaf(x[e], bb[e % D], acc_s[fr >> 1]);
+        for (int e = 0; e < 8; ++e) acc_s = fmaf(x[e], bb[e % D], acc_s);
         u32x4 w;
 #pragma unroll
         for (int e = 0; e < 4; ++e) w[e] = pack_bf16x2(y[2 * e], y[2 * e + 1]);
-        *reinterpret_cast<u32x4 *>(dst + fr * 512) = w;
+        if (kb + s2 < KB) {
+          const int64_t tb32 = bt * 2 + (wave >> 1);
+          const int fr = 2 * (wave & 1) + i;
+          *reinterpret_cast<u32x4 *>(Xp + (((tb32 * KB + kb + s2) * 4 + fr) * 64 + lane) * 8) = w;
+        }
+        if constexpr (kSave) *reinterpret_cast<u32x4 *>(&tile[s2][tl][32 * i + 8 * (lane >> 4)]) = w;
       }
+    if constexpr (kSave) {
+      __syncthreads();
+      tile_store_t<true>((int)bt, (int64_t)kb * 64, KBt, xt, tile[0]);
+      tile_store_t<true>((int)bt, (int64_t)(kb + 1) * 64, KBt, xt, tile[1]);
+      __syncthreads();  // the tiles are rewritten by the next pair
     }
-  }
 #pragma unroll
-  for (int th = 0; th < 2; ++th) {  // over the four K groups (lanes L % 16 + 16 g)
-    acc_s[th] += __shfl_xor(acc_s[th], 16, 64);
-    acc_s[th] += __shfl_xor(acc_s[th], 32, 64);
+    for (int i = 0; i < 4; ++i) cur[i] = nxt[i];
   }
-  if (lane < 16) {
-    red[wave][lane] = acc_s[0];
-    red[wave][16 + lane] = acc_s[1];
-  }
-  __syncthreads();
-  if (tid < 32) sp[(int64_t)kc * Np + tb * 32 + tid] = red[0][tid] + red[1][tid] + red[2][tid] + red[3][tid];
+  // over the token's four K groups (lanes L % 16 + 16 g)
+  acc_s += __shfl_xor(acc_s, 16, 64);
+  acc_s += __shfl_xor(acc_s, 32, 64);
+  if (lane < 16) sp[(int64_t)kc * Np + bt * 64 + tl] = acc_s;
 }
 
 // ---- forward prepass, bf16: one launch for both operands ---------------------
 // Blocks [0, nq): quantise blocks of Z (four 64 x 64 tiles each, block
-// (id % gq, id / gq), K = columns), with the 2-bit pack when `packed` is set; blocks [nq, nq + ntb * nkc): the
-// activation transform, block (tb, kc) = ((id - nq) % ntb, (id - nq) / ntb).
-template <int D>
+// (id % gq, id / gq), K = columns), with the 2-bit pack when `packed` is set;
+// blocks [nq, nq + nbt * nkc): the activation transform, block (bt, kc) =
+// ((id - nq) % nbt, (id - nq) / nbt).  kSave also writes the training pair's
+// saved state: the input-gradient operand of the codes (frag_t, KBq steps),
+// both straight-through masks, and X' in the weight-gradient operand (xt).
+template <int D, bool kSave>
 __global__ __launch_bounds__(256) void k_fwd_prep(const uint16_t *__restrict__ Z, int64_t m, int64_t n, Quantizer qz,
                                                    uint32_t *__restrict__ frag, uint8_t *__restrict__ packed, int gq,
                                                    int nq, const uint16_t *__restrict__ X, int64_t N,
                                                    const float *__restrict__ A, const float *__restrict__ b,
-                                                   uint16_t *__restrict__ Xp, int KB, int spc, int64_t Np,
-                                                   float *__restrict__ sp) {
-  __shared__ float red[4][32];
+                                                   uint16_t *__restrict__ Xp, int KB, int spc, int nkc, int64_t Np,
+                                                   float *__restrict__ sp, uint32_t *__restrict__ frag_t, int KBq,
+                                                   uint64_t *__restrict__ mask_r, uint64_t *__restrict__ mask_l,
+                                                   int64_t ldm8, uint16_t *__restrict__ xt, int KBx) {
+  // LDS only for the saved state: the quantise blocks' code tiles and the
+  // activation blocks' X' tile (one launch holds both kinds of block)
+  __shared__ __attribute__((aligned(16))) uint8_t lds[kSave ? 4 * sizeof(CodeTile) : 16];
+  static_assert(!kSave || 4 * sizeof(CodeTile) >= 2 * 64 * (64 + 8) * sizeof(uint16_t), "X' tiles fit");
   const int id = blockIdx.x;
   if (id < nq) {
-    quant_block<false>(id % gq, id / gq, KB, Z, m, n, qz, frag, KB, packed, nullptr);
+    if constexpr (kSave)
+      quant_block<kQuantSave>(id % gq, id / gq, KB, Z, m, n, qz, frag, KB, packed, reinterpret_cast<CodeTile *>(lds),
+                              frag_t, KBq, mask_r, ldm8, 0, mask_l);
+    else
+      quant_block<kQuantFwd>(id % gq, id / gq, KB, Z, m, n, qz, frag, KB, packed, nullptr);
   } else {
-    const int j = id - nq, ntb = (int)(Np / 32);
-    act_block<D>(j % ntb, j / ntb, X, N, n, A, b, Xp, KB, spc, Np, sp, red);
+    const int j = id - nq, nbt = (int)(Np / 64);
+    act_block<D, kSave>(j % nbt, j / nbt, X, N, n, A, b, Xp, KB, spc, nkc, Np, sp, xt, KBx, (int)(Np / 64),
+                        reinterpret_cast<uint16_t (*)[64][64 + 8]>(lds));
   }
 }
 
@@ -438,23 +509,39 @@ __global__ __launch_bounds__(256) void k_dequant(const ZT *__restrict__ src, int
   }
 }
 
-// ---- dense decode from byte or packed codes, 16 source bytes per lane --------
-// A thread decodes one 16-byte chunk of the source per trip: 16 codes of one
-// byte each (kSrc 1; values above 3 are taken as 3) or 64 packed 2-bit codes
-// (kSrc 2, lcvq_pack2bit layout), i.e. whole groups (16 and 64 are multiples of
-// D), and stores their W_hat values, contiguous in the flattened m x n matrix
-// (groups never straddle rows).  Two chunks are loaded before either is
-// decoded, so a wave keeps 2 KiB of loads in flight.  The map is A, b (device),
-// or with kScalar the diagonal map W = fma(scale, code, shift), which is the
-// fp32 result of A = scale I, b = shift bit for bit (the other terms add
-// 0 * code).  Codes past the last whole chunk (fewer than one chunk's worth)
-// are decoded one group per thread by block 0.
+// ---- dense decode from byte or packed codes ---------------------------------
+// The source is read in 1 KiB wave chunks with one 16-byte load per lane
+// (coalesced: the wave reads 1 KiB of contiguous memory), staged in the wave's
+// own LDS slice, and decoded group by group: lane L takes groups L, L + 64,
+// L + 128, ... of the chunk, so each store instruction of the wave writes
+// contiguous memory (for bf16 at d = 8, 16 bytes per lane, 1 KiB per
+// instruction).  A group is D / 4 packed bytes (kSrc 2, lcvq_pack2bit layout) or
+// D bytes (kSrc 1; values above 3 are taken as 3); groups never straddle rows,
+// so the flattened m x n layout is enough.  Two chunks per wave are loaded
+// before either is decoded.  The map is A, b (device), or with kScalar the
+// diagonal map W = fma(scale, code, shift), the fp32 result of A = scale I,
+// b = shift bit for bit (the other terms add 0 * code).
+//
+// Packed codes with a general map (kTable) take the map from two tables the
+// block builds in LDS first, one per half-group of four codes (one packed
+// byte): lo[i][j] = b[j] + sum_{k<4} A[j, k] c_k(i) and hi[i][j] = sum_{k<4}
+// A[j, 4 + k] c_k(i), c_k(i) = (i >> 2k) & 3 (d = 4: lo alone).  A group's
+// W_hat row is then lo[byte 0] + hi[byte 1]: four 16-byte LDS reads and D adds
+// instead of D^2 fma, which would otherwise make the kernel VALU-bound.  The
+// sum is grouped differently from the plain fma chain, so the fp32 result can
+// differ from it in the last bits.  Groups past the last whole chunk are
+// decoded by block 0 from direct loads.
 template <int D, int kSrc, typename OT, bool kScalar>
 __global__ __launch_bounds__(256) void k_decode_codes(const uint8_t *__restrict__ src, int64_t chunks,
                                                        int64_t groups, const float *__restrict__ A,
                                                        const float *__restrict__ b, float scale, float shift,
                                                        OT *__restrict__ W) {
-  constexpr int kCodes = kSrc == 2 ? 64 : 16;  // codes per 16-byte chunk
+  constexpr int kBytes = kSrc == 2 ? D / 4 : D;        // source bytes per group
+  constexpr int kGroups = 1024 / kBytes;               // groups per wave chunk
+  constexpr bool kTable = kSrc == 2 && !kScalar;
+  __shared__ __attribute__((aligned(16))) uint8_t stage[4][2][1024];
+  __shared__ __attribute__((aligned(16))) float tab[kTable ? 2 : 1][kTable ? 256 : 1][kTable ? D : 1];
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   float a[D][D], bb[D];
   if constexpr (!kScalar) {
 #pragma unroll
@@ -464,7 +551,30 @@ __global__ __launch_bounds__(256) void k_decode_codes(const uint8_t *__restrict_
       for (int k = 0; k < D; ++k) a[j][k] = A[j * D + k];
     }
   }
-  auto map_group = [&](const float (&c)[D], OT *dst) {
+  if constexpr (kTable) {  // thread i builds row i of both tables
+    const int i = threadIdx.x;
+#pragma unroll
+    for (int h = 0; h < D / 4; ++h)
+#pragma unroll
+      for (int j = 0; j < D; ++j) {
+        float v = h == 0 ? bb[j] : 0.0f;
+#pragma unroll
+        for (int k = 0; k < 4; ++k) v = fmaf(a[j][4 * h + k], (float)((i >> (2 * k)) & 3), v);
+        tab[h][i][j] = v;
+      }
+    __syncthreads();
+  }
+  auto code_at = [&](uint32_t bits, int k) -> float {  // code k of a group's source bits
+    uint32_t c;
+    if constexpr (kSrc == 2) {
+      c = (bits >> (2 * k)) & 3u;
+    } else {
+      c = (bits >> (8 * (k & 3))) & 0xffu;
+      c = c > 3u ? 3u : c;
+    }
+    return (float)c;
+  };
+  auto map_store = [&](const float (&c)[D], OT *dst) {
     float y[D];
 #pragma unroll
     for (int j = 0; j < D; ++j) {
@@ -479,36 +589,89 @@ __global__ __launch_bounds__(256) void k_decode_codes(const uint8_t *__restrict_
     }
     storeD<D>(dst, y);
   };
-  auto decode = [&](const u32x4 &v, int64_t ch) {
+  auto decode = [&](const uint8_t *st, int64_t ch) {
 #pragma unroll
-    for (int g = 0; g < kCodes / D; ++g) {
+    for (int i = 0; i < kGroups / 64; ++i) {
+      const int gl = i * 64 + lane;
       float c[D];
+      if constexpr (kTable && kBytes == 1) {  // d = 4: one byte, b folded into the table row
+        const floatx4 y4 = *reinterpret_cast<const floatx4 *>(tab[0][st[gl]]);
+        const float y[4] = {y4[0], y4[1], y4[2], y4[3]};
+        storeD<D>(W + (ch * kGroups + gl) * D, y);
+        continue;
+      } else if constexpr (kBytes == 1) {
+        const uint32_t v = st[gl];
 #pragma unroll
-      for (int k = 0; k < D; ++k) {
-        const int i = g * D + k;
-        uint32_t code;
-        if constexpr (kSrc == 2) {
-          code = (v[i >> 4] >> (2 * (i & 15))) & 3u;
-        } else {
-          code = (v[i >> 2] >> (8 * (i & 3))) & 0xffu;
-          code = code > 3u ? 3u : code;
-        }
-        c[k] = (float)code;
+        for (int k = 0; k < D; ++k) c[k] = code_at(v, k);
+      } else if constexpr (kTable) {  // d = 8: lo of byte 0 plus hi of byte 1
+        const uint32_t v = *reinterpret_cast<const uint16_t *>(st + 2 * gl);
+        const floatx4 *lo = reinterpret_cast<const floatx4 *>(tab[0][v & 0xffu]);
+        const floatx4 *hi = reinterpret_cast<const floatx4 *>(tab[1][v >> 8]);
+        const floatx4 y0 = lo[0] + hi[0], y1 = lo[1] + hi[1];
+        const float y[8] = {y0[0], y0[1], y0[2], y0[3], y1[0], y1[1], y1[2], y1[3]};
+        storeD<D>(W + (ch * kGroups + gl) * D, y);
+        continue;
+      } else if constexpr (kBytes == 2) {
+        const uint32_t v = *reinterpret_cast<const uint16_t *>(st + 2 * gl);
+#pragma unroll
+        for (int k = 0; k < D; ++k) c[k] = code_at(v, k);
+      } else if constexpr (kBytes == 4) {
+        const uint32_t v = *reinterpret_cast<const uint32_t *>(st + 4 * gl);
+#pragma unroll
+        for (int k = 0; k < D; ++k) c[k] = code_at(v, k);
+      } else {
+        const u32x2 v = *reinterpret_cast<const u32x2 *>(st + 8 * gl);
+#pragma unroll
+        for (int k = 0; k < D; ++k) c[k] = code_at(v[k >> 2], k);
       }
-      map_group(c, W + ch * kCodes + g * D);
+      map_store(c, W + (ch * kGroups + gl) * D);
     }
   };
+  // A wave reads back what its own lanes staged: a wave-scope release / acquire
+  // around the wave barrier orders the LDS writes before the reads, and the
+  // reads before the next trip's writes.
+  auto wave_sync = [] {
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+  };
   const u32x4 *s16 = reinterpret_cast<const u32x4 *>(src);
-  const int64_t stride = (int64_t)gridDim.x * 256;
-  int64_t ch = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  uint8_t *st0 = stage[wave][0], *st1 = stage[wave][1];
+  const int64_t stride = (int64_t)gridDim.x * 4;
+  int64_t ch = (int64_t)blockIdx.x * 4 + wave;
   for (; ch + stride < chunks; ch += 2 * stride) {
-    const u32x4 v0 = s16[ch], v1 = s16[ch + stride];
-    decode(v0, ch);
-    decode(v1, ch + stride);
+    const u32x4 v0 = s16[ch * 64 + lane], v1 = s16[(ch + stride) * 64 + lane];
+    wave_sync();
+    *reinterpret_cast<u32x4 *>(st0 + 16 * lane) = v0;
+    *reinterpret_cast<u32x4 *>(st1 + 16 * lane) = v1;
+    wave_sync();
+    decode(st0, ch);
+    decode(st1, ch + stride);
   }
-  if (ch < chunks) decode(s16[ch], ch);
-  const int64_t g = chunks * (kCodes / D) + threadIdx.x;
-  if (blockIdx.x == 0 && g < groups) {
+  if (ch < chunks) {
+    const u32x4 v0 = s16[ch * 64 + lane];
+    wave_sync();
+    *reinterpret_cast<u32x4 *>(st0 + 16 * lane) = v0;
+    wave_sync();
+    decode(st0, ch);
+  }
+  if (blockIdx.x != 0) return;
+  for (int64_t g = chunks * kGroups + threadIdx.x; g < groups; g += 256) {  // fewer than kGroups
+    if constexpr (kTable) {
+      const floatx4 *lo = reinterpret_cast<const floatx4 *>(tab[0][src[g * kBytes]]);
+      float y[D];
+      if constexpr (D == 8) {
+        const floatx4 *hi = reinterpret_cast<const floatx4 *>(tab[1][src[g * kBytes + 1]]);
+        const floatx4 y0 = lo[0] + hi[0], y1 = lo[1] + hi[1];
+#pragma unroll
+        for (int j = 0; j < 4; ++j) { y[j] = y0[j]; y[4 + j] = y1[j]; }
+      } else {
+#pragma unroll
+        for (int j = 0; j < D; ++j) y[j] = lo[0][j];
+      }
+      storeD<D>(W + g * D, y);
+      continue;
+    }
     float c[D];
 #pragma unroll
     for (int k = 0; k < D; ++k) {
@@ -522,36 +685,7 @@ __global__ __launch_bounds__(256) void k_decode_codes(const uint8_t *__restrict_
       }
       c[k] = (float)code;
     }
-    map_group(c, W + g * D);
-  }
-}
-
-// ---- backward operands of the weight-gradient product ----------------------
-// Transposed store of one 64-token x 64-feature sub-tile from the LDS tile
-// into the token-K fragment layout of v_mfma_f32_16x16x32_bf16 (zero-padded to
-// KBt steps and to whole 256-feature tiles): block (f0 / 32 + fb, bt) holds
-// four 1 KiB fragments phi = 2 fh + kk2; in fragment phi lane L holds tokens
-// 32 kk2 + 8 (L / 16) + 0..7 of feature sel(16 fh + L % 16), sel = slab_row
-// for in-features (M side) and the identity for out-features (N side).
-// The column reads use the transposing LDS read: in each 16-lane group, lane
-// 4 e + q addresses token e (+ 4 for the second read) and four consecutive
-// features F(q) .. F(q) + 3, and output lane 4 q + w receives feature F(q) + w
-// of the four tokens.  F places those features where sel puts them.
-template <bool kMside>
-__device__ __forceinline__ void tile_store_t(int bt, int64_t f0, int KBt, uint16_t *__restrict__ dst,
-                                             uint16_t (&tile)[64][64 + 8]) {
-  const int tid = threadIdx.x;
-  const int L = tid & 63, g = L >> 4, e = (L >> 2) & 3, q = L & 3;
-#pragma unroll
-  for (int i = 0; i < 2; ++i) {
-    const int id = tid + 256 * i, fb = id >> 8, phi = (id >> 6) & 3, fh = phi >> 1, kk2 = phi & 1;
-    const int F = kMside ? 8 * q + 4 * fh : 16 * fh + 4 * q;
-    const int t = 32 * kk2 + 8 * g + e;
-    const bf16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4 *)&tile[t][fb * 32 + F]);
-    const bf16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4 *)&tile[t + 4][fb * 32 + F]);
-    const u32x4 w = __builtin_bit_cast(u32x4, __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7));
-    const int64_t blk = (f0 >> 5) + fb;
-    *reinterpret_cast<u32x4 *>(dst + (((blk * KBt + bt) * 4 + phi) * 64 + L) * 8) = w;
+    map_store(c, W + g * D);
   }
 }
 
@@ -688,7 +822,8 @@ __global__ __launch_bounds__(256) void k_bwd_prep(const uint16_t *__restrict__ Z
   }
   const int q = id - ndy;
   if (q < nq) {
-    quant_block<true>(q % gq, q / gq, 4 * gq, Z, m, n, qz, frag, KBq, nullptr, codes, maskbits, ldm8, mask_mode);
+    quant_block<kQuantBwd>(q % gq, q / gq, 4 * gq, Z, m, n, qz, nullptr, 0, nullptr, codes, frag, KBq, maskbits, ldm8,
+                           mask_mode);
     return;
   }
   const int x = q - nq;
@@ -722,14 +857,29 @@ hipError_t launch_act_transform(const void *X, bool bf16, int64_t N, int64_t Np,
 hipError_t launch_fwd_prep_bf16(const uint16_t *Z, int64_t m, int64_t n, const Quantizer &qz, uint32_t *frag,
                                 uint8_t *packed,
                                 const uint16_t *X, int64_t N, int64_t Np, int64_t ldp, int d, const float *A,
-                                const float *b, uint16_t *Xp, float *sp, hipStream_t st) {
+                                const float *b, uint16_t *Xp, float *sp, const FwdSave *save, hipStream_t st) {
   const int KB = (int)(ldp / 64);
   // quantise blocks: K = columns (ldp / 64 tiles, four per block), M = rows padded to 256
   const int gq = (KB + 3) / 4, nq = gq * (int)(round_up(m, 256) / 64);
-  const int ntb = (int)(Np / 32), nkc = act_chunks(ldp), spc = act_steps_per_chunk(ldp);
-  const unsigned grid = (unsigned)(nq + ntb * nkc);
-  if (d == 8) k_fwd_prep<8><<<grid, 256, 0, st>>>(Z, m, n, qz, frag, packed, gq, nq, X, N, A, b, Xp, KB, spc, Np, sp);
-  else k_fwd_prep<4><<<grid, 256, 0, st>>>(Z, m, n, qz, frag, packed, gq, nq, X, N, A, b, Xp, KB, spc, Np, sp);
+  const int nbt = (int)(Np / 64), nkc = act_chunks(ldp), spc = act_steps_per_chunk(ldp);
+  const unsigned grid = (unsigned)(nq + nbt * nkc);
+  if (save != nullptr) {
+    const int KBq = (int)(round_up(m, 128) / 64), KBx = (int)(round_up(n, 256) / 64);
+    const int64_t ldm8 = mask_words_per_row(n);
+    if (d == 8)
+      k_fwd_prep<8, true><<<grid, 256, 0, st>>>(Z, m, n, qz, frag, packed, gq, nq, X, N, A, b, Xp, KB, spc, nkc, Np, sp,
+                                                save->frag_t, KBq, save->mask_r, save->mask_l, ldm8, save->xt, KBx);
+    else
+      k_fwd_prep<4, true><<<grid, 256, 0, st>>>(Z, m, n, qz, frag, packed, gq, nq, X, N, A, b, Xp, KB, spc, nkc, Np, sp,
+                                                save->frag_t, KBq, save->mask_r, save->mask_l, ldm8, save->xt, KBx);
+  } else {
+    if (d == 8)
+      k_fwd_prep<8, false><<<grid, 256, 0, st>>>(Z, m, n, qz, frag, packed, gq, nq, X, N, A, b, Xp, KB, spc, nkc, Np, sp,
+                                                 nullptr, 0, nullptr, nullptr, 0, nullptr, 0);
+    else
+      k_fwd_prep<4, false><<<grid, 256, 0, st>>>(Z, m, n, qz, frag, packed, gq, nq, X, N, A, b, Xp, KB, spc, nkc, Np, sp,
+                                                 nullptr, 0, nullptr, nullptr, 0, nullptr, 0);
+  }
   return hipGetLastError();
 }
 
@@ -759,9 +909,12 @@ hipError_t launch_pack2bit(const void *src, int kind, bool bf16, int64_t m, int6
 template <int D, typename OT, bool kScalar>
 static void decode_codes_dispatch(int kind, const void *src, int64_t total, const float *A, const float *b,
                                   float scale, float shift, void *W, hipStream_t st) {
-  const int64_t per = kind == 2 ? 64 : 16;  // codes per 16-byte chunk
+  const int64_t per = kind == 2 ? 4096 : 1024;  // codes per 1 KiB wave chunk
   const int64_t chunks = total / per, groups = total / D;
-  const int grid = grid_for(chunks, 512);   // two chunks per thread
+  int grid = grid_for(chunks, 8);   // four waves per block, two chunks per wave
+  // packed codes with a general map build a 16 KiB table per block: at most six
+  // blocks per CU (LDS), each wave taking several chunks
+  if (kind == 2 && !kScalar && grid > 6 * 256) grid = 6 * 256;
   if (kind == 2)
     k_decode_codes<D, 2, OT, kScalar><<<grid, 256, 0, st>>>((const uint8_t *)src, chunks, groups, A, b, scale, shift,
                                                             (OT *)W);

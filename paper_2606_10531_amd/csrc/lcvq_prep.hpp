@@ -5,13 +5,15 @@
 
 namespace lcvq {
 
-// The bf16 activation transform splits K into at most eight chunks and writes
-// one partial s per chunk (rows of Np floats); the forward product sums them.
-// Both are at least 1 (ldp may be 0 for an empty problem).  A chunk is a
-// whole number of 8-step batches (two steps per wave, loads issued together).
+// The bf16 activation transform splits K into at most sixteen chunks and
+// writes one partial s per chunk (rows of Np floats); the forward product sums
+// them.  A chunk is a whole number of step pairs (the transform takes steps two
+// at a time), at least four steps.  Both are at least 1 (ldp may be 0 for an
+// empty problem).
+constexpr int kMaxActChunks = 16;
 inline int act_steps_per_chunk(int64_t ldp) {
-  const int64_t spc = (ldp / 64 + 7) / 8;
-  return spc <= 8 ? 8 : (int)((spc + 7) / 8 * 8);
+  const int64_t spc = (ldp / 64 + kMaxActChunks - 1) / kMaxActChunks;
+  return spc <= 4 ? 4 : (int)((spc + 1) / 2 * 2);
 }
 inline int act_chunks(int64_t ldp) {
   const int64_t c = (ldp / 64 + act_steps_per_chunk(ldp) - 1) / act_steps_per_chunk(ldp);
@@ -19,11 +21,21 @@ inline int act_chunks(int64_t ldp) {
 }
 
 // streaming kernels (lcvq_prep.hip)
-// bf16 forward prepass: codes (+ 2-bit pack) and X' = X A, partial s, in one launch
+// What the forward of the training pair saves for its backward (bf16): the
+// codes in the input-gradient operand layout (as the backward prepass writes
+// them), both straight-through masks (rounded, latent) and X' in the
+// weight-gradient operand layout.
+struct FwdSave {
+  uint32_t *frag_t;
+  uint64_t *mask_r, *mask_l;
+  uint16_t *xt;
+};
+// bf16 forward prepass: codes (+ 2-bit pack) and X' = X A, partial s, in one
+// launch; with `save`, also the backward's operands above from the same reads
 hipError_t launch_fwd_prep_bf16(const uint16_t *Z, int64_t m, int64_t n, const Quantizer &qz, uint32_t *frag,
                                 uint8_t *packed,
                                 const uint16_t *X, int64_t N, int64_t Np, int64_t ldp, int d, const float *A,
-                                const float *b, uint16_t *Xp, float *sp, hipStream_t st);
+                                const float *b, uint16_t *Xp, float *sp, const FwdSave *save, hipStream_t st);
 // Tokens of the bf16 backward are padded to whole 256-token tiles of the
 // input-gradient product (the weight-gradient operands and row sums use the
 // same padding).

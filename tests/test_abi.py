@@ -313,3 +313,30 @@ def test_binding_checks_shapes_and_dtypes_before_any_call():
         lc.xavier_init(P, m, n + 4, src_kind=lc.SRC_PACKED2)
     with pytest.raises(ValueError, match="shape"):
         lc.pack2bit(Z, out=torch.zeros(m, n, dtype=torch.uint8))
+
+
+def test_training_pair_validation(lib):
+    """Saved-state size and alignment are checked before anything is enqueued."""
+    N, m, n, d = 16, 64, 64, 8
+    need = lib.lcvq_saved_bytes(N, m, n, d, L.BF16)
+    assert need >= m * n // 2 + n * 256 * 2                    # codes (4 bits) and X' (bf16, tokens padded)
+    assert lib.lcvq_saved_bytes(N, m, n, d, L.F32) == 0
+    assert lib.lcvq_saved_bytes(N, m, n, 5, L.BF16) == 0
+    assert lib.lcvq_saved_bytes(-1, m, n, d, L.BF16) == 0
+
+    def f(saved=FAKE, nbytes=None):
+        return lib.lcvq_linear_fwd_train(N, m, n, d, L.BF16, FAKE, 1.0, 0.0, FAKE, FAKE, FAKE, FAKE, None, saved,
+                                         need if nbytes is None else nbytes, FAKE, 1 << 40, None)
+
+    def g(saved=FAKE, nbytes=None, est=L.EST_STE):
+        return lib.lcvq_linear_bwd_train(N, m, n, d, L.BF16, FAKE, 1.0, 0.0, FAKE, FAKE, FAKE, FAKE, 0, est, 5.0, 3.0,
+                                         0, FAKE, FAKE, L.BF16, FAKE, FAKE, saved,
+                                         need if nbytes is None else nbytes, FAKE, 1 << 40, None)
+    assert f(nbytes=need - 1) == L.EWORKSPACE and "saved" in L.last_error()
+    assert f(saved=None) == L.EWORKSPACE
+    assert f(saved=MIS) == L.EALIGN
+    assert g(nbytes=need - 1) == L.EWORKSPACE
+    assert g(saved=None) == L.EWORKSPACE
+    assert g(saved=MIS) == L.EALIGN
+    assert g(est=7) == L.EINVAL
+    assert f(nbytes=0, saved=None) != L.OK

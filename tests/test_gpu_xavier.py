@@ -103,7 +103,9 @@ def test_xavier_quantizer_values(lc):
 @pytest.mark.parametrize("dtype", ["bf16", "f32"])
 def test_xavier_init_round_trip(lc, dtype, src):
     """codes -> W_p = s'(W_z - t) (lcvq_xavier_init) -> forward with the Xavier quantiser
-    returns the same codes; W_p equals lcvq_dequant with A = s' I, b = -s' t bit for bit."""
+    returns the same codes; W_p equals lcvq_dequant with A = s' I, b = -s' t (bit for
+    bit from byte codes, whose decode is the same fma; to fp32 rounding from packed
+    codes, whose decode sums two half-group tables)."""
     import torch
     m, n, d = 200, 264, 8
     codes = synth.rng(5).integers(0, 4, size=(m, n), dtype=np.uint8)
@@ -120,7 +122,10 @@ def test_xavier_init_round_trip(lc, dtype, src):
                     src_kind=lc.SRC_CODES_U8 if src == "u8" else lc.SRC_PACKED2, out_dtype=tdt)
     torch.cuda.synchronize()
     assert np.array_equal(packed.cpu().numpy(), orc.pack2bit(codes))
-    assert torch.equal(W, Wd)
+    if src == "u8":
+        assert torch.equal(W, Wd)
+    else:
+        assert_close(to_host(W), to_host(Wd), 4e-3 if dtype == "bf16" else 1e-7, "W_p vs dequant")
     assert_close(to_host(W), sp * (codes.astype(np.float64) - t), 4e-3 if dtype == "bf16" else 1e-7, "W_p")
 
 
