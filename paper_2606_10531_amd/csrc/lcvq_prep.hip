@@ -133,7 +133,14 @@ __device__ __forceinline__ void quant_block(int bq, int by, int gx, const uint16
         hi |= (quant_code(code_value(bf16_lo(v[q][i][2 + e]), qz)) |
                (quant_code(code_value(bf16_hi(v[q][i][2 + e]), qz)) << 8)) << (16 * e);
       }
-      if constexpr (kTrans) *reinterpret_cast<uint2 *>(&codes[q][rr][cc]) = make_uint2(lo, hi);
+      if constexpr (kTrans) {
+        // tile column pos holds M column slab_row(pos) of its 32-column slab:
+        // columns 8a + 4b + r (a = (cc % 32) / 8) sit at 16 b + 4 a + r, so the
+        // eight codes go out as two runs of four
+        uint8_t *row = &codes[q][rr][(cc & ~31) + 4 * ((cc >> 3) & 3)];
+        *reinterpret_cast<uint32_t *>(row) = lo;
+        *reinterpret_cast<uint32_t *>(row + 16) = hi;
+      }
       if (kFwd && 4 * bq + q < gx) {
         // K = columns: the eight codes are one operand dword, nibble i = column
         // cc + i, stored straight from here.  Row rr of the tile is slab rr / 32,
@@ -176,17 +183,28 @@ __device__ __forceinline__ void quant_block(int bq, int by, int gx, const uint16
   // forward's grid may hold further row tiles, which have nothing to store here
   if (by >= KBt) return;
   __syncthreads();
+  // K = rows: the eight codes of an operand dword are a column of the tile
+  // (rows kloc .. kloc + 7).  The transposing LDS read gathers them: in each
+  // 16-lane group, source lane 2 k + h names row k of its eight rows, tile
+  // positions 8 h .. 8 h + 7 of the 16-position half (16 mb ..) of the slab, and
+  // output lane 8 h + c receives byte c of all eight rows, i.e. MFMA row
+  // 16 mb + 8 h + c, whose column the tile holds at that position.  Wave w
+  // writes dword w of every lane: lane L of group L / 16 reads rows
+  // 32 (w & 1) + 8 (L / 16) + 0..7.
+  const int lane = tid & 63, dw = tid >> 6, g16 = lane >> 4, j16 = lane & 15;
+  const int kloc = 32 * (dw & 1) + 8 * g16 + (j16 >> 1), ploc = 16 * (dw >> 1) + 8 * (j16 & 1);
 #pragma unroll
   for (int q = 0; q < 4; ++q) {
     const int bx = 4 * bq + q;
 #pragma unroll
-    for (int i = 0; i < 2; ++i) {
-      const int id = tid + 256 * i, slab = id >> 8, lane = (id >> 2) & 63, dw = id & 3;
-      const int mloc = slab * 32 + slab_row(16 * (dw >> 1) + (lane & 15)), kloc = 32 * (dw & 1) + 8 * (lane >> 4);
-      // K = rows: the eight codes of a dword are a column of the tile
-      uint32_t w = 0;
-#pragma unroll
-      for (int j = 0; j < 8; ++j) w |= (uint32_t)codes[q][kloc + j][mloc] << (4 * j);
+    for (int slab = 0; slab < 2; ++slab) {
+      typedef int int2v __attribute__((ext_vector_type(2)));
+      typedef __attribute__((address_space(3))) int2v lds_int2v;
+      const int2v v = __builtin_amdgcn_ds_read_tr8_b64_v2i32(
+          (lds_int2v *)(&codes[q][kloc][slab * 32 + ploc]));
+      // eight bytes (codes 0..3) -> eight nibbles
+      const uint32_t x0 = (uint32_t)v[0] | ((uint32_t)v[0] >> 4), x1 = (uint32_t)v[1] | ((uint32_t)v[1] >> 4);
+      const uint32_t w = (x0 & 0xffu) | ((x0 >> 8) & 0xff00u) | ((x1 & 0xffu) << 16) | ((x1 << 8) & 0xff000000u);
       frag_t[frag_dword_index(bx * 2 + slab, by, KBt, lane, dw)] = w;
     }
   }
@@ -750,14 +768,14 @@ __device__ __forceinline__ void x_block(int bt, int fx4, const uint16_t *__restr
 // dY part (bt, p): sub-tiles [sf0, sf1) of 64 out-features for tokens
 // 64 bt .. 64 bt + 63, written transposed into dyt (when set) and summed per
 // row into rsum[0..1] (rows tid / 8 and tid / 8 + 32, totals in threads with
-// tid % 8 == 0).  Sub-tiles are loaded four at a time.
+// tid % 8 == 0).  Sub-tiles are loaded four at a time, the next four while the
+// current ones are stored, and go through the two LDS tiles in pairs (one
+// barrier pair per two sub-tiles).
 __device__ __forceinline__ void dy_part(int bt, int sf0, int sf1, const uint16_t *__restrict__ dY, int64_t m,
                                         int64_t N, int KBt, uint16_t *__restrict__ dyt,
-                                        uint16_t (&tile)[64][64 + 8], float (&rsum)[2]) {
+                                        uint16_t (*tile)[64][64 + 8], float (&rsum)[2]) {
   const int tid = threadIdx.x;
-  for (int base = sf0; base < sf1; base += 4) {
-    u32x4 v[4][2];
-    load_subtiles4(v, dY, m, (int64_t)bt * 64, N, base, sf1 - base);
+  auto process = [&](const u32x4 (&v)[4][2], int base) {
 #pragma unroll
     for (int q = 0; q < 4; ++q) {
       if (base + q >= sf1) break;
@@ -772,13 +790,24 @@ __device__ __forceinline__ void dy_part(int bt, int sf0, int sf1, const uint16_t
         sum += __shfl_xor(sum, 2, 64);
         sum += __shfl_xor(sum, 4, 64);
         rsum[i] += sum;
-        if (dyt != nullptr) *reinterpret_cast<u32x4 *>(&tile[id >> 3][(id & 7) * 8]) = v[q][i];
+        if (dyt != nullptr) *reinterpret_cast<u32x4 *>(&tile[q & 1][id >> 3][(id & 7) * 8]) = v[q][i];
       }
-      if (dyt == nullptr) continue;
+      if (dyt == nullptr || ((q & 1) == 0 && base + q + 1 < sf1)) continue;  // store pairs of sub-tiles
       __syncthreads();
-      tile_store_t<false>(bt, (int64_t)(base + q) * 64, KBt, dyt, tile);
-      __syncthreads();  // the tile is rewritten by the next sub-tile
+      if (q & 1) tile_store_t<false>(bt, (int64_t)(base + q - 1) * 64, KBt, dyt, tile[0]);
+      tile_store_t<false>(bt, (int64_t)(base + q) * 64, KBt, dyt, tile[q & 1]);
+      __syncthreads();  // the tiles are rewritten by the next pair
     }
+  };
+  // two register buffers, statically indexed: trips of eight sub-tiles
+  u32x4 va[4][2], vb[4][2];
+  load_subtiles4(va, dY, m, (int64_t)bt * 64, N, sf0, sf1 - sf0);
+  for (int base = sf0; base < sf1; base += 8) {
+    if (base + 4 < sf1) load_subtiles4(vb, dY, m, (int64_t)bt * 64, N, base + 4, sf1 - base - 4);
+    process(va, base);
+    if (base + 4 >= sf1) break;
+    if (base + 8 < sf1) load_subtiles4(va, dY, m, (int64_t)bt * 64, N, base + 8, sf1 - base - 8);
+    process(vb, base + 4);
   }
 }
 
@@ -801,8 +830,12 @@ __global__ __launch_bounds__(256) void k_bwd_prep(const uint16_t *__restrict__ Z
                                                    float *__restrict__ rsp, uint64_t *__restrict__ maskbits,
                                                    int64_t ldm8, int mask_mode,
                                                    float *__restrict__ za, int nza, float *__restrict__ zb, int nzb) {
-  __shared__ CodeTile codes[4];
-  __shared__ __attribute__((aligned(16))) uint16_t tile[64][64 + 8];
+  // one LDS array: four code tiles (quantise blocks) or two 64 x 64 bf16
+  // tiles (dY parts, X' blocks)
+  __shared__ __attribute__((aligned(16))) uint8_t lds[4 * sizeof(CodeTile)];
+  static_assert(4 * sizeof(CodeTile) >= 2 * 64 * (64 + 8) * sizeof(uint16_t), "bf16 tiles fit");
+  CodeTile *codes = reinterpret_cast<CodeTile *>(lds);
+  uint16_t (*tile)[64][64 + 8] = reinterpret_cast<uint16_t (*)[64][64 + 8]>(lds);
   const int id = blockIdx.x, tid = threadIdx.x;
   if (id == 0) {
     for (int i = tid; i < nza; i += 256) za[i] = 0.0f;
@@ -832,7 +865,7 @@ __global__ __launch_bounds__(256) void k_bwd_prep(const uint16_t *__restrict__ Z
   for (int jj = 0; jj < D; ++jj)
 #pragma unroll
     for (int k = 0; k < D; ++k) a[jj][k] = A[jj * D + k];
-  x_block<D>(x % KBt, x / KBt, X, n, N, a, KBt, xt, tile);
+  x_block<D>(x % KBt, x / KBt, X, n, N, a, KBt, xt, tile[0]);
 }
 
 // ---- launchers -------------------------------------------------------------
