@@ -40,6 +40,8 @@ constexpr int kKStep = 64;   // K per main-loop step
 #define LCVQ_WAIT_ALL() __builtin_amdgcn_s_waitcnt(0)
 // s_waitcnt vmcnt(N) lgkmcnt(0) (gfx9 encoding; expcnt left at its maximum).
 #define LCVQ_WAIT_VM_LGKM0(N) __builtin_amdgcn_s_waitcnt(((N) & 15) | (((N) >> 4) << 14) | (7 << 4))
+// s_waitcnt lgkmcnt(0) only.
+#define LCVQ_WAIT_LGKM0() __builtin_amdgcn_s_waitcnt(15 | (3 << 14) | (7 << 4))
 // Workgroup barrier without the release fence of __syncthreads() (which would
 // drain the prefetch loads); the asm statements keep the compiler from moving
 // memory operations across it.  LDS visibility is ensured by the waits above.
@@ -175,6 +177,34 @@ __global__ __launch_bounds__(256, 1) void k_gemm_codes(
   const uint32_t bstep = kMode == 0 ? 4096u : 128u;
   const int kB_last = kMode == 0 ? KB * 64 : (int)ldB - 8;
 
+  // Input gradient with map gradients: the wave's X tile (its 64 tokens x the
+  // block's 256 columns) is copied to LDS during the main loop, one 1 KiB pair
+  // (16-token block tb, slab mi) per K step, in the order the epilogue reads
+  // it: lane L of pair p = 8 tb + mi holds X[t, c .. c + 7] with t = tw + 16 tb
+  // + L % 16 and c = 256 tm + 32 mi + 8 (L / 16).  The epilogue then finds X
+  // in LDS instead of waiting on HBM latency once per pair.
+  constexpr int kXPairs = 32;
+  __shared__ __attribute__((aligned(1024))) char xs[kMode == 1 ? 4 * kXPairs * 1024 : 16];
+  const bool want_map = kMode == 1 && dA != nullptr;
+  const __amdgpu_buffer_rsrc_t rx = make_rsrc(X + tw * Mvalid, want_map ? (Tvalid - tw) * Mvalid * 2 : 0);
+  if (want_map && (tw + 64 > Tvalid || (int64_t)tm * kTile + kTile > Mvalid)) {
+    // a tile reaching past the tensor: the pairs start as zeros, so rows and
+    // columns outside it read as zero whatever the out-of-range copies leave
+#pragma unroll
+    for (int p = 0; p < kXPairs; ++p)
+      *reinterpret_cast<u32x4 *>(xs + (wave * kXPairs + p) * 1024 + lane * 16) = u32x4{0u, 0u, 0u, 0u};
+    LCVQ_WAIT_LGKM0();
+    asm volatile("" ::: "memory");
+  }
+  auto xprefetch = [&](int p) {
+    if constexpr (kMode == 1) {
+      const int tl = (p >> 3) * 16 + c16;
+      const int64_t c = (int64_t)tm * kTile + 8 * q + (p & 7) * 32;
+      const uint32_t off = c < Mvalid ? (uint32_t)(tl * Mvalid + c) * 2u : kOffNone;
+      buffer_to_lds16(rx, (lds_void *)(xs + (wave * kXPairs + p) * 1024), off);
+    }
+  };
+
   floatx4 acc[16][4];  // [row block 2 mi + rb][16-token block tb]
 #pragma unroll
   for (int i = 0; i < 16; ++i)
@@ -200,6 +230,7 @@ __global__ __launch_bounds__(256, 1) void k_gemm_codes(
         cb[buf][ni][fr] = __builtin_amdgcn_raw_buffer_load_b128(
             rsB, live && kin ? (int)(boff[ni][fr] + (uint32_t)kb * bstep) : (int)kOffNone, 0, 0);
       }
+    if (want_map && kb < kXPairs) xprefetch(kb);
   };
   // 32 A operands per step (sub-step kk2, row block 2 mi + rb), each used by
   // four MFMAs; the conversion of the next one is placed between the second
@@ -241,6 +272,8 @@ __global__ __launch_bounds__(256, 1) void k_gemm_codes(
     load(1, kb + 3);
     __builtin_amdgcn_sched_barrier(0);
   }
+  if (want_map)  // K shorter than the pair count: the rest of the X tile
+    for (int p = KB + 2; p < kXPairs; ++p) xprefetch(p);
   mfma_drain();
 
   // ---------------------------------------------------------------- epilogue
@@ -288,17 +321,10 @@ __global__ __launch_bounds__(256, 1) void k_gemm_codes(
       }
     }
   } else {
-    const bool want_map = dA != nullptr;
-    // X[t, c .. c + 7] of pair p = tb * 8 + mi, fetched two pairs ahead
-    // (three rotating 16-byte buffers)
-    const __amdgpu_buffer_rsrc_t rx = make_rsrc(X + tw * Mvalid, want_map ? (Tvalid - tw) * Mvalid * 2 : 0);
-    u32x4 xv[3];
-    auto xload = [&](int p) {
-      const int tb = p >> 3, mi = p & 7, tl = tb * 16 + c16;
-      const int64_t c = cb0 + mi * 32;
-      const uint32_t off = c < Mvalid ? (uint32_t)(tl * Mvalid + c) * 2u : kOffNone;
-      xv[p % 3] = __builtin_amdgcn_raw_buffer_load_b128(rx, off, 0, 0);
-    };
+    // X pairs in LDS (complete once this wave's loads are; the empty statement
+    // keeps the compiler from moving the LDS reads above the wait)
+    LCVQ_WAIT_VM_LGKM0(0);
+    asm volatile("" ::: "memory");
     // The A^T map on the matrix cores: per slab and 16-token block, dX^T =
     // blockdiag(A) P^T, with M = output column c' (rows in slab_row order, so
     // lane L ends with c' = 8 (L / 16) + 0..7 of token L % 16, one 16-byte
@@ -327,55 +353,70 @@ __global__ __launch_bounds__(256, 1) void k_gemm_codes(
 #pragma unroll
       for (int e = 0; e < 4; ++e) bsel[mb][e] = to_vgpr(bvec[(4 * mb + e) % D]);
     }
-    float gA[D][D], gb[D];
+    // The map gradient on the matrix cores: dA[j, k] = sum over samples (t, g)
+    // of X[t, g D + j] P[t, g D + k], a product with the samples as K.  Both
+    // operands need a pair's samples along each lane's eight K values, i.e. the
+    // pair tile transposed: X from its LDS pair, P (split into bf16 high and
+    // low parts as for dX) after a pass through a two-pair LDS ring, both read
+    // with the transposing LDS load.  Operand row r (M for X, N for P) holds,
+    // at K = 8 G + i (G = lane / 16), element r % 8 of the 16-byte row of the
+    // pair's lane 16 (2 (r / 8) + G / 2) + 8 (G % 2) + i.  For D = 8 that is
+    // column r % 8 of the lane's group, so rows r < 8 and r >= 8 form two slots
+    // of 32 samples each; for D = 4 it is column r % 4 of the lane's group
+    // (r / 4) % 2: four slots.  One 16x16x32 instruction per pair and part, of
+    // which the diagonal slot blocks (r / D == r' / D) are kept.  (Transposing
+    // read: in each 16-lane group G, lane 4 e + u addresses row 16 (2 (u / 2)
+    // + G / 2) + 8 (G % 2) + e, + 4 for the second read, at column 4 (u % 2);
+    // output lane 4 u + w gets column 4 (u % 2) + w of the eight rows.)
+    // db[j] = sum X[t, g D + j] rs[t] stays on the vector units.
+    __shared__ __attribute__((aligned(1024))) char pst[kMode == 1 ? 4 * 2 * 2048 : 16];
+    const int tq = c16 & 3, te = c16 >> 2;
+    const int toff = 16 * (16 * (2 * (tq >> 1) + (q >> 1)) + 8 * (q & 1) + te) + 8 * (tq & 1);
+    auto tr8 = [&](const char *base) {
+      const bf16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4 *)(base + toff));
+      const bf16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4 *)(base + toff + 64));
+      return __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
+    };
+    floatx4 dah = floatx4{0.0f, 0.0f, 0.0f, 0.0f}, dal = dah;
+    float gb[D];
 #pragma unroll
-    for (int j = 0; j < D; ++j) {
-      gb[j] = 0.0f;
-#pragma unroll
-      for (int k = 0; k < D; ++k) gA[j][k] = 0.0f;
-    }
-    xload(0);
-    xload(1);
+    for (int j = 0; j < D; ++j) gb[j] = 0.0f;
 #pragma unroll
     for (int p = 0; p < 32; ++p) {
       const int tb = p >> 3, mi = p & 7, tl = tb * 16 + c16;
-      if (p + 2 < 32) xload(p + 2);
-      float y[8], x[8], pv8[8];
-#pragma unroll
-      for (int e = 0; e < 4; ++e) {
-        x[2 * e] = bf16_lo(xv[p % 3][e]);
-        x[2 * e + 1] = bf16_hi(xv[p % 3][e]);
-      }
+      const char *xp = xs + (wave * kXPairs + p) * 1024;
+      float y[8], pv8[8];
 #pragma unroll
       for (int i = 0; i < 8; ++i) pv8[i] = d8(mi, tb, i);
-      {
-        u32x4 ph, pl;
+      u32x4 ph, pl;
 #pragma unroll
-        for (int e = 0; e < 4; ++e) {
-          ph[e] = pack_bf16x2(pv8[2 * e], pv8[2 * e + 1]);
-          pl[e] = pack_bf16x2(pv8[2 * e] - bf16_lo(ph[e]), pv8[2 * e + 1] - bf16_hi(ph[e]));
-        }
-        const bf16x8 bh = __builtin_bit_cast(bf16x8, ph), bl = __builtin_bit_cast(bf16x8, pl);
-#pragma unroll
-        for (int mb = 0; mb < 2; ++mb) {
-          floatx4 cacc;
-#pragma unroll
-          for (int e = 0; e < 4; ++e) cacc[e] = vt[tb] * bsel[mb][e];
-          cacc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(amh[mb], bh, cacc, 0, 0, 0);
-          cacc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(aml[mb], bh, cacc, 0, 0, 0);
-          cacc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(amh[mb], bl, cacc, 0, 0, 0);
-#pragma unroll
-          for (int e = 0; e < 4; ++e) y[4 * mb + e] = cacc[e];
-        }
+      for (int e = 0; e < 4; ++e) {
+        ph[e] = pack_bf16x2(pv8[2 * e], pv8[2 * e + 1]);
+        pl[e] = pack_bf16x2(pv8[2 * e] - bf16_lo(ph[e]), pv8[2 * e + 1] - bf16_hi(ph[e]));
       }
+      const bf16x8 bh = __builtin_bit_cast(bf16x8, ph), bl = __builtin_bit_cast(bf16x8, pl);
 #pragma unroll
-      for (int g = 0; g < 8 / D; ++g) {
+      for (int mb = 0; mb < 2; ++mb) {
+        floatx4 cacc;
 #pragma unroll
-        for (int j = 0; j < D; ++j) {
+        for (int e = 0; e < 4; ++e) cacc[e] = vt[tb] * bsel[mb][e];
+        cacc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(amh[mb], bh, cacc, 0, 0, 0);
+        cacc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(aml[mb], bh, cacc, 0, 0, 0);
+        cacc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(amh[mb], bl, cacc, 0, 0, 0);
 #pragma unroll
-          for (int k = 0; k < D; ++k) gA[j][k] = fmaf(x[g * D + j], pv8[g * D + k], gA[j][k]);
-          gb[j] = fmaf(x[g * D + j], vt[tb], gb[j]);
-        }
+        for (int e = 0; e < 4; ++e) y[4 * mb + e] = cacc[e];
+      }
+      if (want_map) {
+        char *pp = pst + (wave * 2 + (p & 1)) * 2048;
+        *reinterpret_cast<u32x4 *>(pp + lane * 16) = ph;
+        *reinterpret_cast<u32x4 *>(pp + 1024 + lane * 16) = pl;
+        const bf16x8 xa = tr8(xp), pbh = tr8(pp), pbl = tr8(pp + 1024);
+        dah = __builtin_amdgcn_mfma_f32_16x16x32_bf16(xa, pbh, dah, 0, 0, 0);
+        dal = __builtin_amdgcn_mfma_f32_16x16x32_bf16(xa, pbl, dal, 0, 0, 0);
+        const u32x4 xv = *reinterpret_cast<const u32x4 *>(xp + lane * 16);
+#pragma unroll
+        for (int e = 0; e < 8; ++e)
+          gb[e % D] = fmaf((e & 1) ? bf16_hi(xv[e >> 1]) : bf16_lo(xv[e >> 1]), vt[tb], gb[e % D]);
       }
       const int64_t c = cb0 + mi * 32;
       const uint32_t off = c < Mvalid ? (uint32_t)(tl * ldo + c) * 2u : kOffNone;
@@ -385,28 +426,36 @@ __global__ __launch_bounds__(256, 1) void k_gemm_codes(
       __builtin_amdgcn_raw_buffer_store_b128(w, ro, off, 0, 0);
     }
     if (want_map) {
-      // lanes -> wave (shuffles), waves -> block (LDS), one atomic per entry
-      __shared__ float red[4][D * D + D];
+      // lane L holds rows 4 (L / 16) + 0..3 of column L % 16; slot blocks on the
+      // diagonal go to LDS per wave and slot, db by shuffles; then one atomic
+      // per entry and block
+      constexpr int kSlots = 16 / D;
+      __shared__ float red[4][kSlots * D * D + D];
 #pragma unroll
-      for (int j = 0; j < D; ++j) {
+      for (int e = 0; e < 4; ++e) {
+        const int mrow = 4 * q + e;
+        if (mrow / D == c16 / D) red[wave][(mrow / D) * D * D + (mrow % D) * D + c16 % D] = dah[e] + dal[e];
+      }
 #pragma unroll
-        for (int k = 0; k < D; ++k)
-#pragma unroll
-          for (int o = 32; o >= 1; o >>= 1) gA[j][k] += __shfl_xor(gA[j][k], o, 64);
+      for (int j = 0; j < D; ++j)
 #pragma unroll
         for (int o = 32; o >= 1; o >>= 1) gb[j] += __shfl_xor(gb[j], o, 64);
-      }
       if (lane == 0) {
 #pragma unroll
-        for (int j = 0; j < D; ++j) {
-          red[wave][D * D + j] = gb[j];
-#pragma unroll
-          for (int k = 0; k < D; ++k) red[wave][j * D + k] = gA[j][k];
-        }
+        for (int j = 0; j < D; ++j) red[wave][kSlots * D * D + j] = gb[j];
       }
       __syncthreads();
       if (tid < D * D + D) {
-        const float v = red[0][tid] + red[1][tid] + red[2][tid] + red[3][tid];
+        float v = 0.0f;
+#pragma unroll
+        for (int w = 0; w < 4; ++w) {
+          if (tid < D * D) {
+#pragma unroll
+            for (int sl = 0; sl < kSlots; ++sl) v += red[w][sl * D * D + tid];
+          } else {
+            v += red[w][kSlots * D * D + tid - D * D];
+          }
+        }
         if (tid < D * D) unsafeAtomicAdd(dA + tid, v);
         else unsafeAtomicAdd(db + (tid - D * D), v);
       }
