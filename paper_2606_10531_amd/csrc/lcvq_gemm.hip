@@ -294,7 +294,7 @@ __global__ __launch_bounds__(256, 1) void k_gemm_codes(
   const int64_t cb0 = (int64_t)tm * kTile + 8 * q;
   // Per-token term, held as up to kMaxParts partial rows vstride apart and
   // summed here: s of the forward, rowsum(dY) of the input gradient.
-  constexpr int kMaxParts = kMaxActChunks;  // the row sums of dY have at most eight
+  constexpr int kMaxParts = kMaxActChunks;  // s has at most this many parts, rowsum(dY) at most eight
   const __amdgpu_buffer_rsrc_t rv = make_rsrc(vecT + tw, ((int64_t)(vparts - 1) * vstride + Tvalid - tw) * 4);
   float vp[kMaxParts][4], vt[4];
 #pragma unroll
