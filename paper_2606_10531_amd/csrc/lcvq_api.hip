@@ -94,7 +94,7 @@ BwdLayout bwd_layout(int64_t N, int64_t m, int64_t n, bool bf16) {
     L.dyt = L.xt + up256((size_t)lcvq::round_up(n, 256) * Nt * 2);
     // straight-through mask of Z, one bit per element (rows of whole 64-bit words)
     L.mask = L.dyt + up256((size_t)lcvq::round_up(m, 256) * Nt * 2);
-    L.total = L.mask + up256((size_t)m * lcvq::mask_words_per_row(n) * 8);
+    L.total = L.mask + up256((size_t)lcvq::mask_bytes(m, n));
   } else {
     L.frag = L.xt = L.dyt = L.mask = L.total = up256((size_t)N * 4);
   }
@@ -111,7 +111,7 @@ struct SavedLayout {
 SavedLayout saved_layout(int64_t N, int64_t m, int64_t n) {
   SavedLayout L{};
   const size_t Nt = (size_t)lcvq::bwd_tokens(N);
-  const size_t mask = (size_t)m * lcvq::mask_words_per_row(n) * 8;
+  const size_t mask = (size_t)lcvq::mask_bytes(m, n);
   L.frag_t = 0;
   L.xt = up256((size_t)(lcvq::round_up(n, 256) / 32) * (lcvq::round_up(m, 128) / 64) * 1024);
   L.mask_r = L.xt + up256((size_t)lcvq::round_up(n, 256) * Nt * 2);

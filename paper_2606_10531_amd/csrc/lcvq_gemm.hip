@@ -486,7 +486,7 @@ __global__ __launch_bounds__(256, 1) void k_gemm_codes(
 
 template <bool kDge>
 __global__ __launch_bounds__(256, 1) void k_gemm_dw(const uint16_t *__restrict__ xt, const uint16_t *__restrict__ dyt,
-                                                    int KBt, const uint64_t *__restrict__ maskbits, int64_t ldm8,
+                                                    int KBt, const uint64_t *__restrict__ maskbits, int64_t nbc,
                                                     const uint16_t *__restrict__ Zb, Quantizer qz, int mask_mode,
                                                     GradEst est,
                                                     int accumulate, void *__restrict__ dZ, int dz_bf16, int m, int n,
@@ -593,9 +593,11 @@ __global__ __launch_bounds__(256, 1) void k_gemm_dw(const uint16_t *__restrict__
   // an out-of-range offset.  Every load (mask words or Z, and old dZ when
   // accumulating) of a column block is issued before the stores of the
   // previous one: loads and stores share one counter.
-  const __amdgpu_buffer_rsrc_t rmk = make_rsrc(maskbits + (int64_t)r0 * ldm8, kDge ? 0 : (int64_t)(m - r0) * ldm8 * 8);
+  // the bitmap tiles of rows r0 .. r0 + 255 (four 64-row bands of nbc tiles)
+  const __amdgpu_buffer_rsrc_t rmk = make_rsrc((const char *)maskbits + (int64_t)(r0 / 64) * nbc * 2048,
+                                               kDge ? 0 : ((int64_t)(m + 63) / 64 - r0 / 64) * nbc * 2048);
   const __amdgpu_buffer_rsrc_t rz = make_rsrc(Zb + (int64_t)r0 * n, kDge ? (int64_t)(m - r0) * n * 2 : 0);
-  const int64_t mw = (int64_t)tm * 4 + wave;  // this wave's word of each bitmap row
+  // this wave's 64 columns are word `wave` of each row of column block tm
   const int es = dz_bf16 ? 2 : 4;
   const __amdgpu_buffer_rsrc_t rg = make_rsrc((char *)dZ + (int64_t)r0 * n * es, (int64_t)(m - r0) * n * es);
   u32x2 mk[2];        // mask word of the row, per buffer
@@ -610,7 +612,8 @@ __global__ __launch_bounds__(256, 1) void k_gemm_dw(const uint16_t *__restrict__
         zv[buf][mi] = __builtin_amdgcn_raw_buffer_load_b128(rz, c < n ? (uint32_t)(rl * n + c) * 2u : kOffNone, 0, 0);
       }
     } else {
-      mk[buf] = __builtin_amdgcn_raw_buffer_load_b64(rmk, mw < ldm8 ? (int)((rl * ldm8 + mw) * 8) : (int)kOffNone, 0, 0);
+      mk[buf] = __builtin_amdgcn_raw_buffer_load_b64(
+          rmk, r0 + rl < m ? (int)((((rl >> 6) * nbc + tm) * 64 + (rl & 63)) * 32 + wave * 8) : (int)kOffNone, 0, 0);
     }
     if (!accumulate) return;
 #pragma unroll
@@ -722,11 +725,11 @@ hipError_t launch_dw_bf16(const uint16_t *xt, const uint16_t *dyt, const uint64_
   const int tiles_m = (int)ceil_div(n, kTile), tiles_n = (int)ceil_div(m, kTile);
   const int KBt = (int)(bwd_tokens(N) / 64);  // even
   if (est.dge)
-    k_gemm_dw<true><<<tiles_m * tiles_n, 256, 0, st>>>(xt, dyt, KBt, nullptr, mask_words_per_row(n), Z, qz,
+    k_gemm_dw<true><<<tiles_m * tiles_n, 256, 0, st>>>(xt, dyt, KBt, nullptr, mask_col_blocks(n), Z, qz,
                                                        mask_mode, est, accumulate, dZ, dz_bf16 ? 1 : 0, (int)m, (int)n, tiles_m,
                                                        tiles_n);
   else
-    k_gemm_dw<false><<<tiles_m * tiles_n, 256, 0, st>>>(xt, dyt, KBt, maskbits, mask_words_per_row(n), nullptr,
+    k_gemm_dw<false><<<tiles_m * tiles_n, 256, 0, st>>>(xt, dyt, KBt, maskbits, mask_col_blocks(n), nullptr,
                                                         qz, mask_mode, est, accumulate, dZ, dz_bf16 ? 1 : 0, (int)m,
                                                         (int)n, tiles_m, tiles_n);
   return hipGetLastError();

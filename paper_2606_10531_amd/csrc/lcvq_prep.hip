@@ -107,7 +107,7 @@ __device__ __forceinline__ void quant_block(int bq, int by, int gx, const uint16
                                             int64_t n, const Quantizer &qz, uint32_t *__restrict__ frag, int KB,
                                             uint8_t *__restrict__ packed, CodeTile *codes,
                                             uint32_t *__restrict__ frag_t = nullptr, int KBt = 0,
-                                            uint64_t *__restrict__ maskbits = nullptr, int64_t ldm8 = 0,
+                                            uint64_t *__restrict__ maskbits = nullptr, int64_t nbc = 0,
                                             int mask_mode = 0, uint64_t *__restrict__ maskbits2 = nullptr) {
   constexpr bool kFwd = kMode != kQuantBwd, kTrans = kMode != kQuantFwd;
   const int tid = threadIdx.x;
@@ -123,7 +123,8 @@ __device__ __forceinline__ void quant_block(int bq, int by, int gx, const uint16
       if (r < m && c < n) v[q][i] = *reinterpret_cast<const u32x4 *>(Z + r * n + c);
     }
   // straight-through mask of the eight latents of (q, i) -> byte (cc / 8) of
-  // the row's 64-bit word; threads cc / 8 = 0 and 4 store the two halves
+  // word q of the row in the block's bitmap tile; threads cc / 8 = 0 and 4
+  // store the two halves
   auto store_mask = [&](int q, int i, uint64_t *__restrict__ bits, int mode) {
     const int id = tid + 256 * i, rr = id >> 3, cc = (id & 7) * 8;
     const int64_t r = r0 + rr, c = (int64_t)(4 * bq + q) * 64 + cc;
@@ -137,8 +138,8 @@ __device__ __forceinline__ void quant_block(int bq, int by, int gx, const uint16
     mb <<= 8 * (id & 3);
     mb |= (uint32_t)__shfl_xor((int)mb, 1, 64);
     mb |= (uint32_t)__shfl_xor((int)mb, 2, 64);
-    const int64_t wc = c / 64;
-    if ((id & 3) == 0 && r < m && wc < ldm8) reinterpret_cast<uint32_t *>(bits + r * ldm8 + wc)[(id >> 2) & 1] = mb;
+    if ((id & 3) == 0 && r < m)
+      reinterpret_cast<uint32_t *>(bits + (((int64_t)by * nbc + bq) * 64 + rr) * 4 + q)[(id >> 2) & 1] = mb;
   };
 #pragma unroll
   for (int q = 0; q < 4; ++q)
@@ -417,7 +418,7 @@ __global__ __launch_bounds__(256) void k_fwd_prep(const uint16_t *__restrict__ Z
                                                    uint16_t *__restrict__ Xp, int KB, int spc, int nkc, int64_t Np,
                                                    float *__restrict__ sp, uint32_t *__restrict__ frag_t, int KBq,
                                                    uint64_t *__restrict__ mask_r, uint64_t *__restrict__ mask_l,
-                                                   int64_t ldm8, uint16_t *__restrict__ xt, int KBx) {
+                                                   int64_t nbc, uint16_t *__restrict__ xt, int KBx) {
   // LDS only for the saved state: the quantise blocks' code tiles and the
   // activation blocks' X' tile (one launch holds both kinds of block)
   __shared__ __attribute__((aligned(16))) uint8_t lds[kSave ? 4 * sizeof(CodeTile) : 16];
@@ -428,7 +429,7 @@ __global__ __launch_bounds__(256) void k_fwd_prep(const uint16_t *__restrict__ Z
     quant_tile_of_block(id, gq, nq, bq, by);
     if constexpr (kSave)
       quant_block<kQuantSave>(bq, by, KB, Z, m, n, qz, frag, KB, packed, reinterpret_cast<CodeTile *>(lds), frag_t,
-                              KBq, mask_r, ldm8, 0, mask_l);
+                              KBq, mask_r, nbc, 0, mask_l);
     else
       quant_block<kQuantFwd>(bq, by, KB, Z, m, n, qz, frag, KB, packed, nullptr);
   } else {
@@ -850,7 +851,7 @@ __global__ __launch_bounds__(256) void k_bwd_prep(const uint16_t *__restrict__ Z
                                                    int nfy, int spf, int nrp,
                                                    uint16_t *__restrict__ xt, uint16_t *__restrict__ dyt,
                                                    float *__restrict__ rsp, uint64_t *__restrict__ maskbits,
-                                                   int64_t ldm8, int mask_mode,
+                                                   int64_t nbc, int mask_mode,
                                                    float *__restrict__ za, int nza, float *__restrict__ zb, int nzb) {
   // one LDS array: four code tiles (quantise blocks) or two 64 x 64 bf16
   // tiles (dY parts, X' blocks)
@@ -879,7 +880,7 @@ __global__ __launch_bounds__(256) void k_bwd_prep(const uint16_t *__restrict__ Z
   if (q < nq) {
     int bq, by;
     quant_tile_of_block(q, gq, nq, bq, by);
-    quant_block<kQuantBwd>(bq, by, 4 * gq, Z, m, n, qz, nullptr, 0, nullptr, codes, frag, KBq, maskbits, ldm8,
+    quant_block<kQuantBwd>(bq, by, 4 * gq, Z, m, n, qz, nullptr, 0, nullptr, codes, frag, KBq, maskbits, nbc,
                            mask_mode);
     return;
   }
@@ -922,13 +923,13 @@ hipError_t launch_fwd_prep_bf16(const uint16_t *Z, int64_t m, int64_t n, const Q
   const unsigned grid = (unsigned)(nq + nbt * nkc);
   if (save != nullptr) {
     const int KBq = (int)(round_up(m, 128) / 64), KBx = (int)(round_up(n, 256) / 64);
-    const int64_t ldm8 = mask_words_per_row(n);
+    const int64_t nbc = mask_col_blocks(n);
     if (d == 8)
       k_fwd_prep<8, true><<<grid, 256, 0, st>>>(Z, m, n, qz, frag, packed, gq, nq, X, N, A, b, Xp, KB, spc, nkc, Np, sp,
-                                                save->frag_t, KBq, save->mask_r, save->mask_l, ldm8, save->xt, KBx);
+                                                save->frag_t, KBq, save->mask_r, save->mask_l, nbc, save->xt, KBx);
     else
       k_fwd_prep<4, true><<<grid, 256, 0, st>>>(Z, m, n, qz, frag, packed, gq, nq, X, N, A, b, Xp, KB, spc, nkc, Np, sp,
-                                                save->frag_t, KBq, save->mask_r, save->mask_l, ldm8, save->xt, KBx);
+                                                save->frag_t, KBq, save->mask_r, save->mask_l, nbc, save->xt, KBx);
   } else {
     if (d == 8)
       k_fwd_prep<8, false><<<grid, 256, 0, st>>>(Z, m, n, qz, frag, packed, gq, nq, X, N, A, b, Xp, KB, spc, nkc, Np, sp,
@@ -1025,7 +1026,7 @@ hipError_t launch_bwd_prep_bf16(const uint16_t *Z, int64_t m, int64_t n, const Q
                                 const uint16_t *dY, const float *A, int d, int64_t N, uint16_t *xt,
                                 uint16_t *dyt, float *rsp, uint64_t *maskbits, int mask_mode, float *za, int nza,
                                 float *zb, int nzb, hipStream_t st) {
-  const int64_t ldm8 = mask_words_per_row(n);
+  const int64_t nbc = mask_col_blocks(n);
   // codes: M = columns of Z padded to 256 (four 64-column tiles per block), K = rows
   // padded to 128 (skipped when frag == nullptr)
   const int gq = (int)(round_up(n, 256) / 256), KBq = (int)(round_up(m, 128) / 64);
@@ -1038,10 +1039,10 @@ hipError_t launch_bwd_prep_bf16(const uint16_t *Z, int64_t m, int64_t n, const Q
   const unsigned grid = (unsigned)(nq + KBt * (nfx4 + nrp));
   if (d == 8)
     k_bwd_prep<8><<<grid, 256, 0, st>>>(Z, m, n, qz, frag, KBq, gq, nq, X, dY, A, N, KBt, nfx4, nfy, spf, nrp,
-                                        xt, dyt, rsp, maskbits, ldm8, mask_mode, za, nza, zb, nzb);
+                                        xt, dyt, rsp, maskbits, nbc, mask_mode, za, nza, zb, nzb);
   else
     k_bwd_prep<4><<<grid, 256, 0, st>>>(Z, m, n, qz, frag, KBq, gq, nq, X, dY, A, N, KBt, nfx4, nfy, spf, nrp,
-                                        xt, dyt, rsp, maskbits, ldm8, mask_mode, za, nza, zb, nzb);
+                                        xt, dyt, rsp, maskbits, nbc, mask_mode, za, nza, zb, nzb);
   return hipGetLastError();
 }
 }  // namespace lcvq

@@ -54,9 +54,13 @@ inline int rowsum_parts(int64_t m) {
   const int64_t p = (nfy + rowsum_subtiles_per_part(m) - 1) / rowsum_subtiles_per_part(m);
   return p < 1 ? 1 : (int)p;
 }
-// Row stride, in 64-bit words, of the straight-through mask bitmap of an m x n
-// matrix (bit c % 64 of word r * stride + c / 64 is the mask of Z[r, c]).
-inline int64_t mask_words_per_row(int64_t n) { return (n + 63) / 64; }
+// Straight-through mask bitmap of an m x n matrix, in tiles of 64 rows x 256
+// columns (2 KiB each, row-band-major, mask_col_blocks(n) tiles per band).
+// Within a tile, row i holds four 64-bit words (32 bytes), word j for columns
+// 64 j .. 64 j + 63 of the tile, bit c % 64 for column c.  Each quantise block
+// writes exactly one tile per bitmap.
+inline int64_t mask_col_blocks(int64_t n) { return (n + 255) / 256; }
+inline int64_t mask_bytes(int64_t m, int64_t n) { return (m + 63) / 64 * mask_col_blocks(n) * 2048; }
 
 // bf16 backward prepass in one launch: codes of the input-gradient product
 // (frag, optional; that product reads dY in place), the weight-gradient operands (xt, dyt; skipped when xt is nullptr), the partial
