@@ -130,23 +130,26 @@ __device__ __forceinline__ uint32_t as_u(float f) { return __float_as_uint(f); }
 
 // ============================================================================
 // Products with codes as the A operand (forward, input gradient).
-// No LDS: wave w of a block owns the 256 weight-side rows x 64 tokens
-// [64 w, 64 w + 64) of the block tile and streams both operands straight into
-// registers: the codes of the block's eight 32-row slabs (operand layout; the
-// four waves share them through the L1) and its own activations: for the
-// forward X' in the matrix-core B layout, as the activation transform writes
-// it; for the input gradient dY itself, row-major, read in place (a lane's B
-// operand, eight consecutive out-features of one token, is 16 contiguous bytes
-// of dY, and the 16 token rows a load touches are each read in whole 128-byte
-// lines by its two K halves).  K is padded to an even number of 64-wide steps;
-// out-features >= ldB read as zero.
+// Each wave owns 256 weight-side rows x 64 tokens (where those sit in the
+// block tile is set at the top of the kernel) and streams both operands
+// straight into registers, with no LDS stage: the codes of its eight 32-row
+// slabs (operand layout; waves on the same rows share them through the L1)
+// and its activations: for the forward X' in the matrix-core B layout, as the
+// activation transform writes it; for the input gradient dY itself,
+// row-major, read in place (a lane's B operand, eight consecutive
+// out-features of one token, is 16 contiguous bytes of dY, and the 16 token
+// rows a load touches are each read in whole 128-byte lines by its two K
+// halves).  K is padded to an even number of 64-wide steps; out-features >=
+// ldB read as zero.  LDS holds only the input gradient's X tile and map-
+// gradient staging (below).
 // ============================================================================
 
 // Input-gradient mode also forms the map gradients from the same accumulator
 // P = dY codes: dA[j, k] = sum_{t,g} X[t, g*D + j] P[t, g*D + k] and
 // db[j] = sum_{t,g} X[t, g*D + j] rs[t] (the chain rule through X' = X blockdiag(A)
-// and s = X b~), reduced lanes -> wave -> block and added with one atomic per
-// block per entry.  X is N x Mvalid row-major; dA == nullptr skips this.
+// and s = X b~): dA on the matrix cores, db on the vector units, reduced
+// lanes -> wave -> block and added with one atomic per block per entry.  X is
+// N x Mvalid row-major; dA == nullptr skips this.
 template <int kMode, int D>  // kMode 0: forward (B = X' fragments), 1: input gradient (B = dY, row length ldB)
 __global__ __launch_bounds__(256, 1) void k_gemm_codes(
     const uint32_t *__restrict__ frag, int KB, const uint16_t *__restrict__ Bsrc, int64_t ldB,
