@@ -40,11 +40,6 @@ constexpr int kKStep = 64;   // K per main-loop step
 #define LCVQ_WAIT_ALL() __builtin_amdgcn_s_waitcnt(0)
 // s_waitcnt vmcnt(N) lgkmcnt(0) (gfx9 encoding; expcnt left at its maximum).
 #define LCVQ_WAIT_VM_LGKM0(N) __builtin_amdgcn_s_waitcnt(((N) & 15) | (((N) >> 4) << 14) | (7 << 4))
-// Cache policy of the dX stores: non-temporal.  dX is written once and read by
-// nobody in this call; streaming it past the caches shortens the end-of-kernel
-// drain of the 256 blocks' stores and leaves the last-level cache to the
-// operands (measured: about 4.5 us on the 4096^3 product).
-constexpr int kNonTemporal = 2;
 // s_waitcnt lgkmcnt(0) only.
 #define LCVQ_WAIT_LGKM0() __builtin_amdgcn_s_waitcnt(15 | (3 << 14) | (7 << 4))
 // Workgroup barrier without the release fence of __syncthreads() (which would
@@ -448,7 +443,7 @@ __global__ __launch_bounds__(256, 1) void k_gemm_codes(
       u32x4 w;
 #pragma unroll
       for (int e = 0; e < 4; ++e) w[e] = pack_bf16x2(y[2 * e], y[2 * e + 1]);
-      __builtin_amdgcn_raw_buffer_store_b128(w, ro, off, 0, kNonTemporal);
+      __builtin_amdgcn_raw_buffer_store_b128(w, ro, off, 0, 0);
     }
     if (want_map) {
       // lane L holds rows 4 (L / 16) + 0..3 of column L % 16; slot blocks on the
