@@ -216,11 +216,14 @@ __global__ __launch_bounds__(256, 1) void k_gemm_codes(
     LCVQ_WAIT_LGKM0();
     asm volatile("" ::: "memory");
   }
+  // this lane's offset for pair 0 and its columns inside the tensor from there
+  const int64_t xcol0 = (int64_t)tm * kTile + 8 * q;
+  const uint32_t xoff0 = (uint32_t)(c16 * Mvalid + xcol0) * 2u;
+  const int xcols = (int)(Mvalid - xcol0 < 256 ? Mvalid - xcol0 : 256);
   auto xprefetch = [&](int p) {
     if constexpr (kMode == 1) {
-      const int tl = (p >> 3) * 16 + c16;
-      const int64_t c = (int64_t)tm * kTile + 8 * q + (p & 7) * 32;
-      const uint32_t off = c < Mvalid ? (uint32_t)(tl * Mvalid + c) * 2u : kOffNone;
+      const int tb = p >> 3, mi = p & 7;
+      const uint32_t off = 32 * mi < xcols ? xoff0 + (uint32_t)(tb * 16 * Mvalid + mi * 32) * 2u : kOffNone;
       buffer_to_lds16(rx, (lds_void *)(xs + (wave * kXPairs + p) * 1024), off);
     }
   };
