@@ -17,15 +17,17 @@
 // nibbles and the fp4 -> bf16 converter turns them into bf16 values 0..3 in
 // registers, so the dense W_hat never exists anywhere.
 //
-// The instructions are issued from inline assembly with the accumulators
-// bound to AGPRs: the compiler's own selection of this instruction moves the
-// accumulators between registers around every loop trip.  The compiler cannot
-// see hazards inside such statements, so the code provides the wait states
-// itself: after the zeroing of the accumulators (acc_fence), before an MFMA
-// that reads a just-converted codes operand (mfma16_valu_a; only the first of
-// a step: the other conversions are themselves inline assembly placed two
-// MFMAs ahead of their consumer), and after the loop (mfma_drain).  All other
-// operands come from loads, which the compiler's waits cover.
+// The main loops issue the instructions from inline assembly with the
+// accumulators bound to AGPRs: the compiler's own selection of this
+// instruction moves the accumulators between registers around every loop
+// trip.  The compiler cannot see hazards inside such statements, so the code
+// provides the wait states itself: after the zeroing of the accumulators
+// (acc_fence), before an MFMA that reads a just-converted codes operand
+// (mfma16_valu_a; only the first of a step: the other conversions are
+// themselves inline assembly placed two MFMAs ahead of their consumer), and
+// after the loop (mfma_drain).  All other operands come from loads, which the
+// compiler's waits cover.  The input gradient's epilogue products (the A-map
+// and the map gradient) use the compiler's builtin, whose hazards it handles.
 #include "lcvq_prep.hpp"
 
 namespace lcvq {

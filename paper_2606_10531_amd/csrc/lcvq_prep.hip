@@ -1,7 +1,11 @@
 // Streaming (HBM-bound) kernels of the LC-VQ layer:
 //   * quantise latents into the matrix-core operand layout (+ 2-bit packing)
 //   * the activation transform X' = X blockdiag(A), s = X b~   (def. forward_x)
-//   * per-token sums of dY
+//   * the training pair's saved state, written by the forward prepass from the
+//     same reads (codes in the input-gradient layout, X' transposed for the
+//     weight gradient, both straight-through masks)
+//   * the backward operands: dY transposed for the weight gradient, per-token
+//     sums of dY
 //   * stand-alone 2-bit packing and dense decode
 #include "lcvq_prep.hpp"
 
