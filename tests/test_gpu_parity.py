@@ -120,6 +120,31 @@ def test_dequant(lc, d, src, out, m, groups):
         assert np.allclose(got, want, rtol=2 ** -8, atol=1e-6)
 
 
+@pytest.mark.parametrize("d", [8, 4])
+@pytest.mark.parametrize("src", ["packed", "u8"])
+def test_dequant_many_chunks_sampled(lc, d, src):
+    """6144 x 8192 codes: every wave of the decode takes several trips of its
+    chunk loop (the next pair of chunks loaded while the current pair is
+    decoded and stored) and the grid ends in a partial stride; sampled rows
+    against the oracle."""
+    import torch
+    m, n = 6144, 8192
+    A, b = synth.draw_map(d, 2)
+    A = (A * 50).astype(np.float32)
+    codes = synth.rng(77 + d).integers(0, 4, size=(m, n), dtype=np.uint8)
+    At, bt = torch.from_numpy(A).cuda(), torch.from_numpy(b).cuda()
+    if src == "packed":
+        W = lc.dequant(torch.from_numpy(orc.pack2bit(codes)).cuda(), At, bt, d, n=n, src_kind=lc.SRC_PACKED2,
+                       out_dtype=torch.bfloat16)
+    else:
+        W = lc.dequant(torch.from_numpy(codes).cuda(), At, bt, d, out_dtype=torch.bfloat16)
+    torch.cuda.synchronize()
+    rows = np.unique(np.concatenate([[0, 1, m // 2, m - 1], synth.rng(78).integers(0, m, 60)]))
+    want = orc.decode(codes[rows], A.astype(np.float64), b.astype(np.float64), d)
+    got = to_host(W[torch.from_numpy(rows).cuda()])
+    assert np.allclose(got, want, rtol=2 ** -8, atol=1e-6)
+
+
 # ---------------------------------------------------------- linear layer ----
 
 def _run_layer(lc, N, m, n, d, dtype, mask_mode=0, z_lo=-0.5, z_hi=3.5, k=0, dz_dtype=None):
