@@ -58,6 +58,32 @@ __device__ __forceinline__ void storeD(T *p, const float v[D]) {
   store4(p, v);
   if constexpr (D == 8) store4(p + 4, v + 4);
 }
+// The same with the non-temporal cache policy, for the dense decode outputs:
+// a stream written once, far larger than the caches and not read back by the
+// kernel (28672 x 8192 -> bf16: packed source 105 -> 89 us, bf16 latents 160 ->
+// 154 us).  p is aligned to the group (D elements).
+template <int D>
+__device__ __forceinline__ void storeD_nt(uint16_t *p, const float v[D]) {
+  if constexpr (D == 8) {
+    u32x4 w;
+#pragma unroll
+    for (int e = 0; e < 4; ++e) w[e] = pack_bf16x2(v[2 * e], v[2 * e + 1]);
+    __builtin_nontemporal_store(w, reinterpret_cast<u32x4 *>(p));
+  } else {
+    u32x2 w;
+    w[0] = pack_bf16x2(v[0], v[1]);
+    w[1] = pack_bf16x2(v[2], v[3]);
+    __builtin_nontemporal_store(w, reinterpret_cast<u32x2 *>(p));
+  }
+}
+template <int D>
+__device__ __forceinline__ void storeD_nt(float *p, const float v[D]) {
+#pragma unroll
+  for (int h = 0; h < D / 4; ++h) {
+    const floatx4 a = {v[4 * h], v[4 * h + 1], v[4 * h + 2], v[4 * h + 3]};
+    __builtin_nontemporal_store(a, reinterpret_cast<floatx4 *>(p + 4 * h));
+  }
+}
 
 __device__ __forceinline__ float block_sum256(float v, float *red /* >= 4 floats of LDS */) {
 #pragma unroll
@@ -550,7 +576,7 @@ __global__ __launch_bounds__(256) void k_dequant(const ZT *__restrict__ src, int
       for (int k = 0; k < D; ++k) v = fmaf(a[j][k], c[k], v);
       y[j] = v;
     }
-    storeD<D>(W + q * D, y);
+    storeD_nt<D>(W + q * D, y);
   }
 }
 
@@ -632,7 +658,7 @@ __global__ __launch_bounds__(256) void k_decode_codes(const uint8_t *__restrict_
         y[j] = v;
       }
     }
-    storeD<D>(dst, y);
+    storeD_nt<D>(dst, y);
   };
   auto decode = [&](const uint8_t *st, int64_t ch) {
 #pragma unroll
@@ -642,7 +668,7 @@ __global__ __launch_bounds__(256) void k_decode_codes(const uint8_t *__restrict_
       if constexpr (kTable && kBytes == 1) {  // d = 4: one byte, b folded into the table row
         const floatx4 y4 = *reinterpret_cast<const floatx4 *>(tab[0][st[gl]]);
         const float y[4] = {y4[0], y4[1], y4[2], y4[3]};
-        storeD<D>(W + (ch * kGroups + gl) * D, y);
+        storeD_nt<D>(W + (ch * kGroups + gl) * D, y);
         continue;
       } else if constexpr (kBytes == 1) {
         const uint32_t v = st[gl];
@@ -654,7 +680,7 @@ __global__ __launch_bounds__(256) void k_decode_codes(const uint8_t *__restrict_
         const floatx4 *hi = reinterpret_cast<const floatx4 *>(tab[1][v >> 8]);
         const floatx4 y0 = lo[0] + hi[0], y1 = lo[1] + hi[1];
         const float y[8] = {y0[0], y0[1], y0[2], y0[3], y1[0], y1[1], y1[2], y1[3]};
-        storeD<D>(W + (ch * kGroups + gl) * D, y);
+        storeD_nt<D>(W + (ch * kGroups + gl) * D, y);
         continue;
       } else if constexpr (kBytes == 2) {
         const uint32_t v = *reinterpret_cast<const uint16_t *>(st + 2 * gl);
@@ -714,7 +740,7 @@ __global__ __launch_bounds__(256) void k_decode_codes(const uint8_t *__restrict_
 #pragma unroll
         for (int j = 0; j < D; ++j) y[j] = lo[0][j];
       }
-      storeD<D>(W + g * D, y);
+      storeD_nt<D>(W + g * D, y);
       continue;
     }
     float c[D];
