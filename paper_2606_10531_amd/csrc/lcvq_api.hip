@@ -51,7 +51,7 @@ struct FwdLayout {
   int64_t Np, ldp;
 };
 struct BwdLayout {
-  size_t rs, frag, xt, dyt, mask, total;
+  size_t rs, frag, xt, dyt, mask, map, total;
 };
 
 FwdLayout fwd_layout(int64_t N, int64_t m, int64_t n, bool bf16) {
@@ -94,9 +94,11 @@ BwdLayout bwd_layout(int64_t N, int64_t m, int64_t n, bool bf16) {
     L.dyt = L.xt + up256((size_t)lcvq::round_up(n, 256) * Nt * 2);
     // straight-through mask of Z, one bit per element (rows of whole 64-bit words)
     L.mask = L.dyt + up256((size_t)lcvq::round_up(m, 256) * Nt * 2);
-    L.total = L.mask + up256((size_t)lcvq::mask_bytes(m, n));
+    // the map gradients' partial sums, one row per group of product blocks
+    L.map = L.mask + up256((size_t)lcvq::mask_bytes(m, n));
+    L.total = L.map + (size_t)lcvq::kMapCopies * lcvq::kMapStride * 4;
   } else {
-    L.frag = L.xt = L.dyt = L.mask = L.total = up256((size_t)N * 4);
+    L.frag = L.xt = L.dyt = L.mask = L.map = L.total = up256((size_t)N * 4);
   }
   return L;
 }
@@ -657,11 +659,13 @@ static lcvq_status_t linear_bwd(int64_t N, int64_t m, int64_t n, int32_t d, int3
     // 1. one prepass launch: codes in the input-gradient operand layout (when
     //    dX or dA/db are wanted), X' = X blockdiag(A) and dY in the
     //    weight-gradient fragments (when dZ is wanted), and the partial row sums
-    //    of dY; its first block clears dA/db when overwriting them
-    // 2. dZ = mask * dY^T X'    3. dX = (dY codes) A-map + rowsum(dY) b (+ dA, db)
+    //    of dY; its first block clears the map gradients' partial sums
+    // 2. dZ = mask * dY^T X'    3. dX = (dY codes) A-map + rowsum(dY) b (+ the
+    //    partial sums of dA, db, then their sum into dA, db)
     //    (the two products are independent; in this order the step measured
     //    slightly shorter)
     const bool run_dx = dX != nullptr || want_map;
+    float *mapp = want_map ? (float *)(ws + L.map) : nullptr;
     uint32_t *frag = (uint32_t *)(ws + L.frag);
     uint16_t *xt = (uint16_t *)(ws + L.xt), *dyt = (uint16_t *)(ws + L.dyt);
     // the straight-through mask as a bitmap (the differentiable estimator reads Z itself)
@@ -687,8 +691,8 @@ static lcvq_status_t linear_bwd(int64_t N, int64_t m, int64_t n, int32_t d, int3
                                              (const uint16_t *)X, (const uint16_t *)dY, A, d, N,
                                              dZ != nullptr && !use_saved ? xt : nullptr,
                                              dZ != nullptr ? dyt : nullptr, rs, use_saved ? nullptr : maskbits, mask_mode,
-                                             clear_map ? dA : nullptr, clear_map ? d * d : 0,
-                                             clear_map ? db : nullptr, clear_map ? d : 0, st));
+                                             mapp, mapp != nullptr ? lcvq::kMapCopies * lcvq::kMapStride : 0,
+                                             nullptr, 0, st));
       if (e != hipSuccess) return hip_fail(e, "backward prepass launch");
     }
     if (dZ != nullptr) {
@@ -699,8 +703,10 @@ static lcvq_status_t linear_bwd(int64_t N, int64_t m, int64_t n, int32_t d, int3
     }
     if (run_dx) {
       Timed tm(LCVQ_K_DX, st);
-      e = tm.done(lcvq::launch_dx_bf16(frag, (const uint16_t *)dY, rs, A, b, d, (uint16_t *)dX, (const uint16_t *)X, dA, db, N, m,
-                                       n, st));
+      e = lcvq::launch_dx_bf16(frag, (const uint16_t *)dY, rs, A, b, d, (uint16_t *)dX, (const uint16_t *)X, mapp, N, m,
+                               n, st);
+      if (e == hipSuccess && want_map) e = lcvq::launch_map_combine(mapp, d, accumulate, dA, db, st);
+      e = tm.done(e);
       if (e != hipSuccess) return hip_fail(e, "input-gradient launch");
     }
     return ok();

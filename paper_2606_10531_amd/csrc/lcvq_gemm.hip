@@ -147,15 +147,16 @@ __device__ __forceinline__ uint32_t as_u(float f) { return __float_as_uint(f); }
 // P = dY codes: dA[j, k] = sum_{t,g} X[t, g*D + j] P[t, g*D + k] and
 // db[j] = sum_{t,g} X[t, g*D + j] rs[t] (the chain rule through X' = X blockdiag(A)
 // and s = X b~): dA on the matrix cores, db on the vector units, reduced
-// lanes -> wave -> block and added with one atomic per block per entry.  X is
-// N x Mvalid row-major; dA == nullptr skips this.
+// lanes -> wave -> block and added with one atomic per block per entry into
+// the block's row of the partial sums mapp.  X is N x Mvalid row-major;
+// mapp == nullptr skips this.
 template <int kMode, int D>  // kMode 0: forward (B = X' fragments), 1: input gradient (B = dY, row length ldB)
 __global__ __launch_bounds__(256, 1) void k_gemm_codes(
     const uint32_t *__restrict__ frag, int KB, const uint16_t *__restrict__ Bsrc, int64_t ldB,
     int tiles_m, int tiles_n, const float *__restrict__ vecT, int vparts,
     int64_t vstride, const float *__restrict__ A, const float *__restrict__ bvec, uint16_t *__restrict__ out,
     int64_t ldo, int64_t Mvalid, int64_t Tvalid, const uint16_t *__restrict__ X,
-    float *__restrict__ dA, float *__restrict__ db) {
+    float *__restrict__ mapp) {
   const int tid = threadIdx.x, lane = tid & 63, q = lane >> 4, c16 = lane & 15;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   // The wave's 256 weight-side rows (256-row tile tm) and 64 tokens from tw.
@@ -209,7 +210,7 @@ __global__ __launch_bounds__(256, 1) void k_gemm_codes(
   // in LDS instead of waiting on HBM latency once per pair.
   constexpr int kXPairs = 32;
   __shared__ __attribute__((aligned(1024))) char xs[kMode == 1 ? 4 * kXPairs * 1024 : 16];
-  const bool want_map = kMode == 1 && dA != nullptr;
+  const bool want_map = kMode == 1 && mapp != nullptr;
   const __amdgpu_buffer_rsrc_t rx = make_rsrc(X + tw * Mvalid, want_map ? (Tvalid - tw) * Mvalid * 2 : 0);
   if (want_map && (tw + 64 > Tvalid || (int64_t)tm * kTile + kTile > Mvalid)) {
     // a tile reaching past the tensor: the pairs start as zeros, so rows and
@@ -493,8 +494,7 @@ __global__ __launch_bounds__(256, 1) void k_gemm_codes(
             v += red[w][kSlots * D * D + tid - D * D];
           }
         }
-        if (tid < D * D) unsafeAtomicAdd(dA + tid, v);
-        else unsafeAtomicAdd(db + (tid - D * D), v);
+        unsafeAtomicAdd(mapp + (blockIdx.x % kMapCopies) * kMapStride + tid, v);
       }
     }
   }
@@ -773,12 +773,12 @@ hipError_t launch_fwd_bf16(const uint32_t *frag, const uint16_t *Xp, int64_t ldp
   const int KB = (int)(ldp / kKStep);  // even: ldp is a multiple of 128
   const int64_t Np = round_up(N, kTile);  // row stride of the partial sums of s
   k_gemm_codes<0, 8><<<tiles_m * tiles_n, 256, 0, st>>>(frag, KB, Xp, 0, tiles_m, tiles_n, s,
-                                                        act_chunks(ldp), Np, nullptr, nullptr, Y, m, m, N, nullptr, nullptr, nullptr);
+                                                        act_chunks(ldp), Np, nullptr, nullptr, Y, m, m, N, nullptr, nullptr);
   return hipGetLastError();
 }
 
 hipError_t launch_dx_bf16(const uint32_t *frag, const uint16_t *dY, const float *rsp, const float *A, const float *b,
-                          int d, uint16_t *dX, const uint16_t *X, float *dA, float *db, int64_t N, int64_t m, int64_t n,
+                          int d, uint16_t *dX, const uint16_t *X, float *mapp, int64_t N, int64_t m, int64_t n,
                           hipStream_t st) {
   const int parts = rowsum_parts(m);
   const int64_t Nt = bwd_tokens(N);  // row stride of the partial row sums
@@ -787,10 +787,27 @@ hipError_t launch_dx_bf16(const uint32_t *frag, const uint16_t *dY, const float 
   // dX == nullptr: the product still runs for dA/db; its stores are dropped.
   if (d == 8)
     k_gemm_codes<1, 8><<<tiles_m * tiles_n, 256, 0, st>>>(frag, KB, dY, m, tiles_m, tiles_n, rsp,
-                                                          parts, Nt, A, b, dX, n, n, N, X, dA, db);
+                                                          parts, Nt, A, b, dX, n, n, N, X, mapp);
   else
     k_gemm_codes<1, 4><<<tiles_m * tiles_n, 256, 0, st>>>(frag, KB, dY, m, tiles_m, tiles_n, rsp,
-                                                          parts, Nt, A, b, dX, n, n, N, X, dA, db);
+                                                          parts, Nt, A, b, dX, n, n, N, X, mapp);
+  return hipGetLastError();
+}
+
+// dA, db = the sum of the kMapCopies rows of partial sums (+ dA, db when accumulating).
+__global__ void k_map_combine(const float *__restrict__ mapp, int D, int accumulate, float *__restrict__ dA,
+                              float *__restrict__ db) {
+  const int i = threadIdx.x;
+  if (i >= D * D + D) return;
+  float v = 0.0f;
+#pragma unroll 8
+  for (int s = 0; s < kMapCopies; ++s) v += mapp[s * kMapStride + i];
+  float *o = i < D * D ? dA + i : db + (i - D * D);
+  *o = accumulate ? *o + v : v;
+}
+
+hipError_t launch_map_combine(const float *mapp, int d, int accumulate, float *dA, float *db, hipStream_t st) {
+  k_map_combine<<<1, 128, 0, st>>>(mapp, d, accumulate, dA, db);
   return hipGetLastError();
 }
 

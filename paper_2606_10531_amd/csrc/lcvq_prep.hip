@@ -871,8 +871,8 @@ __device__ __forceinline__ void dy_part(int bt, int sf0, int sf1, const uint16_t
 // blocks and go first.  Then nq quantise blocks into the input-gradient operand
 // layout (four tiles each, block (q % gq, q / gq), K = rows of Z), then
 // KBt * nfx4 X' blocks of 64 tokens x 256 in-features (block (x % KBt, x / KBt)).
-// Block 0 clears dA (nza floats) and db (nzb) when the backward overwrites them
-// (the input-gradient kernel, launched after this one, accumulates into them).
+// Block 0 clears za (nza floats) and zb (nzb): the map gradients' partial sums,
+// which the input-gradient kernel launched after this one accumulates into.
 template <int D>
 __global__ __launch_bounds__(256) void k_bwd_prep(const uint16_t *__restrict__ Z, int64_t m, int64_t n, Quantizer qz,
                                                    uint32_t *__restrict__ frag, int KBq, int gq, int nq,
