@@ -169,8 +169,8 @@ lcvq_status_t lcvq_encode(int64_t m, int64_t n, int32_t d, const void *W, int32_
  * or lcvq_linear_fwd_packed (op = LCVQ_OP_FWD_PACKED, dtype LCVQ_BF16; the
  * size does not depend on N) for these sizes and element type.  Returns 0 for invalid arguments.  The workspace holds
  * transient, library-private data (transformed activations, codes in the
- * matrix-core operand layout, per-token sums); its contents are undefined
- * between calls.
+ * matrix-core operand layout, per-token sums, partial sums of dA and db); its
+ * contents are undefined between calls.
  */
 size_t lcvq_workspace_bytes(int32_t op, int64_t N, int64_t m, int64_t n, int32_t d, int32_t dtype);
 
@@ -416,7 +416,8 @@ typedef enum {
   LCVQ_K_PACKED_PREP = 9,  /* lcvq_linear_fwd_packed: X' and s of up to 16 tokens */
   LCVQ_K_PACKED = 10,      /* lcvq_linear_fwd_packed: Y from the packed codes */
   LCVQ_K_ENCODE = 11,      /* lcvq_encode */
-  LCVQ_K_COUNT = 12
+  LCVQ_K_MAP_SUM = 12,     /* bf16 backward: dA, db from the input-gradient product's partial sums */
+  LCVQ_K_COUNT = 13
 } lcvq_kernel_t;
 lcvq_status_t lcvq_timer_enable(uint32_t mask);
 lcvq_status_t lcvq_timer_read(int32_t kernel, double *total_ms, int64_t *launches);

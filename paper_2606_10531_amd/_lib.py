@@ -19,7 +19,7 @@ OP_FWD, OP_BWD, OP_FWD_PACKED = 0, 1, 2
 EST_STE, EST_DGE = 0, 1
 # lcvq_kernel_t
 KERNELS = ["fwd_prep", "fwd", "bwd_prep", "dx", "dw", "pack", "dequant", "fill", "adam", "packed_prep",
-           "packed", "encode"]
+           "packed", "encode", "map_sum"]
 
 _P = ctypes.c_void_p
 _I64 = ctypes.c_int64

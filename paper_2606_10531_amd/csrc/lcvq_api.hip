@@ -703,11 +703,14 @@ static lcvq_status_t linear_bwd(int64_t N, int64_t m, int64_t n, int32_t d, int3
     }
     if (run_dx) {
       Timed tm(LCVQ_K_DX, st);
-      e = lcvq::launch_dx_bf16(frag, (const uint16_t *)dY, rs, A, b, d, (uint16_t *)dX, (const uint16_t *)X, mapp, N, m,
-                               n, st);
-      if (e == hipSuccess && want_map) e = lcvq::launch_map_combine(mapp, d, accumulate, dA, db, st);
-      e = tm.done(e);
+      e = tm.done(lcvq::launch_dx_bf16(frag, (const uint16_t *)dY, rs, A, b, d, (uint16_t *)dX, (const uint16_t *)X,
+                                       mapp, N, m, n, st));
       if (e != hipSuccess) return hip_fail(e, "input-gradient launch");
+    }
+    if (want_map) {
+      Timed tm(LCVQ_K_MAP_SUM, st);
+      e = tm.done(lcvq::launch_map_combine(mapp, d, accumulate, dA, db, st));
+      if (e != hipSuccess) return hip_fail(e, "map-gradient sum launch");
     }
     return ok();
   }

@@ -799,11 +799,15 @@ __global__ void k_map_combine(const float *__restrict__ mapp, int D, int accumul
                               float *__restrict__ db) {
   const int i = threadIdx.x;
   if (i >= D * D + D) return;
-  float v = 0.0f;
-#pragma unroll 8
-  for (int s = 0; s < kMapCopies; ++s) v += mapp[s * kMapStride + i];
   float *o = i < D * D ? dA + i : db + (i - D * D);
-  *o = accumulate ? *o + v : v;
+  // every load issued before the first add: one memory round trip
+  float r[kMapCopies];
+#pragma unroll
+  for (int s = 0; s < kMapCopies; ++s) r[s] = mapp[s * kMapStride + i];
+  float v = accumulate ? *o : 0.0f;
+#pragma unroll
+  for (int s = 0; s < kMapCopies; ++s) v += r[s];
+  *o = v;
 }
 
 hipError_t launch_map_combine(const float *mapp, int d, int accumulate, float *dA, float *db, hipStream_t st) {
