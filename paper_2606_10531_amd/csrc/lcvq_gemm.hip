@@ -600,12 +600,14 @@ __global__ __launch_bounds__(256, 1) void k_gemm_dw(const uint16_t *__restrict__
   //   second half-step's MFMAs, the reads of step k + 1's first B between them;
   //     A loads of k + 2, kk2 1.
   // The explicit waits count loads in this issue order, which the scheduling
-  // fences keep.  The wait before a step's barrier lets the loads issued after
+  // fences keep inside the branch-free loop; the compiler may still sink the
+  // prologue's A loads (used only in the loop) past the prologue's barrier, so
+  // that wait does not rely on them.  The wait before a step's barrier lets the loads issued after
   // B of k + 1 stay in flight: A of k, kk2 1 and of k + 1, kk2 0, B of k + 2,
   // A of k + 1, kk2 1 and of k + 2, kk2 0 (24), less the four of A of k, kk2 1,
   // which the second half-step needs anyway; the same count covers steps 0 and
   // 1 after the prologue.  The prologue's wait (16) holds B of step 0 complete
-  // wherever the compiler places the prologue's A loads.
+  // wherever the A loads end up.
   // The loop runs from the barrier of one step to the wait of the next (the
   // last step's second half-step is peeled).  Its head thus comes before the
   // MFMAs that read A loaded a step earlier: at a loop head the compiler's own
