@@ -416,7 +416,7 @@ typedef enum {
   LCVQ_K_PACKED_PREP = 9,  /* lcvq_linear_fwd_packed: X' and s of up to 16 tokens */
   LCVQ_K_PACKED = 10,      /* lcvq_linear_fwd_packed: Y from the packed codes */
   LCVQ_K_ENCODE = 11,      /* lcvq_encode */
-  LCVQ_K_MAP_SUM = 12,     /* bf16 backward: dA, db from the input-gradient product's partial sums */
+  LCVQ_K_MAP_SUM = 12,     /* bf16 backward: dA, db, summed over the input-gradient product's blocks */
   LCVQ_K_COUNT = 13
 } lcvq_kernel_t;
 lcvq_status_t lcvq_timer_enable(uint32_t mask);

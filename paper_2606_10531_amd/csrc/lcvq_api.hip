@@ -94,9 +94,9 @@ BwdLayout bwd_layout(int64_t N, int64_t m, int64_t n, bool bf16) {
     L.dyt = L.xt + up256((size_t)lcvq::round_up(n, 256) * Nt * 2);
     // straight-through mask of Z, one bit per element (rows of whole 64-bit words)
     L.mask = L.dyt + up256((size_t)lcvq::round_up(m, 256) * Nt * 2);
-    // the map gradients' partial sums, one row per group of product blocks
+    // the map gradients' per-block partial sums (d d + d <= 72 entries)
     L.map = L.mask + up256((size_t)lcvq::mask_bytes(m, n));
-    L.total = L.map + (size_t)lcvq::kMapCopies * lcvq::kMapStride * 4;
+    L.total = L.map + up256((size_t)lcvq::map_rows(N, n) * 72 * 4);
   } else {
     L.frag = L.xt = L.dyt = L.mask = L.map = L.total = up256((size_t)N * 4);
   }
@@ -659,9 +659,9 @@ static lcvq_status_t linear_bwd(int64_t N, int64_t m, int64_t n, int32_t d, int3
     // 1. one prepass launch: codes in the input-gradient operand layout (when
     //    dX or dA/db are wanted), X' = X blockdiag(A) and dY in the
     //    weight-gradient fragments (when dZ is wanted), and the partial row sums
-    //    of dY; its first block clears the map gradients' partial sums
+    //    of dY
     // 2. dZ = mask * dY^T X'    3. dX = (dY codes) A-map + rowsum(dY) b (+ the
-    //    partial sums of dA, db, then their sum into dA, db)
+    //    per-block partial sums of dA, db)    4. their sum into dA, db
     //    (the two products are independent; in this order the step measured
     //    slightly shorter)
     const bool run_dx = dX != nullptr || want_map;
@@ -691,8 +691,7 @@ static lcvq_status_t linear_bwd(int64_t N, int64_t m, int64_t n, int32_t d, int3
                                              (const uint16_t *)X, (const uint16_t *)dY, A, d, N,
                                              dZ != nullptr && !use_saved ? xt : nullptr,
                                              dZ != nullptr ? dyt : nullptr, rs, use_saved ? nullptr : maskbits, mask_mode,
-                                             mapp, mapp != nullptr ? lcvq::kMapCopies * lcvq::kMapStride : 0,
-                                             nullptr, 0, st));
+                                             st));
       if (e != hipSuccess) return hip_fail(e, "backward prepass launch");
     }
     if (dZ != nullptr) {
@@ -709,7 +708,7 @@ static lcvq_status_t linear_bwd(int64_t N, int64_t m, int64_t n, int32_t d, int3
     }
     if (want_map) {
       Timed tm(LCVQ_K_MAP_SUM, st);
-      e = tm.done(lcvq::launch_map_combine(mapp, d, accumulate, dA, db, st));
+      e = tm.done(lcvq::launch_map_combine(mapp, lcvq::map_rows(N, n), d, accumulate, dA, db, st));
       if (e != hipSuccess) return hip_fail(e, "map-gradient sum launch");
     }
     return ok();

@@ -147,9 +147,10 @@ __device__ __forceinline__ uint32_t as_u(float f) { return __float_as_uint(f); }
 // P = dY codes: dA[j, k] = sum_{t,g} X[t, g*D + j] P[t, g*D + k] and
 // db[j] = sum_{t,g} X[t, g*D + j] rs[t] (the chain rule through X' = X blockdiag(A)
 // and s = X b~): dA on the matrix cores, db on the vector units, reduced
-// lanes -> wave -> block and added with one atomic per block per entry into
-// the block's row of the partial sums mapp.  X is N x Mvalid row-major;
-// mapp == nullptr skips this.
+// lanes -> wave -> block; entry e of block b is stored (no atomics) at
+// mapp[e * gridDim.x + b], and a later launch sums each entry over the blocks
+// in a fixed order, so dA and db come out the same bit for bit on every call.
+// X is N x Mvalid row-major; mapp == nullptr skips this.
 template <int kMode, int D>  // kMode 0: forward (B = X' fragments), 1: input gradient (B = dY, row length ldB)
 __global__ __launch_bounds__(256, 1) void k_gemm_codes(
     const uint32_t *__restrict__ frag, int KB, const uint16_t *__restrict__ Bsrc, int64_t ldB,
@@ -465,8 +466,8 @@ __global__ __launch_bounds__(256, 1) void k_gemm_codes(
     }
     if (want_map) {
       // lane L holds rows 4 (L / 16) + 0..3 of column L % 16; slot blocks on the
-      // diagonal go to LDS per wave and slot, db by shuffles; then one atomic
-      // per entry and block
+      // diagonal go to LDS per wave and slot, db by shuffles; then the block's
+      // sum of each entry, in a fixed order, to its place in mapp
       constexpr int kSlots = 16 / D;
       __shared__ float red[4][kSlots * D * D + D];
 #pragma unroll
@@ -494,7 +495,7 @@ __global__ __launch_bounds__(256, 1) void k_gemm_codes(
             v += red[w][kSlots * D * D + tid - D * D];
           }
         }
-        unsafeAtomicAdd(mapp + (blockIdx.x % kMapCopies) * kMapStride + tid, v);
+        mapp[(int64_t)tid * gridDim.x + blockIdx.x] = v;
       }
     }
   }
@@ -796,24 +797,33 @@ hipError_t launch_dx_bf16(const uint32_t *frag, const uint16_t *dY, const float 
   return hipGetLastError();
 }
 
-// dA, db = the sum of the kMapCopies rows of partial sums (+ dA, db when accumulating).
-__global__ void k_map_combine(const float *__restrict__ mapp, int D, int accumulate, float *__restrict__ dA,
-                              float *__restrict__ db) {
-  const int i = threadIdx.x;
-  if (i >= D * D + D) return;
-  float *o = i < D * D ? dA + i : db + (i - D * D);
-  // every load issued before the first add: one memory round trip
-  float r[kMapCopies];
+int map_rows(int64_t N, int64_t n) { return (int)(ceil_div(n, kTile) * ceil_div(N, kTile)); }
+
+// Entry blockIdx.x of dA (< D D) or db: the sum of its `rows` per-block
+// partial sums in a fixed order (thread i: rows i, i + 256, ...; then a
+// butterfly over each wave and the four wave totals in order), plus the old
+// value when accumulating.
+__global__ __launch_bounds__(256) void k_map_combine(const float *__restrict__ mapp, int rows, int D, int accumulate,
+                                                     float *__restrict__ dA, float *__restrict__ db) {
+  __shared__ float part[4];
+  const int e = blockIdx.x, tid = threadIdx.x;
+  const float *src = mapp + (int64_t)e * rows;
+  float v = 0.0f;
+  for (int r = tid; r < rows; r += 256) v += src[r];
 #pragma unroll
-  for (int s = 0; s < kMapCopies; ++s) r[s] = mapp[s * kMapStride + i];
-  float v = accumulate ? *o : 0.0f;
-#pragma unroll
-  for (int s = 0; s < kMapCopies; ++s) v += r[s];
-  *o = v;
+  for (int o = 32; o >= 1; o >>= 1) v += __shfl_xor(v, o, 64);
+  if ((tid & 63) == 0) part[tid >> 6] = v;
+  __syncthreads();
+  if (tid == 0) {
+    float *o = e < D * D ? dA + e : db + (e - D * D);
+    const float t = (part[0] + part[1]) + (part[2] + part[3]);
+    *o = (accumulate ? *o : 0.0f) + t;
+  }
 }
 
-hipError_t launch_map_combine(const float *mapp, int d, int accumulate, float *dA, float *db, hipStream_t st) {
-  k_map_combine<<<1, 128, 0, st>>>(mapp, d, accumulate, dA, db);
+hipError_t launch_map_combine(const float *mapp, int rows, int d, int accumulate, float *dA, float *db,
+                              hipStream_t st) {
+  k_map_combine<<<d * d + d, 256, 0, st>>>(mapp, rows, d, accumulate, dA, db);
   return hipGetLastError();
 }
 

@@ -871,8 +871,6 @@ __device__ __forceinline__ void dy_part(int bt, int sf0, int sf1, const uint16_t
 // blocks and go first.  Then nq quantise blocks into the input-gradient operand
 // layout (four tiles each, block (q % gq, q / gq), K = rows of Z), then
 // KBt * nfx4 X' blocks of 64 tokens x 256 in-features (block (x % KBt, x / KBt)).
-// Block 0 clears za (nza floats) and zb (nzb): the map gradients' partial sums,
-// which the input-gradient kernel launched after this one accumulates into.
 template <int D>
 __global__ __launch_bounds__(256) void k_bwd_prep(const uint16_t *__restrict__ Z, int64_t m, int64_t n, Quantizer qz,
                                                    uint32_t *__restrict__ frag, int KBq, int gq, int nq,
@@ -881,8 +879,7 @@ __global__ __launch_bounds__(256) void k_bwd_prep(const uint16_t *__restrict__ Z
                                                    int nfy, int spf, int nrp,
                                                    uint16_t *__restrict__ xt, uint16_t *__restrict__ dyt,
                                                    float *__restrict__ rsp, uint64_t *__restrict__ maskbits,
-                                                   int64_t nbc, int mask_mode,
-                                                   float *__restrict__ za, int nza, float *__restrict__ zb, int nzb) {
+                                                   int64_t nbc, int mask_mode) {
   // one LDS array: four code tiles (quantise blocks) or two 64 x 64 bf16
   // tiles (dY parts, X' blocks)
   __shared__ __attribute__((aligned(16))) uint8_t lds[4 * sizeof(CodeTile)];
@@ -890,10 +887,6 @@ __global__ __launch_bounds__(256) void k_bwd_prep(const uint16_t *__restrict__ Z
   CodeTile *codes = reinterpret_cast<CodeTile *>(lds);
   uint16_t (*tile)[64][64 + 8] = reinterpret_cast<uint16_t (*)[64][64 + 8]>(lds);
   const int id = blockIdx.x, tid = threadIdx.x;
-  if (id == 0) {
-    for (int i = tid; i < nza; i += 256) za[i] = 0.0f;
-    for (int i = tid; i < nzb; i += 256) zb[i] = 0.0f;
-  }
   const int ndy = KBt * nrp;
   float rsum[2] = {0.0f, 0.0f};
   if (id < ndy) {
@@ -1054,8 +1047,7 @@ namespace lcvq {
 hipError_t launch_bwd_prep_bf16(const uint16_t *Z, int64_t m, int64_t n, const Quantizer &qz, uint32_t *frag,
                                 const uint16_t *X,
                                 const uint16_t *dY, const float *A, int d, int64_t N, uint16_t *xt,
-                                uint16_t *dyt, float *rsp, uint64_t *maskbits, int mask_mode, float *za, int nza,
-                                float *zb, int nzb, hipStream_t st) {
+                                uint16_t *dyt, float *rsp, uint64_t *maskbits, int mask_mode, hipStream_t st) {
   const int64_t nbc = mask_col_blocks(n);
   // codes: M = columns of Z padded to 256 (four 64-column tiles per block), K = rows
   // padded to 128 (skipped when frag == nullptr)
@@ -1069,10 +1061,10 @@ hipError_t launch_bwd_prep_bf16(const uint16_t *Z, int64_t m, int64_t n, const Q
   const unsigned grid = (unsigned)(nq + KBt * (nfx4 + nrp));
   if (d == 8)
     k_bwd_prep<8><<<grid, 256, 0, st>>>(Z, m, n, qz, frag, KBq, gq, nq, X, dY, A, N, KBt, nfx4, nfy, spf, nrp,
-                                        xt, dyt, rsp, maskbits, nbc, mask_mode, za, nza, zb, nzb);
+                                        xt, dyt, rsp, maskbits, nbc, mask_mode);
   else
     k_bwd_prep<4><<<grid, 256, 0, st>>>(Z, m, n, qz, frag, KBq, gq, nq, X, dY, A, N, KBt, nfx4, nfy, spf, nrp,
-                                        xt, dyt, rsp, maskbits, nbc, mask_mode, za, nza, zb, nzb);
+                                        xt, dyt, rsp, maskbits, nbc, mask_mode);
   return hipGetLastError();
 }
 }  // namespace lcvq

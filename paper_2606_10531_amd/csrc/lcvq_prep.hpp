@@ -70,8 +70,7 @@ inline int64_t mask_bytes(int64_t m, int64_t n) { return (m + 63) / 64 * mask_co
 hipError_t launch_bwd_prep_bf16(const uint16_t *Z, int64_t m, int64_t n, const Quantizer &qz, uint32_t *frag,
                                 const uint16_t *X,
                                 const uint16_t *dY, const float *A, int d, int64_t N, uint16_t *xt,
-                                uint16_t *dyt, float *rsp, uint64_t *maskbits, int mask_mode, float *za, int nza,
-                                float *zb, int nzb, hipStream_t st);
+                                uint16_t *dyt, float *rsp, uint64_t *maskbits, int mask_mode, hipStream_t st);
 hipError_t launch_act_transform(const void *X, bool bf16, int64_t N, int64_t Np, int64_t n, int d,
                                 const float *A, const float *b, void *Xp, int64_t ldp, float *s,
                                 hipStream_t st);
@@ -122,18 +121,17 @@ hipError_t launch_adamw(float *theta, const void *grad, bool grad_bf16, float *m
 // bf16 matrix-core products (lcvq_gemm.hip)
 hipError_t launch_fwd_bf16(const uint32_t *frag, const uint16_t *Xp, int64_t ldp, const float *s,
                            uint16_t *Y, int64_t N, int64_t m, int64_t n, hipStream_t st);
-// Map gradients of the input-gradient product: each block adds its dA (d x d)
-// and db (d) partial sums, as one row of d * d + d floats, into row
-// block % kMapCopies of mapp (kMapCopies rows, kMapStride floats apart,
-// cleared by the backward prepass); launch_map_combine then sums the rows
-// into dA and db (added to them when accumulating).  Spreading the atomics
-// over the rows keeps them from queueing on one address.
-constexpr int kMapCopies = 32;
-constexpr int kMapStride = 128;
+// Map gradients of the input-gradient product: each of its map_rows(N, n)
+// blocks stores its partial sums of dA (d x d) and db (d), entry-major (entry
+// e of block b at mapp[e * map_rows + b]; every place is written, so mapp
+// needs no clearing); launch_map_combine then sums each entry over the blocks
+// in a fixed order into dA and db (added to them when accumulating).
+int map_rows(int64_t N, int64_t n);
 hipError_t launch_dx_bf16(const uint32_t *frag, const uint16_t *dY, const float *rsp, const float *A, const float *b,
                           int d, uint16_t *dX, const uint16_t *X, float *mapp, int64_t N, int64_t m, int64_t n,
                           hipStream_t st);
-hipError_t launch_map_combine(const float *mapp, int d, int accumulate, float *dA, float *db, hipStream_t st);
+hipError_t launch_map_combine(const float *mapp, int rows, int d, int accumulate, float *dA, float *db,
+                              hipStream_t st);
 // maskbits: the straight-through mask; or, with est.dge set, nullptr and the
 // mask and slope are taken from Z (bf16, m x n) under mask_mode
 hipError_t launch_dw_bf16(const uint16_t *xt, const uint16_t *dyt, const uint64_t *maskbits, const uint16_t *Z,
