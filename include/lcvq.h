@@ -268,8 +268,9 @@ size_t lcvq_packed_scratch_bytes(void);
  *   dX, dZ, dA, db  each may be NULL to skip it (dA and db are produced
  *              together: both NULL or both non-NULL)
  *   dz_dtype   element type of dZ: LCVQ_F32, or LCVQ_BF16 when dtype is bf16
- * dA/db are summed with floating-point atomics, so their last bits may vary
- * from run to run.
+ * bf16: dA/db are per-block partial sums added in a fixed order, so repeated
+ * calls give the same bits.  fp32: they are summed with floating-point
+ * atomics, so their last bits may vary from run to run.
  */
 lcvq_status_t lcvq_linear_bwd(int64_t N, int64_t m, int64_t n, int32_t d, int32_t dtype,
                               const void *Z, const float *A, const float *b,

@@ -3,8 +3,9 @@ C ABI: the forward saves the codes in the input-gradient operand layout, both
 straight-through masks and X' in the weight-gradient operand layout, and the
 backward reads them instead of rebuilding them from Z and X.  The kernels are
 the same and so are the values they see, so Y, the packed codes, dX and dZ
-must equal those of the plain calls bit for bit (dA and db are summed with
-atomics in an unspecified order), and everything meets the oracle's bar."""
+must equal those of the plain calls bit for bit (dA and db too: they are
+per-block partial sums added in a fixed order), and everything meets the
+oracle's bar."""
 import numpy as np
 import pytest
 
@@ -70,11 +71,9 @@ def test_training_pair_matches_plain_calls_and_oracle(lc, N, m, n, d, variant):
     saved.fill_(0xA5)                                      # no stale zeros to hide a missing write
     plain = _pair(lc, Z, A, b, X, dY, d, dge=dge, mask_mode=mask_mode, q=q)
     train = _pair(lc, Z, A, b, X, dY, d, saved=saved, dge=dge, mask_mode=mask_mode, q=q)
-    for key in ("Y", "packed", "dX", "dZ"):
+    for key in ("Y", "packed", "dX", "dZ", "dA", "db"):
         assert torch.equal(_bits(train[key]) if key != "packed" else train[key],
                            _bits(plain[key]) if key != "packed" else plain[key]), key
-    for key in ("dA", "db"):
-        assert rel_fro(to_host(train[key]), to_host(plain[key])) <= 1e-6, key
     v = {key: orc.widen(inp[key], "bf16") for key in ("Z", "X", "dY")}
     A64, b64 = inp["A"].astype(np.float64), inp["b"].astype(np.float64)
     qs, qb = np.float32(q[0]), np.float32(q[1])
@@ -130,8 +129,6 @@ def test_training_pair_full_size(lc):
     saved = lc.new_saved(N, m, n, d, torch.bfloat16, "cuda")
     plain = _pair(lc, Z, A, b, X, dY, d)
     train = _pair(lc, Z, A, b, X, dY, d, saved=saved)
-    for key in ("Y", "packed", "dX", "dZ"):
+    for key in ("Y", "packed", "dX", "dZ", "dA", "db"):
         assert torch.equal(_bits(train[key]) if key != "packed" else train[key],
                            _bits(plain[key]) if key != "packed" else plain[key]), key
-    for key in ("dA", "db"):
-        assert rel_fro(to_host(train[key]), to_host(plain[key])) <= 1e-6, key
