@@ -40,6 +40,9 @@ namespace lcvq {
 constexpr int kPkChunk = 4096;  // prepass columns per block (16 per thread)
 constexpr int kPkRows = 64;     // product rows per block (16 per MFMA row block, four row blocks)
 constexpr int kPkStep = 256;    // K columns per product step (64 bytes of codes per row)
+constexpr int kMaxPairs = 6;    // fused product: (token, 256-group run) pairs per thread in the X'' fill
+constexpr int kPrePairs = 2;    // .. of which loaded ahead of the first codes
+constexpr int kPreChunks = 8;   // X'' chunks per thread loaded ahead of the first codes (copied product)
 
 // ---------------------------------------------------------------- prepass --
 // grid (ceil(nP / 4096), 16): block (chunk, t) transforms columns
@@ -176,46 +179,15 @@ __global__ __launch_bounds__(256) void k_packed_gemv(const uint8_t *__restrict__
   u32x4 cw[2][4], xf[2][8];
   const int nch = (j1 - j0) * 32 * Nc;  // kXL: 16-byte chunks in LDS; chunk nch is zero
   // chunk c = ((jj * 8 + i) * 4 + q) * Nc + t holds fragment (j0 + jj, i), lane 16 q + t
-  if constexpr (kXL == 1) {
-    for (int c = tid; c < nch; c += 256) {
-      const int t = c % Nc, fq = c / Nc;
-      xl[c] = __builtin_amdgcn_raw_buffer_load_b128(
-          rX, (uint32_t)(((j0 * 8 + (fq >> 2)) * 64 + (fq & 3) * 16 + t) * 16), 0, 0);
-    }
-    if (tid == 0) xl[nch] = u32x4{0u, 0u, 0u, 0u};
-    __syncthreads();
-  } else if constexpr (kXL == 2) {
-    // token by token, thread tid takes the 16-column groups g16 = tid + 256 i
-    // of the block's steps (step j0 + g16 / 16, lane group (g16 / 4) % 4,
-    // dword g16 % 4); the offsets s are summed in a fixed order (per thread,
-    // across the wave, then across the four waves in the epilogue), so the
-    // result does not depend on scheduling
-    const int ng = (j1 - j0) * 16;
-    for (int t = 0; t < Nc; ++t) {
-      float s = 0.0f;
-      for (int g16 = tid; g16 < ng; g16 += 256) {
-        float x[16];
-        load_x16(X + (int64_t)t * n, (int64_t)j0 * kPkStep + 16 * g16, n, x);
-        u32x4 ev, od;
-        xpp_group<D>(x, A, b, s, ev, od);
-        const int jj = g16 >> 4, qq = (g16 >> 2) & 3, kk = g16 & 3;
-        xl[((jj * 8 + 2 * kk) * 4 + qq) * Nc + t] = ev;
-        xl[((jj * 8 + 2 * kk + 1) * 4 + qq) * Nc + t] = od;
-      }
-#pragma unroll
-      for (int o = 32; o > 0; o >>= 1) s += __shfl_xor(s, o);
-      if (lane == 0) s_red[wave][t] = s;
-    }
-    if (tid == 0) xl[nch] = u32x4{0u, 0u, 0u, 0u};
-    __syncthreads();
-  }
-  auto load = [&](int buf, int j) {
+  auto codes_load = [&](int buf, int j) {
     const bool live = j < j1;
-    const bool xlive = live && tl < Nc;  // X' rows of absent tokens are zero: not loaded
 #pragma unroll
     for (int rb = 0; rb < 4; ++rb)
       cw[buf][rb] = __builtin_amdgcn_raw_buffer_load_b128(
           rP, live ? (uint32_t)((16 * rb + tl) * ldb + 64 * j + 16 * q) : kOffNone, 0, 0);
+  };
+  auto x_load = [&](int buf, int j) {
+    const bool xlive = j < j1 && tl < Nc;  // X' rows of absent tokens are zero: not loaded
     if constexpr (kXL > 0) {
       const int base = xlive ? ((j - j0) * 32 + q) * Nc + tl : nch;
       const int stride = xlive ? 4 * Nc : 0;
@@ -228,6 +200,107 @@ __global__ __launch_bounds__(256) void k_packed_gemv(const uint8_t *__restrict__
             rX, xlive ? (uint32_t)(((j * 8 + i) * 64 + lane) * 16) : kOffNone, 0, 0);
     }
   };
+  auto load = [&](int buf, int j) {
+    codes_load(buf, j);
+    x_load(buf, j);
+  };
+  // With X'' in LDS, the codes of the wave's first two steps are loaded before
+  // the block fills those rows (after the fill's own first loads), so that
+  // their latency passes during the fill; the barrier after the fill waits for
+  // LDS only, not for those loads.
+  int j = j0 + wave;
+  if constexpr (kXL == 1) {
+    auto xoff = [&](int c) {
+      const int t = c % Nc, fq = c / Nc;
+      return c < nch ? (uint32_t)(((j0 * 8 + (fq >> 2)) * 64 + (fq & 3) * 16 + t) * 16) : kOffNone;
+    };
+    u32x4 xc[kPreChunks];
+#pragma unroll
+    for (int ci = 0; ci < kPreChunks; ++ci)
+      xc[ci] = __builtin_amdgcn_raw_buffer_load_b128(rX, xoff(tid + 256 * ci), 0, 0);
+    __builtin_amdgcn_sched_barrier(0);
+    codes_load(0, j);
+    codes_load(1, j + 4);
+    __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+    for (int ci = 0; ci < kPreChunks; ++ci)
+      if (tid + 256 * ci < nch) xl[tid + 256 * ci] = xc[ci];
+    for (int c = tid + 256 * kPreChunks; c < nch; c += 256)  // (these wait behind the codes)
+      xl[c] = __builtin_amdgcn_raw_buffer_load_b128(rX, xoff(c), 0, 0);
+  } else if constexpr (kXL == 2) {
+    // token by token, thread tid takes the 16-column groups g16 = tid + 256 k
+    // (k < G) of the block's steps (step j0 + g16 / 16, lane group (g16 / 4) %
+    // 4, dword g16 % 4): pair p = t G + k, at most kMaxPairs (the rows fit in
+    // 48 KiB); the offsets s are summed in a fixed order (per thread, across
+    // the wave, then across the four waves in the epilogue), so the result
+    // does not depend on scheduling
+    const int ng = (j1 - j0) * 16, G = (ng + 255) >> 8, P = Nc * G;
+    const __amdgpu_buffer_rsrc_t rXr = make_rsrc(X, (int64_t)Nc * n * 2);
+    auto xload = [&](int p, u32x4 (&w)[2]) {
+      const int t = p < P ? p / G : 0, g16 = tid + 256 * (p - t * G);
+      const int64_t c0 = (int64_t)j0 * kPkStep + 16 * g16;
+      const bool in = p < P && g16 < ng && c0 < n;
+      const uint32_t off = in ? (uint32_t)(((int64_t)t * n + c0) * 2) : kOffNone;
+      w[0] = __builtin_amdgcn_raw_buffer_load_b128(rXr, off, 0, 0);
+      w[1] = __builtin_amdgcn_raw_buffer_load_b128(rXr, in ? off + 16u : kOffNone, 0, 0);
+    };
+    u32x4 xr[kPrePairs][2];
+#pragma unroll
+    for (int p = 0; p < kPrePairs; ++p) xload(p, xr[p]);
+    __builtin_amdgcn_sched_barrier(0);
+    codes_load(0, j);
+    codes_load(1, j + 4);
+    __builtin_amdgcn_sched_barrier(0);
+    float s = 0.0f;
+#pragma unroll
+    for (int p = 0; p < kMaxPairs; ++p) {
+      if (p < P) {
+        const int t = p / G, k = p - t * G, g16 = tid + 256 * k;
+        u32x4 w[2];
+        if (p < kPrePairs) {
+          w[0] = xr[p < kPrePairs ? p : 0][0];
+          w[1] = xr[p < kPrePairs ? p : 0][1];
+        } else {
+          xload(p, w);  // (waits behind the codes)
+        }
+        if (g16 < ng) {
+          float x[16];
+#pragma unroll
+          for (int e = 0; e < 8; ++e) {
+            const uint32_t wd = e < 4 ? w[0][e] : w[1][e - 4];
+            x[2 * e] = bf16_lo(wd);
+            x[2 * e + 1] = bf16_hi(wd);
+          }
+          u32x4 ev, od;
+          xpp_group<D>(x, A, b, s, ev, od);
+          const int jj = g16 >> 4, qq = (g16 >> 2) & 3, kk = g16 & 3;
+          xl[((jj * 8 + 2 * kk) * 4 + qq) * Nc + t] = ev;
+          xl[((jj * 8 + 2 * kk + 1) * 4 + qq) * Nc + t] = od;
+        }
+        if (k == G - 1) {
+#pragma unroll
+          for (int o = 32; o > 0; o >>= 1) s += __shfl_xor(s, o);
+          if (lane == 0) s_red[wave][t] = s;
+          s = 0.0f;
+        }
+      }
+    }
+  }
+  if constexpr (kXL > 0) {
+    if (tid == 0) xl[nch] = u32x4{0u, 0u, 0u, 0u};
+    // barrier over the LDS fill only (no wait for the codes in flight)
+    asm volatile("" ::: "memory");
+    __builtin_amdgcn_s_waitcnt(15 | (3 << 14) | (7 << 4));  // lgkmcnt(0)
+    __builtin_amdgcn_s_barrier();
+    asm volatile("" ::: "memory");
+    x_load(0, j);
+    x_load(1, j + 4);
+  } else {
+    load(0, j);
+    __builtin_amdgcn_sched_barrier(0);
+    load(1, j + 4);
+  }
+  __builtin_amdgcn_sched_barrier(0);
   // bf16 1.0 in both halves, held in a vector register: with the mask from a
   // scalar register each operand dword is then one v_and_or_b32 (a literal
   // would not fit that instruction and costs a separate and + or)
@@ -264,14 +337,9 @@ __global__ __launch_bounds__(256) void k_packed_gemv(const uint8_t *__restrict__
     }
   };
   // two register buffers, the loads of a wave's step after next issued once
-  // the current step's MFMAs are
+  // the current step's MFMAs are (the first two steps' loads are issued above)
   // (the scheduling fences keep each buffer's loads together, so the wait
   // before a step covers that step's loads only)
-  int j = j0 + wave;
-  load(0, j);
-  __builtin_amdgcn_sched_barrier(0);
-  load(1, j + 4);
-  __builtin_amdgcn_sched_barrier(0);
   for (; j < j1; j += 8) {
     compute(0);
     __builtin_amdgcn_sched_barrier(0);
@@ -374,7 +442,8 @@ hipError_t launch_packed_prep(const uint16_t *X, int Nc, int64_t m, int64_t n, i
 // block has enough steps to repay the copy and its barrier (on short K ranges
 // the product is latency-bound and the copy only adds to it).
 static bool packed_xl(const PackedPlan &p, int Nc) {
-  return ((size_t)p.spb * 32 * Nc + 1) * 16 <= 48 * 1024 && p.spb >= 24;
+  // (the 48 KiB bound with spb >= 24 also keeps the fused fill's pairs within kMaxPairs)
+  return ((size_t)p.spb * 32 * Nc + 1) * 16 <= 48 * 1024 && p.spb >= 24 && Nc * ((p.spb + 15) / 16) <= kMaxPairs;
 }
 
 bool packed_fused(int64_t m, int64_t n, int Nc) {
