@@ -347,39 +347,73 @@ def step_distribution(torch, step, K):
     return {"median_ms": round(t[len(t) // 2], 4), "min_ms": round(t[0], 4), "max_ms": round(t[-1], 4), "steps": K}
 
 
-def sample_sclk(torch, step, seconds=2.0):
-    """The shader clock level the driver marks as current in sysfs
-    (pp_dpm_sclk), read while steps keep the GPU busy; None where no such file
-    is readable.  A plain file read: no helper program is started."""
+def sample_sclk(torch, step, seconds=2.5):
+    """Shader clock while steps keep the GPU busy, from a helper thread: the
+    level the driver marks as current in sysfs (pp_dpm_sclk), and, where the
+    amdsmi module is importable, the power-management firmware's current
+    graphics clock of each XCD and the socket power (readings from the first
+    second are dropped: the firmware's figures lag the load).  Plain reads: no
+    helper program is started; None where nothing is readable."""
     import glob
     import re
     import threading
     import time
     files = sorted(glob.glob("/sys/class/drm/card*/device/pp_dpm_sclk"))
-    if not files:
-        return None
-    readings = []
+    smi = None
+    try:
+        import amdsmi
+        amdsmi.amdsmi_init()
+        handles = amdsmi.amdsmi_get_processor_handles()
+        smi = (amdsmi, handles[0]) if handles else None
+    except Exception:
+        smi = None
+    levels, xcd_clocks, power = [], [], []
 
     def probe():
-        time.sleep(0.2)
-        for f in files:
-            try:
-                txt = open(f).read()
-            except OSError:
-                continue
-            m = re.search(r"(\d+)\s*mhz\s*\*", txt, re.IGNORECASE)
-            if m:
-                readings.append(int(m.group(1)))
+        t_start = time.time()
+        while time.time() - t_start < seconds - 0.1:
+            time.sleep(0.25)
+            for f in files:
+                try:
+                    m = re.search(r"(\d+)\s*mhz\s*\*", open(f).read(), re.IGNORECASE)
+                except OSError:
+                    continue
+                if m:
+                    levels.append(int(m.group(1)))
+            if smi is not None and time.time() - t_start > 1.0:
+                try:
+                    met = smi[0].amdsmi_get_gpu_metrics_info(smi[1])
+                    clk = [int(c) for c in met.get("current_gfxclks", []) if isinstance(c, int) and 0 < c < 10000]
+                    if clk:
+                        xcd_clocks.append(clk)
+                    pw = met.get("current_socket_power")
+                    if isinstance(pw, int) and pw > 0:
+                        power.append(pw)
+                except Exception:
+                    pass
 
     th = threading.Thread(target=probe)
     th.start()
     t0 = time.time()
-    while th.is_alive() and time.time() - t0 < seconds:
+    while th.is_alive() and time.time() - t0 < seconds + 1.0:
         for _ in range(20):
             step()
         torch.cuda.synchronize()
     th.join()
-    return {"sclk_mhz": max(readings) if readings else None, "source": "sysfs pp_dpm_sclk (current level) during steps"}
+    if smi is not None:
+        try:
+            smi[0].amdsmi_shut_down()
+        except Exception:
+            pass
+    out = {"sclk_mhz": max(levels) if levels else None, "source": "sysfs pp_dpm_sclk (current level) during steps"}
+    if xcd_clocks:
+        mean = sum(sum(c) / len(c) for c in xcd_clocks) / len(xcd_clocks)
+        out["gfxclk_mhz"] = round(mean, 1)
+        out["gfxclk_mhz_per_xcd_last"] = xcd_clocks[-1]
+        out["socket_power_w"] = round(sum(power) / len(power), 1) if power else None
+        out["gfxclk_source"] = ("amdsmi gpu metrics current_gfxclks (mean over XCDs and over the readings "
+                                "after the first second of steps)")
+    return out
 
 
 def library_gemm(torch, N, m, n):
@@ -586,6 +620,8 @@ def main():
                                      "ms_per_step_with_kernel_events"),
         "step_distribution": dist,
         "gpu_clock": sclk,
+        "frac_of_peak_at_measured_clock": (round(value / (PEAK_MFMA_BF16 * sclk["gfxclk_mhz"] / 2400.0), 4)
+                                           if sclk and sclk.get("gfxclk_mhz") else None),
     }
     res["plain_step"] = variant_step(lc, torch, layers, args.steps, "step_plain",
                                      "the plain calls: the backward rebuilds codes, mask and X' from Z and X")
