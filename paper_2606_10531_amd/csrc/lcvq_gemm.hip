@@ -317,22 +317,30 @@ __global__ __launch_bounds__(256, 1) void k_gemm_codes(
   const __amdgpu_buffer_rsrc_t ro = make_rsrc(out + tw * ldo, out == nullptr ? 0 : (Tvalid - tw) * ldo * 2);
   const int64_t cb0 = (int64_t)tm * kTile + 8 * q;
   // Per-token term, held as up to kMaxParts partial rows vstride apart and
-  // summed here: s of the forward, rowsum(dY) of the input gradient.
-  constexpr int kMaxParts = kMaxActChunks;  // s has at most this many parts, rowsum(dY) at most eight
+  // summed here: s of the forward, rowsum(dY) of the input gradient.  The
+  // four lanes of a token (L % 16 + 16 q) split the parts (lane q adds parts
+  // q, q + 4, ..., in that order) and then exchange their sums: (q0 + q1) +
+  // (q2 + q3) in every one of them, the same bits in all four.
+  constexpr int kMaxParts = kMaxActChunks;  // s and rowsum(dY) have at most this many parts
+  static_assert(kMaxParts % 4 == 0, "whole parts per lane");
   const __amdgpu_buffer_rsrc_t rv = make_rsrc(vecT + tw, ((int64_t)(vparts - 1) * vstride + Tvalid - tw) * 4);
-  float vp[kMaxParts][4], vt[4];
+  float vp[kMaxParts / 4][4], vt[4];
 #pragma unroll
-  for (int p = 0; p < kMaxParts; ++p)
+  for (int i = 0; i < kMaxParts / 4; ++i)
 #pragma unroll
-    for (int tb = 0; tb < 4; ++tb)
-      vp[p][tb] = p < vparts ? as_f(__builtin_amdgcn_raw_buffer_load_b32(rv, (int)((p * vstride + tb * 16 + c16) * 4),
+    for (int tb = 0; tb < 4; ++tb) {
+      const int p = 4 * i + q;
+      vp[i][tb] = p < vparts ? as_f(__builtin_amdgcn_raw_buffer_load_b32(rv, (int)((p * vstride + tb * 16 + c16) * 4),
                                                                         0, 0))
                              : 0.0f;
+    }
 #pragma unroll
   for (int tb = 0; tb < 4; ++tb) {
-    vt[tb] = vp[0][tb];
+    float v = vp[0][tb];
 #pragma unroll
-    for (int p = 1; p < kMaxParts; ++p) vt[tb] += vp[p][tb];
+    for (int i = 1; i < kMaxParts / 4; ++i) v += vp[i][tb];
+    const float h = v + __shfl_xor(v, 16, 64);
+    vt[tb] = h + __shfl_xor(h, 32, 64);
   }
   // Each accumulator is read out of its AGPR at its use, one ordered statement
   // per value (the drain's wait states cover them).  Left to the compiler, the

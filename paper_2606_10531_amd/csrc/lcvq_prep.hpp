@@ -41,12 +41,13 @@ hipError_t launch_fwd_prep_bf16(const uint16_t *Z, int64_t m, int64_t n, const Q
 // same padding).
 inline int64_t bwd_tokens(int64_t N) { return (N + 255) / 256 * 256; }
 
-// The bf16 backward prepass sums each dY row in at most eight parts (runs of
+// The bf16 backward prepass sums each dY row in at most sixteen parts (runs of
 // 64-feature sub-tiles of the out-features, padded to 256); the input-gradient
-// product adds the parts.
+// product adds the parts.  (Sixteen parts: four blocks per CU at 4096 x 4096
+// instead of two, 13.7 -> 12.2 us.)
 inline int rowsum_subtiles_per_part(int64_t m) {
   const int64_t nfy = (m + 255) / 256 * 4;
-  const int64_t spf = (nfy + 7) / 8;
+  const int64_t spf = (nfy + 15) / 16;
   return spf < 1 ? 1 : (int)spf;
 }
 inline int rowsum_parts(int64_t m) {
